@@ -1,0 +1,259 @@
+"""Benchmark of the Thinker decoder layer on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-decode] [--no-cpu]
+
+A step is one tri_layer_prefill call of the 7B-class dense layer over 8
+sequences x 2048 tokens (hidden 3584, 28/4 heads, head_dim 128, SwiGLU 18944),
+inputs seeded and already resident in HBM.  K timed steps are bracketed by
+torch.cuda.synchronize() and HIP events on the launch stream; per-stage
+durations come from the library's own HIP-event timers over the same timed
+region.  One JSON line is printed.  The decode workload (batch 64, KV 4096,
+32 steps) is timed as a secondary result in the same line.
+
+Roofline: the dominant kernel of prefill is the fused gate/up + SwiGLU GEMM
+(2 * 16384 * 37888 * 3584 flop per launch), priced against 2.5 PFLOP/s dense
+bf16; decode's dominant kernel is split-KV attention, priced against 8 TB/s
+on the K/V bytes it must read.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import subprocess
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+METRIC = "Thinker-layer prefill & decode tokens/s; % MFMA / HBM roofline; J/token"
+
+
+def linear_params(cfg) -> int:
+    H, D = cfg.hidden, cfg.head_dim
+    return H * cfg.qkv_rows + cfg.n_q_heads * D * H + 3 * cfg.ffn_dim * H
+
+
+def prefill_flops(cfg, batch) -> float:
+    pairs = sum((c + q) * (c + q + 1) // 2 - c * (c + 1) // 2 for c, q in zip(batch.ctx_len, batch.q_len))
+    return 2.0 * linear_params(cfg) * batch.n_tokens + 4.0 * cfg.head_dim * cfg.n_q_heads * pairs
+
+
+def energy_j():
+    """Board energy counter in joules via amd-smi, or None if unavailable."""
+    try:
+        out = subprocess.run(["amd-smi", "metric", "--energy", "--json"], capture_output=True,
+                             text=True, timeout=20).stdout
+        d = json.loads(out)
+        d = d[0] if isinstance(d, list) else d
+        e = d.get("energy", d)
+        v = e.get("total_energy_consumption", e)
+        if isinstance(v, dict):
+            val, unit = float(v["value"]), v.get("unit", "J")
+        else:
+            val, unit = float(str(v).split()[0]), (str(v).split() + ["J"])[1]
+        scale = {"J": 1.0, "mJ": 1e-3, "uJ": 1e-6, "kJ": 1e3}.get(unit, 1.0)
+        return val * scale
+    except Exception:
+        return None
+
+
+def cpu_baseline(wl, wb, kb, vb, xb, budget_s=20.0):
+    """The CPU oracle (plain fp32 NumPy) on a bounded sample: whole sequences of
+    the same workload, repeated until the time budget is used."""
+    import oracle
+    from synth import Batch, bf16_to_f32
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=os.cpu_count())
+    except Exception:
+        threads = os.cpu_count()
+    w = {k: bf16_to_f32(v) for k, v in wb.items()}
+    q = int(wl.batch.q_len[0])
+    sub = Batch(wl.batch.slot[:1], wl.batch.ctx_len[:1], wl.batch.q_len[:1])
+    x = bf16_to_f32(xb[:q])
+    t0 = time.perf_counter()
+    n_tok = 0
+    reps = 0
+    while True:
+        oracle.layer_forward(wl.cfg, w, kb, vb, sub, x, dtype=np.float32)
+        n_tok += q
+        reps += 1
+        if time.perf_counter() - t0 > budget_s / 2 or reps >= 4:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": n_tok / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{reps} x one {q}-token causal prefill sequence of the same layer "
+                      f"(fp32 NumPy oracle), {dt:.1f} s"}
+
+
+def run_prefill(args, tri, wl, wb, kb, vb, xb):
+    import torch
+    from paper_2606_29629_amd.workload import DeviceLayer, device_batch, device_cache, to_device_bf16
+    dl = DeviceLayer(wl.cfg, wb)
+    cache = device_cache(kb, vb)
+    x = to_device_bf16(xb)
+    db = device_batch(wl.batch)
+    out = torch.empty_like(x)
+    ws = torch.empty(tri.workspace_size(dl.cfg, db), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        tri.layer_prefill(dl.cfg, dl.w, cache, db, x, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    tri.profile_enable(True)
+    e_start = energy_j()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        tri.layer_prefill(dl.cfg, dl.w, cache, db, x, out=out, workspace=ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    e_end = energy_j()
+    ms = e0.elapsed_time(e1) / args.steps
+    prof = tri.profile_read()
+    tri.profile_enable(False)
+    del dl, cache, x, out, ws
+    torch.cuda.empty_cache()
+    return ms, wall, prof, (None if e_start is None or e_end is None else e_end - e_start)
+
+
+def run_decode(args, tri):
+    import torch
+    from paper_2606_29629_amd.workload import DeviceLayer, device_batch, device_cache, to_device_bf16
+    from synth import make_cache, make_weights, make_x, workload
+    wl = workload("dense_decode")
+    wb = make_weights(wl.cfg, wl.seed)
+    kb, vb = make_cache(wl.cfg, wl.n_slots, wl.max_seq, wl.seed)
+    dl = DeviceLayer(wl.cfg, wb)
+    cache = device_cache(kb, vb)
+    del kb, vb
+    steps = wl.decode_steps + 1
+    batches, xs = [], []
+    b = wl.batch
+    for s in range(steps):
+        batches.append(device_batch(b))
+        xs.append(to_device_bf16(make_x(wl.cfg, b.n_tokens, wl.seed, step=s)))
+        b = b.advanced()
+    out = torch.empty_like(xs[0])
+    ws_bytes = max(tri.workspace_size(dl.cfg, db) for db in batches)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    for s in range(min(steps, 4)):
+        tri.layer_decode(dl.cfg, dl.w, cache, batches[s], xs[s], out=out, workspace=ws)
+    torch.cuda.synchronize()
+    reps = max(1, args.decode_reps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    tri.profile_enable(True)
+    e_start = energy_j()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        for s in range(steps):
+            tri.layer_decode(dl.cfg, dl.w, cache, batches[s], xs[s], out=out, workspace=ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    e_end = energy_j()
+    total_ms = e0.elapsed_time(e1)
+    prof = tri.profile_read()
+    tri.profile_enable(False)
+    n_tok = reps * steps * wl.batch.n_seqs
+    kv_bytes = sum(int(bb.host["ctx_len"].astype(np.int64).sum() + bb.n_seqs) for bb in batches) \
+        * wl.cfg.n_kv_heads * wl.cfg.head_dim * 2 * 2
+    act_bytes = steps * wl.batch.n_seqs * wl.cfg.n_q_heads * wl.cfg.head_dim * 2 * 2
+    attn = prof["attn_decode"]
+    attn_s = attn["total_ms"] / 1e3 / reps
+    attn_gbs = (kv_bytes + act_bytes) / attn_s / 1e9
+    step_bytes = (2 * linear_params(wl.cfg) + kv_bytes / steps)
+    res = {
+        "workload": "dense_decode: batch 64, KV 4096 -> 4127, 32 one-token steps",
+        "tokens_per_s": n_tok / (total_ms / 1e3),
+        "ms_per_step": total_ms / (reps * steps),
+        "hbm_frac_step": step_bytes / (total_ms / 1e3 / (reps * steps)) / 1e9 / PEAK_HBM_GBS,
+        "roofline": {"kernel": "attn_decode (split-KV + combine)", "bound": "hbm",
+                     "achieved": attn_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": attn_gbs / PEAK_HBM_GBS, "traffic": None},
+        "stages_ms_per_step": {k: v["total_ms"] / (reps * steps) for k, v in prof.items() if v["launches"]},
+    }
+    if e_start is not None and e_end is not None:
+        res["joules_per_token"] = (e_end - e_start) / n_tok
+    del dl, cache, xs, out, ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--decode-reps", type=int, default=5)
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); "
+              "the layer is not sharded across GPUs.", file=sys.stderr)
+        return 2
+    import torch
+    import paper_2606_29629_amd as tri
+    from synth import make_cache, make_weights, make_x, workload
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    wl = workload("dense_prefill")
+    wb = make_weights(wl.cfg, wl.seed)
+    kb, vb = make_cache(wl.cfg, wl.n_slots, wl.max_seq, wl.seed)
+    xb = make_x(wl.cfg, wl.batch.n_tokens, wl.seed)
+    ms, wall, prof, joules = run_prefill(args, tri, wl, wb, kb, vb, xb)
+    T = wl.batch.n_tokens
+    flops = prefill_flops(wl.cfg, wl.batch)
+    gu = prof["gate_up"]
+    gu_ms = gu["total_ms"] / max(gu["launches"], 1)
+    gu_flops = 2.0 * T * 2 * wl.cfg.ffn_dim * wl.cfg.hidden
+    gu_tflops = gu_flops / (gu_ms / 1e3) / 1e12
+    res = {
+        "metric": METRIC,
+        "value": T / (ms / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations, N(0,0.02) random-init weights)",
+        "config": {"workload": "dense_prefill: 7B-class dense Thinker layer, 8 x 2048-token causal prefill",
+                   "hidden": wl.cfg.hidden, "q_heads": wl.cfg.n_q_heads, "kv_heads": wl.cfg.n_kv_heads,
+                   "head_dim": wl.cfg.head_dim, "ffn": wl.cfg.ffn_dim, "batch": 8, "seq_len": 2048,
+                   "parallelism": "single GPU"},
+        "layer_tflops": flops / (ms / 1e3) / 1e12,
+        "layer_mfma_frac": flops / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+        "roofline": {"kernel": "gate_up (fused SwiGLU GEMM)", "bound": "mfma", "achieved": gu_tflops,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": gu_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": None},
+        "stages_ms_per_step": {k: v["total_ms"] / args.steps for k, v in prof.items() if v["launches"]},
+        "wall_s_timed": wall,
+    }
+    if joules is not None:
+        res["joules_per_token"] = joules / (T * args.steps)
+    if not args.no_decode:
+        res["decode"] = run_decode(args, tri)
+    if not args.no_cpu:
+        from synth import bf16_to_f32
+        res["cpu_baseline"] = cpu_baseline(wl, wb, bf16_to_f32(kb), bf16_to_f32(vb), xb)
+    print(json.dumps(res))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,220 @@
+/*
+ * tri.h -- C ABI of libtri: the Thinker decoder-layer forward on one MI355X
+ * (gfx950), in the two arithmetic-intensity regimes the paper contrasts.
+ *
+ * The paper's Thinker stage (Section II-A) consumes its token stream in a
+ * compute-bound prefill and then decodes autoregressively over a KV cache;
+ * Section II-C (Observation 2) attributes prefill to dense GEMM kernels and
+ * decode to GEMV-like operators, and Section III-A1 labels each scheduler step
+ * prefill, decode or mixed from its per-request scheduled-token counts.  This
+ * library computes one decoder layer for such a step:
+ *
+ *   h   = RMSNorm(x; attn_norm)                      y = x / sqrt(mean(x^2)+eps) * g
+ *   q,k,v = h W_qkv^T (+ b_qkv), rotary embedding on q and k at each token's
+ *         position (rotate-half pairs (i, i+D/2), angle pos * base^(-2i/D)
+ *         formed in double precision), k and v appended to the cache
+ *   o   = causal grouped-query softmax attention over the cache (query head j
+ *         reads KV head floor(j*Hkv/Hq)), scale 1/sqrt(D)
+ *   x1  = x + o W_o^T
+ *   h2  = RMSNorm(x1; mlp_norm)
+ *   out = x1 + SwiGLU(h2)                             dense
+ *   out = x1 + sum_j w_j SwiGLU_{e_j}(h2)             MoE, top-k softmax routing
+ *
+ * The paper gives no layer equations; the structure is the Qwen2-family
+ * pre-norm decoder of the model it serves (Section IV-A), and every
+ * convention above is a declared reading.
+ *
+ * Conventions common to all entry points
+ *  - Every pointer named "device" is a device (HBM) address; host structs are
+ *    read during the call only.  The caller owns every buffer (weights, cache,
+ *    activations, outputs, workspace); the library allocates nothing and keeps
+ *    no pointer after returning.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *    stream) and never synchronise with the host.
+ *  - Arguments are validated on the host before any launch; a negative status
+ *    means nothing was launched and nothing was written.  TRI_ERR_HIP means a
+ *    launch failed: outputs and this call's cache rows are then unspecified.
+ *  - Device-side index arrays (cu_q, ctx_len, slot, pos) cannot be checked on
+ *    the host.  Kernels never read or write outside the buffers described
+ *    here: a token whose slot is >= n_slots or whose cache row is >= max_seq
+ *    is skipped (its outputs are unspecified).
+ *  - Element type: bfloat16 storage (TRI_BF16), float32 accumulation.
+ *    Weights are row-major [out, in].  All device buffers must be 16-byte
+ *    aligned.
+ */
+#ifndef TRI_H
+#define TRI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TRI_OK = 0,
+  TRI_ERR_NULL = -1,        /* a required pointer is NULL                         */
+  TRI_ERR_SHAPE = -2,       /* inconsistent sizes                                 */
+  TRI_ERR_UNSUPPORTED = -3, /* valid but not implemented (dtype, head_dim, flag)  */
+  TRI_ERR_RANGE = -4,       /* a size exceeds a buffer (e.g. ctx + q > max_seq)   */
+  TRI_ERR_ALIGN = -5,       /* a device pointer is not 16-byte aligned            */
+  TRI_ERR_WORKSPACE = -6,   /* workspace smaller than tri_workspace_size()        */
+  TRI_ERR_HIP = -7,         /* a HIP launch failed                                */
+  TRI_ERR_ALIAS = -8        /* an output overlaps an input it must not overlap    */
+} tri_status;
+
+typedef enum { TRI_BF16 = 0, TRI_F32 = 1 } tri_dtype;
+
+enum {
+  TRI_F_QKV_BIAS = 1,   /* add b_qkv after the q/k/v projection                   */
+  TRI_F_MOE = 2,        /* mixture-of-experts FFN instead of the dense SwiGLU      */
+  TRI_F_MOE_RENORM = 4, /* renormalise the top-k routing weights to sum to 1       */
+  TRI_F_ALL = 7
+};
+
+typedef struct {
+  int32_t hidden;         /* H; multiple of 64                                      */
+  int32_t n_q_heads;      /* Hq                                                     */
+  int32_t n_kv_heads;     /* Hkv; Hq % Hkv == 0                                     */
+  int32_t head_dim;       /* D in {64, 128}                                         */
+  int32_t ffn_dim;        /* dense SwiGLU width F; multiple of 64 (dense only)      */
+  int32_t n_experts;      /* E (MoE only), 1..256                                   */
+  int32_t top_k;          /* k (MoE only), 1..min(E, 16)                            */
+  int32_t expert_ffn_dim; /* per-expert SwiGLU width (MoE only); multiple of 64     */
+  float rms_eps;          /* RMSNorm epsilon (>= 0)                                 */
+  float rope_base;        /* rotary base (> 0)                                      */
+  int32_t dtype;          /* tri_dtype; only TRI_BF16 is implemented                */
+  int32_t flags;          /* TRI_F_* bits                                           */
+} tri_layer_config;
+
+/* Device pointers to one layer's weights, row-major [out, in], bfloat16.       */
+typedef struct {
+  const void* attn_norm; /* [H]                                                    */
+  const void* w_qkv;     /* [(Hq + 2 Hkv) D, H]: q heads, then k heads, then v     */
+  const void* b_qkv;     /* [(Hq + 2 Hkv) D]; required iff TRI_F_QKV_BIAS          */
+  const void* w_o;       /* [H, Hq D]                                              */
+  const void* mlp_norm;  /* [H]                                                    */
+  const void* w_gate_up; /* dense [2F, H] (gate rows [0,F), up rows [F,2F));
+                            MoE   [E, 2Fe, H] (same split per expert)             */
+  const void* w_down;    /* dense [H, F]; MoE [E, H, Fe]                           */
+  const void* w_router;  /* MoE [E, H]; NULL for a dense layer                     */
+} tri_layer_weights;
+
+/* KV cache: K and V each [n_slots, Hkv, max_seq, D] bfloat16 (device).  Keys
+ * are stored after the rotary embedding.  Row r of a slot holds the token at
+ * position r of the sequence occupying that slot.                              */
+typedef struct {
+  void* k;
+  void* v;
+  int32_t n_slots;
+  int32_t max_seq;
+} tri_kv_cache;
+
+/* A ragged batch (one scheduler step).  Host scalars size the launches; the
+ * arrays are device int32.  Sequence s owns new tokens cu_q[s] .. cu_q[s+1]-1
+ * of x; its new token i is written to cache row ctx_len[s] + i of slot
+ * slot[s] and attends to rows 0 .. ctx_len[s] + i.  pos[t] is the rotary
+ * position of token t (normally ctx_len + i).                                  */
+typedef struct {
+  int32_t n_seqs;      /* >= 0                                                     */
+  int32_t n_tokens;    /* T = cu_q[n_seqs]                                         */
+  int32_t max_q_len;   /* >= max_s (cu_q[s+1] - cu_q[s])                           */
+  int32_t max_ctx_len; /* >= max_s ctx_len[s]; max_ctx_len + max_q_len <= max_seq  */
+  const int32_t* cu_q;    /* [n_seqs + 1], cu_q[0] = 0, non-decreasing             */
+  const int32_t* ctx_len; /* [n_seqs]                                              */
+  const int32_t* slot;    /* [n_seqs], distinct                                    */
+  const int32_t* pos;     /* [n_tokens]                                            */
+} tri_batch;
+
+/* Byte offsets of the layer's intermediates inside the workspace (for
+ * inspection after a call; contents are valid once the stream has finished).  */
+typedef struct {
+  size_t h;      /* [T, H]   bf16  RMSNorm(x)                                       */
+  size_t q;      /* [T, Hq, D] bf16  rotated queries                                */
+  size_t attn;   /* [T, Hq D] bf16  attention output                                */
+  size_t x1;     /* [T, H]   bf16  x + attn W_o^T                                   */
+  size_t h2;     /* [T, H]   bf16  RMSNorm(x1)                                      */
+  size_t act;    /* dense: [T, F] bf16 SwiGLU activation silu(g)*u                  */
+  size_t total;  /* == tri_workspace_size()                                         */
+} tri_workspace_map;
+
+/* Workspace bytes needed by tri_layer_prefill / tri_layer_decode for a batch
+ * with these host scalars (device arrays are not read).                        */
+tri_status tri_workspace_size(const tri_layer_config* cfg, const tri_batch* batch,
+                              size_t* bytes);
+
+/* The workspace layout used for this config and batch.                        */
+tri_status tri_workspace_layout(const tri_layer_config* cfg, const tri_batch* batch,
+                                tri_workspace_map* map);
+
+/* One decoder layer over a ragged batch (prefill, chunked prefill with a
+ * cached prefix, decode, or any mix: the mixed step of Section III-A1).
+ *  x_in      device [T, H] bf16, token activations in batch order
+ *  x_out     device [T, H] bf16, layer output; must not overlap x_in
+ *  route_idx device [T, top_k] int32 or NULL (MoE: chosen experts, descending
+ *            logit, ties to the lower expert index)
+ *  route_w   device [T, top_k] float or NULL (MoE: routing weights)
+ *  workspace device, >= tri_workspace_size() bytes, 256-byte aligned
+ * Cache rows ctx_len[s] .. ctx_len[s] + q_len - 1 of every sequence are
+ * written; no other cache row is touched.                                      */
+tri_status tri_layer_prefill(const tri_layer_config* cfg, const tri_layer_weights* w,
+                             const tri_kv_cache* cache, const tri_batch* batch,
+                             const void* x_in, void* x_out, int32_t* route_idx,
+                             float* route_w, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* The decode step (every sequence has exactly one new token: n_tokens ==
+ * n_seqs, max_q_len == 1), on the memory-bound path: skinny projections that
+ * stream each weight once and split-KV attention.  Same arguments and
+ * results as tri_layer_prefill.                                                */
+tri_status tri_layer_decode(const tri_layer_config* cfg, const tri_layer_weights* w,
+                            const tri_kv_cache* cache, const tri_batch* batch,
+                            const void* x_in, void* x_out, int32_t* route_idx,
+                            float* route_w, void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/* KV-cache append (the cache write of Section II-A's decode loop, done inside
+ * the layer calls as well): for every new token t of sequence s,
+ *   k[slot[s]][h][ctx_len[s] + i][:] = k_new[t][h][:]   (same for v).
+ *  k_new, v_new  device [T, Hkv, D] bf16.                                       */
+tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* cache,
+                              const tri_batch* batch, const void* k_new, const void* v_new,
+                              void* stream);
+
+/* MoE routing alone (test hook for bit-exact routing): logits = h2 W_r^T in
+ * float32, softmax over all experts, top_k by logit (descending, ties to the
+ * lower index), weights p[idx] (renormalised if TRI_F_MOE_RENORM).
+ *  h2        device [n_tokens, H] float32
+ *  w_router  device [E, H] bf16
+ *  idx, w    device [n_tokens, top_k] int32 / float32                          */
+tri_status tri_moe_route(const tri_layer_config* cfg, const float* h2, const void* w_router,
+                         int32_t n_tokens, int32_t* idx, float* w, void* stream);
+
+/* Per-stage timing for benchmarks.  While enabled, the layer entry points
+ * record a HIP event pair on the caller's stream around every stage (the
+ * stage names are listed in tri_profile.name).  tri_profile_enable(1) resets
+ * the counters; tri_profile_read waits for the recorded events and returns
+ * launches and total milliseconds per stage.  Not thread-safe with
+ * concurrent layer calls from several host threads.                          */
+#define TRI_MAX_STAGES 16
+typedef struct {
+  int32_t n_stages;
+  const char* name[TRI_MAX_STAGES];
+  int32_t launches[TRI_MAX_STAGES];
+  double total_ms[TRI_MAX_STAGES];
+} tri_profile;
+
+tri_status tri_profile_enable(int32_t on);
+tri_status tri_profile_read(tri_profile* out);
+
+/* Static description of a status code.                                         */
+const char* tri_status_string(tri_status s);
+
+/* Library version: major * 10000 + minor * 100 + patch.                         */
+int32_t tri_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TRI_H */

@@ -1,0 +1,13 @@
+"""MI355X-native Thinker decoder layer (prefill, decode, mixed steps).
+
+The compute path is libtri.so (hand-written HIP kernels for gfx950 behind the
+C ABI in include/tri.h); this package is its thin ctypes binding.
+"""
+from ._lib import (DeviceBatch, LayerConfig, TriError, kvcache_append, layer_decode,
+                   profile_enable, profile_read,
+                   layer_prefill, lib, make_config, moe_route, status_string, workspace_layout,
+                   workspace_size)
+
+__all__ = ["DeviceBatch", "LayerConfig", "TriError", "kvcache_append", "layer_decode",
+           "layer_prefill", "lib", "profile_enable", "profile_read", "make_config", "moe_route", "status_string",
+           "workspace_layout", "workspace_size"]

@@ -1,0 +1,411 @@
+// libtri C ABI: host-side validation, workspace layout and the launch
+// sequences of the decoder layer.  No kernel is launched unless every check
+// passes; nothing is allocated.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+#include <vector>
+
+#include "../../include/tri.h"
+#include "kernels.hpp"
+
+using namespace tri;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Projections with at most this many rows take the weight-streaming path.
+constexpr int kSkinnyMaxRows = 128;
+
+tri_status check_config(const tri_layer_config* c) {
+  if (!c) return TRI_ERR_NULL;
+  if (c->dtype != TRI_BF16) return TRI_ERR_UNSUPPORTED;
+  if (c->flags & ~TRI_F_ALL) return TRI_ERR_UNSUPPORTED;
+  if (c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0)
+    return TRI_ERR_SHAPE;
+  if (c->head_dim != 64 && c->head_dim != 128) return TRI_ERR_UNSUPPORTED;
+  if (c->hidden % 64 != 0 || c->hidden > 8192) return TRI_ERR_UNSUPPORTED;
+  if (c->n_q_heads % c->n_kv_heads != 0) return TRI_ERR_SHAPE;
+  if (c->n_q_heads / c->n_kv_heads > 8) return TRI_ERR_UNSUPPORTED;
+  if ((int64_t)c->n_q_heads * c->head_dim % 64 != 0) return TRI_ERR_UNSUPPORTED;
+  if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return TRI_ERR_RANGE;
+  if (c->flags & TRI_F_MOE) {
+    if (c->n_experts < 1 || c->n_experts > 256) return TRI_ERR_UNSUPPORTED;
+    if (c->top_k < 1 || c->top_k > c->n_experts || c->top_k > 16) return TRI_ERR_SHAPE;
+    if (c->expert_ffn_dim <= 0 || c->expert_ffn_dim % 64 != 0) return TRI_ERR_UNSUPPORTED;
+    return TRI_ERR_UNSUPPORTED;  // MoE FFN not built into this library version
+  } else {
+    if (c->ffn_dim <= 0 || c->ffn_dim % 64 != 0) return TRI_ERR_UNSUPPORTED;
+  }
+  return TRI_OK;
+}
+
+tri_status check_batch_scalars(const tri_batch* b) {
+  if (!b) return TRI_ERR_NULL;
+  if (b->n_seqs < 0 || b->n_tokens < 0 || b->max_q_len < 0 || b->max_ctx_len < 0)
+    return TRI_ERR_SHAPE;
+  if (b->n_tokens > 0 && b->n_seqs == 0) return TRI_ERR_SHAPE;
+  if (b->n_tokens > 0 && b->max_q_len == 0) return TRI_ERR_SHAPE;
+  if ((int64_t)b->max_q_len > b->n_tokens) return TRI_ERR_SHAPE;
+  if ((int64_t)b->n_seqs > 0 && (int64_t)b->max_q_len * b->n_seqs < b->n_tokens) return TRI_ERR_SHAPE;
+  return TRI_OK;
+}
+
+struct Layout {
+  size_t tok_slot, tok_row, rope, h, q, attn, x1, h2, act, part, total;
+};
+
+size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
+  const int T = b->n_tokens, H = c->hidden, D = c->head_dim;
+  const int Nqkv = (c->n_q_heads + 2 * c->n_kv_heads) * D;
+  size_t p = attn_decode_partial_bytes(T, c->n_q_heads, D, b->max_ctx_len + 1);
+  if (T > 0 && T <= kSkinnyMaxRows) {
+    size_t g = gemv_partial_bytes(T, Nqkv, H);
+    g = g > gemv_partial_bytes(T, H, c->n_q_heads * D) ? g : gemv_partial_bytes(T, H, c->n_q_heads * D);
+    g = g > gemv_partial_bytes(T, 2 * c->ffn_dim, H) ? g : gemv_partial_bytes(T, 2 * c->ffn_dim, H);
+    g = g > gemv_partial_bytes(T, H, c->ffn_dim) ? g : gemv_partial_bytes(T, H, c->ffn_dim);
+    p = p > g ? p : g;
+  }
+  return p;
+}
+
+Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
+  const size_t T = (size_t)b->n_tokens, H = c->hidden, D = c->head_dim;
+  Layout l;
+  size_t o = 0;
+  l.tok_slot = o; o += up(T * 4);
+  l.tok_row = o;  o += up(T * 4);
+  l.rope = o;     o += up(T * (D / 2) * 8);
+  l.h = o;        o += up(T * H * 2);
+  l.q = o;        o += up(T * c->n_q_heads * D * 2);
+  l.attn = o;     o += up(T * c->n_q_heads * D * 2);
+  l.x1 = o;       o += up(T * H * 2);
+  l.h2 = o;       o += up(T * H * 2);
+  l.act = o;      o += up(T * (size_t)c->ffn_dim * 2);
+  l.part = o;     o += up(part_bytes(c, b));
+  l.total = o;
+  return l;
+}
+
+// ------------------------------------------------------------ profiling --
+enum Stage {
+  ST_TOKMAP, ST_NORM1, ST_QKV, ST_ATTN_PREFILL, ST_ATTN_DECODE, ST_OPROJ, ST_NORM2, ST_GATEUP,
+  ST_DOWN, ST_ROUTER, ST_MOE, ST_APPEND, ST_COUNT
+};
+const char* const kStageName[ST_COUNT] = {"token_map", "rmsnorm_attn", "qkv_rope", "attn_prefill",
+                                          "attn_decode", "o_proj", "rmsnorm_mlp", "gate_up",
+                                          "down", "moe_router", "moe_ffn", "kv_append"};
+
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  struct Rec { int stage; hipEvent_t a, b; };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  int launches[ST_COUNT] = {};
+  double ms[ST_COUNT] = {};
+  hipEvent_t get() {
+    if (!pool.empty()) { hipEvent_t e = pool.back(); pool.pop_back(); return e; }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Profiler& prof() { static Profiler p; return p; }
+
+// Records an event pair around one stage when profiling is on.
+struct StageTimer {
+  int stage;
+  hipStream_t s;
+  hipEvent_t a = nullptr, b = nullptr;
+  StageTimer(int st, hipStream_t str) : stage(st), s(str) {
+    Profiler& p = prof();
+    if (!p.on) return;
+    std::lock_guard<std::mutex> g(p.mu);
+    a = p.get();
+    b = p.get();
+    if (a && b) hipEventRecord(a, s);
+  }
+  ~StageTimer() {
+    if (!a || !b) return;
+    Profiler& p = prof();
+    hipEventRecord(b, s);
+    std::lock_guard<std::mutex> g(p.mu);
+    p.pending.push_back({stage, a, b});
+  }
+};
+
+template <typename T>
+T* at(void* ws, size_t off) { return (T*)((char*)ws + off); }
+
+#define TRI_HIP(expr)                         \
+  do {                                        \
+    if ((expr) != hipSuccess) return TRI_ERR_HIP; \
+  } while (0)
+
+tri_status run_linear(const void* A, int lda, const void* B, int M, int N, int K, const Epi& epi,
+                      float* part, hipStream_t s) {
+  if (M <= kSkinnyMaxRows) TRI_HIP(launch_gemv(A, lda, B, K, M, N, K, epi, part, s));
+  else TRI_HIP(launch_gemm(A, lda, B, K, M, N, K, epi, s));
+  return TRI_OK;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weights* w,
+                 const tri_kv_cache* cache, const tri_batch* b, const void* x_in, void* x_out,
+                 int32_t* route_idx, float* route_w, void* ws, size_t ws_bytes, void* stream) {
+  (void)route_idx;
+  (void)route_w;
+  tri_status st = check_config(cfg);
+  if (st != TRI_OK) return st;
+  if (!w || !cache) return TRI_ERR_NULL;
+  if ((st = check_batch_scalars(b)) != TRI_OK) return st;
+  if (decode && (b->n_tokens != b->n_seqs || b->max_q_len > 1)) return TRI_ERR_SHAPE;
+  if (b->n_tokens == 0) return TRI_OK;
+  if (!x_in || !x_out || !ws || !b->cu_q || !b->ctx_len || !b->slot || !b->pos) return TRI_ERR_NULL;
+  if (!cache->k || !cache->v) return TRI_ERR_NULL;
+  if (!w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up || !w->w_down)
+    return TRI_ERR_NULL;
+  const bool bias = (cfg->flags & TRI_F_QKV_BIAS) != 0;
+  if (bias && !w->b_qkv) return TRI_ERR_NULL;
+  if (cache->n_slots <= 0 || cache->max_seq <= 0) return TRI_ERR_SHAPE;
+  if ((int64_t)b->max_ctx_len + b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
+  const void* ptrs[] = {x_in, x_out, ws, cache->k, cache->v, w->attn_norm, w->w_qkv, w->w_o,
+                        w->mlp_norm, w->w_gate_up, w->w_down};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return TRI_ERR_ALIGN;
+  if (bias && !aligned16(w->b_qkv)) return TRI_ERR_ALIGN;
+  if (((uintptr_t)ws & (kAlign - 1)) != 0) return TRI_ERR_ALIGN;
+  const Layout L = layout_of(cfg, b);
+  if (ws_bytes < L.total) return TRI_ERR_WORKSPACE;
+  const size_t act_bytes = (size_t)b->n_tokens * cfg->hidden * 2;
+  if (overlaps(x_in, act_bytes, x_out, act_bytes)) return TRI_ERR_ALIAS;
+  if (overlaps(ws, L.total, x_in, act_bytes) || overlaps(ws, L.total, x_out, act_bytes))
+    return TRI_ERR_ALIAS;
+
+  hipStream_t s = (hipStream_t)stream;
+  const int T = b->n_tokens, H = cfg->hidden, D = cfg->head_dim;
+  const int Hq = cfg->n_q_heads, Hkv = cfg->n_kv_heads, F = cfg->ffn_dim;
+  const int Nqkv = (Hq + 2 * Hkv) * D;
+  BatchDev bd{b->cu_q, b->ctx_len, b->slot, b->pos, b->n_seqs, b->n_tokens, b->max_q_len,
+              b->max_ctx_len};
+  int32_t* tok_slot = at<int32_t>(ws, L.tok_slot);
+  int32_t* tok_row = at<int32_t>(ws, L.tok_row);
+  float2* rope = at<float2>(ws, L.rope);
+  void* h = at<void>(ws, L.h);
+  void* q = at<void>(ws, L.q);
+  void* attn = at<void>(ws, L.attn);
+  void* x1 = at<void>(ws, L.x1);
+  void* h2 = at<void>(ws, L.h2);
+  void* act = at<void>(ws, L.act);
+  float* part = at<float>(ws, L.part);
+
+  { StageTimer st_(ST_TOKMAP, s);
+  TRI_HIP(launch_token_map(bd, cache->n_slots, cache->max_seq, D, cfg->rope_base, tok_slot,
+                           tok_row, rope, s)); }
+  { StageTimer st_(ST_NORM1, s);
+  TRI_HIP(launch_rmsnorm(x_in, w->attn_norm, h, nullptr, T, H, cfg->rms_eps, s)); }
+
+  Epi e{};
+  e.kind = EPI_QKV;
+  e.bias = bias ? w->b_qkv : nullptr;
+  e.q = q;
+  e.kc = cache->k;
+  e.vc = cache->v;
+  e.tok_slot = tok_slot;
+  e.tok_row = tok_row;
+  e.rope = rope;
+  e.n_q_heads = Hq;
+  e.n_kv_heads = Hkv;
+  e.head_dim = D;
+  e.max_seq = cache->max_seq;
+  { StageTimer st_(ST_QKV, s);
+  if ((st = run_linear(h, H, w->w_qkv, T, Nqkv, H, e, part, s)) != TRI_OK) return st; }
+
+  if (!decode && b->max_q_len > 1) {
+    StageTimer st_(ST_ATTN_PREFILL, s);
+    TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, cache->n_slots, cache->max_seq,
+                                Hq, Hkv, D, 0, s));
+  }
+  { StageTimer st_(ST_ATTN_DECODE, s);
+  TRI_HIP(launch_attn_decode(q, cache->k, cache->v, attn, part, bd, cache->n_slots,
+                             cache->max_seq, Hq, Hkv, D, s)); }
+
+  e = Epi{};
+  e.kind = EPI_RESID;
+  e.out = x1;
+  e.ldo = H;
+  e.resid = x_in;
+  e.ldr = H;
+  { StageTimer st_(ST_OPROJ, s);
+  if ((st = run_linear(attn, Hq * D, w->w_o, T, H, Hq * D, e, part, s)) != TRI_OK) return st; }
+
+  { StageTimer st_(ST_NORM2, s);
+  TRI_HIP(launch_rmsnorm(x1, w->mlp_norm, h2, nullptr, T, H, cfg->rms_eps, s)); }
+
+  e = Epi{};
+  e.kind = EPI_SWIGLU;
+  e.out = act;
+  e.ldo = F;
+  e.ffn = F;
+  { StageTimer st_(ST_GATEUP, s);
+  if ((st = run_linear(h2, H, w->w_gate_up, T, 2 * F, H, e, part, s)) != TRI_OK) return st; }
+
+  e = Epi{};
+  e.kind = EPI_RESID;
+  e.out = x_out;
+  e.ldo = H;
+  e.resid = x1;
+  e.ldr = H;
+  { StageTimer st_(ST_DOWN, s);
+  if ((st = run_linear(act, F, w->w_down, T, H, F, e, part, s)) != TRI_OK) return st; }
+  return TRI_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tri_status tri_workspace_size(const tri_layer_config* cfg, const tri_batch* batch, size_t* bytes) {
+  if (!bytes) return TRI_ERR_NULL;
+  tri_status st = check_config(cfg);
+  if (st != TRI_OK) return st;
+  if ((st = check_batch_scalars(batch)) != TRI_OK) return st;
+  *bytes = layout_of(cfg, batch).total;
+  return TRI_OK;
+}
+
+tri_status tri_workspace_layout(const tri_layer_config* cfg, const tri_batch* batch,
+                                tri_workspace_map* map) {
+  if (!map) return TRI_ERR_NULL;
+  tri_status st = check_config(cfg);
+  if (st != TRI_OK) return st;
+  if ((st = check_batch_scalars(batch)) != TRI_OK) return st;
+  const Layout l = layout_of(cfg, batch);
+  map->h = l.h;
+  map->q = l.q;
+  map->attn = l.attn;
+  map->x1 = l.x1;
+  map->h2 = l.h2;
+  map->act = l.act;
+  map->total = l.total;
+  return TRI_OK;
+}
+
+tri_status tri_layer_prefill(const tri_layer_config* cfg, const tri_layer_weights* w,
+                             const tri_kv_cache* cache, const tri_batch* batch, const void* x_in,
+                             void* x_out, int32_t* route_idx, float* route_w, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  return layer(false, cfg, w, cache, batch, x_in, x_out, route_idx, route_w, workspace,
+               workspace_bytes, stream);
+}
+
+tri_status tri_layer_decode(const tri_layer_config* cfg, const tri_layer_weights* w,
+                            const tri_kv_cache* cache, const tri_batch* batch, const void* x_in,
+                            void* x_out, int32_t* route_idx, float* route_w, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  return layer(true, cfg, w, cache, batch, x_in, x_out, route_idx, route_w, workspace,
+               workspace_bytes, stream);
+}
+
+tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* cache,
+                              const tri_batch* b, const void* k_new, const void* v_new,
+                              void* stream) {
+  if (!cfg) return TRI_ERR_NULL;
+  if (cfg->head_dim != 64 && cfg->head_dim != 128) return TRI_ERR_UNSUPPORTED;
+  if (cfg->n_kv_heads <= 0) return TRI_ERR_SHAPE;
+  if (cfg->dtype != TRI_BF16) return TRI_ERR_UNSUPPORTED;
+  if (!cache) return TRI_ERR_NULL;
+  tri_status st = check_batch_scalars(b);
+  if (st != TRI_OK) return st;
+  if (b->n_tokens == 0) return TRI_OK;
+  if (!k_new || !v_new || !cache->k || !cache->v || !b->cu_q || !b->ctx_len || !b->slot)
+    return TRI_ERR_NULL;
+  if (cache->n_slots <= 0 || cache->max_seq <= 0) return TRI_ERR_SHAPE;
+  if ((int64_t)b->max_ctx_len + b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
+  const void* ptrs[] = {k_new, v_new, cache->k, cache->v};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return TRI_ERR_ALIGN;
+  BatchDev bd{b->cu_q, b->ctx_len, b->slot, b->pos, b->n_seqs, b->n_tokens, b->max_q_len,
+              b->max_ctx_len};
+  StageTimer st_(ST_APPEND, (hipStream_t)stream);
+  TRI_HIP(launch_kv_append_direct(bd, cache->n_slots, cache->max_seq, cfg->n_kv_heads,
+                                  cfg->head_dim, k_new, v_new, cache->k, cache->v,
+                                  (hipStream_t)stream));
+  return TRI_OK;
+}
+
+tri_status tri_moe_route(const tri_layer_config* cfg, const float* h2, const void* w_router,
+                         int32_t n_tokens, int32_t* idx, float* w, void* stream) {
+  (void)stream;
+  if (!cfg) return TRI_ERR_NULL;
+  if (n_tokens < 0) return TRI_ERR_SHAPE;
+  if (!(cfg->flags & TRI_F_MOE)) return TRI_ERR_SHAPE;
+  if (n_tokens > 0 && (!h2 || !w_router || !idx || !w)) return TRI_ERR_NULL;
+  return TRI_ERR_UNSUPPORTED;
+}
+
+tri_status tri_profile_enable(int32_t on) {
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  for (auto& r : p.pending) {
+    hipEventSynchronize(r.b);
+    p.pool.push_back(r.a);
+    p.pool.push_back(r.b);
+  }
+  p.pending.clear();
+  for (int i = 0; i < ST_COUNT; ++i) { p.launches[i] = 0; p.ms[i] = 0.0; }
+  p.on = on != 0;
+  return TRI_OK;
+}
+
+tri_status tri_profile_read(tri_profile* out) {
+  if (!out) return TRI_ERR_NULL;
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  for (auto& r : p.pending) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return TRI_ERR_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return TRI_ERR_HIP;
+    p.launches[r.stage] += 1;
+    p.ms[r.stage] += ms;
+    p.pool.push_back(r.a);
+    p.pool.push_back(r.b);
+  }
+  p.pending.clear();
+  out->n_stages = ST_COUNT;
+  for (int i = 0; i < TRI_MAX_STAGES; ++i) {
+    out->name[i] = i < ST_COUNT ? kStageName[i] : nullptr;
+    out->launches[i] = i < ST_COUNT ? p.launches[i] : 0;
+    out->total_ms[i] = i < ST_COUNT ? p.ms[i] : 0.0;
+  }
+  return TRI_OK;
+}
+
+const char* tri_status_string(tri_status s) {
+  switch (s) {
+    case TRI_OK: return "ok";
+    case TRI_ERR_NULL: return "a required pointer is NULL";
+    case TRI_ERR_SHAPE: return "inconsistent sizes";
+    case TRI_ERR_UNSUPPORTED: return "unsupported configuration";
+    case TRI_ERR_RANGE: return "size exceeds a buffer";
+    case TRI_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case TRI_ERR_WORKSPACE: return "workspace too small";
+    case TRI_ERR_HIP: return "HIP launch failed";
+    case TRI_ERR_ALIAS: return "output overlaps an input";
+  }
+  return "unknown status";
+}
+
+int32_t tri_version(void) { return 100; }
+
+}  // extern "C"

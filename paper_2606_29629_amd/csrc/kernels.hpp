@@ -1,0 +1,94 @@
+// Internal launchers of libtri (host side).  Every launcher enqueues on
+// `stream` and returns the hipError_t of its launch.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tri {
+
+struct BatchDev {
+  const int32_t* cu_q;
+  const int32_t* ctx_len;
+  const int32_t* slot;
+  const int32_t* pos;
+  int n_seqs, n_tokens, max_q_len, max_ctx_len;
+};
+
+// Epilogue applied to C = A B^T (fp32 accumulators) by the GEMM kernels.
+enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+
+struct Epi {
+  int kind;
+  void* out;          // STORE / RESID / SWIGLU: bf16 [M, ldo]
+  int ldo;
+  const void* resid;  // RESID: bf16 [M, ldr]
+  int ldr;
+  int ffn;            // SWIGLU: F; B rows [0,F) are gate, [F,2F) up; out has F cols
+  // QKV: columns are q heads, then k heads, then v heads (head_dim each)
+  const void* bias;   // nullable, [(Hq + 2 Hkv) D]
+  void* q;            // bf16 [M, Hq, D]
+  void* kc;           // cache K [n_slots, Hkv, max_seq, D]
+  void* vc;           // cache V
+  const int32_t* tok_slot;  // [M] cache slot of each token, -1 = skip the cache write
+  const int32_t* tok_row;   // [M] cache row of each token
+  const float2* rope;       // [M, D/2] (cos, sin)
+  int n_q_heads, n_kv_heads, head_dim, max_seq;
+};
+
+// Per-token map: slot and cache row of every token (-1 when out of range),
+// and the rotary table rope[t][i] = (cos, sin)(pos[t] * base^(-2i/D)), the
+// angle formed in double precision.
+hipError_t launch_token_map(const BatchDev& b, int n_slots, int max_seq, int head_dim,
+                            float rope_base, int32_t* tok_slot, int32_t* tok_row,
+                            float2* rope, hipStream_t s);
+
+// y = x / sqrt(mean(x^2) + eps) * g   (bf16 out, optional fp32 copy)
+hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int rows,
+                          int hidden, float eps, hipStream_t s);
+
+// cache[slot][h][row][:] = src[t][h][:] for every token with a valid map entry.
+hipError_t launch_kv_append(const void* k_new, const void* v_new, void* kc, void* vc,
+                            const int32_t* tok_slot, const int32_t* tok_row, int n_tokens,
+                            int n_kv_heads, int head_dim, int max_seq, hipStream_t s);
+
+// The same append for a batch given only by its device arrays (the sequence
+// of each token is found by binary search over cu_q).
+hipError_t launch_kv_append_direct(const BatchDev& b, int n_slots, int max_seq, int n_kv_heads,
+                                   int head_dim, const void* k_new, const void* v_new, void* kc,
+                                   void* vc, hipStream_t s);
+
+// Prefill GEMM (large M): C[M,N] = A[M,K] B[N,K]^T with the fused epilogue.
+hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
+                       const Epi& epi, hipStream_t s);
+
+// Decode GEMM (M <= 128): streams B once; fp32 split-K partials in `part`,
+// then the epilogue kernel reduces them and applies `epi`.
+int gemv_splits(int M, int N, int K);
+size_t gemv_partial_bytes(int M, int N, int K);
+hipError_t launch_gemv(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
+                       const Epi& epi, float* part, hipStream_t s);
+
+// Causal flash attention for sequences with q_len > 1 (or all when
+// include_single != 0).
+hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, void* out,
+                               const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
+                               int n_kv_heads, int head_dim, int include_single, hipStream_t s);
+
+// Split-KV attention for sequences with q_len == 1, plus the combine.
+int attn_decode_splits(int max_kv);
+size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv);
+hipError_t launch_attn_decode(const void* q, const void* kc, const void* vc, void* out,
+                              float* part, const BatchDev& b, int n_slots, int max_seq,
+                              int n_q_heads, int n_kv_heads, int head_dim, hipStream_t s);
+
+// MoE
+size_t moe_workspace_bytes(int n_tokens, int hidden, int n_experts, int top_k, int expert_ffn);
+hipError_t launch_moe_route(const float* h32, const void* w_router, int n_tokens, int hidden,
+                            int n_experts, int top_k, int renorm, int32_t* idx, float* w,
+                            hipStream_t s);
+hipError_t launch_moe_ffn(const void* h2, const void* x1, const int32_t* idx, const float* w,
+                          const void* w_gate_up, const void* w_down, void* out, int n_tokens,
+                          int hidden, int n_experts, int top_k, int expert_ffn, void* ws,
+                          hipStream_t s);
+
+}  // namespace tri

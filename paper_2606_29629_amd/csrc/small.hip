@@ -1,0 +1,171 @@
+// Bandwidth-bound helper kernels: token map + rotary table, RMSNorm, KV append.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace tri {
+
+// One thread per (token, rotary pair).  Sequence of token t: the s with
+// cu_q[s] <= t < cu_q[s+1] (binary search over the non-decreasing offsets).
+__global__ void token_map_kernel(BatchDev b, int n_slots, int max_seq, int half, double base,
+                                 int32_t* tok_slot, int32_t* tok_row, float2* rope) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= (int64_t)b.n_tokens * half) return;
+  const int t = (int)(gid / half);
+  const int i = (int)(gid - (int64_t)t * half);
+  if (i == 0) {
+    int lo = 0, hi = b.n_seqs;  // find largest s with cu_q[s] <= t
+    while (hi - lo > 1) {
+      int mid = (lo + hi) >> 1;
+      if (b.cu_q[mid] <= t) lo = mid; else hi = mid;
+    }
+    const int s = lo;
+    const int sl = b.slot[s];
+    const int row = b.ctx_len[s] + (t - b.cu_q[s]);
+    const bool ok = sl >= 0 && sl < n_slots && row >= 0 && row < max_seq && t < b.cu_q[s + 1];
+    tok_slot[t] = ok ? sl : -1;
+    tok_row[t] = ok ? row : -1;
+  }
+  const double inv_freq = pow(base, -2.0 * (double)i / (double)(2 * half));
+  const double ang = (double)b.pos[t] * inv_freq;
+  double sn, cs;
+  sincos(ang, &sn, &cs);
+  rope[gid] = make_float2((float)cs, (float)sn);
+}
+
+hipError_t launch_token_map(const BatchDev& b, int n_slots, int max_seq, int head_dim,
+                            float rope_base, int32_t* tok_slot, int32_t* tok_row, float2* rope,
+                            hipStream_t s) {
+  const int half = head_dim / 2;
+  const int64_t n = (int64_t)b.n_tokens * half;
+  if (n == 0) return hipSuccess;
+  token_map_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(b, n_slots, max_seq, half,
+                                                               (double)rope_base, tok_slot,
+                                                               tok_row, rope);
+  return hipGetLastError();
+}
+
+// RMSNorm: one wave per row, 8 bf16 per lane per pass, fp32 sum of squares.
+constexpr int kNormMaxChunks = 16;  // hidden <= 64 lanes * 8 * 16 = 8192
+
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const bf16* __restrict__ x,
+                                                      const bf16* __restrict__ g,
+                                                      bf16* __restrict__ y,
+                                                      float* __restrict__ y32, int rows,
+                                                      int hidden, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const bf16* xr = x + (int64_t)row * hidden;
+  const int nchunk = hidden / 8;
+  Pack8 v[kNormMaxChunks];
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < kNormMaxChunks; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nchunk) {
+      v[c].u = ldg16(xr + ch * 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float f = bf2f(v[c].e[e]);
+        ss += f * f;
+      }
+    }
+  }
+  ss = wave_sum(ss);
+  const float r = 1.0f / sqrtf(ss / (float)hidden + eps);
+#pragma unroll
+  for (int c = 0; c < kNormMaxChunks; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nchunk) {
+      Pack8 gg, o;
+      gg.u = ldg16(g + ch * 8);
+      float f[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        f[e] = bf2f(v[c].e[e]) * r * bf2f(gg.e[e]);
+        o.e[e] = f2bf(f[e]);
+      }
+      stg16(y + (int64_t)row * hidden + ch * 8, o.u);
+      if (y32) {
+        float* d = y32 + (int64_t)row * hidden + ch * 8;
+        *(f32x4*)d = f32x4{f[0], f[1], f[2], f[3]};
+        *(f32x4*)(d + 4) = f32x4{f[4], f[5], f[6], f[7]};
+      }
+    }
+  }
+}
+
+hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int rows, int hidden,
+                          float eps, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  rmsnorm_kernel<<<cdiv(rows, 4), 256, 0, s>>>((const bf16*)x, (const bf16*)g, (bf16*)y, y32,
+                                               rows, hidden, eps);
+  return hipGetLastError();
+}
+
+// One thread per 16-byte chunk of a new K/V row.
+__global__ void kv_append_kernel(const bf16* __restrict__ kn, const bf16* __restrict__ vn,
+                                 bf16* __restrict__ kc, bf16* __restrict__ vc,
+                                 const int32_t* __restrict__ tok_slot,
+                                 const int32_t* __restrict__ tok_row, int n_tokens, int hkv,
+                                 int d, int max_seq) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = d / 8;  // chunks per row
+  if (gid >= (int64_t)n_tokens * hkv * cpr) return;
+  const int t = (int)(gid / (hkv * cpr));
+  const int rem = (int)(gid - (int64_t)t * hkv * cpr);
+  const int h = rem / cpr, c = rem - h * cpr;
+  const int sl = tok_slot[t];
+  if (sl < 0) return;
+  const int64_t dst = (((int64_t)sl * hkv + h) * max_seq + tok_row[t]) * d + c * 8;
+  const int64_t src = ((int64_t)t * hkv + h) * d + c * 8;
+  stg16(kc + dst, ldg16(kn + src));
+  stg16(vc + dst, ldg16(vn + src));
+}
+
+hipError_t launch_kv_append(const void* k_new, const void* v_new, void* kc, void* vc,
+                            const int32_t* tok_slot, const int32_t* tok_row, int n_tokens,
+                            int n_kv_heads, int head_dim, int max_seq, hipStream_t s) {
+  const int64_t n = (int64_t)n_tokens * n_kv_heads * (head_dim / 8);
+  if (n == 0) return hipSuccess;
+  kv_append_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(
+      (const bf16*)k_new, (const bf16*)v_new, (bf16*)kc, (bf16*)vc, tok_slot, tok_row, n_tokens,
+      n_kv_heads, head_dim, max_seq);
+  return hipGetLastError();
+}
+
+__global__ void kv_append_direct_kernel(BatchDev b, int n_slots, int max_seq, int hkv, int d,
+                                        const bf16* __restrict__ kn, const bf16* __restrict__ vn,
+                                        bf16* __restrict__ kc, bf16* __restrict__ vc) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cpr = d / 8;
+  if (gid >= (int64_t)b.n_tokens * hkv * cpr) return;
+  const int t = (int)(gid / (hkv * cpr));
+  const int rem = (int)(gid - (int64_t)t * hkv * cpr);
+  const int h = rem / cpr, c = rem - h * cpr;
+  int lo = 0, hi = b.n_seqs;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (b.cu_q[mid] <= t) lo = mid; else hi = mid;
+  }
+  const int sl = b.slot[lo];
+  const int row = b.ctx_len[lo] + (t - b.cu_q[lo]);
+  if (sl < 0 || sl >= n_slots || row < 0 || row >= max_seq || t >= b.cu_q[lo + 1]) return;
+  const int64_t dst = (((int64_t)sl * hkv + h) * max_seq + row) * d + c * 8;
+  const int64_t src = ((int64_t)t * hkv + h) * d + c * 8;
+  stg16(kc + dst, ldg16(kn + src));
+  stg16(vc + dst, ldg16(vn + src));
+}
+
+hipError_t launch_kv_append_direct(const BatchDev& b, int n_slots, int max_seq, int n_kv_heads,
+                                   int head_dim, const void* k_new, const void* v_new, void* kc,
+                                   void* vc, hipStream_t s) {
+  const int64_t n = (int64_t)b.n_tokens * n_kv_heads * (head_dim / 8);
+  if (n == 0 || b.n_seqs == 0) return hipSuccess;
+  kv_append_direct_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(
+      b, n_slots, max_seq, n_kv_heads, head_dim, (const bf16*)k_new, (const bf16*)v_new,
+      (bf16*)kc, (bf16*)vc);
+  return hipGetLastError();
+}
+
+}  // namespace tri

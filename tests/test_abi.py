@@ -1,0 +1,204 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+declared in include/tri.h, its structs match the ctypes mirrors, and host-side
+validation rejects bad arguments before any launch.
+
+Every call below fails validation, so no kernel is ever launched (the fake
+device addresses are never dereferenced).
+"""
+import ctypes
+import os
+import re
+import subprocess
+import tempfile
+
+import pytest
+
+from paper_2606_29629_amd import _lib as T
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tri.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("fake-address validation tests run only where no GPU is visible")
+    if not os.path.exists(T.LIB_PATH):
+        pytest.skip("libtri.so not built (run python -m paper_2606_29629_amd.build)")
+    return T.lib()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tri_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_function(lib):
+    names = declared_functions()
+    assert "tri_layer_prefill" in names and "tri_kvcache_append" in names
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    exported = set(re.findall(r" T (tri_\w+)", out))
+    assert set(names) <= exported
+    assert lib.tri_version() >= 100
+
+
+STRUCTS = {
+    "tri_layer_config": (T.LayerConfig, [f for f, _ in T.LayerConfig._fields_]),
+    "tri_layer_weights": (T.LayerWeights, [f for f, _ in T.LayerWeights._fields_]),
+    "tri_kv_cache": (T.KVCache, [f for f, _ in T.KVCache._fields_]),
+    "tri_batch": (T.BatchStruct, [f for f, _ in T.BatchStruct._fields_]),
+    "tri_workspace_map": (T.WorkspaceMap, [f for f, _ in T.WorkspaceMap._fields_]),
+}
+
+
+def test_struct_layout_matches_header():
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "tri.h"', "int main(void){"]
+    for cname, (_, fields) in STRUCTS.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f in fields:
+            lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines.append("return 0;}")
+    with tempfile.TemporaryDirectory() as d:
+        c = os.path.join(d, "probe.c")
+        open(c, "w").write("\n".join(lines))
+        exe = os.path.join(d, "probe")
+        subprocess.run(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), c, "-o", exe], check=True)
+        out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout
+    got = {}
+    for line in out.splitlines():
+        a, b, v = line.split()
+        got[(a, b)] = int(v)
+    for cname, (cls, fields) in STRUCTS.items():
+        assert got[(cname, "size")] == ctypes.sizeof(cls), cname
+        for f in fields:
+            assert got[(cname, f)] == getattr(cls, f).offset, (cname, f)
+
+
+# ------------------------------------------------------------ validation --
+
+FAKE = 0x7F0000000000  # 256-byte aligned fake device address, never dereferenced
+
+
+def cfg(**kw):
+    base = dict(hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=64, ffn_dim=1024,
+                n_experts=0, top_k=0, expert_ffn_dim=0, rms_eps=1e-6, rope_base=1e6,
+                dtype=T.TRI_BF16, flags=0)
+    base.update(kw)
+    return T.LayerConfig(**base)
+
+
+def batch(n_seqs=1, n_tokens=4, max_q=4, max_ctx=0, ptr=FAKE):
+    return T.BatchStruct(n_seqs, n_tokens, max_q, max_ctx, ptr, ptr + 256, ptr + 512, ptr + 768)
+
+
+def weights(ptr=FAKE):
+    w = T.LayerWeights(*[ptr + 4096 * i for i in range(8)])
+    w.b_qkv = None
+    w.w_router = None
+    return w
+
+
+def call(lib, fn="tri_layer_prefill", c=None, w=None, kv=None, b=None, x=FAKE + (1 << 20),
+         out=FAKE + (2 << 20), ws=FAKE + (3 << 20), ws_bytes=1 << 30):
+    c = cfg() if c is None else c
+    w = weights() if w is None else w
+    kv = T.KVCache(FAKE + (4 << 20), FAKE + (5 << 20), 1, 64) if kv is None else kv
+    b = batch() if b is None else b
+    return getattr(lib, fn)(ctypes.byref(c), ctypes.byref(w), ctypes.byref(kv), ctypes.byref(b),
+                            x, out, None, None, ws, ws_bytes, None)
+
+
+def test_null_and_unsupported(lib):
+    assert lib.tri_layer_prefill(None, None, None, None, None, None, None, None, None, 0,
+                                 None) == T.TRI_ERR_NULL
+    assert call(lib, c=cfg(head_dim=96)) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, c=cfg(dtype=T.TRI_F32)) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, c=cfg(flags=64)) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, c=cfg(hidden=200)) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, c=cfg(ffn_dim=100)) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, c=cfg(n_q_heads=5)) == T.TRI_ERR_SHAPE
+    assert call(lib, c=cfg(n_q_heads=32, n_kv_heads=2)) == T.TRI_ERR_UNSUPPORTED  # group > 8
+    assert call(lib, c=cfg(rope_base=0.0)) == T.TRI_ERR_RANGE
+    assert call(lib, w=T.LayerWeights()) == T.TRI_ERR_NULL
+    assert call(lib, x=None) == T.TRI_ERR_NULL
+    assert call(lib, c=cfg(flags=T.TRI_F_QKV_BIAS)) == T.TRI_ERR_NULL    # bias flag, no bias
+    bb = batch()
+    bb.cu_q = None
+    assert call(lib, b=bb) == T.TRI_ERR_NULL
+
+
+def test_moe_config_checks(lib):
+    moe = dict(flags=T.TRI_F_MOE, n_experts=8, top_k=2, expert_ffn_dim=128, ffn_dim=0)
+    assert call(lib, c=cfg(**dict(moe, top_k=9))) == T.TRI_ERR_SHAPE
+    assert call(lib, c=cfg(**dict(moe, top_k=0))) == T.TRI_ERR_SHAPE
+    assert call(lib, c=cfg(**dict(moe, n_experts=300))) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, c=cfg(**dict(moe, expert_ffn_dim=100))) == T.TRI_ERR_UNSUPPORTED
+
+
+def test_batch_checks(lib):
+    assert call(lib, b=batch(n_seqs=0, n_tokens=4)) == T.TRI_ERR_SHAPE
+    assert call(lib, b=batch(n_seqs=1, n_tokens=4, max_q=2)) == T.TRI_ERR_SHAPE
+    assert call(lib, b=batch(n_seqs=-1)) == T.TRI_ERR_SHAPE
+    assert call(lib, b=batch(max_ctx=61)) == T.TRI_ERR_RANGE               # 61 + 4 > 64
+    assert call(lib, kv=T.KVCache(FAKE, FAKE + 256, 0, 64)) == T.TRI_ERR_SHAPE
+    # decode needs one token per sequence
+    assert call(lib, fn="tri_layer_decode", b=batch(n_seqs=2, n_tokens=4, max_q=2)) == T.TRI_ERR_SHAPE
+
+
+def test_alignment_workspace_alias(lib):
+    assert call(lib, x=FAKE + (1 << 20) + 8) == T.TRI_ERR_ALIGN
+    assert call(lib, ws=FAKE + (3 << 20) + 16) == T.TRI_ERR_ALIGN   # workspace needs 256 B
+    w = weights()
+    w.w_o = FAKE + 2
+    assert call(lib, w=w) == T.TRI_ERR_ALIGN
+    assert call(lib, ws_bytes=1024) == T.TRI_ERR_WORKSPACE
+    assert call(lib, out=FAKE + (1 << 20) + 256) == T.TRI_ERR_ALIAS          # overlaps x_in
+    assert call(lib, ws=FAKE + (1 << 20)) == T.TRI_ERR_ALIAS
+
+
+def test_empty_batch_is_a_noop(lib):
+    # n_tokens == 0: nothing to do, nothing launched, null data pointers allowed
+    assert call(lib, b=batch(n_seqs=0, n_tokens=0, max_q=0), x=None, out=None, ws=None) == T.TRI_OK
+
+
+def test_workspace_size_and_layout(lib):
+    c = cfg()
+    sizes = []
+    for n in (1, 32, 200, 4096):
+        b = batch(n_seqs=1, n_tokens=n, max_q=n, max_ctx=0)
+        s = ctypes.c_size_t()
+        assert lib.tri_workspace_size(ctypes.byref(c), ctypes.byref(b), ctypes.byref(s)) == 0
+        m = T.WorkspaceMap()
+        assert lib.tri_workspace_layout(ctypes.byref(c), ctypes.byref(b), ctypes.byref(m)) == 0
+        assert m.total == s.value
+        offs = [m.h, m.q, m.attn, m.x1, m.h2, m.act]
+        assert offs == sorted(offs) and all(o % 256 == 0 for o in offs)
+        assert m.act + n * 1024 * 2 <= m.total
+        sizes.append(s.value)
+    assert sizes == sorted(sizes)
+    assert lib.tri_workspace_size(ctypes.byref(c), None, None) == T.TRI_ERR_NULL
+
+
+def test_kvcache_append_and_route_validation(lib):
+    c = cfg()
+    kv = T.KVCache(FAKE, FAKE + 4096, 1, 64)
+    b = batch(max_ctx=62)
+    assert lib.tri_kvcache_append(ctypes.byref(c), ctypes.byref(kv), ctypes.byref(b), FAKE,
+                                  FAKE, None) == T.TRI_ERR_RANGE
+    b = batch()
+    assert lib.tri_kvcache_append(ctypes.byref(c), ctypes.byref(kv), ctypes.byref(b), FAKE + 8,
+                                  FAKE, None) == T.TRI_ERR_ALIGN
+    assert lib.tri_kvcache_append(ctypes.byref(c), ctypes.byref(kv), ctypes.byref(b), None,
+                                  FAKE, None) == T.TRI_ERR_NULL
+    assert lib.tri_moe_route(ctypes.byref(c), FAKE, FAKE, 4, FAKE, FAKE, None) == T.TRI_ERR_SHAPE
+
+
+def test_status_strings(lib):
+    for s in range(-8, 1):
+        assert T.status_string(s) and T.status_string(s) != "unknown status"
+    assert T.status_string(-99) == "unknown status"

@@ -1,0 +1,298 @@
+"""GPU parity of the HIP decoder layer against the CPU oracle, through the C ABI.
+
+Bar (bf16 storage, fp32 accumulation): elementwise |gpu - oracle| <=
+max(2e-2, 1e-2 |oracle|); integer/index results bit-exact.  The oracle runs in
+float64 on the same seeded bf16 inputs.  Sizes span several GEMM / attention
+tiles with ragged tails; the full-size workloads are checked on sampled rows
+in the launch configuration the bench times.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_29629_amd import _lib as T
+from paper_2606_29629_amd.workload import (DeviceLayer, device_batch, device_cache,
+                                           to_device_bf16, to_host_f64)
+from synth import (Batch, LayerConfig, bf16_to_f32, layer_7b, layer_c1, make_cache,
+                   make_weights, make_x, workload)
+
+pytestmark = pytest.mark.gpu
+
+ATOL, RTOL = 2e-2, 1e-2
+
+
+def assert_close(got, ref, what, atol=ATOL, rtol=RTOL):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    err = np.abs(got - ref)
+    bound = np.maximum(atol, rtol * np.abs(ref))
+    bad = err > bound
+    if bad.any():
+        i = np.unravel_index(np.argmax(err / bound), err.shape)
+        raise AssertionError(f"{what}: {int(bad.sum())}/{bad.size} out of tolerance; worst at {i}: "
+                             f"gpu {got[i]:.6g} oracle {ref[i]:.6g} (max abs err {err.max():.3g})")
+
+
+def f64(bits):
+    return bf16_to_f32(bits).astype(np.float64)
+
+
+class Case:
+    """Seeded inputs of one layer call, resident on host (bits) and device."""
+
+    def __init__(self, cfg, batch, n_slots, max_seq, seed=0, x_step=None):
+        import torch
+        self.cfg, self.batch = cfg, batch
+        self.wb = make_weights(cfg, seed)
+        self.kb, self.vb = make_cache(cfg, n_slots, max_seq, seed)
+        self.xb = make_x(cfg, batch.n_tokens, seed, step=x_step)
+        self.dl = DeviceLayer(cfg, self.wb)
+        self.cache = device_cache(self.kb, self.vb)
+        self.x = to_device_bf16(self.xb)
+        self.db = device_batch(batch)
+        torch.cuda.synchronize()
+
+    def run(self, decode=False, x=None):
+        import torch
+        fn = T.layer_decode if decode else T.layer_prefill
+        out, ws = fn(self.dl.cfg, self.dl.w, self.cache, self.db, self.x if x is None else x)
+        torch.cuda.synchronize()
+        return out, ws
+
+    def oracle(self, rows=None, x_bits=None):
+        w = {k: f64(v) for k, v in self.wb.items()}
+        return oracle.layer_forward(self.cfg, w, f64(self.kb), f64(self.vb), self.batch,
+                                    f64(self.xb if x_bits is None else x_bits), rows=rows)
+
+    def cache_rows(self):
+        """GPU cache rows written by this call, as [T, Hkv, D] (K and V)."""
+        k, v = self.cache
+        ks, vs = [], []
+        for s, c, q in zip(self.batch.slot, self.batch.ctx_len, self.batch.q_len):
+            ks.append(to_host_f64(k[s, :, c:c + q]).transpose(1, 0, 2))
+            vs.append(to_host_f64(v[s, :, c:c + q]).transpose(1, 0, 2))
+        return np.concatenate(ks), np.concatenate(vs)
+
+
+def B(slot, ctx, q):
+    return Batch(np.asarray(slot, np.int32), np.asarray(ctx, np.int32), np.asarray(q, np.int32))
+
+
+def ws_view(ws, off, shape):
+    import torch
+    n = int(np.prod(shape))
+    return ws[off:off + 2 * n].view(torch.bfloat16).view(*shape)
+
+
+# ------------------------------------------------------------- tiny layer --
+
+def test_tiny_prefill_then_16_decode_steps():
+    wl = workload("tiny")
+    cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
+    out, _ = cs.run()
+    ref = cs.oracle()
+    assert_close(to_host_f64(out), ref["out"], "tiny prefill out")
+    kr, vr = cs.cache_rows()
+    assert_close(kr, ref["k_new"], "tiny prefill K rows")
+    assert_close(vr, ref["v_new"], "tiny prefill V rows")
+    # decode: fresh N(0,1) input each step, oracle fed the GPU-written cache
+    batch = wl.batch
+    for step in range(wl.decode_steps):
+        batch = batch.advanced()
+        cs.batch, cs.db = batch, device_batch(batch)
+        xb = make_x(wl.cfg, batch.n_tokens, wl.seed, step=step)
+        k, v = cs.cache
+        ref = oracle.layer_forward(wl.cfg, {kk: f64(vv) for kk, vv in cs.wb.items()},
+                                   to_host_f64(k), to_host_f64(v), batch, f64(xb))
+        out, _ = cs.run(decode=True, x=to_device_bf16(xb))
+        assert_close(to_host_f64(out), ref["out"], f"tiny decode step {step}")
+        kr, vr = cs.cache_rows()
+        assert_close(kr, ref["k_new"], f"tiny decode K row {step}")
+        assert_close(vr, ref["v_new"], f"tiny decode V row {step}")
+
+
+def test_tiny_intermediates():
+    cfg = layer_c1()
+    batch = B([0, 1], [0, 5], [37, 20])
+    cs = Case(cfg, batch, 2, 64)
+    out, ws = cs.run()
+    ref = cs.oracle()
+    m = T.workspace_layout(cs.dl.cfg, cs.db)
+    Tn, H, D, Hq = batch.n_tokens, cfg.hidden, cfg.head_dim, cfg.n_q_heads
+    assert_close(to_host_f64(ws_view(ws, m.h, (Tn, H))), ref["h"], "h")
+    assert_close(to_host_f64(ws_view(ws, m.q, (Tn, Hq, D))), ref["q"], "q")
+    assert_close(to_host_f64(ws_view(ws, m.attn, (Tn, Hq * D))), ref["attn"], "attn")
+    assert_close(to_host_f64(ws_view(ws, m.x1, (Tn, H))), ref["x1"], "x1")
+    assert_close(to_host_f64(ws_view(ws, m.h2, (Tn, H))), ref["h2"], "h2")
+    assert_close(to_host_f64(out), ref["out"], "out")
+
+
+@pytest.mark.parametrize("bias", [False, True])
+def test_tiny_ragged_mixed_batch(bias):
+    import dataclasses
+    cfg = dataclasses.replace(layer_c1(), qkv_bias=bias)
+    # a long prefill over two flash tiles, a chunk with cached prefix, decodes
+    batch = B([3, 0, 2, 1, 4], [0, 40, 7, 0, 150], [200, 9, 1, 1, 1])
+    cs = Case(cfg, batch, 5, 256, seed=3)
+    out, _ = cs.run()
+    ref = cs.oracle()
+    assert_close(to_host_f64(out), ref["out"], "ragged out")
+    kr, vr = cs.cache_rows()
+    assert_close(kr, ref["k_new"], "ragged K")
+    assert_close(vr, ref["v_new"], "ragged V")
+
+
+# --------------------------------------------------------- 7B layer shapes --
+
+def test_7b_ragged_prefill_sampled_rows():
+    cfg = layer_7b()
+    # M = 494 (> the skinny threshold): big GEMM tiles with a ragged M tail,
+    # flash tiles with ragged tails, a cached-prefix chunk and a decode sequence
+    batch = B([0, 1, 2, 3], [0, 37, 500, 0], [300, 129, 1, 64])
+    cs = Case(cfg, batch, 4, 640, seed=1)
+    out, _ = cs.run()
+    rows = np.array([0, 1, 127, 128, 255, 256, 299, 300, 301, 365, 428, 429, 430, 460, 493])
+    ref = cs.oracle(rows=rows)
+    assert_close(to_host_f64(out)[rows], ref["out"], "7B ragged prefill rows")
+    kr, vr = cs.cache_rows()
+    assert_close(kr, ref["k_new"], "7B K rows")
+    assert_close(vr, ref["v_new"], "7B V rows")
+
+
+def test_7b_decode_step_all_rows():
+    cfg = layer_7b()
+    ctx = [1, 63, 64, 127, 128, 129, 1000, 4095]
+    batch = B(list(range(8)), ctx, [1] * 8)
+    cs = Case(cfg, batch, 8, 4100, seed=2)
+    out, _ = cs.run(decode=True)
+    ref = cs.oracle()
+    assert_close(to_host_f64(out), ref["out"], "7B decode out")
+    kr, vr = cs.cache_rows()
+    assert_close(kr, ref["k_new"], "7B decode K")
+    assert_close(vr, ref["v_new"], "7B decode V")
+
+
+def test_full_size_dense_prefill_sampled():
+    """8 x 2048 tokens (the bench's prefill launch), rows sampled from one sequence."""
+    wl = workload("dense_prefill")
+    cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
+    out, _ = cs.run()
+    s = 5
+    sub = B([s], [0], [2048])
+    local = np.array([0, 1, 255, 256, 1023, 1024, 2046, 2047])
+    w = {k: f64(v) for k, v in cs.wb.items()}
+    ref = oracle.layer_forward(wl.cfg, w, f64(cs.kb), f64(cs.vb), sub,
+                               f64(cs.xb[s * 2048:(s + 1) * 2048]), rows=local)
+    assert_close(to_host_f64(out)[s * 2048 + local], ref["out"], "full prefill sampled rows")
+
+
+def test_full_size_dense_decode_sampled():
+    """64 sequences at KV 4096 (the decode launch), 6 sequences checked."""
+    wl = workload("dense_decode")
+    cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
+    out, _ = cs.run(decode=True)
+    pick = np.array([0, 1, 17, 31, 62, 63])
+    # the oracle sees only the picked slots' caches, renumbered 0..5
+    sub = B(np.arange(len(pick)), wl.batch.ctx_len[pick], wl.batch.q_len[pick])
+    w = {k: f64(v) for k, v in cs.wb.items()}
+    ref = oracle.layer_forward(wl.cfg, w, f64(cs.kb[wl.batch.slot[pick]]),
+                               f64(cs.vb[wl.batch.slot[pick]]), sub, f64(cs.xb[pick]))
+    assert_close(to_host_f64(out)[pick], ref["out"], "full decode sampled rows")
+
+
+# ------------------------------------------------------------- invariants --
+
+def test_zero_projections_give_exact_identity():
+    import torch
+    cfg = layer_c1()
+    batch = B([0, 1], [0, 3], [50, 1])
+    cs = Case(cfg, batch, 2, 64)
+    cs.dl.w["w_o"].zero_()
+    cs.dl.w["w_down"].zero_()
+    out, _ = cs.run()
+    assert torch.equal(out, cs.x)
+
+
+def test_first_query_returns_its_value_exactly():
+    cfg = layer_7b()
+    batch = B([0, 1], [0, 0], [130, 1])   # a flash-path prefill and a decode-path single token
+    cs = Case(cfg, batch, 2, 256)
+    out, ws = cs.run()
+    m = T.workspace_layout(cs.dl.cfg, cs.db)
+    attn = ws_view(ws, m.attn, (131, cfg.n_q_heads, cfg.head_dim))
+    v = cs.cache[1]
+    g = cfg.n_q_heads // cfg.n_kv_heads
+    import torch
+    for t, sl in ((0, 0), (130, 1)):
+        for j in range(cfg.n_q_heads):
+            assert torch.equal(attn[t, j], v[sl, j // g, 0]), (t, j)
+
+
+def test_causal_invariance_bit_exact():
+    import torch
+    cfg = layer_c1()
+    batch = B([0], [0], [150])
+    cs = Case(cfg, batch, 1, 256)
+    out0, _ = cs.run()
+    out0 = out0.clone()
+    x2 = cs.x.clone()
+    x2[100:] = torch.randn_like(x2[100:].float()).to(torch.bfloat16) * 3
+    out1, _ = cs.run(x=x2)
+    assert torch.equal(out0[:100], out1[:100])
+    assert not torch.equal(out0[100:], out1[100:])
+
+
+def test_run_twice_bit_identical():
+    import torch
+    cfg = layer_7b()
+    batch = B([0, 1, 2], [0, 100, 2000], [200, 1, 1])
+    cs = Case(cfg, batch, 3, 2304)
+    a, _ = cs.run()
+    a = a.clone()
+    b, _ = cs.run()
+    assert torch.equal(a, b)
+
+
+def test_decode_equals_recompute():
+    cfg = layer_c1()
+    n = 70
+    full = Case(cfg, B([0], [0], [n + 1]), 1, 128, seed=5)
+    ref_out, _ = full.run()
+    ref_row = to_host_f64(ref_out)[n]
+    # prefill n tokens, then decode token n from the cache the prefill wrote
+    part = Case(cfg, B([0], [0], [n]), 1, 128, seed=5)
+    part.x = full.x[:n].contiguous()
+    part.run()
+    part.batch = B([0], [n], [1])
+    part.db = device_batch(part.batch)
+    out, _ = part.run(decode=True, x=full.x[n:n + 1].contiguous())
+    assert_close(to_host_f64(out)[0], ref_row, "decode vs recompute")
+
+
+def test_kvcache_append_and_canaries():
+    import torch
+    cfg = layer_c1()
+    batch = B([2, 0], [5, 0], [3, 4])
+    k = torch.full((3, cfg.n_kv_heads, 16, cfg.head_dim), 7.0, dtype=torch.bfloat16, device="cuda")
+    v = k.clone()
+    kn = torch.randn(7, cfg.n_kv_heads, cfg.head_dim, device="cuda").to(torch.bfloat16)
+    vn = torch.randn_like(kn.float()).to(torch.bfloat16)
+    T.kvcache_append(T.make_config(cfg), (k, v), device_batch(batch), kn, vn)
+    torch.cuda.synchronize()
+    ck, cv = oracle.kvcache_append(to_host_f64(k) * 0 + 7, to_host_f64(v) * 0 + 7, batch,
+                                   to_host_f64(kn), to_host_f64(vn))
+    assert np.array_equal(to_host_f64(k), ck)
+    assert np.array_equal(to_host_f64(v), cv)
+
+
+def test_output_buffer_canary():
+    import torch
+    cfg = layer_c1()
+    batch = B([0], [0], [33])
+    cs = Case(cfg, batch, 1, 64)
+    big = torch.full((40, cfg.hidden), -3.0, dtype=torch.bfloat16, device="cuda")
+    T.layer_prefill(cs.dl.cfg, cs.dl.w, cs.cache, cs.db, cs.x, out=big[:33])
+    torch.cuda.synchronize()
+    assert torch.all(big[33:] == -3.0)
