@@ -115,12 +115,14 @@ typedef struct {
  * arrays are device int32.  Sequence s owns new tokens cu_q[s] .. cu_q[s+1]-1
  * of x; its new token i is written to cache row ctx_len[s] + i of slot
  * slot[s] and attends to rows 0 .. ctx_len[s] + i.  pos[t] is the rotary
- * position of token t (normally ctx_len + i).                                  */
+ * position of token t (normally ctx_len + i).  The caller guarantees
+ * ctx_len[s] + q_len[s] <= max_seq for every sequence; a sequence violating it
+ * is skipped on the device (no access outside the cache).                     */
 typedef struct {
   int32_t n_seqs;      /* >= 0                                                     */
   int32_t n_tokens;    /* T = cu_q[n_seqs]                                         */
   int32_t max_q_len;   /* >= max_s (cu_q[s+1] - cu_q[s])                           */
-  int32_t max_ctx_len; /* >= max_s ctx_len[s]; max_ctx_len + max_q_len <= max_seq  */
+  int32_t max_ctx_len; /* >= max_s ctx_len[s]; < max_seq (TRI_ERR_RANGE otherwise) */
   const int32_t* cu_q;    /* [n_seqs + 1], cu_q[0] = 0, non-decreasing             */
   const int32_t* ctx_len; /* [n_seqs]                                              */
   const int32_t* slot;    /* [n_seqs], distinct                                    */

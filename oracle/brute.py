@@ -24,9 +24,13 @@ def _matvec(wmat, vec):
 
 def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
                 ctx_lens: List[int], q_lens: List[int], x: List[List[float]],
-                forced_routes: Optional[List[List[int]]] = None):
+                forced_routes: Optional[List[List[int]]] = None, store=None):
     """Arguments are nested Python lists of floats (cache_k[slot][h][row][d]).
+    ``store`` (scalar -> scalar), if given, is applied to every activation value
+    at the storage points: h, q, k, v, attention output, x1, h2, the SwiGLU
+    activation and the output.
     Returns (out rows, k_new, v_new, route_idx, route_w)."""
+    S = (lambda v: v) if store is None else store
     H, Hq, Hkv, D = cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     eps = cfg.rms_eps
     T = len(x)
@@ -53,13 +57,13 @@ def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
     for s in range(len(slots)):
         for i in range(q_lens[s]):
             p = ctx_lens[s] + i
-            h = norm(x[t], w["attn_norm"])
+            h = [S(v) for v in norm(x[t], w["attn_norm"])]
             qkv = _matvec(w["w_qkv"], h)
             if w.get("b_qkv") is not None:
                 qkv = [qkv[j] + w["b_qkv"][j] for j in range(len(qkv))]
-            qh = [rotate(qkv[j * D:(j + 1) * D], p) for j in range(Hq)]
-            kh = [rotate(qkv[(Hq + j) * D:(Hq + j + 1) * D], p) for j in range(Hkv)]
-            vh = [qkv[(Hq + Hkv + j) * D:(Hq + Hkv + j + 1) * D] for j in range(Hkv)]
+            qh = [[S(v) for v in rotate(qkv[j * D:(j + 1) * D], p)] for j in range(Hq)]
+            kh = [[S(v) for v in rotate(qkv[(Hq + j) * D:(Hq + j + 1) * D], p)] for j in range(Hkv)]
+            vh = [[S(v) for v in qkv[(Hq + Hkv + j) * D:(Hq + Hkv + j + 1) * D]] for j in range(Hkv)]
             toks.append((s, p, qh, kh, vh))
             k_rows.append(kh)
             v_rows.append(vh)
@@ -85,15 +89,15 @@ def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
             mx = max(sc)
             e = [math.exp(z - mx) for z in sc]
             den = sum(e)
-            o.extend(sum(e[m] / den * vals[m][g][d] for m in range(p + 1)) for d in range(D))
-        x1 = [x[t][i] + v for i, v in enumerate(_matvec(w["w_o"], o))]
-        h2 = norm(x1, w["mlp_norm"])
+            o.extend(S(sum(e[m] / den * vals[m][g][d] for m in range(p + 1))) for d in range(D))
+        x1 = [S(x[t][i] + v) for i, v in enumerate(_matvec(w["w_o"], o))]
+        h2 = [S(v) for v in norm(x1, w["mlp_norm"])]
 
         def expert_ffn(wgu, wd):
             f = len(wgu) // 2
             gate = _matvec(wgu[:f], h2)
             up = _matvec(wgu[f:], h2)
-            a = [gate[i] / (1.0 + math.exp(-gate[i])) * up[i] for i in range(f)]
+            a = [S(gate[i] / (1.0 + math.exp(-gate[i])) * up[i]) for i in range(f)]
             return _matvec(wd, a)
 
         if cfg.n_experts > 0:
@@ -127,5 +131,5 @@ def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
             rw.append(ws)
         else:
             y = expert_ffn(w["w_gate_up"], w["w_down"])
-        out.append([x1[i] + y[i] for i in range(H)])
+        out.append([S(x1[i] + y[i]) for i in range(H)])
     return out, k_rows, v_rows, ridx, rw

@@ -28,12 +28,28 @@ fix is a declared reading:
 This is the plain definition: full softmax attention (flash or split-KV
 attention are exact re-orderings of it), no blocking, no fusion.  Arithmetic is
 float64 by default; ``dtype=np.float32`` gives the plain fp32 layer.
+
+Storage precision (a declared reading; the paper states none).  With
+``storage="bf16"`` the layer's activations are held in bfloat16 between
+operations, as a bf16 deployment of the model stores them: the value at each
+storage point is rounded to the nearest bfloat16 (ties to even) and the
+arithmetic between storage points stays exact.  The storage points are the
+normalised input h, the rotated q and k and the value v (the KV cache is
+bf16), the attention output, the residual x1, the normalised h2, the SwiGLU
+activation, and the layer output.  ``storage=None`` rounds nothing.
 """
 from __future__ import annotations
 
 from typing import Dict, Optional
 
 import numpy as np
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Nearest bfloat16 value (8 significant bits, ties to even), same dtype back."""
+    x = np.asarray(x)
+    m, e = np.frexp(x.astype(np.float64))          # x = m 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8).astype(x.dtype)
 
 
 def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
@@ -89,12 +105,14 @@ def silu(z: np.ndarray) -> np.ndarray:
     return z / (z.dtype.type(1) + np.exp(-z))
 
 
-def swiglu(h: np.ndarray, w_gate_up: np.ndarray, w_down: np.ndarray) -> np.ndarray:
-    """SwiGLU FFN: gate rows [0, F), up rows [F, 2F) of w_gate_up [2F, H]; w_down [H, F]."""
+def swiglu(h: np.ndarray, w_gate_up: np.ndarray, w_down: np.ndarray,
+           store=lambda a: a) -> np.ndarray:
+    """SwiGLU FFN: gate rows [0, F), up rows [F, 2F) of w_gate_up [2F, H]; w_down [H, F].
+    ``store`` is applied to the activation silu(g) * u (its storage precision)."""
     f = w_gate_up.shape[0] // 2
     g = h @ w_gate_up[:f].T
     u = h @ w_gate_up[f:].T
-    return (silu(g) * u) @ w_down.T
+    return store(silu(g) * u) @ w_down.T
 
 
 def topk_lower_index(logits: np.ndarray, k: int) -> np.ndarray:
@@ -116,13 +134,13 @@ def moe_route(h: np.ndarray, w_router: np.ndarray, k: int, renorm: bool = True):
 
 
 def moe_ffn(h: np.ndarray, idx: np.ndarray, wts: np.ndarray,
-            w_gate_up: np.ndarray, w_down: np.ndarray) -> np.ndarray:
+            w_gate_up: np.ndarray, w_down: np.ndarray, store=lambda a: a) -> np.ndarray:
     """Weighted sum of the chosen experts' SwiGLU outputs.
     w_gate_up [E, 2Fe, H]; w_down [E, H, Fe]."""
     y = np.zeros_like(h)
     for e in np.unique(idx):
         t, j = np.nonzero(idx == e)
-        y_e = swiglu(h[t], w_gate_up[e], w_down[e])
+        y_e = swiglu(h[t], w_gate_up[e], w_down[e], store)
         np.add.at(y, t, wts[t, j][:, None] * y_e)
     return y
 
@@ -134,7 +152,8 @@ def _as(a, dtype):
 def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: np.ndarray,
                   batch, x: np.ndarray, *, dtype=np.float64,
                   forced_routes: Optional[np.ndarray] = None,
-                  rows: Optional[np.ndarray] = None) -> Dict[str, np.ndarray]:
+                  rows: Optional[np.ndarray] = None,
+                  storage: Optional[str] = None) -> Dict[str, np.ndarray]:
     """One decoder-layer forward over a ragged batch.
 
     cfg      object with hidden, n_q_heads, n_kv_heads, head_dim, ffn_dim,
@@ -148,6 +167,8 @@ def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: n
     forced_routes  optional [T, k] expert indices used instead of the router's.
     rows     optional token indices: outputs are produced only for these rows
              (keys and values are still computed for every token).
+    storage  None (exact) or "bf16" (activations rounded to bfloat16 at the
+             storage points listed in the module docstring).
 
     Returns a dict with ``out`` [len(rows) or T, H], ``k_new``/``v_new``
     [T, Hkv, D] (the rows written to the cache), and the intermediates
@@ -155,6 +176,9 @@ def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: n
     ``route_idx``/``route_w``/``logits`` for an MoE layer.
     """
     H, Hq, Hkv, D = cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    if storage not in (None, "bf16"):
+        raise ValueError(storage)
+    st = round_bf16 if storage == "bf16" else (lambda a: a)
     x = _as(x, dtype)
     T = x.shape[0]
     rows = np.arange(T) if rows is None else np.asarray(rows)
@@ -165,15 +189,15 @@ def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: n
     pos = np.concatenate([np.arange(c, c + q) for c, q in zip(ctx, qlen)])
 
     # Attention block: RMSNorm, fused q/k/v projection, rotary embedding.
-    h = rmsnorm(x, _as(w["attn_norm"], dtype), cfg.rms_eps)
+    h = st(rmsnorm(x, _as(w["attn_norm"], dtype), cfg.rms_eps))
     w_qkv = _as(w["w_qkv"], dtype)
     qkv = h @ w_qkv.T
     if w.get("b_qkv") is not None:
         qkv = qkv + _as(w["b_qkv"], dtype)
     ang = rope_angles(pos, D, cfg.rope_base)
-    q = rope(qkv[:, :Hq * D].reshape(T, Hq, D), ang)
-    k_new = rope(qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D), ang)
-    v_new = qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D)
+    q = st(rope(qkv[:, :Hq * D].reshape(T, Hq, D), ang))
+    k_new = st(rope(qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D), ang))
+    v_new = st(qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D))
 
     # Causal attention per sequence over its cached prefix plus its new rows.
     attn = np.zeros((T, Hq, D), dtype=dtype)
@@ -189,11 +213,11 @@ def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: n
                              k_new[a:b].transpose(1, 0, 2)], axis=1)
         vv = np.concatenate([_as(cache_v[slot[s], :, :c], dtype),
                              v_new[a:b].transpose(1, 0, 2)], axis=1)
-        attn[a + sel] = attention(q[a + sel], kk, vv, c + sel)
+        attn[a + sel] = st(attention(q[a + sel], kk, vv, c + sel))
 
     xr = x[rows]
-    x1 = xr + attn[rows].reshape(len(rows), Hq * D) @ _as(w["w_o"], dtype).T
-    h2 = rmsnorm(x1, _as(w["mlp_norm"], dtype), cfg.rms_eps)
+    x1 = st(xr + attn[rows].reshape(len(rows), Hq * D) @ _as(w["w_o"], dtype).T)
+    h2 = st(rmsnorm(x1, _as(w["mlp_norm"], dtype), cfg.rms_eps))
     res = {"h": h[rows], "q": q[rows], "k_new": k_new, "v_new": v_new,
            "attn": attn[rows].reshape(len(rows), Hq * D), "x1": x1, "h2": h2}
     if cfg.n_experts > 0:
@@ -204,11 +228,11 @@ def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: n
             wts = np.take_along_axis(p, idx, axis=-1)
             if cfg.moe_renorm:
                 wts = wts / np.sum(wts, axis=-1, keepdims=True)
-        y = moe_ffn(h2, idx, wts, _as(w["w_gate_up"], dtype), _as(w["w_down"], dtype))
+        y = moe_ffn(h2, idx, wts, _as(w["w_gate_up"], dtype), _as(w["w_down"], dtype), st)
         res.update(route_idx=idx, route_w=wts, logits=logits)
     else:
-        y = swiglu(h2, _as(w["w_gate_up"], dtype), _as(w["w_down"], dtype))
-    res["out"] = x1 + y
+        y = swiglu(h2, _as(w["w_gate_up"], dtype), _as(w["w_down"], dtype), st)
+    res["out"] = st(x1 + y)
     return res
 
 

@@ -178,7 +178,8 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   const bool bias = (cfg->flags & TRI_F_QKV_BIAS) != 0;
   if (bias && !w->b_qkv) return TRI_ERR_NULL;
   if (cache->n_slots <= 0 || cache->max_seq <= 0) return TRI_ERR_SHAPE;
-  if ((int64_t)b->max_ctx_len + b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
+  if (b->max_ctx_len >= cache->max_seq || b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
+  if (decode && (int64_t)b->max_ctx_len + 1 > cache->max_seq) return TRI_ERR_RANGE;
   const void* ptrs[] = {x_in, x_out, ws, cache->k, cache->v, w->attn_norm, w->w_qkv, w->w_o,
                         w->mlp_norm, w->w_gate_up, w->w_down};
   for (const void* p : ptrs)
@@ -331,7 +332,7 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
   if (!k_new || !v_new || !cache->k || !cache->v || !b->cu_q || !b->ctx_len || !b->slot)
     return TRI_ERR_NULL;
   if (cache->n_slots <= 0 || cache->max_seq <= 0) return TRI_ERR_SHAPE;
-  if ((int64_t)b->max_ctx_len + b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
+  if (b->max_ctx_len >= cache->max_seq || b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
   const void* ptrs[] = {k_new, v_new, cache->k, cache->v};
   for (const void* p : ptrs)
     if (!aligned16(p)) return TRI_ERR_ALIGN;

@@ -144,7 +144,9 @@ def test_batch_checks(lib):
     assert call(lib, b=batch(n_seqs=0, n_tokens=4)) == T.TRI_ERR_SHAPE
     assert call(lib, b=batch(n_seqs=1, n_tokens=4, max_q=2)) == T.TRI_ERR_SHAPE
     assert call(lib, b=batch(n_seqs=-1)) == T.TRI_ERR_SHAPE
-    assert call(lib, b=batch(max_ctx=61)) == T.TRI_ERR_RANGE               # 61 + 4 > 64
+    assert call(lib, b=batch(max_ctx=64)) == T.TRI_ERR_RANGE               # no row left
+    assert call(lib, b=batch(n_seqs=2, n_tokens=65, max_q=65)) == T.TRI_ERR_RANGE
+    assert call(lib, fn="tri_layer_decode", b=batch(n_seqs=1, n_tokens=1, max_q=1, max_ctx=64)) == T.TRI_ERR_RANGE
     assert call(lib, kv=T.KVCache(FAKE, FAKE + 256, 0, 64)) == T.TRI_ERR_SHAPE
     # decode needs one token per sequence
     assert call(lib, fn="tri_layer_decode", b=batch(n_seqs=2, n_tokens=4, max_q=2)) == T.TRI_ERR_SHAPE
@@ -187,7 +189,7 @@ def test_workspace_size_and_layout(lib):
 def test_kvcache_append_and_route_validation(lib):
     c = cfg()
     kv = T.KVCache(FAKE, FAKE + 4096, 1, 64)
-    b = batch(max_ctx=62)
+    b = batch(max_ctx=64)
     assert lib.tri_kvcache_append(ctypes.byref(c), ctypes.byref(kv), ctypes.byref(b), FAKE,
                                   FAKE, None) == T.TRI_ERR_RANGE
     b = batch()

@@ -1,10 +1,19 @@
 """GPU parity of the HIP decoder layer against the CPU oracle, through the C ABI.
 
-Bar (bf16 storage, fp32 accumulation): elementwise |gpu - oracle| <=
-max(2e-2, 1e-2 |oracle|); integer/index results bit-exact.  The oracle runs in
-float64 on the same seeded bf16 inputs.  Sizes span several GEMM / attention
-tiles with ragged tails; the full-size workloads are checked on sampled rows
-in the launch configuration the bench times.
+The HIP path stores activations in bfloat16 between kernels (fp32
+accumulation inside them).  Bar, on the same seeded bf16 inputs:
+
+* elementwise |gpu - ref| <= max(2e-2, 1e-2 |ref|) against the float64 oracle
+  with the bf16 storage reading (exact arithmetic, activations rounded to
+  bf16 at the layer's storage points);
+* normwise ||gpu - ref||_2 <= 1e-2 ||ref||_2 against the exact float64 oracle
+  (no rounding at all): the rounding of the storage points alone gives about
+  5e-3 there at the 7B shapes, so this bounds everything else;
+* integer / index results bit-exact.
+
+Sizes span several GEMM / attention tiles with ragged tails; the full-size
+workloads are checked on sampled rows in the launch configuration the bench
+times.
 """
 import numpy as np
 import pytest
@@ -21,11 +30,15 @@ pytestmark = pytest.mark.gpu
 ATOL, RTOL = 2e-2, 1e-2
 
 
-def assert_close(got, ref, what, atol=ATOL, rtol=RTOL):
+def assert_close(got, ref, what, atol=ATOL, rtol=RTOL, exact=None, norm_rtol=1e-2):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (what, got.shape, ref.shape)
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    if exact is not None:
+        exact = np.asarray(exact, np.float64)
+        nrm = np.linalg.norm(got - exact) / max(np.linalg.norm(exact), 1e-30)
+        assert nrm <= norm_rtol, f"{what}: normwise error vs exact oracle {nrm:.3g} > {norm_rtol}"
     err = np.abs(got - ref)
     bound = np.maximum(atol, rtol * np.abs(ref))
     bad = err > bound
@@ -61,10 +74,11 @@ class Case:
         torch.cuda.synchronize()
         return out, ws
 
-    def oracle(self, rows=None, x_bits=None):
+    def oracle(self, rows=None, x_bits=None, storage="bf16"):
         w = {k: f64(v) for k, v in self.wb.items()}
         return oracle.layer_forward(self.cfg, w, f64(self.kb), f64(self.vb), self.batch,
-                                    f64(self.xb if x_bits is None else x_bits), rows=rows)
+                                    f64(self.xb if x_bits is None else x_bits), rows=rows,
+                                    storage=storage)
 
     def cache_rows(self):
         """GPU cache rows written by this call, as [T, Hkv, D] (K and V)."""
@@ -93,7 +107,8 @@ def test_tiny_prefill_then_16_decode_steps():
     cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
     out, _ = cs.run()
     ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "tiny prefill out")
+    assert_close(to_host_f64(out), ref["out"], "tiny prefill out",
+                 exact=cs.oracle(storage=None)["out"])
     kr, vr = cs.cache_rows()
     assert_close(kr, ref["k_new"], "tiny prefill K rows")
     assert_close(vr, ref["v_new"], "tiny prefill V rows")
@@ -104,10 +119,12 @@ def test_tiny_prefill_then_16_decode_steps():
         cs.batch, cs.db = batch, device_batch(batch)
         xb = make_x(wl.cfg, batch.n_tokens, wl.seed, step=step)
         k, v = cs.cache
-        ref = oracle.layer_forward(wl.cfg, {kk: f64(vv) for kk, vv in cs.wb.items()},
-                                   to_host_f64(k), to_host_f64(v), batch, f64(xb))
+        w64 = {kk: f64(vv) for kk, vv in cs.wb.items()}
+        ref = oracle.layer_forward(wl.cfg, w64, to_host_f64(k), to_host_f64(v), batch, f64(xb),
+                                   storage="bf16")
+        ex = oracle.layer_forward(wl.cfg, w64, to_host_f64(k), to_host_f64(v), batch, f64(xb))
         out, _ = cs.run(decode=True, x=to_device_bf16(xb))
-        assert_close(to_host_f64(out), ref["out"], f"tiny decode step {step}")
+        assert_close(to_host_f64(out), ref["out"], f"tiny decode step {step}", exact=ex["out"])
         kr, vr = cs.cache_rows()
         assert_close(kr, ref["k_new"], f"tiny decode K row {step}")
         assert_close(vr, ref["v_new"], f"tiny decode V row {step}")
@@ -126,7 +143,7 @@ def test_tiny_intermediates():
     assert_close(to_host_f64(ws_view(ws, m.attn, (Tn, Hq * D))), ref["attn"], "attn")
     assert_close(to_host_f64(ws_view(ws, m.x1, (Tn, H))), ref["x1"], "x1")
     assert_close(to_host_f64(ws_view(ws, m.h2, (Tn, H))), ref["h2"], "h2")
-    assert_close(to_host_f64(out), ref["out"], "out")
+    assert_close(to_host_f64(out), ref["out"], "out", exact=cs.oracle(storage=None)["out"])
 
 
 @pytest.mark.parametrize("bias", [False, True])
@@ -138,7 +155,7 @@ def test_tiny_ragged_mixed_batch(bias):
     cs = Case(cfg, batch, 5, 256, seed=3)
     out, _ = cs.run()
     ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "ragged out")
+    assert_close(to_host_f64(out), ref["out"], "ragged out", exact=cs.oracle(storage=None)["out"])
     kr, vr = cs.cache_rows()
     assert_close(kr, ref["k_new"], "ragged K")
     assert_close(vr, ref["v_new"], "ragged V")
@@ -155,7 +172,8 @@ def test_7b_ragged_prefill_sampled_rows():
     out, _ = cs.run()
     rows = np.array([0, 1, 127, 128, 255, 256, 299, 300, 301, 365, 428, 429, 430, 460, 493])
     ref = cs.oracle(rows=rows)
-    assert_close(to_host_f64(out)[rows], ref["out"], "7B ragged prefill rows")
+    assert_close(to_host_f64(out)[rows], ref["out"], "7B ragged prefill rows",
+                 exact=cs.oracle(rows=rows, storage=None)["out"])
     kr, vr = cs.cache_rows()
     assert_close(kr, ref["k_new"], "7B K rows")
     assert_close(vr, ref["v_new"], "7B V rows")
@@ -168,7 +186,7 @@ def test_7b_decode_step_all_rows():
     cs = Case(cfg, batch, 8, 4100, seed=2)
     out, _ = cs.run(decode=True)
     ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "7B decode out")
+    assert_close(to_host_f64(out), ref["out"], "7B decode out", exact=cs.oracle(storage=None)["out"])
     kr, vr = cs.cache_rows()
     assert_close(kr, ref["k_new"], "7B decode K")
     assert_close(vr, ref["v_new"], "7B decode V")
@@ -183,9 +201,11 @@ def test_full_size_dense_prefill_sampled():
     sub = B([s], [0], [2048])
     local = np.array([0, 1, 255, 256, 1023, 1024, 2046, 2047])
     w = {k: f64(v) for k, v in cs.wb.items()}
-    ref = oracle.layer_forward(wl.cfg, w, f64(cs.kb), f64(cs.vb), sub,
-                               f64(cs.xb[s * 2048:(s + 1) * 2048]), rows=local)
-    assert_close(to_host_f64(out)[s * 2048 + local], ref["out"], "full prefill sampled rows")
+    args = (wl.cfg, w, f64(cs.kb), f64(cs.vb), sub, f64(cs.xb[s * 2048:(s + 1) * 2048]))
+    ref = oracle.layer_forward(*args, rows=local, storage="bf16")
+    ex = oracle.layer_forward(*args, rows=local)
+    assert_close(to_host_f64(out)[s * 2048 + local], ref["out"], "full prefill sampled rows",
+                 exact=ex["out"])
 
 
 def test_full_size_dense_decode_sampled():
@@ -197,9 +217,11 @@ def test_full_size_dense_decode_sampled():
     # the oracle sees only the picked slots' caches, renumbered 0..5
     sub = B(np.arange(len(pick)), wl.batch.ctx_len[pick], wl.batch.q_len[pick])
     w = {k: f64(v) for k, v in cs.wb.items()}
-    ref = oracle.layer_forward(wl.cfg, w, f64(cs.kb[wl.batch.slot[pick]]),
-                               f64(cs.vb[wl.batch.slot[pick]]), sub, f64(cs.xb[pick]))
-    assert_close(to_host_f64(out)[pick], ref["out"], "full decode sampled rows")
+    args = (wl.cfg, w, f64(cs.kb[wl.batch.slot[pick]]), f64(cs.vb[wl.batch.slot[pick]]), sub,
+            f64(cs.xb[pick]))
+    ref = oracle.layer_forward(*args, storage="bf16")
+    assert_close(to_host_f64(out)[pick], ref["out"], "full decode sampled rows",
+                 exact=oracle.layer_forward(*args)["out"])
 
 
 # ------------------------------------------------------------- invariants --

@@ -348,3 +348,50 @@ def test_kvcache_append_rows():
     assert np.array_equal(ck2[1, :, 2:5], kn[:3].transpose(1, 0, 2))
     assert np.array_equal(ck2[0, :, 5], kn[3])
     assert np.count_nonzero(ck2) == kn.size
+
+
+# ------------------------------------------------------- bf16 storage reading --
+
+def test_round_bf16_ties_to_even_and_matches_bit_rounding():
+    assert L.round_bf16(np.array([1.0 + 2.0 ** -8]))[0] == 1.0                     # tie -> even
+    assert L.round_bf16(np.array([1.0 + 3 * 2.0 ** -8]))[0] == 1.0 + 2.0 ** -6      # tie -> even
+    assert L.round_bf16(np.array([1.0 + 2.0 ** -8 + 2.0 ** -20]))[0] == 1.0 + 2.0 ** -7
+    assert L.round_bf16(np.array([-0.0, 0.0, 2.0 ** -130])).tolist() == [-0.0, 0.0, 2.0 ** -130]
+    from synth import to_bf16_bits
+    v = (np.random.default_rng(11).standard_normal(100000) *
+         np.exp(np.random.default_rng(12).uniform(-20, 20, 100000))).astype(np.float32)
+    assert np.array_equal(L.round_bf16(v.astype(np.float64)), bf16_to_f32(to_bf16_bits(v)).astype(np.float64))
+
+
+def test_bf16_storage_rounds_exactly_the_declared_points():
+    cfg = TINY
+    b = B([0, 1], [2, 0], [5, 3])
+    w, ck, cv, x = setup(cfg, b, 2, 8)
+    r = L.layer_forward(cfg, w, ck, cv, b, x, storage="bf16")
+    for k in ("h", "q", "k_new", "v_new", "attn", "x1", "h2", "out"):
+        assert np.array_equal(L.round_bf16(r[k]), r[k]), k
+    exact = L.layer_forward(cfg, w, ck, cv, b, x)
+    assert np.allclose(r["out"], exact["out"], rtol=3e-2, atol=3e-2)
+    assert not np.array_equal(r["out"], exact["out"])
+
+
+@pytest.mark.parametrize("cfg", [TINY, TINY_MOE])
+def test_bf16_storage_matches_brute_force_with_bit_rounding(cfg):
+    """The storage points of the vectorised oracle agree with the brute force
+    given an independent (bit-pattern) bf16 rounding."""
+    import struct
+    from synth import to_bf16_bits
+
+    def bit_round(v):
+        f32 = np.float32(struct.unpack("f", struct.pack("f", v))[0])  # nearest fp32 first
+        return float(bf16_to_f32(to_bf16_bits(np.array([f32])))[0])
+
+    b = B([1, 0], [3, 0], [3, 4])
+    w, ck, cv, x = setup(cfg, b, 2, 8)
+    r = L.layer_forward(cfg, w, ck, cv, b, x, storage="bf16")
+    wl = {k: _lists(v) for k, v in w.items()}
+    out, kr, vr, ridx, rw = oracle.layer_brute(cfg, wl, _lists(ck), _lists(cv), b.slot.tolist(),
+                                               b.ctx_len.tolist(), b.q_len.tolist(), _lists(x),
+                                               store=bit_round)
+    assert np.allclose(r["k_new"], np.array(kr), rtol=1e-12, atol=1e-12)
+    assert np.allclose(r["out"], np.array(out), rtol=1e-12, atol=1e-12)
