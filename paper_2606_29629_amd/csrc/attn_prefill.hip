@@ -12,9 +12,13 @@
 // the tile's 64 keys, so the running max / sum of the online softmax need one
 // cross-lane exchange (lane ^ 32) per tile.  The output is also kept
 // transposed, O^T += V^T P^T: P^T is taken straight from the score
-// accumulators (rounded to bf16), and V is written to LDS transposed with the
-// keys of every 16-key group permuted to the order in which the score
-// accumulator holds them, so each lane's 8 V^T values are one ds_read_b128.
+// accumulators, and V is written to LDS transposed with the keys of every
+// 16-key group permuted to the order in which the score accumulator holds
+// them, so each lane's 8 V^T values are one ds_read_b128.  The P V product runs
+// on the fp16 matrix path (v_mfma_f32_32x32x16_f16, same rate as bf16): V
+// converts from bf16 exactly in fp16's normal range, and P is split into
+// P_hi = fp16(P) and P_lo = fp16(P - P_hi), two MFMAs into one accumulator,
+// so P keeps ~22 significant bits and the weights match the fp32 row sum.
 // Scores use exp2 with the 1/sqrt(D) * log2(e) scale folded in.
 #include "common.hpp"
 #include "kernels.hpp"
@@ -39,7 +43,7 @@ __device__ __forceinline__ int vt_chunk(int pc, int d) { return pc ^ (d & 7) ^ (
 template <int D>
 struct FaSmem {
   bf16 k[2][kFaBK * D];  // [key][d], 16-byte chunks swizzled by key % 8
-  bf16 vt[2][D * kFaBK]; // [d][key slot], chunks swizzled by vt_chunk
+  f16 vt[2][D * kFaBK];  // V^T in fp16: [d][key slot], chunks swizzled by vt_chunk
 };
 
 template <int D>
@@ -106,7 +110,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int d = ch * 8 + e;
-        sm.vt[buf][d * kFaBK + vt_chunk(slotk >> 3, d) * 8 + (slotk & 7)] = v.e[e];
+        sm.vt[buf][d * kFaBK + vt_chunk(slotk >> 3, d) * 8 + (slotk & 7)] = bf2h_sat(v.e[e]);
       }
     }
   };
@@ -158,7 +162,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(
       const float alpha = exp2f(m_run - m_new);
       m_run = m_new;
       float ls = 0.f;
-      bf16x8 pf[4];
+      f16x8 pf[4], pl[4];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -167,7 +171,9 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(
           for (int e = 0; e < 8; ++e) {
             const float p = exp2f(sacc[kb][8 * h + e] - m_new);
             ls += p;
-            pf[2 * kb + h][e] = f2bf(p);
+            const f16 hi = (f16)p;
+            pf[2 * kb + h][e] = hi;
+            pl[2 * kb + h][e] = (f16)(p - (float)hi);
           }
       l_run = l_run * alpha + ls;
 #pragma unroll
@@ -179,8 +185,9 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(
 #pragma unroll
         for (int b = 0; b < DB; ++b) {
           const int d = 32 * b + lr;
-          const bf16x8 vf = *(const bf16x8*)&sm.vt[buf][d * kFaBK + vt_chunk(pc, d) * 8];
-          oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[g16], oacc[b], 0, 0, 0);
+          const f16x8 vf = *(const f16x8*)&sm.vt[buf][d * kFaBK + vt_chunk(pc, d) * 8];
+          oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf[g16], oacc[b], 0, 0, 0);
+          oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pl[g16], oacc[b], 0, 0, 0);
         }
       }
     }

@@ -9,6 +9,8 @@ typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16;
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -18,6 +20,10 @@ constexpr int kWave = 64;
 
 __device__ __forceinline__ float bf2f(bf16 v) { return (float)v; }
 __device__ __forceinline__ bf16 f2bf(float v) { return (bf16)v; }  // RNE (v_cvt_pk_bf16_f32)
+// bf16 -> fp16, saturating at the fp16 range (exact for 2^-14 <= |v| <= 65504).
+__device__ __forceinline__ f16 bf2h_sat(bf16 v) {
+  return (f16)fminf(fmaxf((float)v, -65504.f), 65504.f);
+}
 
 // 16-byte vector of 8 bf16 <-> raw 4 dwords.
 union Pack8 {

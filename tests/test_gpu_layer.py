@@ -1,51 +1,88 @@
 """GPU parity of the HIP decoder layer against the CPU oracle, through the C ABI.
 
-The HIP path stores activations in bfloat16 between kernels (fp32
-accumulation inside them).  Bar, on the same seeded bf16 inputs:
+The HIP path stores activations in bfloat16 between kernels and accumulates
+in fp32 inside them.  Two gates, on the same seeded bf16 inputs:
 
-* elementwise |gpu - ref| <= max(2e-2, 1e-2 |ref|) against the float64 oracle
-  with the bf16 storage reading (exact arithmetic, activations rounded to
-  bf16 at the layer's storage points);
-* normwise ||gpu - ref||_2 <= 1e-2 ||ref||_2 against the exact float64 oracle
-  (no rounding at all): the rounding of the storage points alone gives about
-  5e-3 there at the 7B shapes, so this bounds everything else;
-* integer / index results bit-exact.
+1. Per-kernel parity on identical inputs (the tight gate).  Every stage's GPU
+   output is compared with the oracle's definition of that stage evaluated in
+   float64 on the GPU's own inputs to the stage (read back from the
+   workspace) and rounded to bf16: each element must be that value or an
+   adjacent bf16 value (<= 1 ulp; a flip is possible when the exact value lies
+   within fp32 error of a rounding boundary), and at most 1% of elements may
+   be the adjacent one.
+2. End to end.  Against the oracle with the bf16 storage reading,
+   |gpu - ref| <= max(2e-2, 1e-2 |ref|) for >= 99.9% of elements and within 4x
+   that bound for all; against the exact float64 oracle the normwise error of
+   every row is <= 1e-2.  (Two correct bf16 computations whose fp32 sums differ
+   in the last bits round some intermediates to adjacent bf16 values; these
+   flips cascade through q/k -> attention -> residual -> FFN, so at the 7B
+   shapes a few in 10^4 output elements sit 2-4 ulps apart.  A CPU emulation of
+   the bf16 storage points reproduces the GPU's deviation from the exact
+   oracle.)
 
-Sizes span several GEMM / attention tiles with ragged tails; the full-size
-workloads are checked on sampled rows in the launch configuration the bench
-times.
+Index results are bit-exact.  Sizes span several GEMM / attention tiles with
+ragged tails; the full-size workloads are checked on sampled rows in the
+launch configuration the bench times.
 """
 import numpy as np
 import pytest
 
 import oracle
+from oracle import layer as OL
 from paper_2606_29629_amd import _lib as T
 from paper_2606_29629_amd.workload import (DeviceLayer, device_batch, device_cache,
                                            to_device_bf16, to_host_f64)
 from synth import (Batch, LayerConfig, bf16_to_f32, layer_7b, layer_c1, make_cache,
-                   make_weights, make_x, workload)
+                   make_weights, make_x, to_bf16_bits, workload)
 
 pytestmark = pytest.mark.gpu
 
 ATOL, RTOL = 2e-2, 1e-2
 
 
-def assert_close(got, ref, what, atol=ATOL, rtol=RTOL, exact=None, norm_rtol=1e-2):
+def assert_close(got, ref, what, atol=ATOL, rtol=RTOL, exact=None, norm_rtol=1e-2,
+                 min_frac=0.999, cap=4.0):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (what, got.shape, ref.shape)
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
     if exact is not None:
-        exact = np.asarray(exact, np.float64)
-        nrm = np.linalg.norm(got - exact) / max(np.linalg.norm(exact), 1e-30)
-        assert nrm <= norm_rtol, f"{what}: normwise error vs exact oracle {nrm:.3g} > {norm_rtol}"
+        exact = np.asarray(exact, np.float64).reshape(got.shape[0], -1)
+        g2 = got.reshape(got.shape[0], -1)
+        nrm = np.linalg.norm(g2 - exact, axis=1) / np.maximum(np.linalg.norm(exact, axis=1), 1e-30)
+        assert nrm.max() <= norm_rtol, f"{what}: row normwise error vs exact oracle {nrm.max():.3g}"
     err = np.abs(got - ref)
     bound = np.maximum(atol, rtol * np.abs(ref))
-    bad = err > bound
-    if bad.any():
+    frac_ok = np.mean(err <= bound)
+    worst = np.max(err / bound)
+    if frac_ok < min_frac or worst > cap:
         i = np.unravel_index(np.argmax(err / bound), err.shape)
-        raise AssertionError(f"{what}: {int(bad.sum())}/{bad.size} out of tolerance; worst at {i}: "
-                             f"gpu {got[i]:.6g} oracle {ref[i]:.6g} (max abs err {err.max():.3g})")
+        raise AssertionError(f"{what}: {np.sum(err > bound)}/{err.size} outside the bound "
+                             f"(worst {worst:.2f}x at {i}: gpu {got[i]:.6g} oracle {ref[i]:.6g})")
+
+
+def bf16_ordinal(a):
+    """Monotone integer index of bf16 values (adjacent bf16 values differ by 1)."""
+    b = to_bf16_bits(np.asarray(a, np.float32)).astype(np.int64)
+    return np.where(b & 0x8000, -(b & 0x7FFF), b)
+
+
+def assert_rounded(got, exact, what, max_flip_frac=0.01):
+    """got (bf16 values) is the bf16 rounding of `exact` or an adjacent bf16 value."""
+    got = np.asarray(got, np.float64)
+    exact = np.asarray(exact, np.float64)
+    assert got.shape == exact.shape, (what, got.shape, exact.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite"
+    d = np.abs(bf16_ordinal(got) - bf16_ordinal(OL.round_bf16(exact)))
+    tiny = np.abs(got - exact) <= 1e-5 * np.sqrt(np.mean(exact ** 2))  # values near 0
+    bad = (d > 1) & ~tiny
+    if bad.any():
+        i = np.unravel_index(np.argmax(np.where(tiny, 0, d)), d.shape)
+        raise AssertionError(f"{what}: {int(bad.sum())}/{d.size} elements > 1 ulp from the "
+                             f"rounded exact value (worst {d[i]} ulps at {i}: gpu {got[i]:.6g} "
+                             f"exact {exact[i]:.6g})")
+    frac = np.mean((d == 1) & ~tiny)
+    assert frac <= max_flip_frac, f"{what}: {frac:.3%} of elements one ulp off"
 
 
 def f64(bits):
@@ -100,6 +137,60 @@ def ws_view(ws, off, shape):
     return ws[off:off + 2 * n].view(torch.bfloat16).view(*shape)
 
 
+def stage_parity(cs, ws, rows, x_bits=None, label=""):
+    """Per-kernel parity on identical inputs for the given token rows."""
+    import torch
+    cfg, b = cs.cfg, cs.batch
+    m = T.workspace_layout(cs.dl.cfg, cs.db)
+    Tn, H, D, Hq, Hkv = b.n_tokens, cfg.hidden, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
+    F = cfg.ffn_dim
+    rows = np.asarray(rows)
+    ridx = torch.as_tensor(rows, device=ws.device)
+
+    def rd(off, n, shape):
+        return to_host_f64(ws_view(ws, off, (Tn, n))[ridx]).reshape(len(rows), *shape)
+
+    h, q = rd(m.h, H, (H,)), rd(m.q, Hq * D, (Hq, D))
+    attn, x1, h2 = rd(m.attn, Hq * D, (Hq * D,)), rd(m.x1, H, (H,)), rd(m.h2, H, (H,))
+    act = rd(m.act, F, (F,))
+    w = {k: f64(v) for k, v in cs.wb.items()}
+    x = f64((cs.xb if x_bits is None else x_bits)[rows])
+    # token -> (sequence, cache slot, cache row); only the slots involved are read back
+    seq = np.searchsorted(b.cu_q, rows, side="right") - 1
+    crow = b.ctx_len[seq] + rows - b.cu_q[seq]
+    slots, sidx = np.unique(b.slot[seq], return_inverse=True)
+    st = torch.as_tensor(slots, device=ws.device)
+    kc, vc = to_host_f64(cs.cache[0][st]), to_host_f64(cs.cache[1][st])
+    # RMSNorm
+    assert_rounded(h, OL.rmsnorm(x, w["attn_norm"], cfg.rms_eps), f"{label} rmsnorm_attn")
+    # q/k/v projection + rotary + cache write
+    hq = h @ w["w_qkv"].T
+    if "b_qkv" in w:
+        hq = hq + w["b_qkv"]
+    ang = OL.rope_angles(b.pos[rows], D, cfg.rope_base)
+    assert_rounded(q, OL.rope(hq[:, :Hq * D].reshape(-1, Hq, D), ang), f"{label} q")
+    k_ref = OL.rope(hq[:, Hq * D:(Hq + Hkv) * D].reshape(-1, Hkv, D), ang)
+    v_ref = hq[:, (Hq + Hkv) * D:].reshape(-1, Hkv, D)
+    assert_rounded(kc[sidx, :, crow], k_ref, f"{label} k cache rows")
+    assert_rounded(vc[sidx, :, crow], v_ref, f"{label} v cache rows")
+    # attention over the GPU-written cache
+    att_ref = np.stack([OL.attention(q[i:i + 1], kc[sidx[i], :, :crow[i] + 1],
+                                     vc[sidx[i], :, :crow[i] + 1], np.array([crow[i]]))[0]
+                        for i in range(len(rows))]).reshape(len(rows), Hq * D)
+    assert_rounded(attn, att_ref, f"{label} attention")
+    assert_rounded(x1, x + attn @ w["w_o"].T, f"{label} o_proj + residual")
+    assert_rounded(h2, OL.rmsnorm(x1, w["mlp_norm"], cfg.rms_eps), f"{label} rmsnorm_mlp")
+    g = h2 @ w["w_gate_up"][:F].T
+    u = h2 @ w["w_gate_up"][F:].T
+    assert_rounded(act, OL.silu(g) * u, f"{label} gate_up + SwiGLU")
+    return x1, act, w
+
+
+def check_down(cs, out, x1, act, w, rows, label=""):
+    assert_rounded(to_host_f64(out)[np.asarray(rows)], x1 + act @ w["w_down"].T,
+                   f"{label} down + residual")
+
+
 # ------------------------------------------------------------- tiny layer --
 
 def test_tiny_prefill_then_16_decode_steps():
@@ -144,6 +235,9 @@ def test_tiny_intermediates():
     assert_close(to_host_f64(ws_view(ws, m.x1, (Tn, H))), ref["x1"], "x1")
     assert_close(to_host_f64(ws_view(ws, m.h2, (Tn, H))), ref["h2"], "h2")
     assert_close(to_host_f64(out), ref["out"], "out", exact=cs.oracle(storage=None)["out"])
+    rows = np.arange(batch.n_tokens)
+    x1, act, w = stage_parity(cs, ws, rows, label="tiny")
+    check_down(cs, out, x1, act, w, rows, "tiny")
 
 
 @pytest.mark.parametrize("bias", [False, True])
@@ -153,7 +247,10 @@ def test_tiny_ragged_mixed_batch(bias):
     # a long prefill over two flash tiles, a chunk with cached prefix, decodes
     batch = B([3, 0, 2, 1, 4], [0, 40, 7, 0, 150], [200, 9, 1, 1, 1])
     cs = Case(cfg, batch, 5, 256, seed=3)
-    out, _ = cs.run()
+    out, ws = cs.run()
+    rows = np.arange(batch.n_tokens)
+    x1, act, w = stage_parity(cs, ws, rows, label="ragged")
+    check_down(cs, out, x1, act, w, rows, "ragged")
     ref = cs.oracle()
     assert_close(to_host_f64(out), ref["out"], "ragged out", exact=cs.oracle(storage=None)["out"])
     kr, vr = cs.cache_rows()
@@ -169,8 +266,10 @@ def test_7b_ragged_prefill_sampled_rows():
     # flash tiles with ragged tails, a cached-prefix chunk and a decode sequence
     batch = B([0, 1, 2, 3], [0, 37, 500, 0], [300, 129, 1, 64])
     cs = Case(cfg, batch, 4, 640, seed=1)
-    out, _ = cs.run()
+    out, ws = cs.run()
     rows = np.array([0, 1, 127, 128, 255, 256, 299, 300, 301, 365, 428, 429, 430, 460, 493])
+    x1, act, w = stage_parity(cs, ws, rows, label="7B ragged")
+    check_down(cs, out, x1, act, w, rows, "7B ragged")
     ref = cs.oracle(rows=rows)
     assert_close(to_host_f64(out)[rows], ref["out"], "7B ragged prefill rows",
                  exact=cs.oracle(rows=rows, storage=None)["out"])
@@ -184,7 +283,10 @@ def test_7b_decode_step_all_rows():
     ctx = [1, 63, 64, 127, 128, 129, 1000, 4095]
     batch = B(list(range(8)), ctx, [1] * 8)
     cs = Case(cfg, batch, 8, 4100, seed=2)
-    out, _ = cs.run(decode=True)
+    out, ws = cs.run(decode=True)
+    rows = np.arange(8)
+    x1, act, w = stage_parity(cs, ws, rows, label="7B decode")
+    check_down(cs, out, x1, act, w, rows, "7B decode")
     ref = cs.oracle()
     assert_close(to_host_f64(out), ref["out"], "7B decode out", exact=cs.oracle(storage=None)["out"])
     kr, vr = cs.cache_rows()
@@ -196,7 +298,10 @@ def test_full_size_dense_prefill_sampled():
     """8 x 2048 tokens (the bench's prefill launch), rows sampled from one sequence."""
     wl = workload("dense_prefill")
     cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
-    out, _ = cs.run()
+    out, ws = cs.run()
+    rows = np.array([0, 63, 64, 2047, 2048, 5 * 2048 + 1000, 16383])
+    x1, act, w = stage_parity(cs, ws, rows, label="full prefill")
+    check_down(cs, out, x1, act, w, rows, "full prefill")
     s = 5
     sub = B([s], [0], [2048])
     local = np.array([0, 1, 255, 256, 1023, 1024, 2046, 2047])
@@ -212,8 +317,10 @@ def test_full_size_dense_decode_sampled():
     """64 sequences at KV 4096 (the decode launch), 6 sequences checked."""
     wl = workload("dense_decode")
     cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
-    out, _ = cs.run(decode=True)
+    out, ws = cs.run(decode=True)
     pick = np.array([0, 1, 17, 31, 62, 63])
+    x1, act, w = stage_parity(cs, ws, pick, label="full decode")
+    check_down(cs, out, x1, act, w, pick, "full decode")
     # the oracle sees only the picked slots' caches, renumbered 0..5
     sub = B(np.arange(len(pick)), wl.batch.ctx_len[pick], wl.batch.q_len[pick])
     w = {k: f64(v) for k, v in cs.wb.items()}
