@@ -33,6 +33,15 @@ union Pack8 {
 };
 
 __device__ __forceinline__ u32x4 ldg16(const void* p) { return *(const u32x4*)p; }
+
+// 16 bytes per lane from a buffer straight into LDS (buffer_load_dwordx4 ... lds):
+// the wave's 64 lanes fill 1 KB at `lds` in lane order; `lds` must be
+// wave-uniform.  Offsets at or past the buffer's size read as zero.
+__device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, void* lds,
+                                                  uint32_t voffset, int soffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16,
+                                           voffset, soffset, 0, 0);
+}
 __device__ __forceinline__ void stg16(void* p, u32x4 v) { *(u32x4*)p = v; }
 
 // Wave-level reductions (wave64) through cross-lane shuffles.

@@ -6,11 +6,13 @@
 // activations), which is the native operand layout of v_mfma_f32_32x32x16_bf16:
 // lane l supplies row (l % 32) and 8 consecutive k of slice (l / 32).
 //
-// Tiling: BM x BN x 64 block tile, 4 waves (2 x 2), each wave a (BM/2) x (BN/2)
-// sub-tile of 32x32 MFMA blocks.  A and B tiles are staged through LDS, double
+// Tiling: BM x BN x 64 block tile, WGM x WGN waves (8 = 4 x 2: two waves per
+// SIMD, so one wave's LDS waits overlap the other's MFMAs), each wave a
+// (BM/WGM) x (BN/WGN) sub-tile of 32x32 MFMA blocks.  A and B tiles are staged through LDS, double
 // buffered, with 16-byte chunks XOR-swizzled by (row % 8) so that the eight
-// lanes of a ds_read_b128 phase hit distinct banks.  Global loads for tile
-// k+1 are issued before the MFMAs of tile k.
+// lanes of a ds_read_b128 phase hit distinct banks.  Tiles move from HBM to
+// LDS with buffer_load_dwordx4 ... lds (no register staging); the loads of
+// tile k+1 are in flight while the MFMAs of tile k run.
 //
 // Work distribution: workgroups are dispatched round-robin over the 8 XCDs;
 // the linear block id is remapped so each XCD owns a contiguous range of
@@ -112,20 +114,19 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
   }
 }
 
-template <int BM, int BN, int EK>
-__global__ __launch_bounds__(256) void gemm_kernel(const bf16* __restrict__ A, int lda,
+template <int BM, int BN, int WGM, int WGN, int EK>
+__global__ __launch_bounds__(WGM * WGN * 64) void gemm_kernel(const bf16* __restrict__ A, int lda,
                                                    const bf16* __restrict__ B, int ldb, int M,
                                                    int N, int K, Epi epi, int tiles_m,
                                                    int tiles_n) {
-  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int NT = WGM * WGN * 64;        // threads
+  constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int MI = WM / 32, NI = WN / 32;
-  constexpr int A_LD = BM * kChunks / 256;  // 16-byte loads per thread per tile
-  constexpr int B_LD = BN * kChunks / 256;
   extern __shared__ __align__(16) char smem_raw[];
   GemmSmem<BM, BN>& sm = *reinterpret_cast<GemmSmem<BM, BN>*>(smem_raw);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   int tm, tn;
   tile_of_block(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int n_rows_b = EK == EPI_SWIGLU ? 2 * epi.ffn : N;
@@ -135,19 +136,24 @@ __global__ __launch_bounds__(256) void gemm_kernel(const bf16* __restrict__ A, i
       __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)((int64_t)M * lda * 2), 0x00020000);
   const __amdgpu_buffer_rsrc_t rsrc_b =
       __builtin_amdgcn_make_buffer_rsrc((void*)B, (short)0, (int)((int64_t)n_rows_b * ldb * 2), 0x00020000);
-  // This thread loads 16-byte chunk c of tile rows r0 + 32 i.
-  const int r0 = tid / kChunks, c0 = tid % kChunks;
-  const int lds_off = r0 * kBK + swz(r0, c0) * 8;  // + i * 32 * kBK (swizzle depends on r0 % 8 only)
-  uint32_t a_off[A_LD], b_off[B_LD];
+  // Global -> LDS without registers: each buffer_load_dwordx4 ... lds writes the
+  // 64 lanes' 16 bytes to 1 KB of LDS in lane order, i.e. 8 tile rows.  Lane l
+  // fills physical chunk l % 8 of row l / 8 of its block, so it fetches the
+  // logical chunk (l % 8) ^ (row % 8) of that row (the swizzled layout).
+  constexpr int NW = NT / 64;
+  constexpr int A_BLK = BM / 8 / NW, B_BLK = BN / 8 / NW;  // 1 KB blocks per wave per tile
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
+  uint32_t a_off[A_BLK], b_off[B_BLK];
 #pragma unroll
-  for (int i = 0; i < A_LD; ++i) {
-    const int gr = tm * BM + r0 + 32 * i;
-    a_off[i] = gr < M ? (uint32_t)(((int64_t)gr * lda + c0 * 8) * 2) : 0x80000000u;
+  for (int j = 0; j < A_BLK; ++j) {
+    const int gr = tm * BM + (wv + NW * j) * 8 + lrow;
+    a_off[j] = gr < M ? (uint32_t)(((int64_t)gr * lda + lchunk * 8) * 2) : 0x80000000u;
   }
 #pragma unroll
-  for (int i = 0; i < B_LD; ++i) {
-    const int gr = b_row_of<BN, WN>(EK, tn, r0 + 32 * i, epi.ffn);
-    b_off[i] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + c0 * 8) * 2) : 0x80000000u;
+  for (int j = 0; j < B_BLK; ++j) {
+    const int gr = b_row_of<BN, WN>(EK, tn, (wv + NW * j) * 8 + lrow, epi.ffn);
+    b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + lchunk * 8) * 2) : 0x80000000u;
   }
 
   f32x16 acc[MI][NI];
@@ -156,31 +162,24 @@ __global__ __launch_bounds__(256) void gemm_kernel(const bf16* __restrict__ A, i
 #pragma unroll
     for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{0.f};
 
-  u32x4 ra[A_LD], rb[B_LD];
-  auto gload = [&](int kt) {
+  auto gload = [&](int kt, int buf) {
     const int kb = kt * kBK * 2;
 #pragma unroll
-    for (int i = 0; i < A_LD; ++i)
-      ra[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_a, a_off[i], kb, 0);
+    for (int j = 0; j < A_BLK; ++j)
+      buffer_load_lds16(rsrc_a, &sm.a[buf][(wv + NW * j) * 8 * kBK], a_off[j], kb);
 #pragma unroll
-    for (int i = 0; i < B_LD; ++i)
-      rb[i] = __builtin_amdgcn_raw_buffer_load_b128(rsrc_b, b_off[i], kb, 0);
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < A_LD; ++i) *(u32x4*)&sm.a[buf][lds_off + i * 32 * kBK] = ra[i];
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) *(u32x4*)&sm.b[buf][lds_off + i * 32 * kBK] = rb[i];
+    for (int j = 0; j < B_BLK; ++j)
+      buffer_load_lds16(rsrc_b, &sm.b[buf][(wv + NW * j) * 8 * kBK], b_off[j], kb);
   };
 
   const int KT = K / kBK;
   const int lr = lane & 31, lg = lane >> 5;
-  gload(0);
-  sstore(0);
+  gload(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   for (int kt = 0; kt < KT; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
+    if (kt + 1 < KT) gload(kt + 1, buf ^ 1);  // lands in the other buffer meanwhile
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
       const int ch = kk * 2 + lg;
@@ -201,7 +200,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const bf16* __restrict__ A, i
         for (int j = 0; j < NI; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < KT) sstore(buf ^ 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
@@ -250,7 +249,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const bf16* __restrict__ A, i
   }
 }
 
-template <int BM, int BN, int EK>
+template <int BM, int BN, int WGM, int WGN, int EK>
 static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
                            const Epi& epi, hipStream_t s) {
   const int tiles_m = cdiv(M, BM);
@@ -258,12 +257,12 @@ static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M
   const size_t smem = sizeof(GemmSmem<BM, BN>);
   static bool attr_set = false;  // one-time opt-in to > 64 KB of LDS
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<BM, BN, EK>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<BM, BN, WGM, WGN, EK>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  gemm_kernel<BM, BN, EK><<<tiles_m * tiles_n, 256, smem, s>>>(
+  gemm_kernel<BM, BN, WGM, WGN, EK><<<tiles_m * tiles_n, WGM * WGN * 64, smem, s>>>(
       (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, epi, tiles_m, tiles_n);
   return hipGetLastError();
 }
@@ -272,10 +271,10 @@ hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, in
                        const Epi& epi, hipStream_t s) {
   if (M == 0) return hipSuccess;
   switch (epi.kind) {
-    case EPI_STORE: return run_gemm<256, 256, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, s);
-    case EPI_RESID: return run_gemm<256, 256, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, s);
-    case EPI_SWIGLU: return run_gemm<256, 256, EPI_SWIGLU>(A, lda, B, ldb, M, N, K, epi, s);
-    default: return run_gemm<256, 256, EPI_QKV>(A, lda, B, ldb, M, N, K, epi, s);
+    case EPI_STORE: return run_gemm<256, 256, 4, 2, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, s);
+    case EPI_RESID: return run_gemm<256, 256, 4, 2, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, s);
+    case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU>(A, lda, B, ldb, M, N, K, epi, s);
+    default: return run_gemm<256, 256, 4, 2, EPI_QKV>(A, lda, B, ldb, M, N, K, epi, s);
   }
 }
 
