@@ -45,6 +45,27 @@ def prefill_flops(cfg, batch) -> float:
     return 2.0 * linear_params(cfg) * batch.n_tokens + 4.0 * cfg.head_dim * cfg.n_q_heads * pairs
 
 
+def profiled_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from profiles/traffic.txt (rocprofv3
+    FETCH_SIZE / WRITE_SIZE scaled by the copy calibration), or None when the
+    kernel's source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        f = line.split()
+        if len(f) < 2 or f[0] != "kernel" or f[1] != kernel:
+            continue
+        kv = dict(zip(f[2::2], f[3::2]))
+        src = os.path.join(ROOT, kv["source"])
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != kv["sha256"]:
+            return None
+        return (float(kv["fetch_kib"]) * 1024 * float(kv["fetch_factor"])
+                + float(kv["write_kib"]) * 1024 * float(kv["write_factor"]))
+    return None
+
+
 def energy_j():
     """Board energy counter in joules via amd-smi, or None if unavailable."""
     try:
@@ -178,9 +199,10 @@ def run_decode(args, tri):
         "tokens_per_s": n_tok / (total_ms / 1e3),
         "ms_per_step": total_ms / (reps * steps),
         "hbm_frac_step": step_bytes / (total_ms / 1e3 / (reps * steps)) / 1e9 / PEAK_HBM_GBS,
-        "roofline": {"kernel": "attn_decode (split-KV + combine)", "bound": "hbm",
+        "roofline": {"kernel": "attn_decode (split-KV partials; the LSE combine is a separate stage)",
+                     "bound": "hbm",
                      "achieved": attn_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": attn_gbs / PEAK_HBM_GBS, "traffic": None},
+                     "frac": attn_gbs / PEAK_HBM_GBS, "traffic": profiled_traffic("attn_decode")},
         "stages_ms_per_step": {k: v["total_ms"] / (reps * steps) for k, v in prof.items() if v["launches"]},
     }
     if e_start is not None and e_end is not None:
@@ -198,15 +220,26 @@ def main(argv=None):
     ap.add_argument("--decode-reps", type=int, default=5)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy 3 times (HBM counter calibration)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); "
               "the layer is not sharded across GPUs.", file=sys.stderr)
         return 2
     import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        n = 1 << 30
+        src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": n, "bytes_written": n, "launches": 3}))
+        return 0
     import paper_2606_29629_amd as tri
     from synth import make_cache, make_weights, make_x, workload
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
 
     wl = workload("dense_prefill")
     wb = make_weights(wl.cfg, wl.seed)
@@ -240,7 +273,9 @@ def main(argv=None):
         "layer_mfma_frac": flops / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
         "roofline": {"kernel": "gate_up (fused SwiGLU GEMM)", "bound": "mfma", "achieved": gu_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": gu_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": None},
+                     "traffic": profiled_traffic("gate_up"),
+                     "algorithmic_bytes": 2.0 * (T * wl.cfg.hidden + 2 * wl.cfg.ffn_dim * wl.cfg.hidden
+                                                 + T * wl.cfg.ffn_dim)},
         "stages_ms_per_step": {k: v["total_ms"] / args.steps for k, v in prof.items() if v["launches"]},
         "wall_s_timed": wall,
     }

@@ -95,11 +95,12 @@ Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
 // ------------------------------------------------------------ profiling --
 enum Stage {
   ST_TOKMAP, ST_NORM1, ST_QKV, ST_ATTN_PREFILL, ST_ATTN_DECODE, ST_OPROJ, ST_NORM2, ST_GATEUP,
-  ST_DOWN, ST_ROUTER, ST_MOE, ST_APPEND, ST_COUNT
+  ST_DOWN, ST_ROUTER, ST_MOE, ST_APPEND, ST_ATTN_COMBINE, ST_COUNT
 };
 const char* const kStageName[ST_COUNT] = {"token_map", "rmsnorm_attn", "qkv_rope", "attn_prefill",
                                           "attn_decode", "o_proj", "rmsnorm_mlp", "gate_up",
-                                          "down", "moe_router", "moe_ffn", "kv_append"};
+                                          "down", "moe_router", "moe_ffn", "kv_append",
+                                          "attn_combine"};
 
 struct Profiler {
   std::mutex mu;
@@ -237,9 +238,15 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
     TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, cache->n_slots, cache->max_seq,
                                 Hq, Hkv, D, 0, s));
   }
-  { StageTimer st_(ST_ATTN_DECODE, s);
-  TRI_HIP(launch_attn_decode(q, cache->k, cache->v, attn, part, bd, cache->n_slots,
-                             cache->max_seq, Hq, Hkv, D, s)); }
+  {
+    StageTimer st_(ST_ATTN_DECODE, s);
+    TRI_HIP(launch_attn_decode_split(q, cache->k, cache->v, part, bd, cache->n_slots,
+                                     cache->max_seq, Hq, Hkv, D, s));
+  }
+  {
+    StageTimer st_(ST_ATTN_COMBINE, s);
+    TRI_HIP(launch_attn_decode_combine(part, attn, bd, cache->n_slots, cache->max_seq, Hq, D, s));
+  }
 
   e = Epi{};
   e.kind = EPI_RESID;

@@ -219,31 +219,36 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(
   O[((int64_t)t * Hq + qh) * D + d] = f2bf(o / Lsum);
 }
 
-hipError_t launch_attn_decode(const void* q, const void* kc, const void* vc, void* out,
-                              float* part, const BatchDev& b, int n_slots, int max_seq,
-                              int n_q_heads, int n_kv_heads, int head_dim, hipStream_t s) {
+hipError_t launch_attn_decode_split(const void* q, const void* kc, const void* vc, float* part,
+                                    const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
+                                    int n_kv_heads, int head_dim, hipStream_t s) {
   if (b.n_seqs == 0) return hipSuccess;
   const int nsplit = attn_decode_splits(b.max_ctx_len + 1);
   const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)head_dim));
   dim3 grid(nsplit, n_kv_heads, b.n_seqs);
-  dim3 cgrid(b.n_seqs, n_q_heads);
-  if (head_dim == 128) {
+  if (head_dim == 128)
     attn_decode_kernel<128><<<grid, 256, 0, s>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vc,
                                                  part, b.cu_q, b.ctx_len, b.slot, n_slots, max_seq,
                                                  n_q_heads, n_kv_heads, nsplit, scale_log2e, b.n_tokens);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    attn_combine_kernel<128><<<cgrid, 128, 0, s>>>(part, (bf16*)out, b.cu_q, b.ctx_len, b.slot,
-                                                   n_slots, max_seq, n_q_heads, nsplit, b.n_tokens);
-  } else {
+  else
     attn_decode_kernel<64><<<grid, 256, 0, s>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vc,
                                                 part, b.cu_q, b.ctx_len, b.slot, n_slots, max_seq,
                                                 n_q_heads, n_kv_heads, nsplit, scale_log2e, b.n_tokens);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_decode_combine(const float* part, void* out, const BatchDev& b,
+                                      int n_slots, int max_seq, int n_q_heads, int head_dim,
+                                      hipStream_t s) {
+  if (b.n_seqs == 0) return hipSuccess;
+  const int nsplit = attn_decode_splits(b.max_ctx_len + 1);
+  dim3 cgrid(b.n_seqs, n_q_heads);
+  if (head_dim == 128)
+    attn_combine_kernel<128><<<cgrid, 128, 0, s>>>(part, (bf16*)out, b.cu_q, b.ctx_len, b.slot,
+                                                   n_slots, max_seq, n_q_heads, nsplit, b.n_tokens);
+  else
     attn_combine_kernel<64><<<cgrid, 64, 0, s>>>(part, (bf16*)out, b.cu_q, b.ctx_len, b.slot,
                                                  n_slots, max_seq, n_q_heads, nsplit, b.n_tokens);
-  }
   return hipGetLastError();
 }
 

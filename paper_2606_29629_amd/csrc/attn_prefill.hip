@@ -40,9 +40,19 @@ __device__ __forceinline__ int vt_slot(int kk) {
 // term spreads the transposing 2-byte stores (d = 8 ch + e, same e).
 __device__ __forceinline__ int vt_chunk(int pc, int d) { return pc ^ (d & 7) ^ ((d >> 3) & 7); }
 
+// K tile rows are D * 2 bytes.  With 64 four-byte banks, 16 lanes reading the
+// same chunk of 16 consecutive keys are conflict-free when the chunk is
+// XOR-ed with key % 16 (256-byte rows, D = 128) or with (key / 2) % 8
+// (128-byte rows, D = 64).
+template <int D>
+__device__ __forceinline__ int k_chunk_t(int ch, int key) {
+  return D == 128 ? (ch ^ (key & 15)) : (ch ^ ((key >> 1) & 7));
+}
+#define k_chunk(ch, key) k_chunk_t<D>(ch, key)
+
 template <int D>
 struct FaSmem {
-  bf16 k[2][kFaBK * D];  // [key][d], 16-byte chunks swizzled by key % 8
+  bf16 k[2][kFaBK * D];  // [key][d], 16-byte chunks swizzled by k_chunk
   f16 vt[2][D * kFaBK];  // V^T in fp16: [d][key slot], chunks swizzled by vt_chunk
 };
 
@@ -103,7 +113,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(
 #pragma unroll
     for (int i = 0; i < KLD; ++i) {
       const int id = tid + 256 * i, key = id / DC, ch = id % DC;
-      *(u32x4*)&sm.k[buf][key * D + ((ch ^ (key & 7)) * 8)] = rk[i];
+      *(u32x4*)&sm.k[buf][key * D + k_chunk(ch, key) * 8] = rk[i];
       Pack8 v;
       v.u = rv[i];
       const int slotk = (key & ~15) + vt_slot(key & 15);
@@ -137,7 +147,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(
 #pragma unroll
         for (int t = 0; t < DS; ++t) {
           const int ch = 2 * t + lg;
-          const bf16x8 kf = *(const bf16x8*)&sm.k[buf][key * D + ((ch ^ (key & 7)) * 8)];
+          const bf16x8 kf = *(const bf16x8*)&sm.k[buf][key * D + k_chunk(ch, key) * 8];
           sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t], sacc[kb], 0, 0, 0);
         }
       }

@@ -9,8 +9,8 @@
 // Tiling: BM x BN x 64 block tile, WGM x WGN waves (8 = 4 x 2: two waves per
 // SIMD, so one wave's LDS waits overlap the other's MFMAs), each wave a
 // (BM/WGM) x (BN/WGN) sub-tile of 32x32 MFMA blocks.  A and B tiles are staged through LDS, double
-// buffered, with 16-byte chunks XOR-swizzled by (row % 8) so that the eight
-// lanes of a ds_read_b128 phase hit distinct banks.  Tiles move from HBM to
+// buffered, with 16-byte chunks XOR-swizzled (see swz) so that fragment reads
+// are free of bank conflicts.  Tiles move from HBM to
 // LDS with buffer_load_dwordx4 ... lds (no register staging); the loads of
 // tile k+1 are in flight while the MFMAs of tile k run.
 //
@@ -28,7 +28,12 @@ constexpr int kChunks = kBK / 8;  // 16-byte chunks per tile row
 constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
 
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 7); }
+// LDS has 64 banks of 4 bytes (a 256-byte window).  A tile row is 128 bytes,
+// so rows r and r+1 share a window; a ds_read_b128 phase of 16 lanes reads the
+// same logical chunk of 16 consecutive rows.  XOR-ing the chunk with
+// (row / 2) % 8 gives the 8 even and the 8 odd rows 8 distinct 16-byte slots
+// each, i.e. all 16 slots of the window: no bank conflict.
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
 // Tile index for this block: XCD-contiguous ranges, then grouped-M order.
 __device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n, int& tm,
@@ -138,22 +143,24 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_kernel(const bf16* __rest
       __builtin_amdgcn_make_buffer_rsrc((void*)B, (short)0, (int)((int64_t)n_rows_b * ldb * 2), 0x00020000);
   // Global -> LDS without registers: each buffer_load_dwordx4 ... lds writes the
   // 64 lanes' 16 bytes to 1 KB of LDS in lane order, i.e. 8 tile rows.  Lane l
-  // fills physical chunk l % 8 of row l / 8 of its block, so it fetches the
-  // logical chunk (l % 8) ^ (row % 8) of that row (the swizzled layout).
+  // fills physical chunk l % 8 of row 8 b + l / 8 of its block b, so it fetches
+  // the logical chunk swz(row, l % 8) of that row (swz is an involution).
   constexpr int NW = NT / 64;
   constexpr int A_BLK = BM / 8 / NW, B_BLK = BN / 8 / NW;  // 1 KB blocks per wave per tile
   const int wv = __builtin_amdgcn_readfirstlane(wave);
-  const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
+  const int lrow = lane >> 3;
   uint32_t a_off[A_BLK], b_off[B_BLK];
 #pragma unroll
   for (int j = 0; j < A_BLK; ++j) {
-    const int gr = tm * BM + (wv + NW * j) * 8 + lrow;
-    a_off[j] = gr < M ? (uint32_t)(((int64_t)gr * lda + lchunk * 8) * 2) : 0x80000000u;
+    const int tr = (wv + NW * j) * 8 + lrow;  // tile row
+    const int gr = tm * BM + tr;
+    a_off[j] = gr < M ? (uint32_t)(((int64_t)gr * lda + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
 #pragma unroll
   for (int j = 0; j < B_BLK; ++j) {
-    const int gr = b_row_of<BN, WN>(EK, tn, (wv + NW * j) * 8 + lrow, epi.ffn);
-    b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + lchunk * 8) * 2) : 0x80000000u;
+    const int tr = (wv + NW * j) * 8 + lrow;
+    const int gr = b_row_of<BN, WN>(EK, tn, tr, epi.ffn);
+    b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
 
   f32x16 acc[MI][NI];

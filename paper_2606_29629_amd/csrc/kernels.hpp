@@ -77,9 +77,12 @@ hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, vo
 // Split-KV attention for sequences with q_len == 1, plus the combine.
 int attn_decode_splits(int max_kv);
 size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv);
-hipError_t launch_attn_decode(const void* q, const void* kc, const void* vc, void* out,
-                              float* part, const BatchDev& b, int n_slots, int max_seq,
-                              int n_q_heads, int n_kv_heads, int head_dim, hipStream_t s);
+hipError_t launch_attn_decode_split(const void* q, const void* kc, const void* vc, float* part,
+                                    const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
+                                    int n_kv_heads, int head_dim, hipStream_t s);
+hipError_t launch_attn_decode_combine(const float* part, void* out, const BatchDev& b,
+                                      int n_slots, int max_seq, int n_q_heads, int head_dim,
+                                      hipStream_t s);
 
 // MoE
 size_t moe_workspace_bytes(int n_tokens, int hidden, int n_experts, int top_k, int expert_ffn);
