@@ -137,7 +137,11 @@ typedef struct {
   size_t attn;   /* [T, Hq D] bf16  attention output                                */
   size_t x1;     /* [T, H]   bf16  x + attn W_o^T                                   */
   size_t h2;     /* [T, H]   bf16  RMSNorm(x1)                                      */
-  size_t act;    /* dense: [T, F] bf16 SwiGLU activation silu(g)*u                  */
+  size_t act;    /* dense: [T, F] bf16 SwiGLU activation silu(g)*u;
+                    MoE: [T*top_k, Fe] bf16, rows in routed order                  */
+  size_t perm;   /* MoE: [T*top_k] int32 routed order -> pair id t*top_k + j
+                    (pairs grouped by expert, ascending pair id within an expert)   */
+  size_t y;      /* MoE: [T*top_k, H] fp32 expert outputs, rows in routed order     */
   size_t total;  /* == tri_workspace_size()                                         */
 } tri_workspace_map;
 
@@ -185,8 +189,10 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
                               void* stream);
 
 /* MoE routing alone (test hook for bit-exact routing): logits = h2 W_r^T in
- * float32, softmax over all experts, top_k by logit (descending, ties to the
- * lower index), weights p[idx] (renormalised if TRI_F_MOE_RENORM).
+ * float32 (one fixed summation order per logit), softmax over all experts,
+ * top_k by logit (descending, ties to the lower index), weights p[idx]
+ * (renormalised if TRI_F_MOE_RENORM).  Inside the layer the router reads the
+ * bf16 h2 (widened exactly to float32).
  *  h2        device [n_tokens, H] float32
  *  w_router  device [E, H] bf16
  *  idx, w    device [n_tokens, top_k] int32 / float32                          */

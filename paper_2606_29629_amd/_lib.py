@@ -47,7 +47,8 @@ class BatchStruct(ctypes.Structure):
 
 
 class WorkspaceMap(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_size_t) for n in ("h", "q", "attn", "x1", "h2", "act", "total")]
+    _fields_ = [(n, ctypes.c_size_t) for n in ("h", "q", "attn", "x1", "h2", "act", "perm", "y",
+                                                "total")]
 
 
 class Profile(ctypes.Structure):

@@ -1,6 +1,6 @@
 // libtri C ABI: host-side validation, workspace layout and the launch
 // sequences of the decoder layer.  No kernel is launched unless every check
-// passes; nothing is allocated.
+// passes; no device memory is allocated.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <string.h>
@@ -22,6 +22,8 @@ inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 // Projections with at most this many rows take the weight-streaming path.
 constexpr int kSkinnyMaxRows = 128;
 
+bool is_moe(const tri_layer_config* c) { return (c->flags & TRI_F_MOE) != 0; }
+
 tri_status check_config(const tri_layer_config* c) {
   if (!c) return TRI_ERR_NULL;
   if (c->dtype != TRI_BF16) return TRI_ERR_UNSUPPORTED;
@@ -34,11 +36,10 @@ tri_status check_config(const tri_layer_config* c) {
   if (c->n_q_heads / c->n_kv_heads > 8) return TRI_ERR_UNSUPPORTED;
   if ((int64_t)c->n_q_heads * c->head_dim % 64 != 0) return TRI_ERR_UNSUPPORTED;
   if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return TRI_ERR_RANGE;
-  if (c->flags & TRI_F_MOE) {
+  if (is_moe(c)) {
     if (c->n_experts < 1 || c->n_experts > 256) return TRI_ERR_UNSUPPORTED;
     if (c->top_k < 1 || c->top_k > c->n_experts || c->top_k > 16) return TRI_ERR_SHAPE;
     if (c->expert_ffn_dim <= 0 || c->expert_ffn_dim % 64 != 0) return TRI_ERR_UNSUPPORTED;
-    return TRI_ERR_UNSUPPORTED;  // MoE FFN not built into this library version
   } else {
     if (c->ffn_dim <= 0 || c->ffn_dim % 64 != 0) return TRI_ERR_UNSUPPORTED;
   }
@@ -57,7 +58,10 @@ tri_status check_batch_scalars(const tri_batch* b) {
 }
 
 struct Layout {
-  size_t tok_slot, tok_row, rope, h, q, attn, x1, h2, act, part, total;
+  size_t tok_slot, tok_row, rope, h, q, attn, x1, h2, act, part;
+  // MoE (n_pairs = T * top_k)
+  size_t route_idx, route_w, rank, counts, perm, inv, seg, tile_off, y;
+  size_t total;
 };
 
 size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
@@ -65,18 +69,25 @@ size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
   const int Nqkv = (c->n_q_heads + 2 * c->n_kv_heads) * D;
   size_t p = attn_decode_partial_bytes(T, c->n_q_heads, D, b->max_ctx_len + 1);
   if (T > 0 && T <= kSkinnyMaxRows) {
+    auto mx = [](size_t a, size_t b2) { return a > b2 ? a : b2; };
     size_t g = gemv_partial_bytes(T, Nqkv, H);
-    g = g > gemv_partial_bytes(T, H, c->n_q_heads * D) ? g : gemv_partial_bytes(T, H, c->n_q_heads * D);
-    g = g > gemv_partial_bytes(T, 2 * c->ffn_dim, H) ? g : gemv_partial_bytes(T, 2 * c->ffn_dim, H);
-    g = g > gemv_partial_bytes(T, H, c->ffn_dim) ? g : gemv_partial_bytes(T, H, c->ffn_dim);
-    p = p > g ? p : g;
+    g = mx(g, gemv_partial_bytes(T, H, c->n_q_heads * D));
+    if (!is_moe(c)) {
+      g = mx(g, gemv_partial_bytes(T, 2 * c->ffn_dim, H));
+      g = mx(g, gemv_partial_bytes(T, H, c->ffn_dim));
+    }
+    p = mx(p, g);
   }
   return p;
 }
 
 Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
   const size_t T = (size_t)b->n_tokens, H = c->hidden, D = c->head_dim;
-  Layout l;
+  const bool moe = is_moe(c);
+  const size_t P = moe ? T * c->top_k : 0, E = moe ? c->n_experts : 0;
+  const size_t act_cols = moe ? (size_t)c->expert_ffn_dim : (size_t)c->ffn_dim;
+  const size_t act_rows = moe ? P : T;
+  Layout l{};
   size_t o = 0;
   l.tok_slot = o; o += up(T * 4);
   l.tok_row = o;  o += up(T * 4);
@@ -86,21 +97,32 @@ Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
   l.attn = o;     o += up(T * c->n_q_heads * D * 2);
   l.x1 = o;       o += up(T * H * 2);
   l.h2 = o;       o += up(T * H * 2);
-  l.act = o;      o += up(T * (size_t)c->ffn_dim * 2);
+  l.act = o;      o += up(act_rows * act_cols * 2);
   l.part = o;     o += up(part_bytes(c, b));
+  l.route_idx = o; o += up(P * 4);
+  l.route_w = o;  o += up(P * 4);
+  l.rank = o;     o += up(P * 4);
+  l.counts = o;   o += up(E * 4);
+  l.perm = o;     o += up(P * 4);
+  l.inv = o;      o += up(P * 4);
+  l.seg = o;      o += up((E + 1) * 4);
+  l.tile_off = o; o += up((E + 1) * 4);
+  l.y = o;        o += up(P * H * 4);
   l.total = o;
   return l;
 }
 
 // ------------------------------------------------------------ profiling --
 enum Stage {
-  ST_TOKMAP, ST_NORM1, ST_QKV, ST_ATTN_PREFILL, ST_ATTN_DECODE, ST_OPROJ, ST_NORM2, ST_GATEUP,
-  ST_DOWN, ST_ROUTER, ST_MOE, ST_APPEND, ST_ATTN_COMBINE, ST_COUNT
+  ST_TOKMAP, ST_NORM1, ST_QKV, ST_ATTN_PREFILL, ST_ATTN_DECODE, ST_ATTN_COMBINE, ST_OPROJ,
+  ST_NORM2, ST_GATEUP, ST_DOWN, ST_ROUTER, ST_MOE_PERMUTE, ST_MOE_GATEUP, ST_MOE_DOWN,
+  ST_MOE_COMBINE, ST_APPEND, ST_COUNT
 };
-const char* const kStageName[ST_COUNT] = {"token_map", "rmsnorm_attn", "qkv_rope", "attn_prefill",
-                                          "attn_decode", "o_proj", "rmsnorm_mlp", "gate_up",
-                                          "down", "moe_router", "moe_ffn", "kv_append",
-                                          "attn_combine"};
+static_assert(ST_COUNT <= TRI_MAX_STAGES, "too many stages");
+const char* const kStageName[ST_COUNT] = {
+    "token_map", "rmsnorm_attn", "qkv_rope", "attn_prefill", "attn_decode", "attn_combine",
+    "o_proj", "rmsnorm_mlp", "gate_up", "down", "moe_router", "moe_permute", "moe_gate_up",
+    "moe_down", "moe_combine", "kv_append"};
 
 struct Profiler {
   std::mutex mu;
@@ -144,9 +166,9 @@ struct StageTimer {
 template <typename T>
 T* at(void* ws, size_t off) { return (T*)((char*)ws + off); }
 
-#define TRI_HIP(expr)                         \
-  do {                                        \
-    if ((expr) != hipSuccess) return TRI_ERR_HIP; \
+#define TRI_HIP(expr)                              \
+  do {                                             \
+    if ((expr) != hipSuccess) return TRI_ERR_HIP;  \
   } while (0)
 
 tri_status run_linear(const void* A, int lda, const void* B, int M, int N, int K, const Epi& epi,
@@ -164,8 +186,6 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weights* w,
                  const tri_kv_cache* cache, const tri_batch* b, const void* x_in, void* x_out,
                  int32_t* route_idx, float* route_w, void* ws, size_t ws_bytes, void* stream) {
-  (void)route_idx;
-  (void)route_w;
   tri_status st = check_config(cfg);
   if (st != TRI_OK) return st;
   if (!w || !cache) return TRI_ERR_NULL;
@@ -176,6 +196,8 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   if (!cache->k || !cache->v) return TRI_ERR_NULL;
   if (!w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up || !w->w_down)
     return TRI_ERR_NULL;
+  const bool moe = is_moe(cfg);
+  if (moe && !w->w_router) return TRI_ERR_NULL;
   const bool bias = (cfg->flags & TRI_F_QKV_BIAS) != 0;
   if (bias && !w->b_qkv) return TRI_ERR_NULL;
   if (cache->n_slots <= 0 || cache->max_seq <= 0) return TRI_ERR_SHAPE;
@@ -186,6 +208,7 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   for (const void* p : ptrs)
     if (!aligned16(p)) return TRI_ERR_ALIGN;
   if (bias && !aligned16(w->b_qkv)) return TRI_ERR_ALIGN;
+  if (moe && !aligned16(w->w_router)) return TRI_ERR_ALIGN;
   if (((uintptr_t)ws & (kAlign - 1)) != 0) return TRI_ERR_ALIGN;
   const Layout L = layout_of(cfg, b);
   if (ws_bytes < L.total) return TRI_ERR_WORKSPACE;
@@ -211,12 +234,15 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   void* act = at<void>(ws, L.act);
   float* part = at<float>(ws, L.part);
 
-  { StageTimer st_(ST_TOKMAP, s);
-  TRI_HIP(launch_token_map(bd, cache->n_slots, cache->max_seq, D, cfg->rope_base, tok_slot,
-                           tok_row, rope, s)); }
-  { StageTimer st_(ST_NORM1, s);
-  TRI_HIP(launch_rmsnorm(x_in, w->attn_norm, h, nullptr, T, H, cfg->rms_eps, s)); }
-
+  {
+    StageTimer t_(ST_TOKMAP, s);
+    TRI_HIP(launch_token_map(bd, cache->n_slots, cache->max_seq, D, cfg->rope_base, tok_slot,
+                             tok_row, rope, s));
+  }
+  {
+    StageTimer t_(ST_NORM1, s);
+    TRI_HIP(launch_rmsnorm(x_in, w->attn_norm, h, nullptr, T, H, cfg->rms_eps, s));
+  }
   Epi e{};
   e.kind = EPI_QKV;
   e.bias = bias ? w->b_qkv : nullptr;
@@ -230,52 +256,105 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   e.n_kv_heads = Hkv;
   e.head_dim = D;
   e.max_seq = cache->max_seq;
-  { StageTimer st_(ST_QKV, s);
-  if ((st = run_linear(h, H, w->w_qkv, T, Nqkv, H, e, part, s)) != TRI_OK) return st; }
-
+  {
+    StageTimer t_(ST_QKV, s);
+    if ((st = run_linear(h, H, w->w_qkv, T, Nqkv, H, e, part, s)) != TRI_OK) return st;
+  }
   if (!decode && b->max_q_len > 1) {
-    StageTimer st_(ST_ATTN_PREFILL, s);
+    StageTimer t_(ST_ATTN_PREFILL, s);
     TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, cache->n_slots, cache->max_seq,
                                 Hq, Hkv, D, 0, s));
   }
   {
-    StageTimer st_(ST_ATTN_DECODE, s);
+    StageTimer t_(ST_ATTN_DECODE, s);
     TRI_HIP(launch_attn_decode_split(q, cache->k, cache->v, part, bd, cache->n_slots,
                                      cache->max_seq, Hq, Hkv, D, s));
   }
   {
-    StageTimer st_(ST_ATTN_COMBINE, s);
+    StageTimer t_(ST_ATTN_COMBINE, s);
     TRI_HIP(launch_attn_decode_combine(part, attn, bd, cache->n_slots, cache->max_seq, Hq, D, s));
   }
-
   e = Epi{};
   e.kind = EPI_RESID;
   e.out = x1;
   e.ldo = H;
   e.resid = x_in;
   e.ldr = H;
-  { StageTimer st_(ST_OPROJ, s);
-  if ((st = run_linear(attn, Hq * D, w->w_o, T, H, Hq * D, e, part, s)) != TRI_OK) return st; }
+  {
+    StageTimer t_(ST_OPROJ, s);
+    if ((st = run_linear(attn, Hq * D, w->w_o, T, H, Hq * D, e, part, s)) != TRI_OK) return st;
+  }
+  {
+    StageTimer t_(ST_NORM2, s);
+    TRI_HIP(launch_rmsnorm(x1, w->mlp_norm, h2, nullptr, T, H, cfg->rms_eps, s));
+  }
 
-  { StageTimer st_(ST_NORM2, s);
-  TRI_HIP(launch_rmsnorm(x1, w->mlp_norm, h2, nullptr, T, H, cfg->rms_eps, s)); }
+  if (!moe) {
+    e = Epi{};
+    e.kind = EPI_SWIGLU;
+    e.out = act;
+    e.ldo = F;
+    e.ffn = F;
+    {
+      StageTimer t_(ST_GATEUP, s);
+      if ((st = run_linear(h2, H, w->w_gate_up, T, 2 * F, H, e, part, s)) != TRI_OK) return st;
+    }
+    e = Epi{};
+    e.kind = EPI_RESID;
+    e.out = x_out;
+    e.ldo = H;
+    e.resid = x1;
+    e.ldr = H;
+    {
+      StageTimer t_(ST_DOWN, s);
+      if ((st = run_linear(act, F, w->w_down, T, H, F, e, part, s)) != TRI_OK) return st;
+    }
+    return TRI_OK;
+  }
 
+  // ---- mixture of experts
+  const int E = cfg->n_experts, k = cfg->top_k, Fe = cfg->expert_ffn_dim;
+  const int P = T * k;
+  int32_t* idx = route_idx ? route_idx : at<int32_t>(ws, L.route_idx);
+  float* rw = route_w ? route_w : at<float>(ws, L.route_w);
+  int32_t* perm = at<int32_t>(ws, L.perm);
+  int32_t* inv = at<int32_t>(ws, L.inv);
+  int32_t* seg = at<int32_t>(ws, L.seg);
+  int32_t* tile_off = at<int32_t>(ws, L.tile_off);
+  float* y = at<float>(ws, L.y);
+  {
+    StageTimer t_(ST_ROUTER, s);
+    TRI_HIP(launch_moe_route_bf16(h2, w->w_router, T, H, E, k,
+                                  (cfg->flags & TRI_F_MOE_RENORM) ? 1 : 0, idx, rw, s));
+  }
+  {
+    StageTimer t_(ST_MOE_PERMUTE, s);
+    TRI_HIP(launch_moe_permute(idx, P, E, moe_tile_rows(P, E), at<int32_t>(ws, L.rank),
+                               at<int32_t>(ws, L.counts), perm, inv, seg, tile_off, s));
+  }
   e = Epi{};
   e.kind = EPI_SWIGLU;
   e.out = act;
-  e.ldo = F;
-  e.ffn = F;
-  { StageTimer st_(ST_GATEUP, s);
-  if ((st = run_linear(h2, H, w->w_gate_up, T, 2 * F, H, e, part, s)) != TRI_OK) return st; }
-
+  e.ldo = Fe;
+  e.ffn = Fe;
+  {
+    StageTimer t_(ST_MOE_GATEUP, s);
+    TRI_HIP(launch_gemm_grouped(h2, H, T, perm, k, w->w_gate_up, (int64_t)2 * Fe * H, 2 * Fe, H,
+                                seg, tile_off, E, P, e, s));
+  }
   e = Epi{};
-  e.kind = EPI_RESID;
-  e.out = x_out;
+  e.kind = EPI_STORE_F32;
+  e.out = y;
   e.ldo = H;
-  e.resid = x1;
-  e.ldr = H;
-  { StageTimer st_(ST_DOWN, s);
-  if ((st = run_linear(act, F, w->w_down, T, H, F, e, part, s)) != TRI_OK) return st; }
+  {
+    StageTimer t_(ST_MOE_DOWN, s);
+    TRI_HIP(launch_gemm_grouped(act, Fe, P, nullptr, k, w->w_down, (int64_t)H * Fe, H, Fe, seg,
+                                tile_off, E, P, e, s));
+  }
+  {
+    StageTimer t_(ST_MOE_COMBINE, s);
+    TRI_HIP(launch_moe_combine(x1, y, inv, rw, T, H, k, x_out, s));
+  }
   return TRI_OK;
 }
 
@@ -305,6 +384,8 @@ tri_status tri_workspace_layout(const tri_layer_config* cfg, const tri_batch* ba
   map->x1 = l.x1;
   map->h2 = l.h2;
   map->act = l.act;
+  map->perm = l.perm;
+  map->y = l.y;
   map->total = l.total;
   return TRI_OK;
 }
@@ -345,7 +426,7 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
     if (!aligned16(p)) return TRI_ERR_ALIGN;
   BatchDev bd{b->cu_q, b->ctx_len, b->slot, b->pos, b->n_seqs, b->n_tokens, b->max_q_len,
               b->max_ctx_len};
-  StageTimer st_(ST_APPEND, (hipStream_t)stream);
+  StageTimer t_(ST_APPEND, (hipStream_t)stream);
   TRI_HIP(launch_kv_append_direct(bd, cache->n_slots, cache->max_seq, cfg->n_kv_heads,
                                   cfg->head_dim, k_new, v_new, cache->k, cache->v,
                                   (hipStream_t)stream));
@@ -354,12 +435,18 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
 
 tri_status tri_moe_route(const tri_layer_config* cfg, const float* h2, const void* w_router,
                          int32_t n_tokens, int32_t* idx, float* w, void* stream) {
-  (void)stream;
-  if (!cfg) return TRI_ERR_NULL;
+  tri_status st = check_config(cfg);
+  if (st != TRI_OK) return st;
+  if (!is_moe(cfg)) return TRI_ERR_SHAPE;
   if (n_tokens < 0) return TRI_ERR_SHAPE;
-  if (!(cfg->flags & TRI_F_MOE)) return TRI_ERR_SHAPE;
-  if (n_tokens > 0 && (!h2 || !w_router || !idx || !w)) return TRI_ERR_NULL;
-  return TRI_ERR_UNSUPPORTED;
+  if (n_tokens == 0) return TRI_OK;
+  if (!h2 || !w_router || !idx || !w) return TRI_ERR_NULL;
+  if (!aligned16(h2) || !aligned16(w_router)) return TRI_ERR_ALIGN;
+  StageTimer t_(ST_ROUTER, (hipStream_t)stream);
+  TRI_HIP(launch_moe_route_f32(h2, w_router, n_tokens, cfg->hidden, cfg->n_experts, cfg->top_k,
+                               (cfg->flags & TRI_F_MOE_RENORM) ? 1 : 0, idx, w,
+                               (hipStream_t)stream));
+  return TRI_OK;
 }
 
 tri_status tri_profile_enable(int32_t on) {
@@ -414,6 +501,6 @@ const char* tri_status_string(tri_status s) {
   return "unknown status";
 }
 
-int32_t tri_version(void) { return 100; }
+int32_t tri_version(void) { return 200; }
 
 }  // extern "C"

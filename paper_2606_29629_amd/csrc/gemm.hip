@@ -1,30 +1,36 @@
-// Prefill GEMM on the matrix cores: C[M,N] = A[M,K] B[N,K]^T, bf16 operands,
+// Prefill GEMMs on the matrix cores: C[M,N] = A[M,K] B[N,K]^T, bf16 operands,
 // fp32 accumulation, with the layer's epilogues fused (residual add, SwiGLU,
-// q/k/v split + rotary embedding + KV-cache write).
+// q/k/v split + rotary embedding + KV-cache write, fp32 store).
 //
 // Both operands are K-contiguous ("nn.Linear" weights [out, in] and row-major
 // activations), which is the native operand layout of v_mfma_f32_32x32x16_bf16:
 // lane l supplies row (l % 32) and 8 consecutive k of slice (l / 32).
 //
-// Tiling: BM x BN x 64 block tile, WGM x WGN waves (8 = 4 x 2: two waves per
-// SIMD, so one wave's LDS waits overlap the other's MFMAs), each wave a
-// (BM/WGM) x (BN/WGN) sub-tile of 32x32 MFMA blocks.  A and B tiles are staged through LDS, double
+// Tiling: BM x BN x 64 block tile, WGM x WGN waves (two waves per SIMD, so one
+// wave's LDS waits overlap the other's MFMAs), each wave a (BM/WGM) x (BN/WGN)
+// sub-tile of 32x32 MFMA blocks.  A and B tiles are staged through LDS, double
 // buffered, with 16-byte chunks XOR-swizzled (see swz) so that fragment reads
-// are free of bank conflicts.  Tiles move from HBM to
-// LDS with buffer_load_dwordx4 ... lds (no register staging); the loads of
-// tile k+1 are in flight while the MFMAs of tile k run.
+// are free of bank conflicts.  Tiles move from HBM to LDS with
+// buffer_load_dwordx4 ... lds (no register staging); the loads of tile k+1
+// are in flight while the MFMAs of tile k run.
 //
-// Work distribution: workgroups are dispatched round-robin over the 8 XCDs;
-// the linear block id is remapped so each XCD owns a contiguous range of
-// tiles, walked in groups of 8 M-tiles so co-resident tiles share A and B
-// panels in that XCD's L2.
+// Dense kernel: workgroups are dispatched round-robin over the 8 XCDs; the
+// linear block id is remapped so each XCD owns a contiguous range of tiles,
+// walked in groups of 8 M-tiles so co-resident tiles share A and B panels in
+// that XCD's L2.
+//
+// Grouped kernel (mixture of experts): the rows of each expert are a
+// contiguous segment of the routed (permuted) order; a device-side tile table
+// maps every M-tile to its expert, A rows are gathered through the
+// permutation, and B is that expert's weight matrix.  The grid is sized from
+// an upper bound on the tile count and surplus workgroups exit, so no count is
+// read back to the host.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace tri {
 
 constexpr int kBK = 64;
-constexpr int kChunks = kBK / 8;  // 16-byte chunks per tile row
 constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
 
@@ -67,6 +73,120 @@ __device__ __forceinline__ int b_row_of(int kind, int tn, int nt, int ffn) {
     return w < WN / 2 ? f : ffn + f;
   }
   return tn * BN + nt;
+}
+
+// The shared K loop.  a_off / b_off: byte offset (within the buffer) of chunk
+// swz(row, lane % 8) of this lane's row in each of its 1 KB LDS blocks (at or
+// beyond the buffer size for rows that must read as zero).
+template <int BM, int BN, int WGM, int WGN>
+struct Mainloop {
+  static constexpr int NT = WGM * WGN * 64;
+  static constexpr int NW = NT / 64;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
+  static constexpr int MI = WM / 32, NI = WN / 32;
+  static constexpr int A_BLK = BM / 8 / NW, B_BLK = BN / 8 / NW;  // 1 KB blocks per wave
+
+  __device__ __forceinline__ static void run(GemmSmem<BM, BN>& sm, __amdgpu_buffer_rsrc_t ra,
+                                             const uint32_t (&a_off)[A_BLK],
+                                             __amdgpu_buffer_rsrc_t rb,
+                                             const uint32_t (&b_off)[B_BLK], int K, int wv,
+                                             int lane, f32x16 (&acc)[MI][NI]) {
+    const int wm = wv / WGN, wn = wv % WGN;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{0.f};
+    auto gload = [&](int kt, int buf) {
+      const int kb = kt * kBK * 2;
+#pragma unroll
+      for (int j = 0; j < A_BLK; ++j)
+        buffer_load_lds16(ra, &sm.a[buf][(wv + NW * j) * 8 * kBK], a_off[j], kb);
+#pragma unroll
+      for (int j = 0; j < B_BLK; ++j)
+        buffer_load_lds16(rb, &sm.b[buf][(wv + NW * j) * 8 * kBK], b_off[j], kb);
+    };
+    const int KT = K / kBK;
+    const int lr = lane & 31, lg = lane >> 5;
+    gload(0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    for (int kt = 0; kt < KT; ++kt) {
+      const int buf = kt & 1;
+      if (kt + 1 < KT) gload(kt + 1, buf ^ 1);  // lands in the other buffer meanwhile
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        const int ch = kk * 2 + lg;
+        bf16x8 af[MI], bfr[NI];
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int r = wm * WM + i * 32 + lr;
+          af[i] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
+        }
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+          const int r = wn * WN + j * 32 + lr;
+          bfr[j] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
+        }
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int j = 0; j < NI; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+    }
+  }
+};
+
+// Accumulator element r of block (i, j): row 32i + 8(r/4) + 4(lane/32) + r%4,
+// column 32j + lane%32 of the wave sub-tile.  row0 = output row of the wave's
+// first accumulator row (including 4 * (lane / 32)); rows >= row_lim are
+// not written.
+template <int MI, int NI, int EK>
+__device__ __forceinline__ void plain_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
+                                               int row0, int row_lim, int col0, int N) {
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int col = col0 + 32 * j;
+      if (col >= N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
+        if (row >= row_lim) continue;
+        float v = acc[i][j][r];
+        if constexpr (EK == EPI_STORE_F32) {
+          ((float*)epi.out)[(int64_t)row * epi.ldo + col] = v;
+        } else {
+          if constexpr (EK == EPI_RESID)
+            v += bf2f(((const bf16*)epi.resid)[(int64_t)row * epi.ldr + col]);
+          ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(v);
+        }
+      }
+    }
+}
+
+// SwiGLU: blocks j < NI/2 hold gate, j + NI/2 the matching up; f0 = output
+// column (intermediate index) of block 0 for this lane.
+template <int MI, int NI>
+__device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
+                                                int row0, int row_lim, int f0) {
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI / 2; ++j) {
+      const int f = f0 + 32 * j;
+      if (f >= epi.ffn) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
+        if (row >= row_lim) continue;
+        const float gt = acc[i][j][r], up = acc[i][j + NI / 2][r];
+        ((bf16*)epi.out)[(int64_t)row * epi.ldo + f] = f2bf(silu(gt) * up);
+      }
+    }
 }
 
 // q/k/v split + bias + rotary embedding + KV-cache write on the accumulators.
@@ -124,14 +244,14 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_kernel(const bf16* __rest
                                                    const bf16* __restrict__ B, int ldb, int M,
                                                    int N, int K, Epi epi, int tiles_m,
                                                    int tiles_n) {
-  constexpr int NT = WGM * WGN * 64;        // threads
-  constexpr int WM = BM / WGM, WN = BN / WGN;
-  constexpr int MI = WM / 32, NI = WN / 32;
+  using ML = Mainloop<BM, BN, WGM, WGN>;
+  constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
   extern __shared__ __align__(16) char smem_raw[];
   GemmSmem<BM, BN>& sm = *reinterpret_cast<GemmSmem<BM, BN>*>(smem_raw);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wv / WGN, wn = wv % WGN;
   int tm, tn;
   tile_of_block(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int n_rows_b = EK == EPI_SWIGLU ? 2 * epi.ffn : N;
@@ -145,115 +265,107 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_kernel(const bf16* __rest
   // 64 lanes' 16 bytes to 1 KB of LDS in lane order, i.e. 8 tile rows.  Lane l
   // fills physical chunk l % 8 of row 8 b + l / 8 of its block b, so it fetches
   // the logical chunk swz(row, l % 8) of that row (swz is an involution).
-  constexpr int NW = NT / 64;
-  constexpr int A_BLK = BM / 8 / NW, B_BLK = BN / 8 / NW;  // 1 KB blocks per wave per tile
-  const int wv = __builtin_amdgcn_readfirstlane(wave);
   const int lrow = lane >> 3;
-  uint32_t a_off[A_BLK], b_off[B_BLK];
+  uint32_t a_off[ML::A_BLK], b_off[ML::B_BLK];
 #pragma unroll
-  for (int j = 0; j < A_BLK; ++j) {
+  for (int j = 0; j < ML::A_BLK; ++j) {
     const int tr = (wv + NW * j) * 8 + lrow;  // tile row
     const int gr = tm * BM + tr;
     a_off[j] = gr < M ? (uint32_t)(((int64_t)gr * lda + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
 #pragma unroll
-  for (int j = 0; j < B_BLK; ++j) {
+  for (int j = 0; j < ML::B_BLK; ++j) {
     const int tr = (wv + NW * j) * 8 + lrow;
     const int gr = b_row_of<BN, WN>(EK, tn, tr, epi.ffn);
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
-
   f32x16 acc[MI][NI];
-#pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{0.f};
+  ML::run(sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
 
-  auto gload = [&](int kt, int buf) {
-    const int kb = kt * kBK * 2;
-#pragma unroll
-    for (int j = 0; j < A_BLK; ++j)
-      buffer_load_lds16(rsrc_a, &sm.a[buf][(wv + NW * j) * 8 * kBK], a_off[j], kb);
-#pragma unroll
-    for (int j = 0; j < B_BLK; ++j)
-      buffer_load_lds16(rsrc_b, &sm.b[buf][(wv + NW * j) * 8 * kBK], b_off[j], kb);
-  };
-
-  const int KT = K / kBK;
   const int lr = lane & 31, lg = lane >> 5;
-  gload(0, 0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1, buf ^ 1);  // lands in the other buffer meanwhile
-#pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      const int ch = kk * 2 + lg;
-      bf16x8 af[MI], bfr[NI];
-#pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int r = wm * WM + i * 32 + lr;
-        af[i] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
-      }
-#pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        const int r = wn * WN + j * 32 + lr;
-        bfr[j] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
-      }
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-  }
-
-  // ---------------------------------------------------------------- epilogue
-  // Accumulator element r of block (i, j): row 32i + 8(r/4) + 4(lane/32) + r%4,
-  // column 32j + lane%32 of the wave sub-tile.
   const int row0 = tm * BM + wm * WM + 4 * lg;
-  if constexpr (EK == EPI_STORE || EK == EPI_RESID) {
-    const int col0 = tn * BN + wn * WN + lr;
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        const int col = col0 + 32 * j;
-        if (col >= N) continue;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
-          if (row >= M) continue;
-          float v = acc[i][j][r];
-          if constexpr (EK == EPI_RESID)
-            v += bf2f(((const bf16*)epi.resid)[(int64_t)row * epi.ldr + col]);
-          ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(v);
-        }
-      }
+  if constexpr (EK == EPI_STORE || EK == EPI_RESID || EK == EPI_STORE_F32) {
+    plain_epilogue<MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + lr, N);
   } else if constexpr (EK == EPI_SWIGLU) {
-    const int f0 = tn * (BN / 2) + wn * (WN / 2) + lr;
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int j = 0; j < NI / 2; ++j) {
-        const int f = f0 + 32 * j;
-        if (f >= epi.ffn) continue;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
-          if (row >= M) continue;
-          const float gt = acc[i][j][r], up = acc[i][j + NI / 2][r];
-          ((bf16*)epi.out)[(int64_t)row * epi.ldo + f] = f2bf(silu(gt) * up);
-        }
-      }
+    swiglu_epilogue<MI, NI>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + lr);
   } else if (epi.head_dim == 128) {
-    qkv_epilogue<MI, NI, 2>(acc, epi, tm * BM + wm * WM + 4 * lg, tn * BN + wn * WN + lr, M, N);
+    qkv_epilogue<MI, NI, 2>(acc, epi, row0, tn * BN + wn * WN + lr, M, N);
   } else {
-    qkv_epilogue<MI, NI, 1>(acc, epi, tm * BM + wm * WM + 4 * lg, tn * BN + wn * WN + lr, M, N);
+    qkv_epilogue<MI, NI, 1>(acc, epi, row0, tn * BN + wn * WN + lr, M, N);
   }
+}
+
+// Grouped expert GEMM.  Rows [seg[e], seg[e+1]) of the routed order belong to
+// expert e; tile_off[e] .. tile_off[e+1]-1 are its M-tiles (BM rows each).  For
+// the gate/up pass (EPI_SWIGLU) A row p is token perm[p] / top_k of A; for the
+// down pass (EPI_STORE_F32) A row p is row p of A.  B of expert e starts at
+// B + e * b_stride elements.  Output row = routed position p.
+template <int BM, int BN, int WGM, int WGN, int EK>
+__global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
+    const bf16* __restrict__ A, int lda, int a_rows, const int32_t* __restrict__ perm, int top_k,
+    const bf16* __restrict__ B, int64_t b_stride, int N, int K,
+    const int32_t* __restrict__ seg, const int32_t* __restrict__ tile_off, int n_experts,
+    int tiles_n, Epi epi) {
+  using ML = Mainloop<BM, BN, WGM, WGN>;
+  constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
+  extern __shared__ __align__(16) char smem_raw[];
+  GemmSmem<BM, BN>& sm = *reinterpret_cast<GemmSmem<BM, BN>*>(smem_raw);
+
+  const int tn = blockIdx.x % tiles_n, mt = blockIdx.x / tiles_n;
+  if (mt >= tile_off[n_experts]) return;  // surplus tile
+  int lo = 0, hi = n_experts;             // expert e with tile_off[e] <= mt < tile_off[e+1]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (tile_off[mid] <= mt) lo = mid; else hi = mid;
+  }
+  const int e = lo;
+  const int p0 = seg[e] + (mt - tile_off[e]) * BM;  // first routed row of this tile
+  const int p_end = seg[e + 1];
+  const int n_rows_b = EK == EPI_SWIGLU ? 2 * epi.ffn : N;
+
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wv / WGN, wn = wv % WGN;
+  const __amdgpu_buffer_rsrc_t rsrc_a =
+      __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)((int64_t)a_rows * lda * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc_b = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(B + (int64_t)e * b_stride), (short)0, (int)((int64_t)n_rows_b * K * 2), 0x00020000);
+  const int lrow = lane >> 3;
+  uint32_t a_off[ML::A_BLK], b_off[ML::B_BLK];
+#pragma unroll
+  for (int j = 0; j < ML::A_BLK; ++j) {
+    const int tr = (wv + NW * j) * 8 + lrow;
+    const int p = p0 + tr;
+    int src = -1;
+    if (p < p_end) src = perm ? perm[p] / top_k : p;
+    a_off[j] = (src >= 0 && src < a_rows)
+                   ? (uint32_t)(((int64_t)src * lda + swz(tr, lane & 7) * 8) * 2)
+                   : 0x80000000u;
+  }
+#pragma unroll
+  for (int j = 0; j < ML::B_BLK; ++j) {
+    const int tr = (wv + NW * j) * 8 + lrow;
+    const int gr = b_row_of<BN, WN>(EK, tn, tr, epi.ffn);
+    b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * K + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
+  }
+  f32x16 acc[MI][NI];
+  ML::run(sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
+
+  const int lr = lane & 31, lg = lane >> 5;
+  const int row0 = p0 + wm * WM + 4 * lg;
+  if constexpr (EK == EPI_SWIGLU)
+    swiglu_epilogue<MI, NI>(acc, epi, row0, p_end, tn * (BN / 2) + wn * (WN / 2) + lr);
+  else
+    plain_epilogue<MI, NI, EK>(acc, epi, row0, p_end, tn * BN + wn * WN + lr, N);
+}
+
+template <typename Kern>
+static hipError_t opt_in_lds(Kern k, size_t smem, bool& done) {
+  if (done) return hipSuccess;  // one-time opt-in to > 64 KB of LDS
+  hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)smem);
+  if (e == hipSuccess) done = true;
+  return e;
 }
 
 template <int BM, int BN, int WGM, int WGN, int EK>
@@ -262,13 +374,9 @@ static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M
   const int tiles_m = cdiv(M, BM);
   const int tiles_n = EK == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
   const size_t smem = sizeof(GemmSmem<BM, BN>);
-  static bool attr_set = false;  // one-time opt-in to > 64 KB of LDS
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<BM, BN, WGM, WGN, EK>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static bool attr_set = false;
+  hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK>, smem, attr_set);
+  if (e != hipSuccess) return e;
   gemm_kernel<BM, BN, WGM, WGN, EK><<<tiles_m * tiles_n, WGM * WGN * 64, smem, s>>>(
       (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, epi, tiles_m, tiles_n);
   return hipGetLastError();
@@ -281,8 +389,50 @@ hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, in
     case EPI_STORE: return run_gemm<256, 256, 4, 2, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, s);
     case EPI_RESID: return run_gemm<256, 256, 4, 2, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, s);
     case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU>(A, lda, B, ldb, M, N, K, epi, s);
+    case EPI_STORE_F32: return run_gemm<256, 256, 4, 2, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, epi, s);
     default: return run_gemm<256, 256, 4, 2, EPI_QKV>(A, lda, B, ldb, M, N, K, epi, s);
   }
+}
+
+int moe_tile_rows(int n_pairs, int n_experts) {
+  return n_pairs <= 48 * n_experts ? 32 : 128;  // skinny tiles when experts see few rows
+}
+
+template <int BM, int BN, int WGM, int WGN, int EK>
+static hipError_t run_grouped(const void* A, int lda, int a_rows, const int32_t* perm, int top_k,
+                              const void* B, int64_t b_stride, int N, int K, const int32_t* seg,
+                              const int32_t* tile_off, int n_experts, int max_tiles_m,
+                              const Epi& epi, hipStream_t s) {
+  const int tiles_n = EK == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
+  const size_t smem = sizeof(GemmSmem<BM, BN>);
+  static bool attr_set = false;
+  hipError_t e = opt_in_lds(gemm_grouped_kernel<BM, BN, WGM, WGN, EK>, smem, attr_set);
+  if (e != hipSuccess) return e;
+  gemm_grouped_kernel<BM, BN, WGM, WGN, EK><<<max_tiles_m * tiles_n, WGM * WGN * 64, smem, s>>>(
+      (const bf16*)A, lda, a_rows, perm, top_k, (const bf16*)B, b_stride, N, K, seg, tile_off,
+      n_experts, tiles_n, epi);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_grouped(const void* A, int lda, int a_rows, const int32_t* perm, int top_k,
+                               const void* B, int64_t b_stride, int N, int K, const int32_t* seg,
+                               const int32_t* tile_off, int n_experts, int n_pairs,
+                               const Epi& epi, hipStream_t s) {
+  if (n_pairs == 0) return hipSuccess;
+  const int bm = moe_tile_rows(n_pairs, n_experts);
+  const int max_tiles_m = cdiv(n_pairs, bm) + n_experts;  // each expert adds <= 1 partial tile
+  if (bm == 32) {
+    if (epi.kind == EPI_SWIGLU)
+      return run_grouped<32, 256, 1, 4, EPI_SWIGLU>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
+                                                     seg, tile_off, n_experts, max_tiles_m, epi, s);
+    return run_grouped<32, 256, 1, 4, EPI_STORE_F32>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
+                                                      seg, tile_off, n_experts, max_tiles_m, epi, s);
+  }
+  if (epi.kind == EPI_SWIGLU)
+    return run_grouped<128, 256, 2, 4, EPI_SWIGLU>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
+                                                    seg, tile_off, n_experts, max_tiles_m, epi, s);
+  return run_grouped<128, 256, 2, 4, EPI_STORE_F32>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
+                                                     seg, tile_off, n_experts, max_tiles_m, epi, s);
 }
 
 }  // namespace tri

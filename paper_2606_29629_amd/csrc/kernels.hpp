@@ -15,11 +15,11 @@ struct BatchDev {
 };
 
 // Epilogue applied to C = A B^T (fp32 accumulators) by the GEMM kernels.
-enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_STORE_F32 = 4 };
 
 struct Epi {
   int kind;
-  void* out;          // STORE / RESID / SWIGLU: bf16 [M, ldo]
+  void* out;          // STORE / RESID / SWIGLU: bf16 [M, ldo]; STORE_F32: float [M, ldo]
   int ldo;
   const void* resid;  // RESID: bf16 [M, ldr]
   int ldr;
@@ -84,14 +84,23 @@ hipError_t launch_attn_decode_combine(const float* part, void* out, const BatchD
                                       int n_slots, int max_seq, int n_q_heads, int head_dim,
                                       hipStream_t s);
 
-// MoE
-size_t moe_workspace_bytes(int n_tokens, int hidden, int n_experts, int top_k, int expert_ffn);
-hipError_t launch_moe_route(const float* h32, const void* w_router, int n_tokens, int hidden,
-                            int n_experts, int top_k, int renorm, int32_t* idx, float* w,
-                            hipStream_t s);
-hipError_t launch_moe_ffn(const void* h2, const void* x1, const int32_t* idx, const float* w,
-                          const void* w_gate_up, const void* w_down, void* out, int n_tokens,
-                          int hidden, int n_experts, int top_k, int expert_ffn, void* ws,
-                          hipStream_t s);
+// Mixture of experts.  Grouped GEMM over experts: rows [seg[e], seg[e+1]) of
+// the routed order belong to expert e; the gate/up pass gathers A rows
+// perm[p] / top_k (perm = routed pair ids), the down pass reads A rows in
+// routed order.  Tiles of moe_tile_rows(n_pairs, n_experts) rows.
+int moe_tile_rows(int n_pairs, int n_experts);
+hipError_t launch_gemm_grouped(const void* A, int lda, int a_rows, const int32_t* perm, int top_k,
+                               const void* B, int64_t b_stride, int N, int K, const int32_t* seg,
+                               const int32_t* tile_off, int n_experts, int n_pairs,
+                               const Epi& epi, hipStream_t s);
+hipError_t launch_moe_route_f32(const float* h32, const void* w_router, int T, int H, int E,
+                                int k, int renorm, int32_t* idx, float* w, hipStream_t s);
+hipError_t launch_moe_route_bf16(const void* h, const void* w_router, int T, int H, int E, int k,
+                                 int renorm, int32_t* idx, float* w, hipStream_t s);
+hipError_t launch_moe_permute(const int32_t* idx, int n_pairs, int E, int bm, int32_t* rank,
+                              int32_t* counts, int32_t* perm, int32_t* inv, int32_t* seg,
+                              int32_t* tile_off, hipStream_t s);
+hipError_t launch_moe_combine(const void* x1, const float* y, const int32_t* inv, const float* w,
+                              int T, int H, int k, void* out, hipStream_t s);
 
 }  // namespace tri

@@ -1,0 +1,242 @@
+// Mixture-of-experts routing, permutation and combine.
+//
+// Router: logits = h W_r^T in fp32 (fixed summation order per logit), softmax
+// over all experts, top-k by logit with ties to the lower expert index,
+// weights p[idx] (renormalised over the k chosen when asked).
+//
+// Permutation (a counting sort, deterministic): for every expert e, one
+// workgroup scans the (token, slot) pairs in order and ranks the pairs routed
+// to e with wave ballots; a second kernel turns counts into segment offsets
+// (routed order = by expert, then by pair index) and per-expert M-tile offsets
+// for the grouped GEMM, and scatters perm[pos] = pair, inv[pair] = pos.
+//
+// Combine: out[t] = bf16(x1[t] + sum_j w[t][j] * y[inv[t k + j]]), j in order.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace tri {
+
+constexpr int kRouteTok = 8;     // tokens per router workgroup
+constexpr int kRouteChunk = 1024;  // hidden columns staged per pass
+
+template <typename InT>
+__device__ __forceinline__ float to_f32(InT v) { return (float)v; }
+
+template <typename InT>
+__global__ __launch_bounds__(256) void moe_router_kernel(const InT* __restrict__ h,
+                                                         const bf16* __restrict__ wr, int T, int H,
+                                                         int E, int k, int renorm,
+                                                         int32_t* __restrict__ idx_out,
+                                                         float* __restrict__ w_out) {
+  __shared__ __align__(16) float hs[kRouteTok][kRouteChunk];
+  __shared__ float logit[kRouteTok][256];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * kRouteTok;
+  const int el = tid & 127, tg = tid >> 7;  // expert within group; tokens 4 tg .. 4 tg + 3
+  for (int eb = 0; eb < E; eb += 128) {
+    const int e = eb + el;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int hc = 0; hc < H; hc += kRouteChunk) {
+      const int hn = min(kRouteChunk, H - hc);
+      __syncthreads();
+      for (int i = tid; i < kRouteTok * kRouteChunk; i += 256) {
+        const int r = i / kRouteChunk, c = i % kRouteChunk;
+        hs[r][c] = (t0 + r < T && c < hn) ? to_f32(h[(int64_t)(t0 + r) * H + hc + c]) : 0.f;
+      }
+      __syncthreads();
+      if (e < E) {
+        const bf16* wrow = wr + (int64_t)e * H + hc;
+        for (int j = 0; j < hn; j += 8) {
+          Pack8 w8;
+          w8.u = ldg16(wrow + j);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float* hp = &hs[4 * tg + i][j];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[i] = fmaf(bf2f(w8.e[q]), hp[q], acc[i]);
+          }
+        }
+      }
+    }
+    if (e < E)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) logit[4 * tg + i][e] = acc[i];
+  }
+  __syncthreads();
+
+  // Top-k and softmax weights: wave w handles tokens 2w and 2w + 1.
+  for (int tt = 0; tt < 2; ++tt) {
+    const int r = 2 * wave + tt, t = t0 + r;
+    if (t >= T) break;
+    float v[4], orig[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane + 64 * q;
+      v[q] = e < E ? logit[r][e] : -INFINITY;
+      orig[q] = v[q];
+    }
+    float top_v[16];
+    int top_i[16];
+    for (int s = 0; s < k; ++s) {
+      // this lane's best (highest value, then lowest expert index)
+      float bv = v[0];
+      int bi = lane;
+#pragma unroll
+      for (int q = 1; q < 4; ++q) {
+        const int e = lane + 64 * q;
+        if (v[q] > bv) { bv = v[q]; bi = e; }
+      }
+      if (bv == -INFINITY) bi = 0x7fffffff;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+      }
+      top_v[s] = bv;
+      top_i[s] = bi;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (lane + 64 * q == bi) v[q] = -INFINITY;
+    }
+    const float m = top_v[0];
+    float z = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (lane + 64 * q < E) z += expf(orig[q] - m);
+    z = wave_sum(z);
+    float zk = 0.f;
+    for (int s = 0; s < k; ++s) zk += expf(top_v[s] - m);
+    if (lane < k) {
+      float p = 0.f;
+      int ii = 0;
+      for (int s = 0; s < k; ++s)
+        if (s == lane) { p = expf(top_v[s] - m); ii = top_i[s]; }
+      idx_out[(int64_t)t * k + lane] = ii;
+      w_out[(int64_t)t * k + lane] = renorm ? p / zk : p / z;
+    }
+  }
+}
+
+hipError_t launch_moe_route_f32(const float* h32, const void* w_router, int T, int H, int E,
+                                int k, int renorm, int32_t* idx, float* w, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  moe_router_kernel<float><<<cdiv(T, kRouteTok), 256, 0, s>>>(h32, (const bf16*)w_router, T, H, E,
+                                                               k, renorm, idx, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_moe_route_bf16(const void* h, const void* w_router, int T, int H, int E, int k,
+                                 int renorm, int32_t* idx, float* w, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  moe_router_kernel<bf16><<<cdiv(T, kRouteTok), 256, 0, s>>>((const bf16*)h, (const bf16*)w_router,
+                                                              T, H, E, k, renorm, idx, w);
+  return hipGetLastError();
+}
+
+// One workgroup per expert: rank of every pair routed to it, in pair order.
+__global__ __launch_bounds__(256) void moe_count_kernel(const int32_t* __restrict__ idx,
+                                                        int n_pairs, int32_t* __restrict__ rank,
+                                                        int32_t* __restrict__ counts) {
+  __shared__ int wsum[4];
+  const int e = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int base = 0;
+  for (int p0 = 0; p0 < n_pairs; p0 += 256) {
+    const int p = p0 + tid;
+    const bool f = p < n_pairs && idx[p] == e;
+    const unsigned long long m = __ballot(f);
+    const int within = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wave] = __popcll(m);
+    __syncthreads();
+    int pre = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      pre += w < wave ? wsum[w] : 0;
+      tot += wsum[w];
+    }
+    if (f) rank[p] = base + pre + within;
+    base += tot;
+    __syncthreads();
+  }
+  if (tid == 0) counts[e] = base;
+}
+
+// Segment offsets, M-tile offsets (tiles of bm rows) and the scatter.
+__global__ __launch_bounds__(256) void moe_scatter_kernel(
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ rank,
+    const int32_t* __restrict__ counts, int n_pairs, int E, int bm, int32_t* __restrict__ perm,
+    int32_t* __restrict__ inv, int32_t* __restrict__ seg, int32_t* __restrict__ tile_off) {
+  __shared__ int off[257], toff[257];
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    int s = 0, t = 0;
+    for (int e = 0; e < E; ++e) {
+      off[e] = s;
+      toff[e] = t;
+      s += counts[e];
+      t += cdiv(counts[e], bm);
+    }
+    off[E] = s;
+    toff[E] = t;
+  }
+  __syncthreads();
+  if (blockIdx.x == 0)
+    for (int i = tid; i <= E; i += 256) {
+      seg[i] = off[i];
+      tile_off[i] = toff[i];
+    }
+  const int p = blockIdx.x * 256 + tid;
+  if (p < n_pairs) {
+    const int pos = off[idx[p]] + rank[p];
+    perm[pos] = p;
+    inv[p] = pos;
+  }
+}
+
+hipError_t launch_moe_permute(const int32_t* idx, int n_pairs, int E, int bm, int32_t* rank,
+                              int32_t* counts, int32_t* perm, int32_t* inv, int32_t* seg,
+                              int32_t* tile_off, hipStream_t s) {
+  if (n_pairs == 0) return hipSuccess;
+  moe_count_kernel<<<E, 256, 0, s>>>(idx, n_pairs, rank, counts);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  moe_scatter_kernel<<<cdiv(n_pairs, 256), 256, 0, s>>>(idx, rank, counts, n_pairs, E, bm, perm,
+                                                        inv, seg, tile_off);
+  return hipGetLastError();
+}
+
+// out[t] = x1[t] + sum_j w[t][j] y[inv[t k + j]], 8 columns per thread.
+__global__ __launch_bounds__(256) void moe_combine_kernel(const bf16* __restrict__ x1,
+                                                          const float* __restrict__ y,
+                                                          const int32_t* __restrict__ inv,
+                                                          const float* __restrict__ w, int T,
+                                                          int H, int k, bf16* __restrict__ out) {
+  const int t = blockIdx.x;
+  for (int c = threadIdx.x * 8; c < H; c += 256 * 8) {
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < k; ++j) {
+      const float wj = w[(int64_t)t * k + j];
+      const float* yp = y + (int64_t)inv[(int64_t)t * k + j] * H + c;
+      const f32x4 a = *(const f32x4*)yp, b = *(const f32x4*)(yp + 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[q] = fmaf(wj, a[q], acc[q]);
+        acc[q + 4] = fmaf(wj, b[q], acc[q + 4]);
+      }
+    }
+    Pack8 xv, o;
+    xv.u = ldg16(x1 + (int64_t)t * H + c);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) o.e[q] = f2bf(bf2f(xv.e[q]) + acc[q]);
+    stg16(out + (int64_t)t * H + c, o.u);
+  }
+}
+
+hipError_t launch_moe_combine(const void* x1, const float* y, const int32_t* inv, const float* w,
+                              int T, int H, int k, void* out, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  moe_combine_kernel<<<T, 256, 0, s>>>((const bf16*)x1, y, inv, w, T, H, k, (bf16*)out);
+  return hipGetLastError();
+}
+
+}  // namespace tri

@@ -138,6 +138,7 @@ def test_moe_config_checks(lib):
     assert call(lib, c=cfg(**dict(moe, top_k=0))) == T.TRI_ERR_SHAPE
     assert call(lib, c=cfg(**dict(moe, n_experts=300))) == T.TRI_ERR_UNSUPPORTED
     assert call(lib, c=cfg(**dict(moe, expert_ffn_dim=100))) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, c=cfg(**moe)) == T.TRI_ERR_NULL          # MoE needs w_router
 
 
 def test_batch_checks(lib):
@@ -198,6 +199,10 @@ def test_kvcache_append_and_route_validation(lib):
     assert lib.tri_kvcache_append(ctypes.byref(c), ctypes.byref(kv), ctypes.byref(b), None,
                                   FAKE, None) == T.TRI_ERR_NULL
     assert lib.tri_moe_route(ctypes.byref(c), FAKE, FAKE, 4, FAKE, FAKE, None) == T.TRI_ERR_SHAPE
+    m = cfg(flags=T.TRI_F_MOE, n_experts=8, top_k=2, expert_ffn_dim=128, ffn_dim=0)
+    assert lib.tri_moe_route(ctypes.byref(m), None, FAKE, 4, FAKE, FAKE, None) == T.TRI_ERR_NULL
+    assert lib.tri_moe_route(ctypes.byref(m), FAKE + 4, FAKE, 4, FAKE, FAKE, None) == T.TRI_ERR_ALIGN
+    assert lib.tri_moe_route(ctypes.byref(m), FAKE, FAKE, -1, FAKE, FAKE, None) == T.TRI_ERR_SHAPE
 
 
 def test_status_strings(lib):
