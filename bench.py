@@ -212,6 +212,56 @@ def run_decode(args, tri):
     return res
 
 
+def run_secondary(args, tri, name):
+    """Time another workload (tokens/s and per-stage ms) for context."""
+    import torch
+    from paper_2606_29629_amd.workload import DeviceLayer, device_batch, device_cache, to_device_bf16
+    from synth import make_cache, make_weights, make_x, workload
+    wl = workload(name)
+    wb = make_weights(wl.cfg, wl.seed)
+    kb, vb = make_cache(wl.cfg, wl.n_slots, wl.max_seq, wl.seed)
+    dl = DeviceLayer(wl.cfg, wb)
+    cache = device_cache(kb, vb)
+    del kb, vb, wb
+    steps = wl.decode_steps + 1
+    batches, xs = [], []
+    b = wl.batch
+    for s in range(steps):
+        batches.append(device_batch(b))
+        xs.append(to_device_bf16(make_x(wl.cfg, b.n_tokens, wl.seed, step=None if s == 0 and
+                                        int(b.q_len.max()) > 1 else s)))
+        b = b.advanced()
+    decode = wl.batch.q_len.max() == 1
+    fn = tri.layer_decode if decode else tri.layer_prefill
+    out = torch.empty_like(xs[0])
+    ws = torch.empty(max(tri.workspace_size(dl.cfg, db) for db in batches), dtype=torch.uint8,
+                     device="cuda")
+    for s in range(min(steps, 2)):
+        fn(dl.cfg, dl.w, cache, batches[s], xs[s], out=out, workspace=ws)
+    torch.cuda.synchronize()
+    reps = 3
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    tri.profile_enable(True)
+    e0.record(stream)
+    for _ in range(reps):
+        for s in range(steps):
+            fn(dl.cfg, dl.w, cache, batches[s], xs[s], out=out, workspace=ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / (reps * steps)
+    prof = tri.profile_read()
+    tri.profile_enable(False)
+    n_tok = wl.batch.n_tokens if not decode else wl.batch.n_seqs
+    res = {"workload": f"{name}: {wl.description}", "ms_per_step": ms,
+           "tokens_per_s": n_tok / (ms / 1e3),
+           "stages_ms_per_step": {k: v["total_ms"] / (reps * steps) for k, v in prof.items()
+                                  if v["launches"]}}
+    del dl, cache, xs, out, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -220,6 +270,8 @@ def main(argv=None):
     ap.add_argument("--decode-reps", type=int, default=5)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the MoE prefill / MoE decode / mixed-step context numbers")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 3 times (HBM counter calibration)")
     args = ap.parse_args(argv)
@@ -283,6 +335,8 @@ def main(argv=None):
         res["joules_per_token"] = joules / (T * args.steps)
     if not args.no_decode:
         res["decode"] = run_decode(args, tri)
+    if not args.no_secondary:
+        res["secondary"] = [run_secondary(args, tri, n) for n in ("moe_prefill", "moe_decode", "mixed")]
     if not args.no_cpu:
         from synth import bf16_to_f32
         res["cpu_baseline"] = cpu_baseline(wl, wb, bf16_to_f32(kb), bf16_to_f32(vb), xb)

@@ -425,3 +425,30 @@ def test_output_buffer_canary():
     T.layer_prefill(cs.dl.cfg, cs.dl.w, cs.cache, cs.db, cs.x, out=big[:33])
     torch.cuda.synchronize()
     assert torch.all(big[33:] == -3.0)
+
+
+def test_full_size_mixed_step_sampled():
+    """One call: a 512-token chunk at ctx 6144 plus 32 decode sequences with KV
+    lengths U[1024, 8192] (flash and split-KV paths in one launch sequence)."""
+    wl = workload("mixed")
+    cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
+    out, ws = cs.run()
+    rows = np.array([0, 1, 255, 256, 511, 512, 513, 530, 543])
+    x1, act, w = stage_parity(cs, ws, rows, label="mixed")
+    check_down(cs, out, x1, act, w, rows, "mixed")
+    # end to end for two decode sequences and the chunk's last rows
+    pick = np.array([1, 7, 32])                      # sequences (0 = the chunk)
+    sub = B(np.arange(3), wl.batch.ctx_len[pick], wl.batch.q_len[pick])
+    w64 = {k: f64(v) for k, v in cs.wb.items()}
+    tok = wl.batch.cu_q[pick]
+    args = (wl.cfg, w64, f64(cs.kb[wl.batch.slot[pick]]), f64(cs.vb[wl.batch.slot[pick]]), sub,
+            f64(cs.xb[tok]))
+    ref = oracle.layer_forward(*args, storage="bf16")
+    assert_close(to_host_f64(out)[tok], ref["out"], "mixed decode rows",
+                 exact=oracle.layer_forward(*args)["out"])
+    chunk = B([0], [wl.batch.ctx_len[0]], [512])
+    args = (wl.cfg, w64, f64(cs.kb[:1]), f64(cs.vb[:1]), chunk, f64(cs.xb[:512]))
+    local = np.array([0, 300, 511])
+    ref = oracle.layer_forward(*args, rows=local, storage="bf16")
+    assert_close(to_host_f64(out)[local], ref["out"], "mixed chunk rows",
+                 exact=oracle.layer_forward(*args, rows=local)["out"])
