@@ -2,24 +2,24 @@
 //
 // One workgroup = one (sequence, query head, 128-query tile); 4 waves of 32
 // queries.  Keys and values come from the KV cache (the q/k/v projection has
-// already written this call's rows), 64 keys per tile, staged through LDS and
-// double buffered; the next tile's global loads are issued before the current
-// tile's MFMAs.
+// already written this call's rows), 64 keys per tile.  K and V tiles go from
+// HBM straight into LDS with buffer_load_dwordx4 ... lds, double buffered: the
+// loads of tile k+1 are in flight while tile k is processed.  Key rows past
+// the visible range read as zero (buffer range check) and are masked.
 //
-// The score block is computed transposed, S^T = K Q^T, with
-// v_mfma_f32_32x32x16_bf16 (A = K rows from LDS, B = the wave's queries held in
-// registers for the whole loop).  A lane then owns one query column and 32 of
-// the tile's 64 keys, so the running max / sum of the online softmax need one
-// cross-lane exchange (lane ^ 32) per tile.  The output is also kept
-// transposed, O^T += V^T P^T: P^T is taken straight from the score
-// accumulators, and V is written to LDS transposed with the keys of every
-// 16-key group permuted to the order in which the score accumulator holds
-// them, so each lane's 8 V^T values are one ds_read_b128.  The P V product runs
-// on the fp16 matrix path (v_mfma_f32_32x32x16_f16, same rate as bf16): V
-// converts from bf16 exactly in fp16's normal range, and P is split into
-// P_hi = fp16(P) and P_lo = fp16(P - P_hi), two MFMAs into one accumulator,
-// so P keeps ~22 significant bits and the weights match the fp32 row sum.
-// Scores use exp2 with the 1/sqrt(D) * log2(e) scale folded in.
+// Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16
+// (A = K rows from LDS, B = the wave's queries held in registers for the whole
+// loop).  A lane then owns one query column and 32 of the tile's 64 keys, so
+// the running max / sum of the online softmax need one cross-lane exchange
+// (lane ^ 32) per tile.  The output is kept transposed too, O^T += V^T P^T.
+// P^T comes straight from the score accumulators.  V stays in its natural
+// [key][d] layout and its MFMA operand is read with ds_read_b64_tr_b16: within
+// each 16-lane group, the lanes of quad j point at key row j (4 dims each) and
+// the instruction hands lane i the value at dim d0 + i of those four keys; two
+// such reads give a lane its 8 keys in the order in which the score
+// accumulator holds them.  P is split into P_hi = bf16(P) and
+// P_lo = bf16(P - P_hi), two MFMAs into one accumulator, so the weights keep
+// 16 significant bits.  Scores use exp2 with 1/sqrt(D) * log2(e) folded in.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -28,44 +28,45 @@ namespace tri {
 constexpr int kFaBQ = 128;  // queries per workgroup
 constexpr int kFaBK = 64;   // keys per tile
 
-// Position inside a 16-key group at which key kk is stored in V^T (the order in
-// which a score-accumulator lane holds keys: lane half g, element e <->
-// key (e % 4) + 8 (e / 4) + 4 g).
-__device__ __forceinline__ int vt_slot(int kk) {
-  return 8 * ((kk >> 2) & 1) + (kk & 3) + 4 * (kk >> 3);
-}
-
-// Physical 16-byte chunk of logical chunk pc in V^T row d.  The (d % 8) term
-// spreads the 8 lanes of a ds_read_b128 phase (consecutive d); the (d / 8)
-// term spreads the transposing 2-byte stores (d = 8 ch + e, same e).
-__device__ __forceinline__ int vt_chunk(int pc, int d) { return pc ^ (d & 7) ^ ((d >> 3) & 7); }
-
-// K tile rows are D * 2 bytes.  With 64 four-byte banks, 16 lanes reading the
-// same chunk of 16 consecutive keys are conflict-free when the chunk is
-// XOR-ed with key % 16 (256-byte rows, D = 128) or with (key / 2) % 8
-// (128-byte rows, D = 64).
+// Physical 16-byte chunk of logical chunk c in K/V tile row r (LDS: 64 banks
+// of 4 bytes).
+//  D = 128 (256-byte rows): c ^ g(r), g(r) = 4 (r % 4) + (r / 4) % 4.  g is a
+//    bijection on 16 consecutive rows (K fragment reads: 16 rows, one chunk,
+//    per 16-lane phase) and takes 4 distinct values of g / 4 on 4 aligned
+//    rows (transposing V reads: 4 rows x 4 aligned chunks per 32 lanes).
+//  D = 64 (128-byte rows, two per bank window): c ^ g(r / 2),
+//    g(i) = 4 (i % 2) + (i / 2) % 4, distinct over the 8 rows of one parity
+//    among 16, and differing in bit 2 between rows 4a and 4a + 2.
 template <int D>
-__device__ __forceinline__ int k_chunk_t(int ch, int key) {
-  return D == 128 ? (ch ^ (key & 15)) : (ch ^ ((key >> 1) & 7));
+__device__ __forceinline__ int kv_chunk(int c, int r) {
+  if constexpr (D == 128) return c ^ (((r & 3) << 2) | ((r >> 2) & 3));
+  else return c ^ (((r & 2) << 1) | ((r >> 2) & 3));
 }
-#define k_chunk(ch, key) k_chunk_t<D>(ch, key)
 
 template <int D>
 struct FaSmem {
-  bf16 k[2][kFaBK * D];  // [key][d], 16-byte chunks swizzled by k_chunk
-  f16 vt[2][D * kFaBK];  // V^T in fp16: [d][key slot], chunks swizzled by vt_chunk
+  bf16 k[2][kFaBK * D];  // [key][d], chunks swizzled by kv_chunk
+  bf16 v[2][kFaBK * D];  // [key][d], chunks swizzled by kv_chunk
 };
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ s16x4 lds_read_tr16(const bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(p));
+}
+
 template <int D>
-__global__ __launch_bounds__(256) void attn_prefill_kernel(
+__global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
     bf16* __restrict__ O, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ ctx_len,
     const int32_t* __restrict__ slot, int n_slots, int max_seq, int Hq, int Hkv,
     float scale_log2e, int include_single, int n_tokens) {
-  constexpr int DC = D / 8;             // 16-byte chunks per K row
-  constexpr int KLD = kFaBK * DC / 256; // K chunks per thread per tile
-  constexpr int DS = D / 16;            // MFMA k-steps over d
-  constexpr int DB = D / 32;            // 32-row d blocks of O^T
+  constexpr int DC = D / 8;                     // 16-byte chunks per row
+  constexpr int ROWS_PER_KB = 64 / DC;          // tile rows filled by one 1 KB wave load
+  constexpr int BLK = kFaBK / ROWS_PER_KB / 4;  // 1 KB loads per wave per operand and tile
+  constexpr int DS = D / 16;                    // MFMA k-steps over d
+  constexpr int DB = D / 32;                    // 32-row d blocks of O^T
   extern __shared__ __align__(16) char smem_raw[];
   FaSmem<D>& sm = *reinterpret_cast<FaSmem<D>*>(smem_raw);
 
@@ -78,13 +79,38 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(
   if (sl < 0 || sl >= n_slots || c < 0 || c + n > max_seq) return;
   const int kvh = (qh * Hkv) / Hq;
   const int64_t cache_off = ((int64_t)sl * Hkv + kvh) * max_seq * D;
-  const bf16* Kp = Kc + cache_off;
-  const bf16* Vp = Vc + cache_off;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 31, lg = lane >> 5;
   const int kv_len = c + min(n, (qt + 1) * kFaBQ);
   const int nkt = cdiv(kv_len, kFaBK);
+
+  // The whole offset goes in the per-lane operand so that the range check
+  // (offset >= kv_len rows -> zero) covers it.
+  const uint32_t kv_bytes = (uint32_t)kv_len * D * 2;
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(Kc + cache_off), (short)0, kv_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(Vc + cache_off), (short)0, kv_bytes, 0x00020000);
+  // Lane l of a 1 KB wave load fills physical chunk l % DC of tile row
+  // l / DC of its block, i.e. logical chunk kv_chunk(l % DC, row) (the
+  // swizzle is an involution).
+  uint32_t ld_off[BLK];
+#pragma unroll
+  for (int j = 0; j < BLK; ++j) {
+    const int row = (wave + 4 * j) * ROWS_PER_KB + lane / DC;
+    ld_off[j] = (uint32_t)((row * D + kv_chunk<D>(lane % DC, row) * 8) * 2);
+  }
+  auto gload = [&](int kt, int buf) {
+    const uint32_t kb = (uint32_t)kt * kFaBK * D * 2;
+#pragma unroll
+    for (int j = 0; j < BLK; ++j) {
+      const int blk = (wave + 4 * j) * ROWS_PER_KB * D;
+      buffer_load_lds16(rk, &sm.k[buf][blk], ld_off[j] + kb, 0);
+      buffer_load_lds16(rv, &sm.v[buf][blk], ld_off[j] + kb, 0);
+    }
+  };
 
   // This lane's query (clamped to a valid row; rows >= n are not written).
   const int qi = qt * kFaBQ + wave * 32 + lr;
@@ -98,111 +124,90 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(
     for (int t = 0; t < DS; ++t) qf[t] = *(const bf16x8*)(qp + 16 * t);
   }
 
-  // Global -> register staging of one K/V tile.
-  u32x4 rk[KLD], rv[KLD];
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      const int id = tid + 256 * i, key = id / DC, ch = id % DC;
-      const int kr = min(kt * kFaBK + key, kv_len - 1);
-      rk[i] = ldg16(Kp + (int64_t)kr * D + ch * 8);
-      rv[i] = ldg16(Vp + (int64_t)kr * D + ch * 8);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KLD; ++i) {
-      const int id = tid + 256 * i, key = id / DC, ch = id % DC;
-      *(u32x4*)&sm.k[buf][key * D + k_chunk(ch, key) * 8] = rk[i];
-      Pack8 v;
-      v.u = rv[i];
-      const int slotk = (key & ~15) + vt_slot(key & 15);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int d = ch * 8 + e;
-        sm.vt[buf][d * kFaBK + vt_chunk(slotk >> 3, d) * 8 + (slotk & 7)] = bf2h_sat(v.e[e]);
-      }
-    }
-  };
+  // Transposing V reads: in 16-lane group G (lane / 16), lane i = lane % 16
+  // points at key row 4 (lane / 32) + i / 4 of a 16-key group (+ 8 for the
+  // second read), dims 32 b + 16 (G % 2) + 4 (i % 4) .. + 3.
+  const int tr_key = 4 * lg + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
   f32x16 oacc[DB];
 #pragma unroll
   for (int b = 0; b < DB; ++b) oacc[b] = f32x16{0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
+  gload(0, 0);
   for (int kt = 0; kt < nkt; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nkt) gload(kt + 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // tile kt is in LDS; every wave is done with tile kt - 1
+    if (kt + 1 < nkt) gload(kt + 1, buf ^ 1);
     const int key0 = kt * kFaBK;
-    if (key0 <= wave_qmin + 31) {  // some key of this tile is visible to this wave
-      // S^T = K Q^T for two 32-key blocks.
-      f32x16 sacc[2];
+    if (key0 > wave_qmin + 31) continue;  // no key of this tile is visible to this wave
+    // S^T = K Q^T for two 32-key blocks.
+    f32x16 sacc[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        sacc[kb] = f32x16{0.f};
-        const int key = kb * 32 + lr;
+    for (int kb = 0; kb < 2; ++kb) {
+      sacc[kb] = f32x16{0.f};
+      const int key = kb * 32 + lr;
 #pragma unroll
-        for (int t = 0; t < DS; ++t) {
-          const int ch = 2 * t + lg;
-          const bf16x8 kf = *(const bf16x8*)&sm.k[buf][key * D + k_chunk(ch, key) * 8];
-          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t], sacc[kb], 0, 0, 0);
-        }
-      }
-      // Mask + scale; element r of block kb is key key0 + 32kb + (r%4) + 8(r/4) + 4lg.
-      const bool diag = key0 + kFaBK - 1 > wave_qmin;
-      float mt = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float v = sacc[kb][r] * scale_log2e;
-          if (diag) {
-            const int key = key0 + 32 * kb + (r & 3) + 8 * (r >> 2) + 4 * lg;
-            if (key > qpos) v = -INFINITY;
-          }
-          sacc[kb][r] = v;
-          mt = fmaxf(mt, v);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float m_new = fmaxf(m_run, mt);
-      // m_new is finite: key 0 of the first tile is visible to every query.
-      const float alpha = exp2f(m_run - m_new);
-      m_run = m_new;
-      float ls = 0.f;
-      f16x8 pf[4], pl[4];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float p = exp2f(sacc[kb][8 * h + e] - m_new);
-            ls += p;
-            const f16 hi = (f16)p;
-            pf[2 * kb + h][e] = hi;
-            pl[2 * kb + h][e] = (f16)(p - (float)hi);
-          }
-      l_run = l_run * alpha + ls;
-#pragma unroll
-      for (int b = 0; b < DB; ++b) oacc[b] *= alpha;
-      // O^T += V^T P^T over four 16-key groups.
-#pragma unroll
-      for (int g16 = 0; g16 < 4; ++g16) {
-        const int pc = 2 * g16 + lg;  // chunk of the key slots this lane feeds
-#pragma unroll
-        for (int b = 0; b < DB; ++b) {
-          const int d = 32 * b + lr;
-          const f16x8 vf = *(const f16x8*)&sm.vt[buf][d * kFaBK + vt_chunk(pc, d) * 8];
-          oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pf[g16], oacc[b], 0, 0, 0);
-          oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, pl[g16], oacc[b], 0, 0, 0);
-        }
+      for (int t = 0; t < DS; ++t) {
+        const bf16x8 kf =
+            *(const bf16x8*)&sm.k[buf][key * D + kv_chunk<D>(2 * t + lg, key) * 8];
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t], sacc[kb], 0, 0, 0);
       }
     }
-    if (kt + 1 < nkt) sstore(buf ^ 1);
-    __syncthreads();
+    // Mask + scale; element r of block kb is key key0 + 32kb + (r%4) + 8(r/4) + 4lg.
+    const bool diag = key0 + kFaBK - 1 > wave_qmin;
+    float mt = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = sacc[kb][r] * scale_log2e;
+        if (diag) {
+          const int key = key0 + 32 * kb + (r & 3) + 8 * (r >> 2) + 4 * lg;
+          if (key > qpos) v = -INFINITY;
+        }
+        sacc[kb][r] = v;
+        mt = fmaxf(mt, v);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float m_new = fmaxf(m_run, mt);
+    // m_new is finite: key 0 of the first tile is visible to every query.
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float ls = 0.f;
+    bf16x8 pf[4], pl[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = exp2f(sacc[kb][8 * h + e] - m_new);
+          ls += p;
+          const bf16 hi = f2bf(p);
+          pf[2 * kb + h][e] = hi;
+          pl[2 * kb + h][e] = f2bf(p - bf2f(hi));
+        }
+    l_run = l_run * alpha + ls;
+#pragma unroll
+    for (int b = 0; b < DB; ++b) oacc[b] *= alpha;
+    // O^T += V^T P^T over four 16-key groups.
+    const bf16* vb = sm.v[buf];
+#pragma unroll
+    for (int g16 = 0; g16 < 4; ++g16) {
+      const int k1 = 16 * g16 + tr_key, k2 = k1 + 8;
+#pragma unroll
+      for (int b = 0; b < DB; ++b) {
+        const int col = 32 * b + tr_col;
+        union { s16x4 s[2]; bf16x8 h; } vf;
+        vf.s[0] = lds_read_tr16(vb + k1 * D + kv_chunk<D>(col >> 3, k1) * 8 + (col & 7));
+        vf.s[1] = lds_read_tr16(vb + k2 * D + kv_chunk<D>(col >> 3, k2) * 8 + (col & 7));
+        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.h, pf[g16], oacc[b], 0, 0, 0);
+        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.h, pl[g16], oacc[b], 0, 0, 0);
+      }
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
