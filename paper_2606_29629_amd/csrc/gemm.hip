@@ -78,6 +78,14 @@ __device__ __forceinline__ int b_row_of(int kind, int tn, int nt, int ffn) {
 // The shared K loop.  a_off / b_off: byte offset (within the buffer) of chunk
 // swz(row, lane % 8) of this lane's row in each of its 1 KB LDS blocks (at or
 // beyond the buffer size for rows that must read as zero).
+//
+// Schedule of k-tile t (4 k-steps of 16): the fragments of k-step s + 1 are
+// read from LDS while the MFMAs of step s run.  Before the MFMAs of the last
+// step, each wave waits for its loads of tile t + 1, one barrier makes tile
+// t + 1 visible and retires every read of tile t, the loads of tile t + 2 go
+// into tile t's buffer and the first fragments of tile t + 1 are read -- all
+// under the last step's MFMAs, so the barrier costs no matrix-core time beyond
+// the skew between waves.
 template <int BM, int BN, int WGM, int WGN>
 struct Mainloop {
   static constexpr int NT = WGM * WGN * 64;
@@ -85,6 +93,7 @@ struct Mainloop {
   static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int MI = WM / 32, NI = WN / 32;
   static constexpr int A_BLK = BM / 8 / NW, B_BLK = BN / 8 / NW;  // 1 KB blocks per wave
+  static constexpr int KSTEPS = kBK / 16;
 
   __device__ __forceinline__ static void run(GemmSmem<BM, BN>& sm, __amdgpu_buffer_rsrc_t ra,
                                              const uint32_t (&a_off)[A_BLK],
@@ -96,45 +105,96 @@ struct Mainloop {
     for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{0.f};
-    auto gload = [&](int kt, int buf) {
+    // kill = 0x80000000 pushes every offset past the buffer's range, so the
+    // load writes zeros instead of touching memory (used past the last tile,
+    // keeping the schedule free of branches).
+    auto gload = [&](int kt, int buf, uint32_t kill) {
       const int kb = kt * kBK * 2;
 #pragma unroll
       for (int j = 0; j < A_BLK; ++j)
-        buffer_load_lds16(ra, &sm.a[buf][(wv + NW * j) * 8 * kBK], a_off[j], kb);
+        buffer_load_lds16(ra, &sm.a[buf][(wv + NW * j) * 8 * kBK], a_off[j] | kill, kb);
 #pragma unroll
       for (int j = 0; j < B_BLK; ++j)
-        buffer_load_lds16(rb, &sm.b[buf][(wv + NW * j) * 8 * kBK], b_off[j], kb);
+        buffer_load_lds16(rb, &sm.b[buf][(wv + NW * j) * 8 * kBK], b_off[j] | kill, kb);
     };
-    const int KT = K / kBK;
     const int lr = lane & 31, lg = lane >> 5;
-    gload(0, 0);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    bf16x8 fa[2][MI], fb[2][NI];
+    auto lload = [&](int buf, int ks, int slot) {
+      const int ch = ks * 2 + lg;
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int r = wm * WM + i * 32 + lr;
+        fa[slot][i] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
+      }
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int r = wn * WN + j * 32 + lr;
+        fb[slot][j] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
+      }
+    };
+    // Fragment f of a k-step: f < MI -> A block f, else B block f - MI.
+    auto lread = [&](int buf, int ks, int slot, int f) {
+      const int ch = ks * 2 + lg;
+      if (f < MI) {
+        const int r = wm * WM + f * 32 + lr;
+        fa[slot][f] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
+      } else {
+        const int r = wn * WN + (f - MI) * 32 + lr;
+        fb[slot][f - MI] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
+      }
+    };
+    // Load piece p of a tile: p < A_BLK -> A block p, else B block p - A_BLK.
+    auto gpiece = [&](int kt, int buf, uint32_t kill, int p) {
+      const int kb = kt * kBK * 2;
+      if (p < A_BLK)
+        buffer_load_lds16(ra, &sm.a[buf][(wv + NW * p) * 8 * kBK], a_off[p] | kill, kb);
+      else
+        buffer_load_lds16(rb, &sm.b[buf][(wv + NW * (p - A_BLK)) * 8 * kBK],
+                          b_off[p - A_BLK] | kill, kb);
+    };
+    auto mfma = [&](int slot, int g) {
+      const int i = g / NI, j = g % NI;
+      acc[i][j] =
+          __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j], 0, 0, 0);
+    };
+    constexpr int NMF = MI * NI, NRD = MI + NI, NLD = A_BLK + B_BLK;
+    constexpr int NG = NMF > NRD ? NMF : NRD;
+    constexpr int NGL = NG > NLD ? NG : NLD;
+    const int KT = K / kBK;
+    gload(0, 0, 0);
+    if (KT > 1) {
+      gload(1, 1, 0);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NLD) : "memory");  // tile 0 landed
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
     __syncthreads();
+    lload(0, 0, 0);
+    // The issue order is spelled out: one MFMA, then one LDS read for the next
+    // k-step (and on the last step one or more tile loads), fenced so the
+    // compiler keeps it.
     for (int kt = 0; kt < KT; ++kt) {
       const int buf = kt & 1;
-      if (kt + 1 < KT) gload(kt + 1, buf ^ 1);  // lands in the other buffer meanwhile
 #pragma unroll
-      for (int kk = 0; kk < kBK / 16; ++kk) {
-        const int ch = kk * 2 + lg;
-        bf16x8 af[MI], bfr[NI];
+      for (int ks = 0; ks + 1 < KSTEPS; ++ks) {
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          const int r = wm * WM + i * 32 + lr;
-          af[i] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
+        for (int g = 0; g < NG; ++g) {
+          if (g < NMF) mfma(ks & 1, g);
+          if (g < NRD) lread(buf, ks + 1, (ks + 1) & 1, g);
+          __builtin_amdgcn_sched_barrier(0);
         }
-#pragma unroll
-        for (int j = 0; j < NI; ++j) {
-          const int r = wn * WN + j * 32 + lr;
-          bfr[j] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
-        }
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-          for (int j = 0; j < NI; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
       }
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      constexpr int last = (KSTEPS - 1) & 1;
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's tile t + 1 loads
       __syncthreads();
+      const uint32_t kill = kt + 2 < KT ? 0u : 0x80000000u;
+#pragma unroll
+      for (int g = 0; g < NGL; ++g) {
+        if (g < NMF) mfma(last, g);
+        if (g < NLD) gpiece(kt + 2, buf, kill, g);
+        if (g < NRD) lread(buf ^ 1, 0, last ^ 1, g);  // stale but in-range on the last tile
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
 };
@@ -240,7 +300,7 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
 }
 
 template <int BM, int BN, int WGM, int WGN, int EK>
-__global__ __launch_bounds__(WGM * WGN * 64) void gemm_kernel(const bf16* __restrict__ A, int lda,
+__global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __restrict__ A, int lda,
                                                    const bf16* __restrict__ B, int ldb, int M,
                                                    int N, int K, Epi epi, int tiles_m,
                                                    int tiles_n) {
