@@ -146,7 +146,9 @@ typedef struct {
 } tri_workspace_map;
 
 /* Workspace bytes needed by tri_layer_prefill / tri_layer_decode for a batch
- * with these host scalars (device arrays are not read).                        */
+ * with these host scalars (device arrays are not read).  For a fixed config the
+ * size never decreases as n_tokens grows (other scalars equal), so a workspace
+ * sized for the largest batch serves every smaller one.                        */
 tri_status tri_workspace_size(const tri_layer_config* cfg, const tri_batch* batch,
                               size_t* bytes);
 

@@ -68,13 +68,16 @@ size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
   const int T = b->n_tokens, H = c->hidden, D = c->head_dim;
   const int Nqkv = (c->n_q_heads + 2 * c->n_kv_heads) * D;
   size_t p = attn_decode_partial_bytes(T, c->n_q_heads, D, b->max_ctx_len + 1);
-  if (T > 0 && T <= kSkinnyMaxRows) {
+  if (T > 0) {
+    // Skinny-path partials; a larger batch reserves them for the largest
+    // skinny batch, so that the size never shrinks as n_tokens grows.
+    const int Ts = T <= kSkinnyMaxRows ? T : kSkinnyMaxRows;
     auto mx = [](size_t a, size_t b2) { return a > b2 ? a : b2; };
-    size_t g = gemv_partial_bytes(T, Nqkv, H);
-    g = mx(g, gemv_partial_bytes(T, H, c->n_q_heads * D));
+    size_t g = skinny_partial_bytes(Ts, Nqkv, H, EPI_QKV);
+    g = mx(g, skinny_partial_bytes(Ts, H, c->n_q_heads * D, EPI_RESID));
     if (!is_moe(c)) {
-      g = mx(g, gemv_partial_bytes(T, 2 * c->ffn_dim, H));
-      g = mx(g, gemv_partial_bytes(T, H, c->ffn_dim));
+      g = mx(g, skinny_partial_bytes(Ts, 2 * c->ffn_dim, H, EPI_SWIGLU));
+      g = mx(g, skinny_partial_bytes(Ts, H, c->ffn_dim, EPI_RESID));
     }
     p = mx(p, g);
   }
@@ -173,7 +176,7 @@ T* at(void* ws, size_t off) { return (T*)((char*)ws + off); }
 
 tri_status run_linear(const void* A, int lda, const void* B, int M, int N, int K, const Epi& epi,
                       float* part, hipStream_t s) {
-  if (M <= kSkinnyMaxRows) TRI_HIP(launch_gemv(A, lda, B, K, M, N, K, epi, part, s));
+  if (M <= kSkinnyMaxRows) TRI_HIP(launch_skinny(A, lda, B, K, M, N, K, epi, part, s));
   else TRI_HIP(launch_gemm(A, lda, B, K, M, N, K, epi, s));
   return TRI_OK;
 }

@@ -302,8 +302,8 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
 template <int BM, int BN, int WGM, int WGN, int EK>
 __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __restrict__ A, int lda,
                                                    const bf16* __restrict__ B, int ldb, int M,
-                                                   int N, int K, Epi epi, int tiles_m,
-                                                   int tiles_n) {
+                                                   int N, int K, int kc, Epi epi,
+                                                   int tiles_m, int tiles_n) {
   using ML = Mainloop<BM, BN, WGM, WGN>;
   constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
   extern __shared__ __align__(16) char smem_raw[];
@@ -315,12 +315,18 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
   int tm, tn;
   tile_of_block(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int n_rows_b = EK == EPI_SWIGLU ? 2 * epi.ffn : N;
+  // Split-K (fp32 partial output only): split z covers k in [z kc, z kc + kc)
+  // and writes plane z of the output.
+  const int k0 = blockIdx.y * kc;
+  K = min(kc, K - k0);
+  A += k0;
+  B += k0;
 
   // Buffer descriptors: rows past the end of A or B read as zero.
-  const __amdgpu_buffer_rsrc_t rsrc_a =
-      __builtin_amdgcn_make_buffer_rsrc((void*)A, (short)0, (int)((int64_t)M * lda * 2), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rsrc_b =
-      __builtin_amdgcn_make_buffer_rsrc((void*)B, (short)0, (int)((int64_t)n_rows_b * ldb * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc_a = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)A, (short)0, (int)((int64_t)M * lda * 2 - (int64_t)k0 * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc_b = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)B, (short)0, (int)((int64_t)n_rows_b * ldb * 2 - (int64_t)k0 * 2), 0x00020000);
   // Global -> LDS without registers: each buffer_load_dwordx4 ... lds writes the
   // 64 lanes' 16 bytes to 1 KB of LDS in lane order, i.e. 8 tile rows.  Lane l
   // fills physical chunk l % 8 of row 8 b + l / 8 of its block b, so it fetches
@@ -344,7 +350,11 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
 
   const int lr = lane & 31, lg = lane >> 5;
   const int row0 = tm * BM + wm * WM + 4 * lg;
-  if constexpr (EK == EPI_STORE || EK == EPI_RESID || EK == EPI_STORE_F32) {
+  if constexpr (EK == EPI_STORE_F32) {
+    Epi e = epi;
+    e.out = (float*)epi.out + (int64_t)blockIdx.y * M * epi.ldo;
+    plain_epilogue<MI, NI, EK>(acc, e, row0, M, tn * BN + wn * WN + lr, N);
+  } else if constexpr (EK == EPI_STORE || EK == EPI_RESID) {
     plain_epilogue<MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + lr, N);
   } else if constexpr (EK == EPI_SWIGLU) {
     swiglu_epilogue<MI, NI>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + lr);
@@ -428,17 +438,20 @@ static hipError_t opt_in_lds(Kern k, size_t smem, bool& done) {
   return e;
 }
 
+// splits > 1 only with EPI_STORE_F32 (plane z of epi.out holds split z); K
+// must then be a multiple of 64 * splits.
 template <int BM, int BN, int WGM, int WGN, int EK>
 static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
-                           const Epi& epi, hipStream_t s) {
+                           const Epi& epi, hipStream_t s, int splits = 1) {
   const int tiles_m = cdiv(M, BM);
   const int tiles_n = EK == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
   const size_t smem = sizeof(GemmSmem<BM, BN>);
   static bool attr_set = false;
   hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK>, smem, attr_set);
   if (e != hipSuccess) return e;
-  gemm_kernel<BM, BN, WGM, WGN, EK><<<tiles_m * tiles_n, WGM * WGN * 64, smem, s>>>(
-      (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, epi, tiles_m, tiles_n);
+  const int kc = K / splits;
+  gemm_kernel<BM, BN, WGM, WGN, EK><<<dim3(tiles_m * tiles_n, splits), WGM * WGN * 64, smem, s>>>(
+      (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, kc, epi, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
@@ -493,6 +506,128 @@ hipError_t launch_gemm_grouped(const void* A, int lda, int a_rows, const int32_t
                                                     seg, tile_off, n_experts, max_tiles_m, epi, s);
   return run_grouped<128, 256, 2, 4, EPI_STORE_F32>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
                                                      seg, tile_off, n_experts, max_tiles_m, epi, s);
+}
+
+// Split-K reduction: sum the fp32 partial planes [splits][M][N] in split
+// order (deterministic) and apply the epilogue; one thread per output element
+// (per intermediate column for SwiGLU, per rotary pair for q/k/v).
+__global__ __launch_bounds__(256) void splitk_epi_kernel(const float* __restrict__ part,
+                                                       int splits, int M, int N, Epi epi) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t MN = (int64_t)M * N;
+  auto sum = [&](int row, int col) {
+    float v = 0.f;
+    for (int s = 0; s < splits; ++s) v += part[s * MN + (int64_t)row * N + col];
+    return v;
+  };
+  if (epi.kind == EPI_STORE || epi.kind == EPI_RESID) {
+    if (gid >= MN) return;
+    const int row = (int)(gid / N), col = (int)(gid % N);
+    float v = sum(row, col);
+    if (epi.kind == EPI_RESID) v += bf2f(((const bf16*)epi.resid)[(int64_t)row * epi.ldr + col]);
+    ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(v);
+  } else if (epi.kind == EPI_SWIGLU) {
+    const int F = epi.ffn;
+    if (gid >= (int64_t)M * F) return;
+    const int row = (int)(gid / F), f = (int)(gid % F);
+    const float g = sum(row, f), u = sum(row, F + f);
+    ((bf16*)epi.out)[(int64_t)row * epi.ldo + f] = f2bf(silu(g) * u);
+  } else {  // EPI_QKV: one thread per rotary pair
+    const int D = epi.head_dim, half = D / 2;
+    const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
+    const int pairs = (Hq + 2 * Hkv) * half;
+    if (gid >= (int64_t)M * pairs) return;
+    const int row = (int)(gid / pairs), p = (int)(gid % pairs);
+    const int head = p / half, d = p % half;
+    const int col = head * D + d;
+    float x1 = sum(row, col), x2 = sum(row, col + half);
+    if (epi.bias) {
+      x1 += bf2f(((const bf16*)epi.bias)[col]);
+      x2 += bf2f(((const bf16*)epi.bias)[col + half]);
+    }
+    if (head < Hq + Hkv) {
+      const float2 cs = epi.rope[(int64_t)row * half + d];
+      const float y1 = x1 * cs.x - x2 * cs.y;
+      const float y2 = x2 * cs.x + x1 * cs.y;
+      x1 = y1;
+      x2 = y2;
+    }
+    if (head < Hq) {
+      bf16* qp = (bf16*)epi.q + ((int64_t)row * Hq + head) * D + d;
+      qp[0] = f2bf(x1);
+      qp[half] = f2bf(x2);
+    } else {
+      const int sl = epi.tok_slot[row];
+      if (sl < 0) return;
+      const int kvh = head < Hq + Hkv ? head - Hq : head - Hq - Hkv;
+      bf16* cache = (bf16*)(head < Hq + Hkv ? epi.kc : epi.vc);
+      bf16* cp = cache + (((int64_t)sl * Hkv + kvh) * epi.max_seq + epi.tok_row[row]) * D + d;
+      cp[0] = f2bf(x1);
+      cp[half] = f2bf(x2);
+    }
+  }
+}
+
+// Decode projections (M <= 128 rows).  The arithmetic intensity is ~M flop
+// per weight byte, so the weight stream from HBM sets the time: skinny
+// 64 x 64 tiles (two or four waves) give ~600 workgroups on the large
+// projections -- every one resident at once, each a short run of weight rows,
+// which keeps the HBM pages streaming -- and split-K multiplies the
+// workgroups of the narrow projections until ~400 are in flight.  Without a
+// split the epilogue is fused; with one, fp32 partial planes go to the
+// workspace and splitk_epi_kernel finishes.  q/k/v always splits (its fused
+// epilogue needs a whole head per wave).
+constexpr int kSkinnyBN = 64;
+
+static int skinny_bm(int M) { return M <= 64 ? 64 : 128; }
+
+int skinny_splits(int M, int N, int K, int kind) {
+  const int tiles = cdiv(M, skinny_bm(M)) * cdiv(N, kSkinnyBN);
+  int s = 1;
+  while ((tiles * s < 400 || (kind == EPI_QKV && s == 1)) && s < 16 && K % (kBK * 2 * s) == 0)
+    s *= 2;
+  return s;
+}
+
+size_t skinny_partial_bytes(int M, int N, int K, int kind) {
+  const int s = skinny_splits(M, N, K, kind);
+  return s > 1 ? (size_t)s * M * N * sizeof(float) : 0;
+}
+
+template <int BM, int WGM>
+static hipError_t run_skinny(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
+                             const Epi& epi, float* part, int splits, hipStream_t s) {
+  if (splits == 1) {
+    switch (epi.kind) {
+      case EPI_STORE: return run_gemm<BM, kSkinnyBN, WGM, 1, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, s);
+      case EPI_RESID: return run_gemm<BM, kSkinnyBN, WGM, 1, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, s);
+      case EPI_SWIGLU: return run_gemm<BM, kSkinnyBN, WGM, 1, EPI_SWIGLU>(A, lda, B, ldb, M, N, K, epi, s);
+      case EPI_STORE_F32:
+        return run_gemm<BM, kSkinnyBN, WGM, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, epi, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  Epi pe{};
+  pe.kind = EPI_STORE_F32;
+  pe.out = part;
+  pe.ldo = N;
+  hipError_t e = run_gemm<BM, kSkinnyBN, WGM, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
+  if (e != hipSuccess) return e;
+  int64_t n_out;
+  if (epi.kind == EPI_SWIGLU) n_out = (int64_t)M * epi.ffn;
+  else if (epi.kind == EPI_QKV) n_out = (int64_t)M * (epi.n_q_heads + 2 * epi.n_kv_heads) * (epi.head_dim / 2);
+  else n_out = (int64_t)M * N;
+  splitk_epi_kernel<<<(unsigned)((n_out + 255) / 256), 256, 0, s>>>(part, splits, M, N, epi);
+  return hipGetLastError();
+}
+
+hipError_t launch_skinny(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
+                         const Epi& epi, float* part, hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  const int splits = skinny_splits(M, N, K, epi.kind);
+  if (splits == 1 && epi.kind == EPI_QKV) return launch_gemm(A, lda, B, ldb, M, N, K, epi, s);
+  if (M <= 64) return run_skinny<64, 2>(A, lda, B, ldb, M, N, K, epi, part, splits, s);
+  return run_skinny<128, 4>(A, lda, B, ldb, M, N, K, epi, part, splits, s);
 }
 
 }  // namespace tri

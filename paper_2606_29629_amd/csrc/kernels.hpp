@@ -61,12 +61,12 @@ hipError_t launch_kv_append_direct(const BatchDev& b, int n_slots, int max_seq, 
 hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
                        const Epi& epi, hipStream_t s);
 
-// Decode GEMM (M <= 128): streams B once; fp32 split-K partials in `part`,
-// then the epilogue kernel reduces them and applies `epi`.
-int gemv_splits(int M, int N, int K);
-size_t gemv_partial_bytes(int M, int N, int K);
-hipError_t launch_gemv(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
-                       const Epi& epi, float* part, hipStream_t s);
+// Decode projections (M <= 128): skinny tiles, split-K for narrow N; fp32
+// partials in `part` (skinny_partial_bytes) reduced by an epilogue kernel.
+int skinny_splits(int M, int N, int K, int kind);
+size_t skinny_partial_bytes(int M, int N, int K, int kind);
+hipError_t launch_skinny(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
+                         const Epi& epi, float* part, hipStream_t s);
 
 // Causal flash attention for sequences with q_len > 1 (or all when
 // include_single != 0).
