@@ -76,7 +76,7 @@ enum {
 typedef struct {
   int32_t hidden;         /* H; multiple of 64                                      */
   int32_t n_q_heads;      /* Hq                                                     */
-  int32_t n_kv_heads;     /* Hkv; Hq % Hkv == 0                                     */
+  int32_t n_kv_heads;     /* Hkv; Hq % Hkv == 0, Hq / Hkv <= 32                     */
   int32_t head_dim;       /* D in {64, 128}                                         */
   int32_t ffn_dim;        /* dense SwiGLU width F; multiple of 64 (dense only)      */
   int32_t n_experts;      /* E (MoE only), 1..256                                   */

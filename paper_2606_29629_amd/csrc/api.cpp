@@ -33,7 +33,7 @@ tri_status check_config(const tri_layer_config* c) {
   if (c->head_dim != 64 && c->head_dim != 128) return TRI_ERR_UNSUPPORTED;
   if (c->hidden % 64 != 0 || c->hidden > 8192) return TRI_ERR_UNSUPPORTED;
   if (c->n_q_heads % c->n_kv_heads != 0) return TRI_ERR_SHAPE;
-  if (c->n_q_heads / c->n_kv_heads > 8) return TRI_ERR_UNSUPPORTED;
+  if (c->n_q_heads / c->n_kv_heads > 32) return TRI_ERR_UNSUPPORTED;
   if ((int64_t)c->n_q_heads * c->head_dim % 64 != 0) return TRI_ERR_UNSUPPORTED;
   if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return TRI_ERR_RANGE;
   if (is_moe(c)) {
@@ -275,7 +275,8 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   }
   {
     StageTimer t_(ST_ATTN_COMBINE, s);
-    TRI_HIP(launch_attn_decode_combine(part, attn, bd, cache->n_slots, cache->max_seq, Hq, D, s));
+    TRI_HIP(launch_attn_decode_combine(part, attn, bd, cache->n_slots, cache->max_seq, Hq, Hkv, D,
+                                       s));
   }
   e = Epi{};
   e.kind = EPI_RESID;

@@ -1,197 +1,203 @@
 // Split-KV decode attention for sequences with one new token.
 //
 // Decode attention reads the whole KV cache of every sequence once per step
-// and does ~1 flop per byte, so it is HBM-bound.  The key range of each
-// (sequence, KV head) is split into chunks of kSplitKeys so the grid holds
-// enough workgroups to keep every CU streaming; one workgroup serves all query
-// heads of its KV head (grouped-query reuse: K and V are read once for the
-// whole group).
+// and does ~1 flop per byte, so it is HBM-bound: the kernel is a stream of the
+// cache through LDS with the arithmetic on the matrix cores.
 //
-// Thread layout: D/8 lanes per key row, 8 dims (one 16-byte load) per lane.
-// All K and V loads of the chunk are issued up front.  q.k uses bf16 dot2
-// instructions; the per-head partial dots of the D/8 lanes of a key are
-// reduced with a transposing butterfly (each exchange halves the number of
-// heads a lane carries), so 8 heads cost 8 exchanges instead of 32.  Softmax
-// statistics are per chunk (max in the log2 domain, sum); the combine kernel
-// merges the chunks: M = max m_s, L = sum l_s 2^(m_s - M),
-// o = sum acc_s 2^(m_s - M) / L.
+// Grid: (key split, KV head, sequence); one wave per workgroup.  The key
+// range [0, ctx + 1) of a (sequence, KV head) is cut into splits of
+// `split_keys` so that the grid holds enough waves to keep every CU
+// streaming; the wave serves all query heads of its KV head (grouped-query
+// reuse: K and V are read once for the whole group).
+//
+// The split's keys move in tiles of 32 rows (K and V, contiguous in the cache)
+// from HBM to a wave-private 3-stage LDS ring with buffer_load_dwordx4 ... lds;
+// two tiles are in flight while one is consumed, and only the wave's own
+// vmcnt orders them (no barrier).  Key rows past the sequence read as zero.
+//
+// Per tile, as in the prefill kernel with the group's heads as the query
+// columns: S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K rows from LDS,
+// B = Q of the group's heads, lane column = head); online softmax per head in
+// the log2 domain; O^T += V^T P^T with V^T read by ds_read_b64_tr_b16 and
+// P split into bf16 hi + lo parts (16 significant bits).
+//
+// Output per (token, head, split): the unnormalised accumulator, the running
+// max m (log2 domain) and sum l; the combine kernel merges the splits:
+// M = max m_s, L = sum l_s 2^(m_s - M), o = sum acc_s 2^(m_s - M) / L.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace tri {
 
-constexpr int kSplitKeys = 128;
-constexpr int kMaxGroup = 8;  // query heads per KV head
+constexpr int kDecTile = 32;     // keys per tile
+constexpr int kDecStages = 3;    // LDS ring depth
+constexpr int kDecMinSplit = 128;
 
-int attn_decode_splits(int max_kv) { return cdiv(max_kv < 1 ? 1 : max_kv, kSplitKeys); }
+// Keys per split: 512, or 128 when the grid would otherwise be small.
+int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv) {
+  const int64_t wgs = (int64_t)n_seqs * n_kv_heads * cdiv(max_kv < 1 ? 1 : max_kv, 512);
+  return wgs >= 768 ? 512 : kDecMinSplit;
+}
 
 size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv) {
-  return (size_t)n_tokens * n_q_heads * attn_decode_splits(max_kv) * (head_dim + 2) * sizeof(float);
+  const int ns = cdiv(max_kv < 1 ? 1 : max_kv, kDecMinSplit);  // bound for every split size
+  return (size_t)n_tokens * n_q_heads * ns * (head_dim + 2) * sizeof(float);
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void attn_decode_kernel(
+struct DecSmem {
+  bf16 k[kDecStages][kDecTile * D];  // [key][d], chunks swizzled by kv_chunk
+  bf16 v[kDecStages][kDecTile * D];
+};
+
+template <int D>
+__global__ __launch_bounds__(64) void attn_decode_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
     float* __restrict__ part, const int32_t* __restrict__ cu_q,
     const int32_t* __restrict__ ctx_len, const int32_t* __restrict__ slot, int n_slots,
-    int max_seq, int Hq, int Hkv, int nsplit, float scale_log2e, int n_tokens) {
-  constexpr int LPK = D / 8;          // lanes per key row
-  constexpr int KPR = 256 / LPK;      // keys per round (workgroup)
-  constexpr int ROUNDS = kSplitKeys / KPR;
-  constexpr int G = kMaxGroup;
-  __shared__ __align__(16) float sc[kSplitKeys][G];  // scores, then probabilities
-  __shared__ __align__(16) float red[4][G][D];       // cross-wave reduction of P V
-  __shared__ float stat[2][G];                       // chunk max (log2 domain), sum
+    int max_seq, int Hq, int Hkv, int nsplit, int split_keys, float scale_log2e, int n_tokens) {
+  constexpr int DC = D / 8;                  // 16-byte chunks per row
+  constexpr int TB = kDecTile * D * 2;       // bytes per K (or V) tile
+  constexpr int BLK = TB / 1024;             // 1 KB loads per tile and operand
+  constexpr int LPI = 2 * BLK;               // loads per tile
+  constexpr int DS = D / 16, DB = D / 32;
+  extern __shared__ __align__(16) char smem_raw[];
+  DecSmem<D>& sm = *reinterpret_cast<DecSmem<D>*>(smem_raw);
 
   const int s = blockIdx.z, kvh = blockIdx.y, sp = blockIdx.x;
   const int t = cu_q[s];
   if (cu_q[s + 1] - t != 1 || t < 0 || t >= n_tokens) return;
   const int c = ctx_len[s], sl = slot[s];
   if (sl < 0 || sl >= n_slots || c < 0 || c + 1 > max_seq) return;
-  const int L = c + 1;
-  const int k_begin = sp * kSplitKeys;
-  if (k_begin >= L) return;
-  const int k_end = min(L, k_begin + kSplitKeys);
+  const int k_begin = sp * split_keys;
+  const int k_end = min(c + 1, k_begin + split_keys);
+  if (k_begin >= k_end) return;
+  const int nt = cdiv(k_end - k_begin, kDecTile);
   const int grp = Hq / Hkv;
   const int qh0 = kvh * grp;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kl = tid / LPK, dc = tid % LPK;
-  const int64_t cache_off = ((int64_t)sl * Hkv + kvh) * max_seq * D + dc * 8;
+  const int lane = threadIdx.x;
+  const int r = lane & 31, g = lane >> 5;
+  const int64_t cache_off = ((int64_t)sl * Hkv + kvh) * max_seq * D;
+  // Rows at or past k_end read as zero.
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(Kc + cache_off), (short)0, k_end * D * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(Vc + cache_off), (short)0, k_end * D * 2, 0x00020000);
+  // Lane l of 1 KB block b fills tile row b (64 / DC) + l / DC, physical
+  // chunk l % DC = logical chunk kv_chunk(l % DC, row) (an involution).
+  uint32_t ld_off[BLK];
+#pragma unroll
+  for (int j = 0; j < BLK; ++j) {
+    const int row = j * (64 / DC) + lane / DC;
+    ld_off[j] = (uint32_t)((row * D + kv_chunk<D>(lane % DC, row) * 8) * 2);
+  }
+  // Tile i (keys k_begin + 32 i ...) into stage i % 3; tiles past the split
+  // are issued out of range (zero fill, no traffic) to keep the count uniform.
+  auto issue = [&](int i) {
+    const uint32_t kill = i < nt ? 0u : 0x80000000u;
+    const uint32_t kb = (uint32_t)(k_begin + kDecTile * (i < nt ? i : 0)) * D * 2;
+    const int st = i % kDecStages;
+#pragma unroll
+    for (int j = 0; j < BLK; ++j) {
+      buffer_load_lds16(rk, &sm.k[st][j * 512], (ld_off[j] | kill) + kb, 0);
+      buffer_load_lds16(rv, &sm.v[st][j * 512], (ld_off[j] | kill) + kb, 0);
+    }
+  };
+  // Q of head column r, loaded before the tiles so the first wait covers it
+  // too (heads past the group repeat the last one; their results are not
+  // written).
+  bf16x8 qf[DS];
+  {
+    const bf16* qp = Q + ((int64_t)t * Hq + qh0 + min(r, grp - 1)) * D + 8 * g;
+#pragma unroll
+    for (int k = 0; k < DS; ++k) qf[k] = *(const bf16x8*)(qp + 16 * k);
+  }
+  issue(0);
+  issue(1);
 
-  u32x4 kr[ROUNDS], vr[ROUNDS];
-#pragma unroll
-  for (int r = 0; r < ROUNDS; ++r) {
-    const int key = min(k_begin + r * KPR + kl, k_end - 1);
-    kr[r] = ldg16(Kc + cache_off + (int64_t)key * D);
-  }
-#pragma unroll
-  for (int r = 0; r < ROUNDS; ++r) {
-    const int key = min(k_begin + r * KPR + kl, k_end - 1);
-    vr[r] = ldg16(Vc + cache_off + (int64_t)key * D);
-  }
-  Pack8 qv[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    if (h < grp) qv[h].u = ldg16(Q + ((int64_t)t * Hq + qh0 + h) * D + dc * 8);
-    else qv[h].u = u32x4{0u, 0u, 0u, 0u};
-  }
+  const int tr_key = 4 * g + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  // ---- scores
+  f32x16 oacc[DB];
 #pragma unroll
-  for (int r = 0; r < ROUNDS; ++r) {
-    Pack8 kk;
-    kk.u = kr[r];
-    float v[G];
+  for (int b = 0; b < DB; ++b) oacc[b] = f32x16{0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  for (int i = 0; i < nt; ++i) {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPI) : "memory");  // tile i landed
+    issue(i + 2);  // into the stage of tile i - 1, whose reads fed issued MFMAs
+    const int st = i % kDecStages;
+    const int key0 = k_begin + kDecTile * i;
+    // S^T = K Q^T; element e: key key0 + 8 (e / 4) + 4 g + e % 4, head r.
+    f32x16 sacc = f32x16{0.f};
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float a = 0.f;
+    for (int k = 0; k < DS; ++k) {
+      const bf16x8 kf = *(const bf16x8*)&sm.k[st][r * D + kv_chunk<D>(2 * k + g, r) * 8];
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc, 0, 0, 0);
+    }
+    float mt = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bf16x2 qa = {qv[h].e[2 * e], qv[h].e[2 * e + 1]};
-        const bf16x2 ka = {kk.e[2 * e], kk.e[2 * e + 1]};
-        a = __builtin_amdgcn_fdot2_f32_bf16(qa, ka, a, false);
+    for (int e = 0; e < 16; ++e) {
+      const int key = key0 + 8 * (e >> 2) + 4 * g + (e & 3);
+      const float v = key < k_end ? sacc[e] * scale_log2e : -INFINITY;
+      sacc[e] = v;
+      mt = fmaxf(mt, v);
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float m_new = fmaxf(m_run, mt);  // finite: every tile has a valid key
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float ls = 0.f;
+    bf16x8 pf[2], pl[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = exp2f(sacc[8 * h + e] - m_new);
+        ls += p;
+        const bf16 hi = f2bf(p);
+        pf[h][e] = hi;
+        pl[h][e] = f2bf(p - bf2f(hi));
       }
-      v[h] = a;
-    }
-    // Transposing butterfly over the LPK lanes of this key.
-    int nv = G, head = 0;
+    l_run = l_run * alpha + ls;
 #pragma unroll
-    for (int m = LPK / 2; m >= 1; m >>= 1) {
-      if (nv > 1) {
-        const bool up = (dc & m) != 0;
-        const int hv = nv / 2;
+    for (int b = 0; b < DB; ++b) oacc[b] *= alpha;
+    // O^T += V^T P^T over the two 16-key groups of the tile.
+    const bf16* vb = sm.v[st];
 #pragma unroll
-        for (int i = 0; i < G / 2; ++i) {
-          if (i < hv) {
-            const float send = up ? v[i] : v[i + hv];
-            const float keep = up ? v[i + hv] : v[i];
-            v[i] = keep + __shfl_xor(send, m, 64);
-          }
-        }
-        if (up) head += hv;
-        nv = hv;
-      } else {
-        v[0] += __shfl_xor(v[0], m, 64);
+    for (int h = 0; h < 2; ++h) {
+      const int k1 = 16 * h + tr_key, k2 = k1 + 8;
+#pragma unroll
+      for (int b = 0; b < DB; ++b) {
+        const int col = 32 * b + tr_col;
+        union {
+          s16x4 s[2];
+          bf16x8 v;
+        } vf;
+        vf.s[0] = lds_read_tr16(vb + k1 * D + kv_chunk<D>(col >> 3, k1) * 8 + (col & 7));
+        vf.s[1] = lds_read_tr16(vb + k2 * D + kv_chunk<D>(col >> 3, k2) * 8 + (col & 7));
+        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.v, pf[h], oacc[b], 0, 0, 0);
+        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.v, pl[h], oacc[b], 0, 0, 0);
       }
     }
-    // After the butterfly every lane holds the full dot of head `head`;
-    // lanes of a key carry each head at least once.
-    const int key_local = r * KPR + kl;
-    const bool first = (dc & ((LPK / G > 1) ? (LPK / G - 1) : 0)) == 0;
-    if (first) {
-      const int key = k_begin + key_local;
-      sc[key_local][head] = key < k_end ? v[0] * scale_log2e : -INFINITY;
-    }
   }
-  __syncthreads();
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // no load may land in LDS after exit
 
-  // ---- chunk softmax statistics: wave w handles heads w and w + 4
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  if (r >= grp) return;
+  float* pp = part + (((int64_t)t * Hq + qh0 + r) * nsplit + sp) * (D + 2);
+  // oacc[b] element e: d = 32 b + 8 (e / 4) + 4 g + e % 4.
 #pragma unroll
-  for (int hh = 0; hh < 2; ++hh) {
-    const int h = wave + 4 * hh;
-    float mx = -INFINITY;
-    for (int k = lane; k < kSplitKeys; k += 64) mx = fmaxf(mx, sc[k][h]);
-    mx = wave_max(mx);
-    float sum = 0.f;
-    for (int k = lane; k < kSplitKeys; k += 64) {
-      const float p = exp2f(sc[k][h] - mx);
-      sc[k][h] = p;
-      sum += p;
+  for (int b = 0; b < DB; ++b)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pp[32 * b + 8 * r4 + 4 * g + e] = oacc[b][4 * r4 + e];
     }
-    sum = wave_sum(sum);
-    if (lane == 0) {
-      stat[0][h] = mx;
-      stat[1][h] = sum;
-    }
-  }
-  __syncthreads();
-
-  // ---- P V
-  float acc[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-#pragma unroll
-  for (int r = 0; r < ROUNDS; ++r) {
-    Pack8 vv;
-    vv.u = vr[r];
-    const int key_local = r * KPR + kl;
-    const f32x4 p0 = *(const f32x4*)&sc[key_local][0];
-    const f32x4 p1 = *(const f32x4*)&sc[key_local][4];
-    const float p[G] = {p0[0], p0[1], p0[2], p0[3], p1[0], p1[1], p1[2], p1[3]};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float x = bf2f(vv.e[e]);
-#pragma unroll
-      for (int h = 0; h < G; ++h) acc[h][e] += p[h] * x;
-    }
-  }
-  // lanes of a wave with the same dc: dc + LPK * j
-#pragma unroll
-  for (int m = LPK; m < 64; m <<= 1)
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] += __shfl_xor(acc[h][e], m, 64);
-  if (lane < LPK) {
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) red[wave][h][dc * 8 + e] = acc[h][e];
-  }
-  __syncthreads();
-  for (int i = tid; i < G * D; i += 256) {
-    const int h = i / D, d = i % D;
-    if (h >= grp) continue;
-    const float o = red[0][h][d] + red[1][h][d] + red[2][h][d] + red[3][h][d];
-    float* pp = part + (((int64_t)t * Hq + qh0 + h) * nsplit + sp) * (D + 2);
-    pp[d] = o;
-    if (d == 0) {
-      pp[D] = stat[0][h];
-      pp[D + 1] = stat[1][h];
-    }
+  if (g == 0) {
+    pp[D] = m_run;
+    pp[D + 1] = l_tot;
   }
 }
 
@@ -200,13 +206,13 @@ template <int D>
 __global__ __launch_bounds__(128) void attn_combine_kernel(
     const float* __restrict__ part, bf16* __restrict__ O, const int32_t* __restrict__ cu_q,
     const int32_t* __restrict__ ctx_len, const int32_t* __restrict__ slot, int n_slots,
-    int max_seq, int Hq, int nsplit, int n_tokens) {
+    int max_seq, int Hq, int nsplit, int split_keys, int n_tokens) {
   const int s = blockIdx.x, qh = blockIdx.y, d = threadIdx.x;
   const int t = cu_q[s];
   if (cu_q[s + 1] - t != 1 || t < 0 || t >= n_tokens) return;
   const int c = ctx_len[s], sl = slot[s];
   if (sl < 0 || sl >= n_slots || c < 0 || c + 1 > max_seq) return;
-  const int ns = min(cdiv(c + 1, kSplitKeys), nsplit);  // never past the launched splits
+  const int ns = min(cdiv(c + 1, split_keys), nsplit);  // never past the launched splits
   const float* pp = part + ((int64_t)t * Hq + qh) * nsplit * (D + 2);
   float M = -INFINITY;
   for (int i = 0; i < ns; ++i) M = fmaxf(M, pp[i * (D + 2) + D]);
@@ -219,36 +225,46 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(
   O[((int64_t)t * Hq + qh) * D + d] = f2bf(o / Lsum);
 }
 
+template <int D>
+static hipError_t run_decode(const void* q, const void* kc, const void* vc, float* part,
+                             const BatchDev& b, int n_slots, int max_seq, int Hq, int Hkv,
+                             hipStream_t s) {
+  const int max_kv = b.max_ctx_len + 1;
+  const int split = attn_decode_split_keys(b.n_seqs, Hkv, max_kv);
+  const int nsplit = cdiv(max_kv, split);
+  const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
+  dim3 grid(nsplit, Hkv, b.n_seqs);
+  attn_decode_kernel<D><<<grid, 64, sizeof(DecSmem<D>), s>>>(
+      (const bf16*)q, (const bf16*)kc, (const bf16*)vc, part, b.cu_q, b.ctx_len, b.slot, n_slots,
+      max_seq, Hq, Hkv, nsplit, split, scale_log2e, b.n_tokens);
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_decode_split(const void* q, const void* kc, const void* vc, float* part,
                                     const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
                                     int n_kv_heads, int head_dim, hipStream_t s) {
   if (b.n_seqs == 0) return hipSuccess;
-  const int nsplit = attn_decode_splits(b.max_ctx_len + 1);
-  const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)head_dim));
-  dim3 grid(nsplit, n_kv_heads, b.n_seqs);
   if (head_dim == 128)
-    attn_decode_kernel<128><<<grid, 256, 0, s>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vc,
-                                                 part, b.cu_q, b.ctx_len, b.slot, n_slots, max_seq,
-                                                 n_q_heads, n_kv_heads, nsplit, scale_log2e, b.n_tokens);
-  else
-    attn_decode_kernel<64><<<grid, 256, 0, s>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vc,
-                                                part, b.cu_q, b.ctx_len, b.slot, n_slots, max_seq,
-                                                n_q_heads, n_kv_heads, nsplit, scale_log2e, b.n_tokens);
-  return hipGetLastError();
+    return run_decode<128>(q, kc, vc, part, b, n_slots, max_seq, n_q_heads, n_kv_heads, s);
+  return run_decode<64>(q, kc, vc, part, b, n_slots, max_seq, n_q_heads, n_kv_heads, s);
 }
 
 hipError_t launch_attn_decode_combine(const float* part, void* out, const BatchDev& b,
-                                      int n_slots, int max_seq, int n_q_heads, int head_dim,
-                                      hipStream_t s) {
+                                      int n_slots, int max_seq, int n_q_heads, int n_kv_heads,
+                                      int head_dim, hipStream_t s) {
   if (b.n_seqs == 0) return hipSuccess;
-  const int nsplit = attn_decode_splits(b.max_ctx_len + 1);
+  const int max_kv = b.max_ctx_len + 1;
+  const int split = attn_decode_split_keys(b.n_seqs, n_kv_heads, max_kv);
+  const int nsplit = cdiv(max_kv, split);
   dim3 cgrid(b.n_seqs, n_q_heads);
   if (head_dim == 128)
     attn_combine_kernel<128><<<cgrid, 128, 0, s>>>(part, (bf16*)out, b.cu_q, b.ctx_len, b.slot,
-                                                   n_slots, max_seq, n_q_heads, nsplit, b.n_tokens);
+                                                   n_slots, max_seq, n_q_heads, nsplit, split,
+                                                   b.n_tokens);
   else
     attn_combine_kernel<64><<<cgrid, 64, 0, s>>>(part, (bf16*)out, b.cu_q, b.ctx_len, b.slot,
-                                                 n_slots, max_seq, n_q_heads, nsplit, b.n_tokens);
+                                                 n_slots, max_seq, n_q_heads, nsplit, split,
+                                                 b.n_tokens);
   return hipGetLastError();
 }
 

@@ -28,33 +28,12 @@ namespace tri {
 constexpr int kFaBQ = 128;  // queries per workgroup
 constexpr int kFaBK = 64;   // keys per tile
 
-// Physical 16-byte chunk of logical chunk c in K/V tile row r (LDS: 64 banks
-// of 4 bytes).
-//  D = 128 (256-byte rows): c ^ g(r), g(r) = 4 (r % 4) + (r / 4) % 4.  g is a
-//    bijection on 16 consecutive rows (K fragment reads: 16 rows, one chunk,
-//    per 16-lane phase) and takes 4 distinct values of g / 4 on 4 aligned
-//    rows (transposing V reads: 4 rows x 4 aligned chunks per 32 lanes).
-//  D = 64 (128-byte rows, two per bank window): c ^ g(r / 2),
-//    g(i) = 4 (i % 2) + (i / 2) % 4, distinct over the 8 rows of one parity
-//    among 16, and differing in bit 2 between rows 4a and 4a + 2.
-template <int D>
-__device__ __forceinline__ int kv_chunk(int c, int r) {
-  if constexpr (D == 128) return c ^ (((r & 3) << 2) | ((r >> 2) & 3));
-  else return c ^ (((r & 2) << 1) | ((r >> 2) & 3));
-}
-
+// K/V tile chunk swizzle: kv_chunk (common.hpp).
 template <int D>
 struct FaSmem {
   bf16 k[2][kFaBK * D];  // [key][d], chunks swizzled by kv_chunk
   bf16 v[2][kFaBK * D];  // [key][d], chunks swizzled by kv_chunk
 };
-
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ s16x4 lds_read_tr16(const bf16* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) s16x4*)(p));
-}
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(

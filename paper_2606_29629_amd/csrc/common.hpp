@@ -66,4 +66,30 @@ __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z));
 
 __host__ __device__ constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }
 
+
+// ---- K/V tiles in LDS (attention).  Tile rows are one key's D values
+// (D * 2 bytes); physical 16-byte chunk of logical chunk c in row r:
+//  D = 128 (256-byte rows): c ^ g(r), g(r) = 4 (r % 4) + (r / 4) % 4.  g is a
+//    bijection on 16 consecutive rows (a K fragment read: 16 rows, one chunk,
+//    per 16-lane phase) and takes 4 distinct values of g / 4 on 4 aligned rows
+//    (a transposing V read: 4 rows x 4 aligned chunks per 32 lanes).
+//  D = 64 (128-byte rows, two per bank window): c ^ h(r / 2),
+//    h(i) = 4 (i % 2) + (i / 2) % 4, distinct over the 8 rows of one parity
+//    among 16, and differing in bit 2 between rows 4a and 4a + 2.
+template <int D>
+__device__ __forceinline__ int kv_chunk(int c, int r) {
+  if constexpr (D == 128) return c ^ (((r & 3) << 2) | ((r >> 2) & 3));
+  else return c ^ (((r & 2) << 1) | ((r >> 2) & 3));
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane j receives element
+// m = 0..3 from the 16-bit value at (address of lane 4 m + j / 4) + 2 (j % 4)
+// bytes.  With the lanes of quad q pointing at 4 consecutive values of row q,
+// lane j gets column j of those 4 rows: a 4 x 16 transpose.
+__device__ __forceinline__ s16x4 lds_read_tr16(const bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+}
+
 }  // namespace tri

@@ -122,7 +122,7 @@ def test_null_and_unsupported(lib):
     assert call(lib, c=cfg(hidden=200)) == T.TRI_ERR_UNSUPPORTED
     assert call(lib, c=cfg(ffn_dim=100)) == T.TRI_ERR_UNSUPPORTED
     assert call(lib, c=cfg(n_q_heads=5)) == T.TRI_ERR_SHAPE
-    assert call(lib, c=cfg(n_q_heads=32, n_kv_heads=2)) == T.TRI_ERR_UNSUPPORTED  # group > 8
+    assert call(lib, c=cfg(n_q_heads=66, n_kv_heads=2)) == T.TRI_ERR_UNSUPPORTED  # group > 32
     assert call(lib, c=cfg(rope_base=0.0)) == T.TRI_ERR_RANGE
     assert call(lib, w=T.LayerWeights()) == T.TRI_ERR_NULL
     assert call(lib, x=None) == T.TRI_ERR_NULL
