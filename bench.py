@@ -20,7 +20,6 @@ from __future__ import annotations
 import argparse
 import json
 import os
-import subprocess
 import sys
 import time
 
@@ -66,23 +65,62 @@ def profiled_traffic(kernel: str):
     return None
 
 
-def energy_j():
-    """Board energy counter in joules via amd-smi, or None if unavailable."""
-    try:
-        out = subprocess.run(["amd-smi", "metric", "--energy", "--json"], capture_output=True,
-                             text=True, timeout=20).stdout
-        d = json.loads(out)
-        d = d[0] if isinstance(d, list) else d
-        e = d.get("energy", d)
-        v = e.get("total_energy_consumption", e)
-        if isinstance(v, dict):
-            val, unit = float(v["value"]), v.get("unit", "J")
-        else:
-            val, unit = float(str(v).split()[0]), (str(v).split() + ["J"])[1]
-        scale = {"J": 1.0, "mJ": 1e-3, "uJ": 1e-6, "kJ": 1e3}.get(unit, 1.0)
-        return val * scale
-    except Exception:
+class Energy:
+    """Board energy counter of the GPU in use, read in-process through the
+    amdsmi library (accumulator x resolution, microjoules); None when the
+    library or the counter is unavailable."""
+
+    def __init__(self):
+        self.h = None
+        try:
+            import amdsmi
+            import torch
+            amdsmi.amdsmi_init()
+            handles = amdsmi.amdsmi_get_processor_handles()
+            h = handles[0] if len(handles) == 1 else None
+            bus = getattr(torch.cuda.get_device_properties(0), "pci_bus_id", None)
+            if h is None and bus is not None:
+                for c in handles:
+                    if int(str(amdsmi.amdsmi_get_gpu_device_bdf(c)).split(":")[1], 16) == bus:
+                        h = c
+            if h is not None:
+                amdsmi.amdsmi_get_energy_count(h)
+                self.amdsmi, self.h = amdsmi, h
+        except Exception:
+            self.h = None
+
+    def joules(self):
+        if self.h is None:
+            return None
+        try:
+            e = self.amdsmi.amdsmi_get_energy_count(self.h)
+            return e["energy_accumulator"] * e["counter_resolution"] * 1e-6
+        except Exception:
+            return None
+
+
+def energy_loop(fn, min_s=2.0):
+    """Joules per call of fn over a loop of at least min_s seconds (the counter
+    updates every few ms), with average board power; None without a counter."""
+    import torch
+    meter = Energy()
+    if meter.h is None:
         return None
+    torch.cuda.synchronize()
+    t0, j0, n = time.perf_counter(), meter.joules(), 0
+    while True:
+        fn()
+        n += 1
+        if n % 4 == 0:
+            torch.cuda.synchronize()
+            if time.perf_counter() - t0 >= min_s:
+                break
+    torch.cuda.synchronize()
+    t1, j1 = time.perf_counter(), meter.joules()
+    if j0 is None or j1 is None or j1 <= j0:
+        return None
+    return {"joules_per_call": (j1 - j0) / n, "avg_power_w": (j1 - j0) / (t1 - t0),
+            "calls": n, "seconds": t1 - t0}
 
 
 def cpu_baseline(wl, wb, kb, vb, xb, budget_s=20.0):
@@ -128,23 +166,31 @@ def run_prefill(args, tri, wl, wb, kb, vb, xb):
         tri.layer_prefill(dl.cfg, dl.w, cache, db, x, out=out, workspace=ws)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    tri.profile_enable(True)
-    e_start = energy_j()
+
+    def step():
+        tri.layer_prefill(dl.cfg, dl.w, cache, db, x, out=out, workspace=ws)
+
+    # Timed region: exactly `steps` layer calls, no per-stage events.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        tri.layer_prefill(dl.cfg, dl.w, cache, db, x, out=out, workspace=ws)
+        step()
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    e_end = energy_j()
     ms = e0.elapsed_time(e1) / args.steps
+    # Same steps again with the library's per-stage HIP events (kernel times).
+    tri.profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
     prof = tri.profile_read()
     tri.profile_enable(False)
+    energy = energy_loop(step)
     del dl, cache, x, out, ws
     torch.cuda.empty_cache()
-    return ms, wall, prof, (None if e_start is None or e_end is None else e_end - e_start)
+    return ms, wall, prof, energy
 
 
 def run_decode(args, tri):
@@ -173,19 +219,25 @@ def run_decode(args, tri):
     torch.cuda.synchronize()
     reps = max(1, args.decode_reps)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    tri.profile_enable(True)
-    e_start = energy_j()
+
+    def sweep():
+        for s in range(steps):
+            tri.layer_decode(dl.cfg, dl.w, cache, batches[s], xs[s], out=out, workspace=ws)
+
     torch.cuda.synchronize()
     e0.record(stream)
     for _ in range(reps):
-        for s in range(steps):
-            tri.layer_decode(dl.cfg, dl.w, cache, batches[s], xs[s], out=out, workspace=ws)
+        sweep()
     e1.record(stream)
     torch.cuda.synchronize()
-    e_end = energy_j()
     total_ms = e0.elapsed_time(e1)
+    tri.profile_enable(True)
+    for _ in range(reps):
+        sweep()
+    torch.cuda.synchronize()
     prof = tri.profile_read()
     tri.profile_enable(False)
+    energy = energy_loop(sweep)
     n_tok = reps * steps * wl.batch.n_seqs
     kv_bytes = sum(int(bb.host["ctx_len"].astype(np.int64).sum() + bb.n_seqs) for bb in batches) \
         * wl.cfg.n_kv_heads * wl.cfg.head_dim * 2 * 2
@@ -205,8 +257,10 @@ def run_decode(args, tri):
                      "frac": attn_gbs / PEAK_HBM_GBS, "traffic": profiled_traffic("attn_decode")},
         "stages_ms_per_step": {k: v["total_ms"] / (reps * steps) for k, v in prof.items() if v["launches"]},
     }
-    if e_start is not None and e_end is not None:
-        res["joules_per_token"] = (e_end - e_start) / n_tok
+    if energy is not None:
+        res["energy"] = {"joules_per_token": energy["joules_per_call"] / (steps * wl.batch.n_seqs),
+                         "avg_power_w": energy["avg_power_w"], "seconds": energy["seconds"],
+                         "source": "amdsmi board energy counter"}
     del dl, cache, xs, out, ws
     torch.cuda.empty_cache()
     return res
@@ -297,7 +351,7 @@ def main(argv=None):
     wb = make_weights(wl.cfg, wl.seed)
     kb, vb = make_cache(wl.cfg, wl.n_slots, wl.max_seq, wl.seed)
     xb = make_x(wl.cfg, wl.batch.n_tokens, wl.seed)
-    ms, wall, prof, joules = run_prefill(args, tri, wl, wb, kb, vb, xb)
+    ms, wall, prof, energy = run_prefill(args, tri, wl, wb, kb, vb, xb)
     T = wl.batch.n_tokens
     flops = prefill_flops(wl.cfg, wl.batch)
     gu = prof["gate_up"]
@@ -331,8 +385,10 @@ def main(argv=None):
         "stages_ms_per_step": {k: v["total_ms"] / args.steps for k, v in prof.items() if v["launches"]},
         "wall_s_timed": wall,
     }
-    if joules is not None:
-        res["joules_per_token"] = joules / (T * args.steps)
+    if energy is not None:
+        res["energy"] = {"joules_per_token": energy["joules_per_call"] / T,
+                         "avg_power_w": energy["avg_power_w"], "seconds": energy["seconds"],
+                         "source": "amdsmi board energy counter"}
     if not args.no_decode:
         res["decode"] = run_decode(args, tri)
     if not args.no_secondary:
