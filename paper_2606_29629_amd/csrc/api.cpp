@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -60,7 +61,7 @@ tri_status check_batch_scalars(const tri_batch* b) {
 struct Layout {
   size_t tok_slot, tok_row, rope, h, q, attn, x1, h2, act, part;
   // MoE (n_pairs = T * top_k)
-  size_t route_idx, route_w, rank, counts, perm, inv, seg, tile_off, y;
+  size_t route_idx, route_w, rank, counts, perm, inv, seg, tile_off, y, logits;
   size_t total;
 };
 
@@ -111,6 +112,11 @@ Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
   l.seg = o;      o += up((E + 1) * 4);
   l.tile_off = o; o += up((E + 1) * 4);
   l.y = o;        o += up(P * H * 4);
+  // Router logit planes [S][T][E]: S * T <= max(T, 51200 / ceil(E / 64)) for
+  // every split count the GEMM picks (S > 1 only while S * tiles < 800), a
+  // bound that never decreases with T.
+  const size_t rows = moe ? std::max(T, (size_t)51200 / ((E + 63) / 64)) : 0;
+  l.logits = o;   o += up(rows * E * 4);
   l.total = o;
   return l;
 }
@@ -329,7 +335,8 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   {
     StageTimer t_(ST_ROUTER, s);
     TRI_HIP(launch_moe_route_bf16(h2, w->w_router, T, H, E, k,
-                                  (cfg->flags & TRI_F_MOE_RENORM) ? 1 : 0, idx, rw, s));
+                                  (cfg->flags & TRI_F_MOE_RENORM) ? 1 : 0,
+                                  at<float>(ws, L.logits), idx, rw, s));
   }
   {
     StageTimer t_(ST_MOE_PERMUTE, s);

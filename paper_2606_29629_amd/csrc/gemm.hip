@@ -24,7 +24,8 @@
 // maps every M-tile to its expert, A rows are gathered through the
 // permutation, and B is that expert's weight matrix.  The grid is sized from
 // an upper bound on the tile count and surplus workgroups exit, so no count is
-// read back to the host.
+// read back to the host; the real tiles are dealt to the XCDs in contiguous
+// shares so that an expert's M-tiles share its weights in one L2.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -381,8 +382,16 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
   extern __shared__ __align__(16) char smem_raw[];
   GemmSmem<BM, BN>& sm = *reinterpret_cast<GemmSmem<BM, BN>*>(smem_raw);
 
-  const int tn = blockIdx.x % tiles_n, mt = blockIdx.x / tiles_n;
-  if (mt >= tile_off[n_experts]) return;  // surplus tile
+  // The real tiles (tile_off[E] M-tiles x tiles_n) are dealt to the XCDs in
+  // contiguous shares (block b runs on XCD b % 8), so an expert's M-tiles run
+  // side by side on one XCD and share its weight k-slices in that L2;
+  // surplus blocks exit.
+  const int total = tile_off[n_experts] * tiles_n;
+  const int xcd = blockIdx.x % kXcds, loc = blockIdx.x / kXcds;
+  const int per = total / kXcds, rem = total % kXcds;
+  if (loc >= per + (xcd < rem ? 1 : 0)) return;  // surplus block
+  const int id = xcd * per + min(xcd, rem) + loc;
+  const int tn = id % tiles_n, mt = id / tiles_n;
   int lo = 0, hi = n_experts;             // expert e with tile_off[e] <= mt < tile_off[e+1]
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
@@ -628,6 +637,23 @@ hipError_t launch_skinny(const void* A, int lda, const void* B, int ldb, int M, 
   if (splits == 1 && epi.kind == EPI_QKV) return launch_gemm(A, lda, B, ldb, M, N, K, epi, s);
   if (M <= 64) return run_skinny<64, 2>(A, lda, B, ldb, M, N, K, epi, part, splits, s);
   return run_skinny<128, 4>(A, lda, B, ldb, M, N, K, epi, part, splits, s);
+}
+
+int gemm_planes_splits(int M, int N, int K) {
+  const int tiles = cdiv(M, 64) * cdiv(N, kSkinnyBN);
+  int s = 1;
+  while (tiles * s < 400 && s < 16 && K % (kBK * 2 * s) == 0) s *= 2;
+  return s;
+}
+
+hipError_t launch_gemm_planes(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
+                              float* planes, int splits, hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  Epi pe{};
+  pe.kind = EPI_STORE_F32;
+  pe.out = planes;
+  pe.ldo = N;
+  return run_gemm<64, kSkinnyBN, 2, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
 }
 
 }  // namespace tri

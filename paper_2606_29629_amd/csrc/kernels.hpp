@@ -61,6 +61,12 @@ hipError_t launch_kv_append_direct(const BatchDev& b, int n_slots, int max_seq, 
 hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
                        const Epi& epi, hipStream_t s);
 
+// fp32 C = A B^T as split-K planes [splits][M][N] (the consumer sums them
+// in plane order); gemm_planes_splits picks the split count.
+int gemm_planes_splits(int M, int N, int K);
+hipError_t launch_gemm_planes(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
+                              float* planes, int splits, hipStream_t s);
+
 // Decode projections (M <= 128): skinny tiles, split-K for narrow N; fp32
 // partials in `part` (skinny_partial_bytes) reduced by an epilogue kernel.
 int skinny_splits(int M, int N, int K, int kind);
@@ -95,8 +101,9 @@ hipError_t launch_gemm_grouped(const void* A, int lda, int a_rows, const int32_t
                                const Epi& epi, hipStream_t s);
 hipError_t launch_moe_route_f32(const float* h32, const void* w_router, int T, int H, int E,
                                 int k, int renorm, int32_t* idx, float* w, hipStream_t s);
+size_t moe_route_planes_bytes(int T, int H, int E);
 hipError_t launch_moe_route_bf16(const void* h, const void* w_router, int T, int H, int E, int k,
-                                 int renorm, int32_t* idx, float* w, hipStream_t s);
+                                 int renorm, float* planes, int32_t* idx, float* w, hipStream_t s);
 hipError_t launch_moe_permute(const int32_t* idx, int n_pairs, int E, int bm, int32_t* rank,
                               int32_t* counts, int32_t* perm, int32_t* inv, int32_t* seg,
                               int32_t* tile_off, hipStream_t s);

@@ -1,8 +1,10 @@
 // Mixture-of-experts routing, permutation and combine.
 //
-// Router: logits = h W_r^T in fp32 (fixed summation order per logit), softmax
-// over all experts, top-k by logit with ties to the lower expert index,
-// weights p[idx] (renormalised over the k chosen when asked).
+// Router: logits = h W_r^T accumulated in fp32, softmax over all experts,
+// top-k by logit with ties to the lower expert index, weights p[idx]
+// (renormalised over the k chosen when asked).  Inside the layer (bf16 h2) the
+// logits come from the matrix cores as split-K planes summed in a fixed order;
+// the fp32-input entry point uses a VALU kernel with a fixed summation order.
 //
 // Permutation (a counting sort, deterministic): for every expert e, one
 // workgroup scans the (token, slot) pairs in order and ranks the pairs routed
@@ -21,6 +23,58 @@ constexpr int kRouteChunk = 1024;  // hidden columns staged per pass
 
 template <typename InT>
 __device__ __forceinline__ float to_f32(InT v) { return (float)v; }
+
+// Top-k of one token's logits (lane holds experts lane + 64 q, q < 4; -inf
+// past E) with ties to the lower expert index, then the softmax weights of the
+// chosen experts (over all experts, or renormalised over the k chosen).
+// Lanes < k write slot `lane` of idx / w.
+__device__ __forceinline__ void route_topk(const float (&vin)[4], int E, int k, int renorm,
+                                           int lane, int32_t* __restrict__ idx,
+                                           float* __restrict__ w) {
+  float v[4], orig[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) v[q] = orig[q] = vin[q];
+  float top_v[16];
+  int top_i[16];
+  for (int s = 0; s < k; ++s) {
+    // this lane's best (highest value, then lowest expert index)
+    float bv = v[0];
+    int bi = lane;
+#pragma unroll
+    for (int q = 1; q < 4; ++q) {
+      const int e = lane + 64 * q;
+      if (v[q] > bv) { bv = v[q]; bi = e; }
+    }
+    if (bv == -INFINITY) bi = 0x7fffffff;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+    }
+    top_v[s] = bv;
+    top_i[s] = bi;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (lane + 64 * q == bi) v[q] = -INFINITY;
+  }
+  const float m = top_v[0];
+  float z = 0.f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (lane + 64 * q < E) z += expf(orig[q] - m);
+  z = wave_sum(z);
+  float zk = 0.f;
+  for (int s = 0; s < k; ++s) zk += expf(top_v[s] - m);
+  if (lane < k) {
+    float p = 0.f;
+    int ii = 0;
+    for (int s = 0; s < k; ++s)
+      if (s == lane) { p = expf(top_v[s] - m); ii = top_i[s]; }
+    idx[lane] = ii;
+    w[lane] = renorm ? p / zk : p / z;
+  }
+}
 
 template <typename InT>
 __global__ __launch_bounds__(256) void moe_router_kernel(const InT* __restrict__ h,
@@ -68,54 +122,36 @@ __global__ __launch_bounds__(256) void moe_router_kernel(const InT* __restrict__
   for (int tt = 0; tt < 2; ++tt) {
     const int r = 2 * wave + tt, t = t0 + r;
     if (t >= T) break;
-    float v[4], orig[4];
+    float v[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = lane + 64 * q;
       v[q] = e < E ? logit[r][e] : -INFINITY;
-      orig[q] = v[q];
     }
-    float top_v[16];
-    int top_i[16];
-    for (int s = 0; s < k; ++s) {
-      // this lane's best (highest value, then lowest expert index)
-      float bv = v[0];
-      int bi = lane;
-#pragma unroll
-      for (int q = 1; q < 4; ++q) {
-        const int e = lane + 64 * q;
-        if (v[q] > bv) { bv = v[q]; bi = e; }
-      }
-      if (bv == -INFINITY) bi = 0x7fffffff;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const float ov = __shfl_xor(bv, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
-      }
-      top_v[s] = bv;
-      top_i[s] = bi;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (lane + 64 * q == bi) v[q] = -INFINITY;
-    }
-    const float m = top_v[0];
-    float z = 0.f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (lane + 64 * q < E) z += expf(orig[q] - m);
-    z = wave_sum(z);
-    float zk = 0.f;
-    for (int s = 0; s < k; ++s) zk += expf(top_v[s] - m);
-    if (lane < k) {
-      float p = 0.f;
-      int ii = 0;
-      for (int s = 0; s < k; ++s)
-        if (s == lane) { p = expf(top_v[s] - m); ii = top_i[s]; }
-      idx_out[(int64_t)t * k + lane] = ii;
-      w_out[(int64_t)t * k + lane] = renorm ? p / zk : p / z;
-    }
+    route_topk(v, E, k, renorm, lane, idx_out + (int64_t)t * k, w_out + (int64_t)t * k);
   }
+}
+
+// Router on the matrix cores: the logits arrive as split-K planes
+// [S][T][E] (fp32, from a bf16 GEMM of h2 and W_r with fp32 accumulation);
+// they are summed in plane order (deterministic) before top-k.  One wave per
+// token.
+__global__ __launch_bounds__(256) void moe_topk_kernel(const float* __restrict__ planes, int S,
+                                                       int T, int E, int k, int renorm,
+                                                       int32_t* __restrict__ idx_out,
+                                                       float* __restrict__ w_out) {
+  const int lane = threadIdx.x & 63, t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  float v[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = lane + 64 * q;
+    float a = 0.f;
+    if (e < E)
+      for (int sp = 0; sp < S; ++sp) a += planes[((int64_t)sp * T + t) * E + e];
+    v[q] = e < E ? a : -INFINITY;
+  }
+  route_topk(v, E, k, renorm, lane, idx_out + (int64_t)t * k, w_out + (int64_t)t * k);
 }
 
 hipError_t launch_moe_route_f32(const float* h32, const void* w_router, int T, int H, int E,
@@ -126,11 +162,17 @@ hipError_t launch_moe_route_f32(const float* h32, const void* w_router, int T, i
   return hipGetLastError();
 }
 
+size_t moe_route_planes_bytes(int T, int H, int E) {
+  return (size_t)gemm_planes_splits(T, E, H) * T * E * sizeof(float);
+}
+
 hipError_t launch_moe_route_bf16(const void* h, const void* w_router, int T, int H, int E, int k,
-                                 int renorm, int32_t* idx, float* w, hipStream_t s) {
+                                 int renorm, float* planes, int32_t* idx, float* w, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  moe_router_kernel<bf16><<<cdiv(T, kRouteTok), 256, 0, s>>>((const bf16*)h, (const bf16*)w_router,
-                                                              T, H, E, k, renorm, idx, w);
+  const int S = gemm_planes_splits(T, E, H);
+  hipError_t e = launch_gemm_planes(h, H, w_router, H, T, E, H, planes, S, s);
+  if (e != hipSuccess) return e;
+  moe_topk_kernel<<<cdiv(T, 4), 256, 0, s>>>(planes, S, T, E, k, renorm, idx, w);
   return hipGetLastError();
 }
 
