@@ -18,8 +18,9 @@
 // Per tile, as in the prefill kernel with the group's heads as the query
 // columns: S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K rows from LDS,
 // B = Q of the group's heads, lane column = head); online softmax per head in
-// the log2 domain; O^T += V^T P^T with V^T read by ds_read_b64_tr_b16 and
-// P split into bf16 hi + lo parts (16 significant bits).
+// the log2 domain with a lazily raised max; O^T += V^T P^T with V^T read by
+// ds_read_b64_tr_b16 and P split into bf16 hi + lo parts (16 significant
+// bits).
 //
 // Output per (token, head, split): the unnormalised accumulator, the running
 // max m (log2 domain) and sum l; the combine kernel merges the splits:
@@ -122,7 +123,8 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(
   f32x16 oacc[DB];
 #pragma unroll
   for (int b = 0; b < DB; ++b) oacc[b] = f32x16{0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;  // running max in raw score units
+  const float slack_raw = kSoftmaxSlack / scale_log2e;
 
   for (int i = 0; i < nt; ++i) {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPI) : "memory");  // tile i landed
@@ -140,29 +142,33 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const int key = key0 + 8 * (e >> 2) + 4 * g + (e & 3);
-      const float v = key < k_end ? sacc[e] * scale_log2e : -INFINITY;
-      sacc[e] = v;
-      mt = fmaxf(mt, v);
+      if (key >= k_end) sacc[e] = -INFINITY;
+      mt = fmaxf(mt, sacc[e]);
     }
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);  // finite: every tile has a valid key
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    float ls = 0.f;
+    // Running max in raw score units, raised only past the slack (every tile
+    // has a valid key, so m_run is finite after the first).
+    const bool raise = mt > m_run + slack_raw;
+    if (__builtin_amdgcn_ballot_w64(raise)) {
+      const float m_new = raise ? mt : m_run;
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2e);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < DB; ++b) oacc[b] *= alpha;
+    }
+    const float mc = m_run * scale_log2e;
     bf16x8 pf[2], pl[2];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 2; ++h) {
+      float p8[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = exp2f(sacc[8 * h + e] - m_new);
-        ls += p;
-        const bf16 hi = f2bf(p);
-        pf[h][e] = hi;
-        pl[h][e] = f2bf(p - bf2f(hi));
+        p8[e] = __builtin_amdgcn_exp2f(fmaf(sacc[8 * h + e], scale_log2e, -mc));
+        l_run += p8[e];
       }
-    l_run = l_run * alpha + ls;
-#pragma unroll
-    for (int b = 0; b < DB; ++b) oacc[b] *= alpha;
+      split_hilo8(p8, pf[h], pl[h]);
+    }
     // O^T += V^T P^T over the two 16-key groups of the tile.
     const bf16* vb = sm.v[st];
 #pragma unroll
@@ -196,7 +202,7 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(
       for (int e = 0; e < 4; ++e) pp[32 * b + 8 * r4 + 4 * g + e] = oacc[b][4 * r4 + e];
     }
   if (g == 0) {
-    pp[D] = m_run;
+    pp[D] = m_run * scale_log2e;  // log2 domain for the combine
     pp[D + 1] = l_tot;
   }
 }

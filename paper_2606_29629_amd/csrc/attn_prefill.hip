@@ -19,7 +19,9 @@
 // such reads give a lane its 8 keys in the order in which the score
 // accumulator holds them.  P is split into P_hi = bf16(P) and
 // P_lo = bf16(P - P_hi), two MFMAs into one accumulator, so the weights keep
-// 16 significant bits.  Scores use exp2 with 1/sqrt(D) * log2(e) folded in.
+// 16 significant bits.  Softmax in the log2 domain: one FMA (scale and max)
+// and one v_exp_f32 per score; the running max is raised lazily (only past a
+// slack of 8), so the accumulators are rescaled on few tiles.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -112,7 +114,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   f32x16 oacc[DB];
 #pragma unroll
   for (int b = 0; b < DB; ++b) oacc[b] = f32x16{0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;  // running max in raw score units
+  const float slack_raw = kSoftmaxSlack / scale_log2e;
 
   gload(0, 0);
   for (int kt = 0; kt < nkt; ++kt) {
@@ -135,43 +138,47 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
         sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t], sacc[kb], 0, 0, 0);
       }
     }
-    // Mask + scale; element r of block kb is key key0 + 32kb + (r%4) + 8(r/4) + 4lg.
+    // Mask (raw scores; the scale is applied inside the exponent); element r
+    // of block kb is key key0 + 32kb + (r%4) + 8(r/4) + 4lg.
     const bool diag = key0 + kFaBK - 1 > wave_qmin;
     float mt = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float v = sacc[kb][r] * scale_log2e;
         if (diag) {
           const int key = key0 + 32 * kb + (r & 3) + 8 * (r >> 2) + 4 * lg;
-          if (key > qpos) v = -INFINITY;
+          if (key > qpos) sacc[kb][r] = -INFINITY;
         }
-        sacc[kb][r] = v;
-        mt = fmaxf(mt, v);
+        mt = fmaxf(mt, sacc[kb][r]);
       }
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
-    // m_new is finite: key 0 of the first tile is visible to every query.
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
-    float ls = 0.f;
+    // Raise the running max (raw units) only past the slack; rescale when
+    // any lane of the wave did.  m_run is finite after the first tile (key 0
+    // is visible to every query).
+    const bool raise = mt > m_run + slack_raw;
+    if (__builtin_amdgcn_ballot_w64(raise)) {
+      const float m_new = raise ? mt : m_run;
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2e);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < DB; ++b) oacc[b] *= alpha;
+    }
+    const float mc = m_run * scale_log2e;
     bf16x8 pf[4], pl[4];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < 2; ++h) {
+        float p8[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float p = exp2f(sacc[kb][8 * h + e] - m_new);
-          ls += p;
-          const bf16 hi = f2bf(p);
-          pf[2 * kb + h][e] = hi;
-          pl[2 * kb + h][e] = f2bf(p - bf2f(hi));
+          p8[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 * h + e], scale_log2e, -mc));
+          l_run += p8[e];
         }
-    l_run = l_run * alpha + ls;
-#pragma unroll
-    for (int b = 0; b < DB; ++b) oacc[b] *= alpha;
+        split_hilo8(p8, pf[2 * kb + h], pl[2 * kb + h]);
+      }
     // O^T += V^T P^T over four 16-key groups.
     const bf16* vb = sm.v[buf];
 #pragma unroll

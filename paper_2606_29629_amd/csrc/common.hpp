@@ -92,4 +92,32 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
 }
 
+
+// Two fp32 -> packed bf16 pair (RNE, one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  bf16x2 v = {(bf16)a, (bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Split of 8 fp32 values into bf16 hi + lo MFMA operands: hi = bf16(p)
+// (RNE, packed in pairs), lo = bf16(p - hi) with the difference exact in
+// fp32; hi + lo keeps ~16 significant bits of p.  Six VALU instructions per
+// pair: two conversions, two unpacks (shift / mask) and two subtractions.
+__device__ __forceinline__ void split_hilo8(const float (&p)[8], bf16x8& hi, bf16x8& lo) {
+  u32x4 h, l;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h[i] = pack_bf16x2(p[2 * i], p[2 * i + 1]);
+    l[i] = pack_bf16x2(p[2 * i] - __uint_as_float(h[i] << 16),
+                       p[2 * i + 1] - __uint_as_float(h[i] & 0xffff0000u));
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
+// Online softmax: the running max is only raised when a tile's max exceeds
+// it by more than this many log2 units; weights then stay below 2^8, and
+// the stale max cancels exactly in the final normalisation.
+constexpr float kSoftmaxSlack = 8.0f;
+
 }  // namespace tri
