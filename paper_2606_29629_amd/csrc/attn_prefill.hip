@@ -125,19 +125,44 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     if (kt + 1 < nkt) gload(kt + 1, buf ^ 1);
     const int key0 = kt * kFaBK;
     if (key0 > wave_qmin + 31) continue;  // no key of this tile is visible to this wave
-    // S^T = K Q^T for two 32-key blocks.
-    f32x16 sacc[2];
+    // S^T = K Q^T for two 32-key blocks: the two MFMA chains interleaved,
+    // K fragments read one k-step ahead.
+    f32x16 sacc[2] = {f32x16{0.f}, f32x16{0.f}};
+    bf16x8 kf[2][2];
+    auto kread = [&](int t, bf16x8 (&dst)[2]) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      sacc[kb] = f32x16{0.f};
-      const int key = kb * 32 + lr;
-#pragma unroll
-      for (int t = 0; t < DS; ++t) {
-        const bf16x8 kf =
-            *(const bf16x8*)&sm.k[buf][key * D + kv_chunk<D>(2 * t + lg, key) * 8];
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t], sacc[kb], 0, 0, 0);
+      for (int kb = 0; kb < 2; ++kb) {
+        const int key = kb * 32 + lr;
+        dst[kb] = *(const bf16x8*)&sm.k[buf][key * D + kv_chunk<D>(2 * t + lg, key) * 8];
       }
+    };
+    kread(0, kf[0]);
+    // Matrix phases run at raised wave priority, so that the other wave on
+    // this SIMD fills the gaps with its softmax instead of competing.
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int t = 0; t < DS; ++t) {
+      if (t + 1 < DS) kread(t + 1, kf[(t + 1) & 1]);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t & 1][kb], qf[t], sacc[kb], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
+    // V^T fragments of a 16-key group (two transposing reads per d block),
+    // the first group issued before the softmax.
+    const bf16* vb = sm.v[buf];
+    union VFrag { s16x4 s[2]; bf16x8 h; };
+    VFrag vf[2][DB];
+    auto vread = [&](int g16, VFrag (&dst)[DB]) {
+      const int k1 = 16 * g16 + tr_key, k2 = k1 + 8;
+#pragma unroll
+      for (int bb = 0; bb < DB; ++bb) {
+        const int col = 32 * bb + tr_col;
+        dst[bb].s[0] = lds_read_tr16(vb + k1 * D + kv_chunk<D>(col >> 3, k1) * 8 + (col & 7));
+        dst[bb].s[1] = lds_read_tr16(vb + k2 * D + kv_chunk<D>(col >> 3, k2) * 8 + (col & 7));
+      }
+    };
+    vread(0, vf[0]);
     // Mask (raw scores; the scale is applied inside the exponent); element r
     // of block kb is key key0 + 32kb + (r%4) + 8(r/4) + 4lg.
     const bool diag = key0 + kFaBK - 1 > wave_qmin;
@@ -179,21 +204,21 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
         }
         split_hilo8(p8, pf[2 * kb + h], pl[2 * kb + h]);
       }
-    // O^T += V^T P^T over four 16-key groups.
-    const bf16* vb = sm.v[buf];
+    // O^T += V^T P^T over four 16-key groups: the hi MFMAs of the four d
+    // blocks, then the lo ones (four independent chains), with the next
+    // group's V fragments read meanwhile.
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int g16 = 0; g16 < 4; ++g16) {
-      const int k1 = 16 * g16 + tr_key, k2 = k1 + 8;
+      if (g16 + 1 < 4) vread(g16 + 1, vf[(g16 + 1) & 1]);
 #pragma unroll
-      for (int b = 0; b < DB; ++b) {
-        const int col = 32 * b + tr_col;
-        union { s16x4 s[2]; bf16x8 h; } vf;
-        vf.s[0] = lds_read_tr16(vb + k1 * D + kv_chunk<D>(col >> 3, k1) * 8 + (col & 7));
-        vf.s[1] = lds_read_tr16(vb + k2 * D + kv_chunk<D>(col >> 3, k2) * 8 + (col & 7));
-        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.h, pf[g16], oacc[b], 0, 0, 0);
-        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.h, pl[g16], oacc[b], 0, 0, 0);
-      }
+      for (int bb = 0; bb < DB; ++bb)
+        oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[g16 & 1][bb].h, pf[g16], oacc[bb], 0, 0, 0);
+#pragma unroll
+      for (int bb = 0; bb < DB; ++bb)
+        oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[g16 & 1][bb].h, pl[g16], oacc[bb], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
