@@ -81,6 +81,9 @@ size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
       g = mx(g, skinny_partial_bytes(Ts, H, c->ffn_dim, EPI_RESID));
     }
     p = mx(p, g);
+    // Large-M GEMMs: fp32 partials of their tail tiles (a constant bound, so
+    // the size stays non-decreasing in n_tokens).
+    if (T > kSkinnyMaxRows) p = mx(p, gemm_tail_bytes());
   }
   return p;
 }
@@ -183,7 +186,7 @@ T* at(void* ws, size_t off) { return (T*)((char*)ws + off); }
 tri_status run_linear(const void* A, int lda, const void* B, int M, int N, int K, const Epi& epi,
                       float* part, hipStream_t s) {
   if (M <= kSkinnyMaxRows) TRI_HIP(launch_skinny(A, lda, B, K, M, N, K, epi, part, s));
-  else TRI_HIP(launch_gemm(A, lda, B, K, M, N, K, epi, s));
+  else TRI_HIP(launch_gemm(A, lda, B, K, M, N, K, epi, part, s));
   return TRI_OK;
 }
 

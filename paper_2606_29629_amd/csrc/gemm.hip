@@ -42,19 +42,29 @@ constexpr int kXcds = 8;
 // each, i.e. all 16 slots of the window: no bank conflict.
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-// Tile index for this block: XCD-contiguous ranges, then grouped-M order.
-__device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n, int& tm,
-                                              int& tn) {
-  const int total = tiles_m * tiles_n;
-  const int per = total / kXcds, rem = total % kXcds;
+// XCD-contiguous remap of block id bid among n: the blocks of XCD x (those
+// with bid % 8 == x; dispatch is round-robin over the XCDs) take one
+// contiguous range of ids.
+__device__ __forceinline__ int xcd_id(int bid, int n) {
+  const int per = n / kXcds, rem = n % kXcds;
   const int x = bid % kXcds, loc = bid / kXcds;
-  const int id = x * per + min(x, rem) + loc;
+  return x * per + min(x, rem) + loc;
+}
+
+// Tile of grouped-M order id: groups of kGroupM M-tiles, walked column by
+// column, so co-resident tiles share A and B panels in L2.
+__device__ __forceinline__ void tile_of_id(int id, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int group = id / (kGroupM * tiles_n);
   const int first_m = group * kGroupM;
   const int gm = min(kGroupM, tiles_m - first_m);
   const int in = id - group * kGroupM * tiles_n;
   tm = first_m + in % gm;
   tn = in / gm;
+}
+
+__device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n, int& tm,
+                                              int& tn) {
+  tile_of_id(xcd_id(bid, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
 }
 
 template <int BM, int BN>
@@ -304,7 +314,8 @@ template <int BM, int BN, int WGM, int WGN, int EK>
 __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __restrict__ A, int lda,
                                                    const bf16* __restrict__ B, int ldb, int M,
                                                    int N, int K, int kc, Epi epi,
-                                                   int tiles_m, int tiles_n) {
+                                                   int tiles_m, int tiles_n, int full,
+                                                   int tsplit, float* __restrict__ tail) {
   using ML = Mainloop<BM, BN, WGM, WGN>;
   constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
   extern __shared__ __align__(16) char smem_raw[];
@@ -313,12 +324,21 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wv / WGN, wn = wv % WGN;
-  int tm, tn;
-  tile_of_block(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  // Blocks [0, full) run whole tiles (ids 0 .. full-1 of the grouped order);
+  // the ones after it run the last tiles in `tsplit` K-splits each (fp32
+  // partials to `tail`), so that a final partial round fills every CU.
+  int tm, tn, u = -1;
+  if ((int)blockIdx.x < full) {
+    tile_of_id(xcd_id(blockIdx.x, full), tiles_m, tiles_n, tm, tn);
+  } else {
+    u = blockIdx.x - full;
+    tile_of_id(full + u / tsplit, tiles_m, tiles_n, tm, tn);
+    kc = K / tsplit;
+  }
   const int n_rows_b = EK == EPI_SWIGLU ? 2 * epi.ffn : N;
   // Split-K (fp32 partial output only): split z covers k in [z kc, z kc + kc)
   // and writes plane z of the output.
-  const int k0 = blockIdx.y * kc;
+  const int k0 = (u >= 0 ? u % tsplit : (int)blockIdx.y) * kc;
   K = min(kc, K - k0);
   A += k0;
   B += k0;
@@ -350,6 +370,13 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
   ML::run(sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
 
   const int lr = lane & 31, lg = lane >> 5;
+  if (u >= 0) {  // tail split: the tile's fp32 partial sums, [BM][BN]
+    Epi e{};
+    e.out = tail + (int64_t)u * BM * BN;
+    e.ldo = BN;
+    plain_epilogue<MI, NI, EPI_STORE_F32>(acc, e, wm * WM + 4 * lg, BM, wn * WN + lr, BN);
+    return;
+  }
   const int row0 = tm * BM + wm * WM + 4 * lg;
   if constexpr (EK == EPI_STORE_F32) {
     Epi e = epi;
@@ -460,19 +487,147 @@ static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M
   if (e != hipSuccess) return e;
   const int kc = K / splits;
   gemm_kernel<BM, BN, WGM, WGN, EK><<<dim3(tiles_m * tiles_n, splits), WGM * WGN * 64, smem, s>>>(
-      (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, kc, epi, tiles_m, tiles_n);
+      (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, kc, epi, tiles_m, tiles_n,
+      tiles_m * tiles_n, 1, nullptr);
+  return hipGetLastError();
+}
+
+// Tail split of a large GEMM: with 256 x 256 tiles, one workgroup per CU,
+// the last (tiles % CUs) tiles would run as a partial round; split into
+// `tsplit` K-parts they fill it.  Returns tsplit (1 = no tail split).
+static int cu_count() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n = v;
+    else
+      n = 256;
+  }
+  return n;
+}
+
+static int tail_split(int total, int K, int kind) {
+  const int G = cu_count();
+  const int rem = total % G;
+  if (kind == EPI_SWIGLU || total <= G || rem == 0) return 1;
+  int t = G / rem;
+  if (t > 4) t = 4;
+  while (t > 1 && K % (kBK * t) != 0) --t;
+  return t;
+}
+
+// Bound for every large GEMM: the tail tiles times their splits never exceed
+// one round (the CU count) of 256 x 256 fp32 tiles.
+size_t gemm_tail_bytes() { return (size_t)cu_count() * 256 * 256 * sizeof(float); }
+
+// Sum of a tail tile's split partials in split order + the epilogue.
+// Workgroup (j, chunk): tail tile j (id full + j of the grouped order),
+// elements [chunk * 2048, chunk * 2048 + 2048) of the tile (rotary pairs for
+// q/k/v), 8 per thread.
+constexpr int kTailChunk = 2048;
+
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__ tail, int tsplit,
+                                                       int full, int tiles_m, int tiles_n, int M,
+                                                       int N, Epi epi) {
+  const int j = blockIdx.y;
+  int tm, tn;
+  tile_of_id(full + j, tiles_m, tiles_n, tm, tn);
+  const float* tp = tail + (int64_t)j * tsplit * BM * BN;
+  auto sum = [&](int r, int c) {
+    float v = 0.f;
+    for (int sp = 0; sp < tsplit; ++sp) v += tp[(int64_t)sp * BM * BN + r * BN + c];
+    return v;
+  };
+  const int e0 = blockIdx.x * kTailChunk;
+  if (epi.kind != EPI_QKV) {
+    for (int e = e0 + threadIdx.x; e < e0 + kTailChunk && e < BM * BN; e += 256) {
+      const int r = e / BN, c = e % BN;
+      const int row = tm * BM + r, col = tn * BN + c;
+      if (row >= M || col >= N) continue;
+      float v = sum(r, c);
+      if (epi.kind == EPI_STORE_F32) {
+        ((float*)epi.out)[(int64_t)row * epi.ldo + col] = v;
+        continue;
+      }
+      if (epi.kind == EPI_RESID) v += bf2f(((const bf16*)epi.resid)[(int64_t)row * epi.ldr + col]);
+      ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(v);
+    }
+    return;
+  }
+  // q/k/v + bias + RoPE + cache write: one thread per rotary pair (a head of
+  // D columns lies inside one tile since BN is a multiple of D).
+  const int Dh = epi.head_dim, half = Dh / 2;
+  const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
+  for (int e = e0 + threadIdx.x; e < e0 + kTailChunk && e < BM * (BN / 2); e += 256) {
+    const int r = e / (BN / 2), pc = e % (BN / 2);
+    const int c = (pc / half) * Dh + pc % half;  // first-half column in the tile
+    const int row = tm * BM + r, col = tn * BN + c;
+    if (row >= M || col >= N) continue;
+    const int head = col / Dh, d = col % Dh;
+    float x1 = sum(r, c), x2 = sum(r, c + half);
+    if (epi.bias) {
+      x1 += bf2f(((const bf16*)epi.bias)[col]);
+      x2 += bf2f(((const bf16*)epi.bias)[col + half]);
+    }
+    if (head < Hq + Hkv) {
+      const float2 cs = epi.rope[(int64_t)row * half + d];
+      const float y1 = x1 * cs.x - x2 * cs.y;
+      const float y2 = x2 * cs.x + x1 * cs.y;
+      x1 = y1;
+      x2 = y2;
+    }
+    if (head < Hq) {
+      bf16* qp = (bf16*)epi.q + ((int64_t)row * Hq + head) * Dh + d;
+      qp[0] = f2bf(x1);
+      qp[half] = f2bf(x2);
+    } else {
+      const int sl = epi.tok_slot[row];
+      if (sl < 0) continue;
+      const int kvh = head < Hq + Hkv ? head - Hq : head - Hq - Hkv;
+      bf16* cache = (bf16*)(head < Hq + Hkv ? epi.kc : epi.vc);
+      bf16* cp = cache + (((int64_t)sl * Hkv + kvh) * epi.max_seq + epi.tok_row[row]) * Dh + d;
+      cp[0] = f2bf(x1);
+      cp[half] = f2bf(x2);
+    }
+  }
+}
+
+template <int BM, int BN, int WGM, int WGN, int EK>
+static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, int M, int N,
+                                int K, const Epi& epi, float* tail, hipStream_t s) {
+  const int tiles_m = cdiv(M, BM);
+  const int tiles_n = EK == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
+  const int total = tiles_m * tiles_n;
+  const int t = tail ? tail_split(total, K, EK) : 1;
+  if (t == 1) return run_gemm<BM, BN, WGM, WGN, EK>(A, lda, B, ldb, M, N, K, epi, s);
+  const int n_tail = total % cu_count();
+  const int full = total - n_tail;
+  const size_t smem = sizeof(GemmSmem<BM, BN>);
+  static bool attr_set = false;
+  hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK>, smem, attr_set);
+  if (e != hipSuccess) return e;
+  gemm_kernel<BM, BN, WGM, WGN, EK><<<full + n_tail * t, WGM * WGN * 64, smem, s>>>(
+      (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, K, epi, tiles_m, tiles_n, full, t, tail);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int elems = EK == EPI_QKV ? BM * BN / 2 : BM * BN;
+  tail_epi_kernel<BM, BN><<<dim3(cdiv(elems, kTailChunk), n_tail), 256, 0, s>>>(
+      tail, t, full, tiles_m, tiles_n, M, N, epi);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
-                       const Epi& epi, hipStream_t s) {
+                       const Epi& epi, float* tail, hipStream_t s) {
   if (M == 0) return hipSuccess;
   switch (epi.kind) {
-    case EPI_STORE: return run_gemm<256, 256, 4, 2, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, s);
-    case EPI_RESID: return run_gemm<256, 256, 4, 2, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, s);
+    case EPI_STORE: return run_gemm_tail<256, 256, 4, 2, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, tail, s);
+    case EPI_RESID: return run_gemm_tail<256, 256, 4, 2, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, tail, s);
     case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU>(A, lda, B, ldb, M, N, K, epi, s);
-    case EPI_STORE_F32: return run_gemm<256, 256, 4, 2, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, epi, s);
-    default: return run_gemm<256, 256, 4, 2, EPI_QKV>(A, lda, B, ldb, M, N, K, epi, s);
+    case EPI_STORE_F32: return run_gemm_tail<256, 256, 4, 2, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, epi, tail, s);
+    default: return run_gemm_tail<256, 256, 4, 2, EPI_QKV>(A, lda, B, ldb, M, N, K, epi, tail, s);
   }
 }
 
@@ -634,7 +789,7 @@ hipError_t launch_skinny(const void* A, int lda, const void* B, int ldb, int M, 
                          const Epi& epi, float* part, hipStream_t s) {
   if (M == 0) return hipSuccess;
   const int splits = skinny_splits(M, N, K, epi.kind);
-  if (splits == 1 && epi.kind == EPI_QKV) return launch_gemm(A, lda, B, ldb, M, N, K, epi, s);
+  if (splits == 1 && epi.kind == EPI_QKV) return launch_gemm(A, lda, B, ldb, M, N, K, epi, nullptr, s);
   if (M <= 64) return run_skinny<64, 2>(A, lda, B, ldb, M, N, K, epi, part, splits, s);
   return run_skinny<128, 4>(A, lda, B, ldb, M, N, K, epi, part, splits, s);
 }

@@ -58,8 +58,11 @@ hipError_t launch_kv_append_direct(const BatchDev& b, int n_slots, int max_seq, 
                                    void* vc, hipStream_t s);
 
 // Prefill GEMM (large M): C[M,N] = A[M,K] B[N,K]^T with the fused epilogue.
+// `tail` (gemm_tail_bytes, may be null) holds the fp32 partials of the tiles
+// of a final partial round, which then run split in K.
+size_t gemm_tail_bytes();
 hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
-                       const Epi& epi, hipStream_t s);
+                       const Epi& epi, float* tail, hipStream_t s);
 
 // fp32 C = A B^T as split-K planes [splits][M][N] (the consumer sums them
 // in plane order); gemm_planes_splits picks the split count.
