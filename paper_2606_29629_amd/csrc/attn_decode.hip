@@ -34,10 +34,15 @@ constexpr int kDecTile = 32;     // keys per tile
 constexpr int kDecStages = 3;    // LDS ring depth
 constexpr int kDecMinSplit = 128;
 
-// Keys per split: 512, or 128 when the grid would otherwise be small.
+// Keys per split: the longest context cut into equal pieces of at most 512
+// keys (a multiple of the 32-key tile), or of at most 128 when the grid would
+// otherwise be small.
 int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv) {
-  const int64_t wgs = (int64_t)n_seqs * n_kv_heads * cdiv(max_kv < 1 ? 1 : max_kv, 512);
-  return wgs >= 768 ? 512 : kDecMinSplit;
+  if (max_kv < 1) max_kv = 1;
+  const int64_t wgs = (int64_t)n_seqs * n_kv_heads * cdiv(max_kv, 512);
+  const int cap = wgs >= 768 ? 512 : kDecMinSplit;
+  const int ns = cdiv(max_kv, cap);
+  return cdiv(cdiv(max_kv, ns), kDecTile) * kDecTile;
 }
 
 size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv) {
