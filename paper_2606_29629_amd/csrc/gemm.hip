@@ -493,8 +493,9 @@ static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M
 }
 
 // Tail split of a large GEMM: with 256 x 256 tiles, one workgroup per CU,
-// the last (tiles % CUs) tiles would run as a partial round; split into
-// `tsplit` K-parts they fill it.  Returns tsplit (1 = no tail split).
+// the last (tiles % CUs) tiles -- all of them when there are fewer tiles than
+// CUs -- would run as a partial round; split into `tsplit` K-parts they fill
+// it.
 static int cu_count() {
   static int n = 0;
   if (n == 0) {
@@ -508,12 +509,19 @@ static int cu_count() {
   return n;
 }
 
+// Tiles of the final partial round: total % CUs, or all of them when the
+// GEMM has fewer tiles than CUs.
+static int tail_tiles(int total) {
+  const int G = cu_count();
+  return total > G ? total % G : (total == G ? 0 : total);
+}
+
 static int tail_split(int total, int K, int kind) {
   const int G = cu_count();
-  const int rem = total % G;
-  if (kind == EPI_SWIGLU || total <= G || rem == 0) return 1;
+  const int rem = tail_tiles(total);
+  if (kind == EPI_SWIGLU || rem == 0) return 1;
   int t = G / rem;
-  if (t > 4) t = 4;
+  if (t > 8) t = 8;
   while (t > 1 && K % (kBK * t) != 0) --t;
   return t;
 }
@@ -603,7 +611,7 @@ static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, 
   const int total = tiles_m * tiles_n;
   const int t = tail ? tail_split(total, K, EK) : 1;
   if (t == 1) return run_gemm<BM, BN, WGM, WGN, EK>(A, lda, B, ldb, M, N, K, epi, s);
-  const int n_tail = total % cu_count();
+  const int n_tail = tail_tiles(total);
   const int full = total - n_tail;
   const size_t smem = sizeof(GemmSmem<BM, BN>);
   static bool attr_set = false;
