@@ -126,13 +126,13 @@ Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
 
 // ------------------------------------------------------------ profiling --
 enum Stage {
-  ST_TOKMAP, ST_NORM1, ST_QKV, ST_ATTN_PREFILL, ST_ATTN_DECODE, ST_ATTN_COMBINE, ST_OPROJ,
+  ST_PROLOGUE, ST_QKV, ST_ATTN_PREFILL, ST_ATTN_DECODE, ST_ATTN_COMBINE, ST_OPROJ,
   ST_NORM2, ST_GATEUP, ST_DOWN, ST_ROUTER, ST_MOE_PERMUTE, ST_MOE_GATEUP, ST_MOE_DOWN,
   ST_MOE_COMBINE, ST_APPEND, ST_COUNT
 };
 static_assert(ST_COUNT <= TRI_MAX_STAGES, "too many stages");
 const char* const kStageName[ST_COUNT] = {
-    "token_map", "rmsnorm_attn", "qkv_rope", "attn_prefill", "attn_decode", "attn_combine",
+    "prologue", "qkv_rope", "attn_prefill", "attn_decode", "attn_combine",
     "o_proj", "rmsnorm_mlp", "gate_up", "down", "moe_router", "moe_permute", "moe_gate_up",
     "moe_down", "moe_combine", "kv_append"};
 
@@ -247,13 +247,10 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   float* part = at<float>(ws, L.part);
 
   {
-    StageTimer t_(ST_TOKMAP, s);
-    TRI_HIP(launch_token_map(bd, cache->n_slots, cache->max_seq, D, cfg->rope_base, tok_slot,
-                             tok_row, rope, s));
-  }
-  {
-    StageTimer t_(ST_NORM1, s);
-    TRI_HIP(launch_rmsnorm(x_in, w->attn_norm, h, nullptr, T, H, cfg->rms_eps, s));
+    // token map + rotary table + pre-attention RMSNorm
+    StageTimer t_(ST_PROLOGUE, s);
+    TRI_HIP(launch_prologue(bd, cache->n_slots, cache->max_seq, D, cfg->rope_base, tok_slot,
+                            tok_row, rope, x_in, w->attn_norm, h, H, cfg->rms_eps, s));
   }
   Epi e{};
   e.kind = EPI_QKV;

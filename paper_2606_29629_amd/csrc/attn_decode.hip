@@ -225,13 +225,28 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(
   if (sl < 0 || sl >= n_slots || c < 0 || c + 1 > max_seq) return;
   const int ns = min(cdiv(c + 1, split_keys), nsplit);  // never past the launched splits
   const float* pp = part + ((int64_t)t * Hq + qh) * nsplit * (D + 2);
-  float M = -INFINITY;
-  for (int i = 0; i < ns; ++i) M = fmaxf(M, pp[i * (D + 2) + D]);
-  float Lsum = 0.f, o = 0.f;
-  for (int i = 0; i < ns; ++i) {
-    const float w = exp2f(pp[i * (D + 2) + D] - M);
-    Lsum += pp[i * (D + 2) + D + 1] * w;
-    o += pp[i * (D + 2) + d] * w;
+  // Splits in groups of 8: the group's (m, l, acc) loads are issued together,
+  // then folded in split order into a running (M, L, o).
+  float M = -INFINITY, Lsum = 0.f, o = 0.f;
+  for (int i0 = 0; i0 < ns; i0 += 8) {
+    float m[8], l[8], a[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool ok = i0 + j < ns;
+      const float* q = pp + (ok ? i0 + j : 0) * (D + 2);
+      m[j] = ok ? q[D] : -INFINITY;
+      l[j] = ok ? q[D + 1] : 0.f;
+      a[j] = ok ? q[d] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (i0 + j >= ns) break;
+      const float Mn = fmaxf(M, m[j]);
+      const float sc = exp2f(M - Mn), w = exp2f(m[j] - Mn);
+      Lsum = Lsum * sc + l[j] * w;
+      o = o * sc + a[j] * w;
+      M = Mn;
+    }
   }
   O[((int64_t)t * Hq + qh) * D + d] = f2bf(o / Lsum);
 }

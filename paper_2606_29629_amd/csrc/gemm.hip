@@ -687,9 +687,16 @@ __global__ __launch_bounds__(256) void splitk_epi_kernel(const float* __restrict
                                                        int splits, int M, int N, Epi epi) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t MN = (int64_t)M * N;
+  // All planes' values are loaded before the ordered sum (splits <= 16), so
+  // the loads are in flight together.
   auto sum = [&](int row, int col) {
+    const float* q = part + (int64_t)row * N + col;
+    float t[16];
+#pragma unroll
+    for (int s = 0; s < 16; ++s) t[s] = s < splits ? q[s * MN] : 0.f;
     float v = 0.f;
-    for (int s = 0; s < splits; ++s) v += part[s * MN + (int64_t)row * N + col];
+#pragma unroll
+    for (int s = 0; s < 16; ++s) v += t[s];
     return v;
   };
   if (epi.kind == EPI_STORE || epi.kind == EPI_RESID) {

@@ -35,12 +35,13 @@ struct Epi {
   int n_q_heads, n_kv_heads, head_dim, max_seq;
 };
 
-// Per-token map: slot and cache row of every token (-1 when out of range),
-// and the rotary table rope[t][i] = (cos, sin)(pos[t] * base^(-2i/D)), the
-// angle formed in double precision.
-hipError_t launch_token_map(const BatchDev& b, int n_slots, int max_seq, int head_dim,
-                            float rope_base, int32_t* tok_slot, int32_t* tok_row,
-                            float2* rope, hipStream_t s);
+// Layer prologue: per-token map (slot and cache row of every token, -1 when
+// out of range), the rotary table rope[t][i] = (cos, sin)(pos[t] *
+// base^(-2i/D)) (angle in double precision), and y = RMSNorm(x) * g.
+hipError_t launch_prologue(const BatchDev& b, int n_slots, int max_seq, int head_dim,
+                           float rope_base, int32_t* tok_slot, int32_t* tok_row, float2* rope,
+                           const void* x, const void* g, void* y, int hidden, float eps,
+                           hipStream_t s);
 
 // y = x / sqrt(mean(x^2) + eps) * g   (bf16 out, optional fp32 copy)
 hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int rows,

@@ -1,48 +1,9 @@
-// Bandwidth-bound helper kernels: token map + rotary table, RMSNorm, KV append.
+// Bandwidth-bound helper kernels: layer prologue (token map + rotary table +
+// RMSNorm), RMSNorm, KV append.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace tri {
-
-// One thread per (token, rotary pair).  Sequence of token t: the s with
-// cu_q[s] <= t < cu_q[s+1] (binary search over the non-decreasing offsets).
-__global__ void token_map_kernel(BatchDev b, int n_slots, int max_seq, int half, double base,
-                                 int32_t* tok_slot, int32_t* tok_row, float2* rope) {
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (gid >= (int64_t)b.n_tokens * half) return;
-  const int t = (int)(gid / half);
-  const int i = (int)(gid - (int64_t)t * half);
-  if (i == 0) {
-    int lo = 0, hi = b.n_seqs;  // find largest s with cu_q[s] <= t
-    while (hi - lo > 1) {
-      int mid = (lo + hi) >> 1;
-      if (b.cu_q[mid] <= t) lo = mid; else hi = mid;
-    }
-    const int s = lo;
-    const int sl = b.slot[s];
-    const int row = b.ctx_len[s] + (t - b.cu_q[s]);
-    const bool ok = sl >= 0 && sl < n_slots && row >= 0 && row < max_seq && t < b.cu_q[s + 1];
-    tok_slot[t] = ok ? sl : -1;
-    tok_row[t] = ok ? row : -1;
-  }
-  const double inv_freq = pow(base, -2.0 * (double)i / (double)(2 * half));
-  const double ang = (double)b.pos[t] * inv_freq;
-  double sn, cs;
-  sincos(ang, &sn, &cs);
-  rope[gid] = make_float2((float)cs, (float)sn);
-}
-
-hipError_t launch_token_map(const BatchDev& b, int n_slots, int max_seq, int head_dim,
-                            float rope_base, int32_t* tok_slot, int32_t* tok_row, float2* rope,
-                            hipStream_t s) {
-  const int half = head_dim / 2;
-  const int64_t n = (int64_t)b.n_tokens * half;
-  if (n == 0) return hipSuccess;
-  token_map_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(b, n_slots, max_seq, half,
-                                                               (double)rope_base, tok_slot,
-                                                               tok_row, rope);
-  return hipGetLastError();
-}
 
 // RMSNorm: one wave per row, 8 bf16 per lane per pass, fp32 sum of squares.
 constexpr int kNormMaxChunks = 16;  // hidden <= 64 lanes * 8 * 16 = 8192
@@ -57,13 +18,21 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const bf16* __restrict__ x
   if (row >= rows) return;
   const bf16* xr = x + (int64_t)row * hidden;
   const int nchunk = hidden / 8;
-  Pack8 v[kNormMaxChunks];
+  Pack8 v[kNormMaxChunks], gv[kNormMaxChunks];
   float ss = 0.f;
+  // x and g both loaded up front: one memory round trip before the reduction.
 #pragma unroll
   for (int c = 0; c < kNormMaxChunks; ++c) {
     const int ch = lane + c * 64;
     if (ch < nchunk) {
       v[c].u = ldg16(xr + ch * 8);
+      gv[c].u = ldg16(g + ch * 8);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < kNormMaxChunks; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nchunk) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float f = bf2f(v[c].e[e]);
@@ -77,12 +46,11 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const bf16* __restrict__ x
   for (int c = 0; c < kNormMaxChunks; ++c) {
     const int ch = lane + c * 64;
     if (ch < nchunk) {
-      Pack8 gg, o;
-      gg.u = ldg16(g + ch * 8);
+      Pack8 o;
       float f[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        f[e] = bf2f(v[c].e[e]) * r * bf2f(gg.e[e]);
+        f[e] = bf2f(v[c].e[e]) * r * bf2f(gv[c].e[e]);
         o.e[e] = f2bf(f[e]);
       }
       stg16(y + (int64_t)row * hidden + ch * 8, o.u);
@@ -100,6 +68,94 @@ hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int
   if (rows == 0) return hipSuccess;
   rmsnorm_kernel<<<cdiv(rows, 4), 256, 0, s>>>((const bf16*)x, (const bf16*)g, (bf16*)y, y32,
                                                rows, hidden, eps);
+  return hipGetLastError();
+}
+
+// Layer prologue, one wave per token t:
+//  * token map: the sequence s with cu_q[s] <= t < cu_q[s+1] (binary search
+//    over the non-decreasing offsets) gives the cache slot and row of t
+//    (-1 when out of range);
+//  * rotary table rope[t][i] = (cos, sin)(pos[t] * base^(-2i/D)), the angle
+//    formed in double precision, lane i < D/2;
+//  * RMSNorm of x[t] into y[t] (as rmsnorm_kernel).
+__global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, int n_slots, int max_seq,
+                                                       int half, double base,
+                                                       int32_t* __restrict__ tok_slot,
+                                                       int32_t* __restrict__ tok_row,
+                                                       float2* __restrict__ rope,
+                                                       const bf16* __restrict__ x,
+                                                       const bf16* __restrict__ g,
+                                                       bf16* __restrict__ y, int hidden,
+                                                       float eps) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= b.n_tokens) return;
+  // x and g loads first: their latency overlaps the map and the table.
+  const bf16* xr = x + (int64_t)t * hidden;
+  const int nchunk = hidden / 8;
+  Pack8 v[kNormMaxChunks], gv[kNormMaxChunks];
+#pragma unroll
+  for (int c = 0; c < kNormMaxChunks; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nchunk) {
+      v[c].u = ldg16(xr + ch * 8);
+      gv[c].u = ldg16(g + ch * 8);
+    }
+  }
+  if (lane == 0) {
+    int lo = 0, hi = b.n_seqs;  // largest s with cu_q[s] <= t
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (b.cu_q[mid] <= t) lo = mid; else hi = mid;
+    }
+    const int sq = lo;
+    const int sl = b.slot[sq];
+    const int row = b.ctx_len[sq] + (t - b.cu_q[sq]);
+    const bool ok = sl >= 0 && sl < n_slots && row >= 0 && row < max_seq && t < b.cu_q[sq + 1];
+    tok_slot[t] = ok ? sl : -1;
+    tok_row[t] = ok ? row : -1;
+  }
+  if (lane < half) {
+    const double inv_freq = pow(base, -2.0 * (double)lane / (double)(2 * half));
+    const double ang = (double)b.pos[t] * inv_freq;
+    double sn, cs;
+    sincos(ang, &sn, &cs);
+    rope[(int64_t)t * half + lane] = make_float2((float)cs, (float)sn);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < kNormMaxChunks; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nchunk) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float f = bf2f(v[c].e[e]);
+        ss += f * f;
+      }
+    }
+  }
+  ss = wave_sum(ss);
+  const float r = 1.0f / sqrtf(ss / (float)hidden + eps);
+#pragma unroll
+  for (int c = 0; c < kNormMaxChunks; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nchunk) {
+      Pack8 o;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o.e[e] = f2bf(bf2f(v[c].e[e]) * r * bf2f(gv[c].e[e]));
+      stg16(y + (int64_t)t * hidden + ch * 8, o.u);
+    }
+  }
+}
+
+hipError_t launch_prologue(const BatchDev& b, int n_slots, int max_seq, int head_dim,
+                           float rope_base, int32_t* tok_slot, int32_t* tok_row, float2* rope,
+                           const void* x, const void* g, void* y, int hidden, float eps,
+                           hipStream_t s) {
+  if (b.n_tokens == 0) return hipSuccess;
+  prologue_kernel<<<cdiv(b.n_tokens, 4), 256, 0, s>>>(
+      b, n_slots, max_seq, head_dim / 2, (double)rope_base, tok_slot, tok_row, rope,
+      (const bf16*)x, (const bf16*)g, (bf16*)y, hidden, eps);
   return hipGetLastError();
 }
 
