@@ -10,6 +10,13 @@ durations come from the library's own HIP-event timers over the same timed
 region.  One JSON line is printed.  The decode workload (batch 64, KV 4096,
 32 steps) is timed as a secondary result in the same line.
 
+Phases: for each workload (dense prefill, dense decode, MoE prefill, MoE
+decode, mixed) the line carries the per-stage arithmetic intensity (the
+library's work model: algorithmic flops over compulsory HBM bytes), the
+phase's time-weighted intensity of Eq. 5 (weights: the stage times measured
+in the profiled repetition), achieved TFLOP/s and GB/s per stage, and the
+energy, shader clock, hotspot temperature and socket power over a >= 2 s loop.
+
 Roofline: the dominant kernel of prefill is the fused gate/up + SwiGLU GEMM
 (2 * 16384 * 37888 * 3584 flop per launch), priced against 2.5 PFLOP/s dense
 bf16; decode's dominant kernel is split-KV attention, priced against 8 TB/s
@@ -98,20 +105,51 @@ class Energy:
         except Exception:
             return None
 
+    def sample(self):
+        """Shader clock (MHz, mean over the XCDs that report one), hotspot
+        temperature (C) and socket power (W) from the GPU metrics table."""
+        if self.h is None:
+            return None
+        try:
+            m = self.amdsmi.amdsmi_get_gpu_metrics_info(self.h)
+        except Exception:
+            return None
+
+        def num(v):
+            return float(v) if isinstance(v, (int, float)) and not isinstance(v, bool) else None
+
+        clks = m.get("current_gfxclks")
+        vals = [num(c) for c in clks] if isinstance(clks, (list, tuple)) else []
+        vals = [v for v in vals if v is not None and v > 0]
+        clk = sum(vals) / len(vals) if vals else (num(m.get("current_gfxclk"))
+                                                 or num(m.get("average_gfxclk_frequency")))
+        return {"gfxclk_mhz": clk, "hotspot_c": num(m.get("temperature_hotspot")),
+                "socket_power_w": num(m.get("current_socket_power"))}
+
+
+def _mean(samples, key):
+    v = [x[key] for x in samples if x.get(key) is not None]
+    return sum(v) / len(v) if v else None
+
 
 def energy_loop(fn, min_s=2.0):
     """Joules per call of fn over a loop of at least min_s seconds (the counter
-    updates every few ms), with average board power; None without a counter."""
+    updates every few ms), with average board power and the clock, temperature
+    and power sampled while the GPU is busy; None without a counter."""
     import torch
     meter = Energy()
     if meter.h is None:
         return None
     torch.cuda.synchronize()
     t0, j0, n = time.perf_counter(), meter.joules(), 0
+    samples = []
     while True:
         fn()
         n += 1
         if n % 4 == 0:
+            smp = meter.sample()  # work is still queued: a busy-GPU reading
+            if smp:
+                samples.append(smp)
             torch.cuda.synchronize()
             if time.perf_counter() - t0 >= min_s:
                 break
@@ -120,7 +158,53 @@ def energy_loop(fn, min_s=2.0):
     if j0 is None or j1 is None or j1 <= j0:
         return None
     return {"joules_per_call": (j1 - j0) / n, "avg_power_w": (j1 - j0) / (t1 - t0),
-            "calls": n, "seconds": t1 - t0}
+            "calls": n, "seconds": t1 - t0,
+            "telemetry": {"gfxclk_mhz": _mean(samples, "gfxclk_mhz"),
+                          "hotspot_c": _mean(samples, "hotspot_c"),
+                          "socket_power_w": _mean(samples, "socket_power_w"),
+                          "samples": len(samples)}}
+
+
+def energy_json(energy, tokens_per_call):
+    if energy is None:
+        return None
+    return {"joules_per_token": energy["joules_per_call"] / tokens_per_call,
+            "avg_power_w": energy["avg_power_w"], "seconds": energy["seconds"],
+            "source": "amdsmi board energy counter", "telemetry": energy["telemetry"]}
+
+
+def prof_dict(p):
+    return {p.name[i].decode(): {"launches": p.launches[i], "total_ms": p.total_ms[i]}
+            for i in range(p.n_stages)}
+
+
+def phase_report(tri, cfg, calls, decode, prof, reps, energy=None, tokens_per_call=None):
+    """Per-stage arithmetic intensity (algorithmic flops / compulsory bytes, from
+    the library's work model) and the phase's time-weighted intensity, Eq. 5,
+    weighted by the stage times measured over `reps` repetitions of `calls`
+    (a list of (q_len, ctx_len, expert_rows) host arrays)."""
+    w = tri.work_sum([tri.layer_work(cfg, decode, q, c, er) for q, c, er in calls])
+    ai = tri.phase_intensity(w, prof)
+    stages = {}
+    tot_f = tot_b = tot_ms = 0.0
+    for i in range(w.n_stages):
+        if not w.runs[i] or prof.total_ms[i] <= 0 or w.bytes[i] == 0:
+            continue  # not launched, not timed, or a launch with no work
+        ms = prof.total_ms[i]
+        f, b = w.flops[i] * reps, w.bytes[i] * reps
+        tot_f, tot_b, tot_ms = tot_f + f, tot_b + b, tot_ms + ms
+        stages[w.name[i].decode()] = {
+            "ms_per_call": ms / max(prof.launches[i], 1), "share": ms,
+            "ai_flop_per_byte": w.flops[i] / w.bytes[i],
+            "tflops": f / (ms / 1e3) / 1e12, "gbs": b / (ms / 1e3) / 1e9}
+    for v in stages.values():
+        v["share"] /= tot_ms
+    out = {"ai_time_weighted": ai, "ai_aggregate": tot_f / tot_b,
+           "tflops": tot_f / (tot_ms / 1e3) / 1e12, "gbs": tot_b / (tot_ms / 1e3) / 1e9,
+           "stages": stages}
+    if energy is not None:
+        out["energy"] = energy_json(energy, tokens_per_call)
+    return out
 
 
 def cpu_baseline(wl, wb, kb, vb, xb, budget_s=20.0):
@@ -185,12 +269,14 @@ def run_prefill(args, tri, wl, wb, kb, vb, xb):
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    prof = tri.profile_read()
+    praw = tri.profile_read(raw=True)
     tri.profile_enable(False)
     energy = energy_loop(step)
+    phase = phase_report(tri, dl.cfg, [(wl.batch.q_len, wl.batch.ctx_len, None)], False, praw,
+                         args.steps, energy, wl.batch.n_tokens)
     del dl, cache, x, out, ws
     torch.cuda.empty_cache()
-    return ms, wall, prof, energy
+    return ms, wall, prof_dict(praw), energy, phase
 
 
 def run_decode(args, tri):
@@ -235,9 +321,13 @@ def run_decode(args, tri):
     for _ in range(reps):
         sweep()
     torch.cuda.synchronize()
-    prof = tri.profile_read()
+    praw = tri.profile_read(raw=True)
+    prof = prof_dict(praw)
     tri.profile_enable(False)
     energy = energy_loop(sweep)
+    phase = phase_report(tri, dl.cfg, [(bb.host["q_len"], bb.host["ctx_len"], None)
+                                       for bb in batches], True, praw, reps, energy,
+                         steps * wl.batch.n_seqs)
     n_tok = reps * steps * wl.batch.n_seqs
     kv_bytes = sum(int(bb.host["ctx_len"].astype(np.int64).sum() + bb.n_seqs) for bb in batches) \
         * wl.cfg.n_kv_heads * wl.cfg.head_dim * 2 * 2
@@ -258,12 +348,10 @@ def run_decode(args, tri):
         "stages_ms_per_step": {k: v["total_ms"] / (reps * steps) for k, v in prof.items() if v["launches"]},
     }
     if energy is not None:
-        res["energy"] = {"joules_per_token": energy["joules_per_call"] / (steps * wl.batch.n_seqs),
-                         "avg_power_w": energy["avg_power_w"], "seconds": energy["seconds"],
-                         "source": "amdsmi board energy counter"}
+        res["energy"] = energy_json(energy, steps * wl.batch.n_seqs)
     del dl, cache, xs, out, ws
     torch.cuda.empty_cache()
-    return res
+    return res, phase
 
 
 def run_secondary(args, tri, name):
@@ -296,24 +384,50 @@ def run_secondary(args, tri, name):
     reps = 3
     stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    tri.profile_enable(True)
+
+    def sweep(routes=None):
+        for s in range(steps):
+            r = None if routes is None else routes[s]
+            fn(dl.cfg, dl.w, cache, batches[s], xs[s], out=out, workspace=ws, route_idx=r)
+
     e0.record(stream)
     for _ in range(reps):
-        for s in range(steps):
-            fn(dl.cfg, dl.w, cache, batches[s], xs[s], out=out, workspace=ws)
+        sweep()
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / (reps * steps)
-    prof = tri.profile_read()
+    tri.profile_enable(True)
+    for _ in range(reps):
+        sweep()
+    torch.cuda.synchronize()
+    praw = tri.profile_read(raw=True)
     tri.profile_enable(False)
+    expert_rows = [None] * steps
+    if getattr(wl.cfg, "n_experts", 0):
+        routes = [torch.empty(db.n_tokens, wl.cfg.top_k, dtype=torch.int32, device="cuda")
+                  for db in batches]
+        sweep(routes)
+        torch.cuda.synchronize()
+        expert_rows = [np.bincount(r.cpu().numpy().ravel(), minlength=wl.cfg.n_experts)
+                       for r in routes]
+    energy = energy_loop(sweep)
     n_tok = wl.batch.n_tokens if not decode else wl.batch.n_seqs
+    phase = phase_report(tri, dl.cfg, [(bb.host["q_len"], bb.host["ctx_len"], er)
+                                       for bb, er in zip(batches, expert_rows)], bool(decode),
+                         praw, reps, energy, n_tok * steps)
     res = {"workload": f"{name}: {wl.description}", "ms_per_step": ms,
            "tokens_per_s": n_tok / (ms / 1e3),
-           "stages_ms_per_step": {k: v["total_ms"] / (reps * steps) for k, v in prof.items()
-                                  if v["launches"]}}
+           "stages_ms_per_step": {k: v["total_ms"] / (reps * steps)
+                                  for k, v in prof_dict(praw).items() if v["launches"]}}
+    if expert_rows[0] is not None:
+        loads = np.stack(expert_rows)
+        res["expert_load"] = {"max_over_mean": float((loads.max(1) / loads.mean(1)).mean()),
+                              "experts_touched": float((loads > 0).sum(1).mean())}
+    if energy is not None:
+        res["energy"] = energy_json(energy, n_tok * steps)
     del dl, cache, xs, out, ws
     torch.cuda.empty_cache()
-    return res
+    return res, phase
 
 
 def main(argv=None):
@@ -351,7 +465,7 @@ def main(argv=None):
     wb = make_weights(wl.cfg, wl.seed)
     kb, vb = make_cache(wl.cfg, wl.n_slots, wl.max_seq, wl.seed)
     xb = make_x(wl.cfg, wl.batch.n_tokens, wl.seed)
-    ms, wall, prof, energy = run_prefill(args, tri, wl, wb, kb, vb, xb)
+    ms, wall, prof, energy, prefill_phase = run_prefill(args, tri, wl, wb, kb, vb, xb)
     T = wl.batch.n_tokens
     flops = prefill_flops(wl.cfg, wl.batch)
     gu = prof["gate_up"]
@@ -386,13 +500,19 @@ def main(argv=None):
         "wall_s_timed": wall,
     }
     if energy is not None:
-        res["energy"] = {"joules_per_token": energy["joules_per_call"] / T,
-                         "avg_power_w": energy["avg_power_w"], "seconds": energy["seconds"],
-                         "source": "amdsmi board energy counter"}
+        res["energy"] = energy_json(energy, T)
+    # Time-weighted arithmetic intensity per phase (Eq. 5), per-stage A.I.,
+    # energy, clock and temperature: the inputs of an A.I.-aware frequency policy.
+    phases = {"ridge_flop_per_byte": PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3,
+              "dense_prefill": prefill_phase}
     if not args.no_decode:
-        res["decode"] = run_decode(args, tri)
+        res["decode"], phases["dense_decode"] = run_decode(args, tri)
     if not args.no_secondary:
-        res["secondary"] = [run_secondary(args, tri, n) for n in ("moe_prefill", "moe_decode", "mixed")]
+        res["secondary"] = []
+        for n in ("moe_prefill", "moe_decode", "mixed"):
+            r, phases[n] = run_secondary(args, tri, n)
+            res["secondary"].append(r)
+    res["phases"] = phases
     if not args.no_cpu:
         from synth import bf16_to_f32
         res["cpu_baseline"] = cpu_baseline(wl, wb, bf16_to_f32(kb), bf16_to_f32(vb), xb)

@@ -218,6 +218,52 @@ typedef struct {
 tri_status tri_profile_enable(int32_t on);
 tri_status tri_profile_read(tri_profile* out);
 
+/* Algorithmic work of one layer call, stage by stage: the per-kernel
+ * arithmetic intensity from which Section III-B forms the time-weighted
+ * intensity of a phase (Eq. 5).  Index i and name[i] are the stage of
+ * tri_profile with the same index.  The counts follow the operations'
+ * definitions, not the kernels' internals:
+ *  flops  2 per multiply-add of every matrix product (the projections, the
+ *         two attention products over the causally visible keys, the router,
+ *         the experts); a stage without a product counts its multiply-adds
+ *         (RMSNorm 4 per element, split merge 2 per partial element, MoE
+ *         combine 2 per routed element).  Rotary, softmax and SwiGLU
+ *         transcendentals are not counted.
+ *  bytes  compulsory HBM traffic: every input a stage reads and every output
+ *         it writes, once (weights, activations, the K/V rows attended, once
+ *         per KV head, cache rows written, the split-KV partials passed from
+ *         attn_decode to attn_combine).  On-chip re-reads are not counted.
+ * Arguments (host memory):
+ *  decode         1 for tri_layer_decode's launch sequence, 0 for
+ *                 tri_layer_prefill's
+ *  q_len, ctx_len [n_seqs] new tokens and cached prefix of each sequence
+ *  expert_rows    MoE: [n_experts] routed rows per expert (summing to
+ *                 n_tokens * top_k), or NULL, in which case min(E, T * top_k)
+ *                 experts are taken as touched
+ *  out            every stage filled; runs[i] = 1 iff the call launches stage i
+ * Errors: TRI_ERR_NULL; the config's status; TRI_ERR_SHAPE for a negative
+ * length, a decode sequence with q_len != 1 or expert_rows of the wrong sum.  */
+typedef struct {
+  int32_t n_stages;
+  const char* name[TRI_MAX_STAGES];
+  int32_t runs[TRI_MAX_STAGES];
+  double flops[TRI_MAX_STAGES];
+  double bytes[TRI_MAX_STAGES];
+} tri_work;
+
+tri_status tri_layer_work(const tri_layer_config* cfg, int32_t decode, int32_t n_seqs,
+                          const int32_t* q_len, const int32_t* ctx_len,
+                          const int32_t* expert_rows, tri_work* out);
+
+/* Time-weighted arithmetic intensity of a phase (Section III-B, Eq. 5):
+ *   ai = sum_i d_i (flops_i / bytes_i) / sum_i d_i
+ * over the stages i with work->runs[i] set, d_i = prof->total_ms[i]; stages
+ * with d_i = 0, or with no work (flops and bytes both 0), drop out.  The work of several calls may be summed stage by
+ * stage first; a stage then stands for all its launches.  Host only.
+ * Errors: TRI_ERR_NULL; TRI_ERR_SHAPE if the stage counts differ or no stage
+ * has time; TRI_ERR_RANGE for a negative time or a timed stage with no bytes. */
+tri_status tri_phase_intensity(const tri_work* work, const tri_profile* prof, double* ai);
+
 /* Static description of a status code.                                         */
 const char* tri_status_string(tri_status s);
 

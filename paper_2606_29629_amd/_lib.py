@@ -56,6 +56,12 @@ class Profile(ctypes.Structure):
                 ("launches", ctypes.c_int32 * 16), ("total_ms", ctypes.c_double * 16)]
 
 
+class Work(ctypes.Structure):
+    _fields_ = [("n_stages", ctypes.c_int32), ("name", ctypes.c_char_p * 16),
+                ("runs", ctypes.c_int32 * 16), ("flops", ctypes.c_double * 16),
+                ("bytes", ctypes.c_double * 16)]
+
+
 class TriError(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
@@ -78,6 +84,10 @@ _FUNCS = {
     "tri_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "tri_profile_enable": (ctypes.c_int, [ctypes.c_int32]),
     "tri_profile_read": (ctypes.c_int, [ctypes.c_void_p]),
+    "tri_layer_work": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p]),
+    "tri_phase_intensity": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "tri_version": (ctypes.c_int32, []),
 }
 
@@ -240,9 +250,55 @@ def profile_enable(on: bool = True) -> None:
     _check(lib().tri_profile_enable(1 if on else 0), "tri_profile_enable")
 
 
-def profile_read() -> Dict[str, Dict[str, float]]:
-    """Per-stage launches and total milliseconds recorded since profile_enable(True)."""
+def profile_read(raw: bool = False):
+    """Per-stage launches and total milliseconds recorded since profile_enable(True)
+    (the Profile struct itself if raw)."""
     p = Profile()
     _check(lib().tri_profile_read(ctypes.byref(p)), "tri_profile_read")
+    if raw:
+        return p
     return {p.name[i].decode(): {"launches": p.launches[i], "total_ms": p.total_ms[i]}
             for i in range(p.n_stages)}
+
+
+def _i32_array(v) -> ctypes.Array:
+    v = [int(a) for a in v]
+    return (ctypes.c_int32 * max(len(v), 1))(*v)
+
+
+def layer_work(cfg: LayerConfig, decode: bool, q_len: Sequence[int], ctx_len: Sequence[int],
+               expert_rows: Optional[Sequence[int]] = None) -> Work:
+    """Algorithmic flops and HBM bytes per stage of one layer call (tri_layer_work)."""
+    if len(q_len) != len(ctx_len):
+        raise ValueError("q_len and ctx_len differ in length")
+    w = Work()
+    er = None if expert_rows is None else _i32_array(expert_rows)
+    _check(lib().tri_layer_work(ctypes.byref(cfg), 1 if decode else 0, len(q_len),
+                                _i32_array(q_len), _i32_array(ctx_len), er, ctypes.byref(w)),
+           "tri_layer_work")
+    return w
+
+
+def work_sum(works: Sequence[Work]) -> Work:
+    """Stage-by-stage sum of the work of several calls."""
+    out = Work()
+    out.n_stages = works[0].n_stages
+    for i in range(16):
+        out.name[i] = works[0].name[i]
+        out.runs[i] = int(any(w.runs[i] for w in works))
+        out.flops[i] = sum(w.flops[i] for w in works)
+        out.bytes[i] = sum(w.bytes[i] for w in works)
+    return out
+
+
+def work_dict(w: Work) -> Dict[str, Dict[str, float]]:
+    return {w.name[i].decode(): {"flops": w.flops[i], "bytes": w.bytes[i]}
+            for i in range(w.n_stages) if w.runs[i]}
+
+
+def phase_intensity(work: Work, prof: Profile) -> float:
+    """Time-weighted arithmetic intensity of a phase (tri_phase_intensity, Eq. 5)."""
+    ai = ctypes.c_double()
+    _check(lib().tri_phase_intensity(ctypes.byref(work), ctypes.byref(prof), ctypes.byref(ai)),
+           "tri_phase_intensity")
+    return ai.value

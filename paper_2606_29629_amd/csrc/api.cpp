@@ -10,22 +10,16 @@
 #include <vector>
 
 #include "../../include/tri.h"
+#include "host.hpp"
 #include "kernels.hpp"
 
 using namespace tri;
 
 namespace {
-
-constexpr size_t kAlign = 256;
-inline size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
-inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
-
-// Projections with at most this many rows take the weight-streaming path.
-constexpr int kSkinnyMaxRows = 128;
-
 bool is_moe(const tri_layer_config* c) { return (c->flags & TRI_F_MOE) != 0; }
+}  // namespace
 
-tri_status check_config(const tri_layer_config* c) {
+tri_status tri::check_config(const tri_layer_config* c) {
   if (!c) return TRI_ERR_NULL;
   if (c->dtype != TRI_BF16) return TRI_ERR_UNSUPPORTED;
   if (c->flags & ~TRI_F_ALL) return TRI_ERR_UNSUPPORTED;
@@ -46,6 +40,15 @@ tri_status check_config(const tri_layer_config* c) {
   }
   return TRI_OK;
 }
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Projections with at most this many rows take the weight-streaming path.
+constexpr int kSkinnyMaxRows = 128;
 
 tri_status check_batch_scalars(const tri_batch* b) {
   if (!b) return TRI_ERR_NULL;
@@ -125,17 +128,6 @@ Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
 }
 
 // ------------------------------------------------------------ profiling --
-enum Stage {
-  ST_PROLOGUE, ST_QKV, ST_ATTN_PREFILL, ST_ATTN_DECODE, ST_ATTN_COMBINE, ST_OPROJ,
-  ST_NORM2, ST_GATEUP, ST_DOWN, ST_ROUTER, ST_MOE_PERMUTE, ST_MOE_GATEUP, ST_MOE_DOWN,
-  ST_MOE_COMBINE, ST_APPEND, ST_COUNT
-};
-static_assert(ST_COUNT <= TRI_MAX_STAGES, "too many stages");
-const char* const kStageName[ST_COUNT] = {
-    "prologue", "qkv_rope", "attn_prefill", "attn_decode", "attn_combine",
-    "o_proj", "rmsnorm_mlp", "gate_up", "down", "moe_router", "moe_permute", "moe_gate_up",
-    "moe_down", "moe_combine", "kv_append"};
-
 struct Profiler {
   std::mutex mu;
   bool on = false;

@@ -53,6 +53,8 @@ STRUCTS = {
     "tri_kv_cache": (T.KVCache, [f for f, _ in T.KVCache._fields_]),
     "tri_batch": (T.BatchStruct, [f for f, _ in T.BatchStruct._fields_]),
     "tri_workspace_map": (T.WorkspaceMap, [f for f, _ in T.WorkspaceMap._fields_]),
+    "tri_profile": (T.Profile, [f for f, _ in T.Profile._fields_]),
+    "tri_work": (T.Work, [f for f, _ in T.Work._fields_]),
 }
 
 
