@@ -213,12 +213,28 @@ struct Mainloop {
 // Accumulator element r of block (i, j): row 32i + 8(r/4) + 4(lane/32) + r%4,
 // column 32j + lane%32 of the wave sub-tile.  row0 = output row of the wave's
 // first accumulator row (including 4 * (lane / 32)); rows >= row_lim are
-// not written.
+// not written.  The residual of a whole 32-row block row is loaded before any
+// of its sums is stored, so the loads are in flight together instead of each
+// waiting behind the previous store; out-of-range rows and columns load a
+// clamped (valid, unused) address rather than branching around the load.
 template <int MI, int NI, int EK>
 __device__ __forceinline__ void plain_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                                int row0, int row_lim, int col0, int N) {
+  const bf16* __restrict__ resid = (const bf16*)epi.resid;
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+  for (int i = 0; i < MI; ++i) {
+    float res[NI][16];
+    if constexpr (EK == EPI_RESID) {
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int col = min(col0 + 32 * j, N - 1);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = min(row0 + 32 * i + 8 * (r >> 2) + (r & 3), row_lim - 1);
+          res[j][r] = bf2f(resid[(int64_t)row * epi.ldr + col]);
+        }
+      }
+    }
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
       const int col = col0 + 32 * j;
@@ -231,12 +247,12 @@ __device__ __forceinline__ void plain_epilogue(const f32x16 (&acc)[MI][NI], cons
         if constexpr (EK == EPI_STORE_F32) {
           ((float*)epi.out)[(int64_t)row * epi.ldo + col] = v;
         } else {
-          if constexpr (EK == EPI_RESID)
-            v += bf2f(((const bf16*)epi.resid)[(int64_t)row * epi.ldr + col]);
+          if constexpr (EK == EPI_RESID) v += res[j][r];
           ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(v);
         }
       }
     }
+  }
 }
 
 // SwiGLU: blocks j < NI/2 hold gate, j + NI/2 the matching up; f0 = output
@@ -262,7 +278,65 @@ __device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MI][NI], con
 
 // q/k/v split + bias + rotary embedding + KV-cache write on the accumulators.
 // HB = 32-column blocks per half head (D / 64): block j (first half of a head)
-// pairs with block j + HB (second half), same lane, same element.
+// pairs with block j + HB (second half), same lane, same element.  For each
+// 32-row block the rotary factors (and, for k/v heads, the tokens' cache slot
+// and row) are loaded before any store, so those loads overlap; rows past M
+// load row M - 1 (valid, unused) rather than branching around the load.
+// One 32-row block pair (first-half block j, second-half block j + HB) of a
+// q (KIND 0), k (1) or v (2) head.
+template <int KIND, int MI, int NI, int HB>
+__device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi& epi, int i,
+                                          int j, int row0, int M, int head, int d, float b1,
+                                          float b2) {
+  constexpr int D = HB * 64, half = D / 2;
+  const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
+  const float2* __restrict__ rope = epi.rope;
+  const int32_t* __restrict__ tok_slot = epi.tok_slot;
+  const int32_t* __restrict__ tok_row = epi.tok_row;
+  float2 cs[16];
+  int sl[16], tr[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int rc = min(row0 + 32 * i + 8 * (r >> 2) + (r & 3), M - 1);
+    if constexpr (KIND != 2) cs[r] = rope[(int64_t)rc * half + d];
+    if constexpr (KIND != 0) {
+      sl[r] = tok_slot[rc];
+      tr[r] = tok_row[rc];
+    }
+  }
+  const int kvh = KIND == 1 ? head - Hq : head - Hq - Hkv;
+  bf16* base = (bf16*)(KIND == 0 ? epi.q : (KIND == 1 ? epi.kc : epi.vc));
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
+    float x1 = acc[i][j][r] + b1, x2 = acc[i][j + HB][r] + b2;
+    if constexpr (KIND != 2) {
+      const float y1 = x1 * cs[r].x - x2 * cs[r].y;
+      const float y2 = x2 * cs[r].x + x1 * cs[r].y;
+      x1 = y1;
+      x2 = y2;
+    }
+    int64_t off;
+    bool ok = row < M;
+    if constexpr (KIND == 0) {
+      off = ((int64_t)row * Hq + head) * D + d;
+    } else {
+      ok = ok && sl[r] >= 0;
+      off = (((int64_t)sl[r] * Hkv + kvh) * epi.max_seq + tr[r]) * D + d;
+    }
+    if (ok) {
+      base[off] = f2bf(x1);
+      base[off + half] = f2bf(x2);
+    }
+  }
+}
+
+// q/k/v split + bias + rotary embedding + KV-cache write on the accumulators.
+// HB = 32-column blocks per half head (D / 64): block j (first half of a head)
+// pairs with block j + HB (second half), same lane, same element.  For each
+// 32-row block the rotary factors (and, for k/v heads, the tokens' cache slot
+// and row) are loaded before any store, so those loads overlap; rows past M
+// load row M - 1 (valid, unused) rather than branching around the load.
 template <int MI, int NI, int HB>
 __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                              int row0, int col0, int M, int N) {
@@ -279,34 +353,14 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
       b1 = bf2f(((const bf16*)epi.bias)[col]);
       b2 = bf2f(((const bf16*)epi.bias)[col + half]);
     }
+    // the head, hence its kind, is uniform across the wave
+    const int kind = __builtin_amdgcn_readfirstlane(head < Hq ? 0 : (head < Hq + Hkv ? 1 : 2));
 #pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
-        if (row >= M) continue;
-        float x1 = acc[i][j][r] + b1, x2 = acc[i][j + HB][r] + b2;
-        if (head < Hq + Hkv) {
-          const float2 cs = epi.rope[(int64_t)row * half + d];
-          const float y1 = x1 * cs.x - x2 * cs.y;
-          const float y2 = x2 * cs.x + x1 * cs.y;
-          x1 = y1;
-          x2 = y2;
-        }
-        if (head < Hq) {
-          bf16* qp = (bf16*)epi.q + ((int64_t)row * Hq + head) * D + d;
-          qp[0] = f2bf(x1);
-          qp[half] = f2bf(x2);
-        } else {
-          const int sl = epi.tok_slot[row];
-          if (sl < 0) continue;
-          const int kvh = head < Hq + Hkv ? head - Hq : head - Hq - Hkv;
-          bf16* cache = (bf16*)(head < Hq + Hkv ? epi.kc : epi.vc);
-          bf16* cp = cache + (((int64_t)sl * Hkv + kvh) * epi.max_seq + epi.tok_row[row]) * D + d;
-          cp[0] = f2bf(x1);
-          cp[half] = f2bf(x2);
-        }
-      }
+    for (int i = 0; i < MI; ++i) {
+      if (kind == 0) qkv_block<0, MI, NI, HB>(acc, epi, i, j, row0, M, head, d, b1, b2);
+      else if (kind == 1) qkv_block<1, MI, NI, HB>(acc, epi, i, j, row0, M, head, d, b1, b2);
+      else qkv_block<2, MI, NI, HB>(acc, epi, i, j, row0, M, head, d, b1, b2);
+    }
   }
 }
 
@@ -533,8 +587,11 @@ size_t gemm_tail_bytes() { return (size_t)cu_count() * 256 * 256 * sizeof(float)
 // Sum of a tail tile's split partials in split order + the epilogue.
 // Workgroup (j, chunk): tail tile j (id full + j of the grouped order),
 // elements [chunk * 2048, chunk * 2048 + 2048) of the tile (rotary pairs for
-// q/k/v), 8 per thread.
+// q/k/v), 8 per thread.  Each thread loads its 8 elements' values of one
+// split plane together, then every operand of the epilogue, before any
+// store: tsplit + 1 memory round trips instead of one per element.
 constexpr int kTailChunk = 2048;
+constexpr int kTailPer = kTailChunk / 256;
 
 template <int BM, int BN>
 __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__ tail, int tsplit,
@@ -543,25 +600,39 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
   const int j = blockIdx.y;
   int tm, tn;
   tile_of_id(full + j, tiles_m, tiles_n, tm, tn);
-  const float* tp = tail + (int64_t)j * tsplit * BM * BN;
-  auto sum = [&](int r, int c) {
-    float v = 0.f;
-    for (int sp = 0; sp < tsplit; ++sp) v += tp[(int64_t)sp * BM * BN + r * BN + c];
-    return v;
-  };
-  const int e0 = blockIdx.x * kTailChunk;
+  const float* __restrict__ tp = tail + (int64_t)j * tsplit * BM * BN;
+  const int e0 = blockIdx.x * kTailChunk + threadIdx.x;
   if (epi.kind != EPI_QKV) {
-    for (int e = e0 + threadIdx.x; e < e0 + kTailChunk && e < BM * BN; e += 256) {
-      const int r = e / BN, c = e % BN;
-      const int row = tm * BM + r, col = tn * BN + c;
-      if (row >= M || col >= N) continue;
-      float v = sum(r, c);
-      if (epi.kind == EPI_STORE_F32) {
-        ((float*)epi.out)[(int64_t)row * epi.ldo + col] = v;
-        continue;
+    int idx[kTailPer];
+    float v[kTailPer];
+#pragma unroll
+    for (int q = 0; q < kTailPer; ++q) {
+      idx[q] = min(e0 + 256 * q, BM * BN - 1);
+      v[q] = 0.f;
+    }
+    for (int sp = 0; sp < tsplit; ++sp)
+#pragma unroll
+      for (int q = 0; q < kTailPer; ++q) v[q] += tp[(int64_t)sp * BM * BN + idx[q]];
+    float res[kTailPer];
+    if (epi.kind == EPI_RESID) {
+      const bf16* __restrict__ rp = (const bf16*)epi.resid;
+#pragma unroll
+      for (int q = 0; q < kTailPer; ++q) {
+        const int row = min(tm * BM + idx[q] / BN, M - 1), col = min(tn * BN + idx[q] % BN, N - 1);
+        res[q] = bf2f(rp[(int64_t)row * epi.ldr + col]);
       }
-      if (epi.kind == EPI_RESID) v += bf2f(((const bf16*)epi.resid)[(int64_t)row * epi.ldr + col]);
-      ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(v);
+    }
+#pragma unroll
+    for (int q = 0; q < kTailPer; ++q) {
+      const int e = e0 + 256 * q;
+      const int row = tm * BM + e / BN, col = tn * BN + e % BN;
+      if (e >= BM * BN || row >= M || col >= N) continue;
+      if (epi.kind == EPI_STORE_F32) {
+        ((float*)epi.out)[(int64_t)row * epi.ldo + col] = v[q];
+      } else {
+        const float o = epi.kind == EPI_RESID ? v[q] + res[q] : v[q];
+        ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(o);
+      }
     }
     return;
   }
@@ -569,37 +640,59 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
   // D columns lies inside one tile since BN is a multiple of D).
   const int Dh = epi.head_dim, half = Dh / 2;
   const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
-  for (int e = e0 + threadIdx.x; e < e0 + kTailChunk && e < BM * (BN / 2); e += 256) {
-    const int r = e / (BN / 2), pc = e % (BN / 2);
-    const int c = (pc / half) * Dh + pc % half;  // first-half column in the tile
-    const int row = tm * BM + r, col = tn * BN + c;
-    if (row >= M || col >= N) continue;
+  int rr[kTailPer], cc[kTailPer];
+  float x1[kTailPer], x2[kTailPer];
+#pragma unroll
+  for (int q = 0; q < kTailPer; ++q) {
+    const int e = min(e0 + 256 * q, BM * (BN / 2) - 1);
+    const int pc = e % (BN / 2);
+    rr[q] = e / (BN / 2);
+    cc[q] = (pc / half) * Dh + pc % half;  // first-half column in the tile
+    x1[q] = x2[q] = 0.f;
+  }
+  for (int sp = 0; sp < tsplit; ++sp)
+#pragma unroll
+    for (int q = 0; q < kTailPer; ++q) {
+      const float* pl = tp + (int64_t)sp * BM * BN + rr[q] * BN + cc[q];
+      x1[q] += pl[0];
+      x2[q] += pl[half];
+    }
+  float2 cs[kTailPer];
+  int sl[kTailPer], tr[kTailPer];
+  float b1[kTailPer], b2[kTailPer];
+#pragma unroll
+  for (int q = 0; q < kTailPer; ++q) {
+    const int row = min(tm * BM + rr[q], M - 1), col = min(tn * BN + cc[q], N - 1);
+    const int d = col % Dh;
+    cs[q] = epi.rope[(int64_t)row * half + d];
+    sl[q] = epi.tok_slot[row];
+    tr[q] = epi.tok_row[row];
+    b1[q] = epi.bias ? bf2f(((const bf16*)epi.bias)[col]) : 0.f;
+    b2[q] = epi.bias ? bf2f(((const bf16*)epi.bias)[col + half]) : 0.f;
+  }
+#pragma unroll
+  for (int q = 0; q < kTailPer; ++q) {
+    const int row = tm * BM + rr[q], col = tn * BN + cc[q];
+    if (e0 + 256 * q >= BM * (BN / 2) || row >= M || col >= N) continue;
     const int head = col / Dh, d = col % Dh;
-    float x1 = sum(r, c), x2 = sum(r, c + half);
-    if (epi.bias) {
-      x1 += bf2f(((const bf16*)epi.bias)[col]);
-      x2 += bf2f(((const bf16*)epi.bias)[col + half]);
-    }
+    float y1 = x1[q] + b1[q], y2 = x2[q] + b2[q];
     if (head < Hq + Hkv) {
-      const float2 cs = epi.rope[(int64_t)row * half + d];
-      const float y1 = x1 * cs.x - x2 * cs.y;
-      const float y2 = x2 * cs.x + x1 * cs.y;
-      x1 = y1;
-      x2 = y2;
+      const float r1 = y1 * cs[q].x - y2 * cs[q].y;
+      const float r2 = y2 * cs[q].x + y1 * cs[q].y;
+      y1 = r1;
+      y2 = r2;
     }
+    bf16* dst;
     if (head < Hq) {
-      bf16* qp = (bf16*)epi.q + ((int64_t)row * Hq + head) * Dh + d;
-      qp[0] = f2bf(x1);
-      qp[half] = f2bf(x2);
+      dst = (bf16*)epi.q + ((int64_t)row * Hq + head) * Dh + d;
     } else {
-      const int sl = epi.tok_slot[row];
-      if (sl < 0) continue;
+      if (sl[q] < 0) continue;
       const int kvh = head < Hq + Hkv ? head - Hq : head - Hq - Hkv;
       bf16* cache = (bf16*)(head < Hq + Hkv ? epi.kc : epi.vc);
-      bf16* cp = cache + (((int64_t)sl * Hkv + kvh) * epi.max_seq + epi.tok_row[row]) * Dh + d;
-      cp[0] = f2bf(x1);
-      cp[half] = f2bf(x2);
+      dst = cache + (((int64_t)sl[q] * Hkv + kvh) * epi.max_seq + tr[q]) * Dh + d;
     }
+    dst[0] = f2bf(y1);
+    dst[half] = f2bf(y2);
   }
 }
 
