@@ -10,14 +10,18 @@
 // streaming; the wave serves all query heads of its KV head (grouped-query
 // reuse: K and V are read once for the whole group).
 //
-// The split's keys move in tiles of 32 rows (K and V, contiguous in the cache)
-// from HBM to a wave-private 3-stage LDS ring with buffer_load_dwordx4 ... lds;
-// two tiles are in flight while one is consumed, and only the wave's own
-// vmcnt orders them (no barrier).  Key rows past the sequence read as zero.
+// The split's keys move in tiles of 32 rows (K and V, contiguous in the
+// cache), two tiles in flight while one is consumed, ordered only by the
+// wave's own vmcnt (no barrier).  K goes straight from HBM to registers, in
+// the MFMA operand layout (lane: key l % 32, 8 head-dim values of slice
+// l / 32); V goes to a wave-private 3-stage LDS ring with buffer_load_dwordx4
+// ... lds, because its operand must be transposed.  Keeping K out of LDS
+// halves the LDS per wave, so twice the waves -- and twice the bytes in
+// flight -- fit on a CU.  Key rows past the sequence read as zero.
 //
 // Per tile, as in the prefill kernel with the group's heads as the query
-// columns: S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K rows from LDS,
-// B = Q of the group's heads, lane column = head); online softmax per head in
+// columns: S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (A = K rows, B = Q of
+// the group's heads, lane column = head); online softmax per head in
 // the log2 domain with a lazily raised max; O^T += V^T P^T with V^T read by
 // ds_read_b64_tr_b16 and P split into bf16 hi + lo parts (16 significant
 // bits).
@@ -34,15 +38,29 @@ constexpr int kDecTile = 32;     // keys per tile
 constexpr int kDecStages = 3;    // LDS ring depth
 constexpr int kDecMinSplit = 128;
 
-// Keys per split: the longest context cut into equal pieces of at most 512
-// keys (a multiple of the 32-key tile), or of at most 128 when the grid would
-// otherwise be small.
-int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv) {
+// Waves of this kernel resident on one CU: the LDS (V ring + staged Q) and
+// the register file (two waves per SIMD for D = 128, three for D = 64) bound it.
+static int decode_waves_per_cu(int head_dim, int group) {
+  const int smem = (head_dim == 128 ? kDecStages * kDecTile * 128 * 2 : kDecStages * kDecTile * 64 * 2) +
+                   cdiv(group, 512 / head_dim) * 1024;
+  const int by_lds = (160 * 1024) / smem;
+  const int by_regs = head_dim == 128 ? 8 : 12;
+  return by_lds < by_regs ? by_lds : by_regs;
+}
+
+// Keys per split: every (sequence, KV head) is cut into the same number of
+// splits, as many as make the grid one full round of resident waves (each
+// wave then streams from launch to finish with no second round), but no
+// split shorter than kDecMinSplit keys; the split is a multiple of the
+// 32-key tile.
+int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv, int head_dim, int group) {
   if (max_kv < 1) max_kv = 1;
-  const int64_t wgs = (int64_t)n_seqs * n_kv_heads * cdiv(max_kv, 512);
-  const int cap = wgs >= 768 ? 512 : kDecMinSplit;
-  const int ns = cdiv(max_kv, cap);
-  return cdiv(cdiv(max_kv, ns), kDecTile) * kDecTile;
+  const int64_t pairs = (int64_t)(n_seqs > 0 ? n_seqs : 1) * (n_kv_heads > 0 ? n_kv_heads : 1);
+  const int64_t resident = (int64_t)decode_waves_per_cu(head_dim, group) * cu_count();
+  int64_t ns = resident / pairs;
+  if (ns < 1) ns = 1;
+  if (ns > cdiv(max_kv, kDecMinSplit)) ns = cdiv(max_kv, kDecMinSplit);
+  return cdiv(cdiv(max_kv, (int)ns), kDecTile) * kDecTile;
 }
 
 size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv) {
@@ -52,21 +70,86 @@ size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int 
 
 template <int D>
 struct DecSmem {
-  bf16 k[kDecStages][kDecTile * D];  // [key][d], chunks swizzled by kv_chunk
-  bf16 v[kDecStages][kDecTile * D];
+  bf16 v[kDecStages][kDecTile * D];  // [key][d], chunks swizzled by kv_chunk
 };
 
+template <int N>
+struct IntC {
+  static constexpr int value = N;
+};
+
+__device__ __forceinline__ uint32_t lds_addr(const bf16* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16*)p;
+}
+
+// Four 16-byte LDS reads, then an LDS wait, in one asm block (outside the
+// compiler's LDS-fill tracking; the caller orders them after the fill).
+__device__ __forceinline__ void lds_read_b128_x4(const uint32_t* a, bf16x8 (&v)[4]) {
+  asm volatile(
+      "ds_read_b128 %0, %4\n\t"
+      "ds_read_b128 %1, %5\n\t"
+      "ds_read_b128 %2, %6\n\t"
+      "ds_read_b128 %3, %7\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
+}
+
+// 2 * DB transposing reads (ds_read_b64_tr_b16, see lds_read_tr16) into DB
+// MFMA operands (reads 2b and 2b + 1 form operand b), then an LDS wait.
+template <int DB>
+__device__ __forceinline__ void lds_read_tr16_group(const uint32_t (&a)[2 * DB], bf16x8 (&v)[DB]) {
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  u32x2 o[2 * DB];
+  if constexpr (DB == 4) {
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %8\n\t"
+        "ds_read_b64_tr_b16 %1, %9\n\t"
+        "ds_read_b64_tr_b16 %2, %10\n\t"
+        "ds_read_b64_tr_b16 %3, %11\n\t"
+        "ds_read_b64_tr_b16 %4, %12\n\t"
+        "ds_read_b64_tr_b16 %5, %13\n\t"
+        "ds_read_b64_tr_b16 %6, %14\n\t"
+        "ds_read_b64_tr_b16 %7, %15\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3]), "=&v"(o[4]), "=&v"(o[5]),
+          "=&v"(o[6]), "=&v"(o[7])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(a[4]), "v"(a[5]), "v"(a[6]),
+          "v"(a[7]));
+  } else {
+    static_assert(DB == 2, "head_dim 64 or 128");
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %4\n\t"
+        "ds_read_b64_tr_b16 %1, %5\n\t"
+        "ds_read_b64_tr_b16 %2, %6\n\t"
+        "ds_read_b64_tr_b16 %3, %7\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(o[0]), "=&v"(o[1]), "=&v"(o[2]), "=&v"(o[3])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]));
+  }
+#pragma unroll
+  for (int b = 0; b < DB; ++b) {
+    union {
+      u32x2 s[2];
+      bf16x8 v;
+    } u;
+    u.s[0] = o[2 * b];
+    u.s[1] = o[2 * b + 1];
+    v[b] = u.v;
+  }
+}
+
 template <int D>
-__global__ __launch_bounds__(64) void attn_decode_kernel(
+__global__ __launch_bounds__(64, 2) void attn_decode_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
     float* __restrict__ part, const int32_t* __restrict__ cu_q,
     const int32_t* __restrict__ ctx_len, const int32_t* __restrict__ slot, int n_slots,
     int max_seq, int Hq, int Hkv, int nsplit, int split_keys, float scale_log2e, int n_tokens) {
   constexpr int DC = D / 8;                  // 16-byte chunks per row
   constexpr int TB = kDecTile * D * 2;       // bytes per K (or V) tile
-  constexpr int BLK = TB / 1024;             // 1 KB loads per tile and operand
-  constexpr int LPI = 2 * BLK;               // loads per tile
+  constexpr int BLK = TB / 1024;             // 1 KB loads per V tile
   constexpr int DS = D / 16, DB = D / 32;
+  constexpr int LPI = BLK + DS;              // loads per tile (V to LDS, K to registers)
   extern __shared__ __align__(16) char smem_raw[];
   DecSmem<D>& sm = *reinterpret_cast<DecSmem<D>*>(smem_raw);
 
@@ -90,7 +173,7 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(
       (void*)(Kc + cache_off), (short)0, k_end * D * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(Vc + cache_off), (short)0, k_end * D * 2, 0x00020000);
-  // Lane l of 1 KB block b fills tile row b (64 / DC) + l / DC, physical
+  // V: lane l of 1 KB block b fills tile row b (64 / DC) + l / DC, physical
   // chunk l % DC = logical chunk kv_chunk(l % DC, row) (an involution).
   uint32_t ld_off[BLK];
 #pragma unroll
@@ -98,29 +181,59 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(
     const int row = j * (64 / DC) + lane / DC;
     ld_off[j] = (uint32_t)((row * D + kv_chunk<D>(lane % DC, row) * 8) * 2);
   }
-  // Tile i (keys k_begin + 32 i ...) into stage i % 3; tiles past the split
-  // are issued out of range (zero fill, no traffic) to keep the count uniform.
-  auto issue = [&](int i) {
-    const uint32_t kill = i < nt ? 0u : 0x80000000u;
-    const uint32_t kb = (uint32_t)(k_begin + kDecTile * (i < nt ? i : 0)) * D * 2;
+  // K: k-step k of lane (r, g) is key r, logical chunk 2 k + g.
+  uint32_t k_off[DS];
+#pragma unroll
+  for (int k = 0; k < DS; ++k) k_off[k] = (uint32_t)((r * D + (2 * k + g) * 8) * 2);
+  // Tile i = keys k_begin + 32 i ...; tiles past the split are issued out of
+  // range (zero fill, no traffic) to keep the load count uniform.
+  auto tile_base = [&](int i, uint32_t& kill) {
+    kill = i < nt ? 0u : 0x80000000u;
+    return (uint32_t)(k_begin + kDecTile * (i < nt ? i : 0)) * D * 2;
+  };
+  auto issue_v = [&](int i) {
+    uint32_t kill;
+    const uint32_t kb = tile_base(i, kill);
     const int st = i % kDecStages;
 #pragma unroll
-    for (int j = 0; j < BLK; ++j) {
-      buffer_load_lds16(rk, &sm.k[st][j * 512], (ld_off[j] | kill) + kb, 0);
+    for (int j = 0; j < BLK; ++j)
       buffer_load_lds16(rv, &sm.v[st][j * 512], (ld_off[j] | kill) + kb, 0);
-    }
   };
-  // Q of head column r, loaded before the tiles so the first wait covers it
-  // too (heads past the group repeat the last one; their results are not
-  // written).
-  bf16x8 qf[DS];
-  {
-    const bf16* qp = Q + ((int64_t)t * Hq + qh0 + min(r, grp - 1)) * D + 8 * g;
+  bf16x8 kreg[2][DS];  // K of tile i in slot i % 2
+  auto issue_k = [&](auto slot, int i) {
+    uint32_t kill;
+    const uint32_t kb = tile_base(i, kill);
 #pragma unroll
-    for (int k = 0; k < DS; ++k) qf[k] = *(const bf16x8*)(qp + 16 * k);
+    for (int k = 0; k < DS; ++k)
+      kreg[decltype(slot)::value][k] = __builtin_bit_cast(
+          bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, (k_off[k] | kill) + kb, 0, 0));
+  };
+  // Q of the group's heads, staged once in LDS after the V ring ([grp][D],
+  // chunks swizzled like the K/V tiles so the per-tile fragment reads are
+  // conflict-free) by direct loads issued ahead of the tiles, so the first
+  // tile wait covers them; head column r >= grp repeats the last head (its
+  // results are not written).
+  constexpr int RPB = 64 / DC;  // rows per 1 KB load
+  bf16* qs = reinterpret_cast<bf16*>(smem_raw + sizeof(DecSmem<D>));
+  {
+    const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(Q + ((int64_t)t * Hq + qh0) * D), (short)0, grp * D * 2, 0x00020000);
+    for (int j = 0; j < cdiv(grp, RPB); ++j) {
+      const int row = j * RPB + lane / DC;
+      buffer_load_lds16(rq, &qs[j * 512],
+                        (uint32_t)((row * D + kv_chunk<D>(lane % DC, row) * 8) * 2), 0);
+    }
   }
-  issue(0);
-  issue(1);
+  const int qrow = min(r, grp - 1);
+  uint32_t q_addr[DS];
+#pragma unroll
+  for (int k = 0; k < DS; ++k) q_addr[k] = lds_addr(&qs[qrow * D + kv_chunk<D>(2 * k + g, qrow) * 8]);
+  // Issue order per tile: V (to LDS), then K (to registers); both of tile i
+  // have landed once at most the LPI loads of tile i + 1 are outstanding.
+  issue_v(0);
+  issue_k(IntC<0>{}, 0);
+  issue_v(1);
+  issue_k(IntC<1>{}, 1);
 
   const int tr_key = 4 * g + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -131,18 +244,23 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(
   float m_run = -INFINITY, l_run = 0.f;  // running max in raw score units
   const float slack_raw = kSoftmaxSlack / scale_log2e;
 
-  for (int i = 0; i < nt; ++i) {
+  auto step = [&](auto slot, int i) {
+    constexpr int ks = decltype(slot)::value;
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPI) : "memory");  // tile i landed
-    issue(i + 2);  // into the stage of tile i - 1, whose reads fed issued MFMAs
+    issue_v(i + 2);  // into the stage of tile i - 1, whose reads fed issued MFMAs
     const int st = i % kDecStages;
     const int key0 = k_begin + kDecTile * i;
     // S^T = K Q^T; element e: key key0 + 8 (e / 4) + 4 g + e % 4, head r.
     f32x16 sacc = f32x16{0.f};
 #pragma unroll
-    for (int k = 0; k < DS; ++k) {
-      const bf16x8 kf = *(const bf16x8*)&sm.k[st][r * D + kv_chunk<D>(2 * k + g, r) * 8];
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc, 0, 0, 0);
+    for (int k0 = 0; k0 < DS; k0 += 4) {
+      bf16x8 qf[4];
+      lds_read_b128_x4(&q_addr[k0], qf);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kreg[ks][k0 + k], qf[k], sacc, 0, 0, 0);
     }
+    issue_k(slot, i + 2);  // the slot's K has been read by the MFMAs above
     float mt = -INFINITY;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
@@ -174,26 +292,40 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(
       }
       split_hilo8(p8, pf[h], pl[h]);
     }
-    // O^T += V^T P^T over the two 16-key groups of the tile.
+    // O^T += V^T P^T over the two 16-key groups of the tile.  The
+    // transposing reads of a group are issued together and waited for in one
+    // asm block: the wave's own top-of-step vmcnt wait already orders them
+    // after the tile's LDS fill, and keeping them out of the compiler's view
+    // stops it from also waiting for the fills of later tiles.
     const bf16* vb = sm.v[st];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int k1 = 16 * h + tr_key, k2 = k1 + 8;
+      uint32_t a[2 * DB];
 #pragma unroll
       for (int b = 0; b < DB; ++b) {
         const int col = 32 * b + tr_col;
-        union {
-          s16x4 s[2];
-          bf16x8 v;
-        } vf;
-        vf.s[0] = lds_read_tr16(vb + k1 * D + kv_chunk<D>(col >> 3, k1) * 8 + (col & 7));
-        vf.s[1] = lds_read_tr16(vb + k2 * D + kv_chunk<D>(col >> 3, k2) * 8 + (col & 7));
-        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.v, pf[h], oacc[b], 0, 0, 0);
-        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf.v, pl[h], oacc[b], 0, 0, 0);
+        a[2 * b] = lds_addr(vb + k1 * D + kv_chunk<D>(col >> 3, k1) * 8 + (col & 7));
+        a[2 * b + 1] = lds_addr(vb + k2 * D + kv_chunk<D>(col >> 3, k2) * 8 + (col & 7));
+      }
+      bf16x8 vf[DB];
+      lds_read_tr16_group<DB>(a, vf);
+#pragma unroll
+      for (int b = 0; b < DB; ++b) {
+        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[b], pf[h], oacc[b], 0, 0, 0);
+        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[b], pl[h], oacc[b], 0, 0, 0);
       }
     }
+  };
+  // Both steps of the loop body are unconditional, so the compiler's own
+  // waits for the K registers see exactly two tiles of loads after them.
+  int i = 0;
+  for (; i + 1 < nt; i += 2) {
+    step(IntC<0>{}, i);
+    step(IntC<1>{}, i + 1);
   }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // no load may land in LDS after exit
+  if (i < nt) step(IntC<0>{}, i);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // no load may land after exit
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (r >= grp) return;
@@ -256,11 +388,12 @@ static hipError_t run_decode(const void* q, const void* kc, const void* vc, floa
                              const BatchDev& b, int n_slots, int max_seq, int Hq, int Hkv,
                              hipStream_t s) {
   const int max_kv = b.max_ctx_len + 1;
-  const int split = attn_decode_split_keys(b.n_seqs, Hkv, max_kv);
+  const int split = attn_decode_split_keys(b.n_seqs, Hkv, max_kv, D, Hq / Hkv);
   const int nsplit = cdiv(max_kv, split);
   const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
   dim3 grid(nsplit, Hkv, b.n_seqs);
-  attn_decode_kernel<D><<<grid, 64, sizeof(DecSmem<D>), s>>>(
+  const size_t smem = sizeof(DecSmem<D>) + (size_t)cdiv(Hq / Hkv, 512 / D) * 1024;
+  attn_decode_kernel<D><<<grid, 64, smem, s>>>(
       (const bf16*)q, (const bf16*)kc, (const bf16*)vc, part, b.cu_q, b.ctx_len, b.slot, n_slots,
       max_seq, Hq, Hkv, nsplit, split, scale_log2e, b.n_tokens);
   return hipGetLastError();
@@ -280,7 +413,8 @@ hipError_t launch_attn_decode_combine(const float* part, void* out, const BatchD
                                       int head_dim, hipStream_t s) {
   if (b.n_seqs == 0) return hipSuccess;
   const int max_kv = b.max_ctx_len + 1;
-  const int split = attn_decode_split_keys(b.n_seqs, n_kv_heads, max_kv);
+  const int split = attn_decode_split_keys(b.n_seqs, n_kv_heads, max_kv, head_dim,
+                                           n_q_heads / n_kv_heads);
   const int nsplit = cdiv(max_kv, split);
   dim3 cgrid(b.n_seqs, n_q_heads);
   if (head_dim == 128)

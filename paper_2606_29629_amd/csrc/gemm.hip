@@ -550,7 +550,7 @@ static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M
 // the last (tiles % CUs) tiles -- all of them when there are fewer tiles than
 // CUs -- would run as a partial round; split into `tsplit` K-parts they fill
 // it.
-static int cu_count() {
+int cu_count() {
   static int n = 0;
   if (n == 0) {
     int dev = 0, v = 0;

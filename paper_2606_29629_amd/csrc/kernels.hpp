@@ -85,7 +85,9 @@ hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, vo
                                int n_kv_heads, int head_dim, int include_single, hipStream_t s);
 
 // Split-KV attention for sequences with q_len == 1, plus the combine.
-int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv);
+int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv, int head_dim, int group);
+// Compute units of the current device (256 when it cannot be queried).
+int cu_count();
 size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv);
 hipError_t launch_attn_decode_split(const void* q, const void* kc, const void* vc, float* part,
                                     const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
