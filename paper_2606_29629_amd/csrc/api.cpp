@@ -282,11 +282,17 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   e.ldo = H;
   e.resid = x_in;
   e.ldr = H;
-  {
+  if (skinny_resid_norm_fused(T, H, Hq * D)) {
+    // short batch: the O projection's split-K reduction also adds the
+    // residual and applies the pre-MLP RMSNorm (no separate norm launch)
     StageTimer t_(ST_OPROJ, s);
-    if ((st = run_linear(attn, Hq * D, w->w_o, T, H, Hq * D, e, part, s)) != TRI_OK) return st;
-  }
-  {
+    TRI_HIP(launch_skinny_resid_norm(attn, Hq * D, w->w_o, Hq * D, T, H, Hq * D, x_in, H, x1, H,
+                                     w->mlp_norm, h2, cfg->rms_eps, part, s));
+  } else {
+    {
+      StageTimer t_(ST_OPROJ, s);
+      if ((st = run_linear(attn, Hq * D, w->w_o, T, H, Hq * D, e, part, s)) != TRI_OK) return st;
+    }
     StageTimer t_(ST_NORM2, s);
     TRI_HIP(launch_rmsnorm(x1, w->mlp_norm, h2, nullptr, T, H, cfg->rms_eps, s));
   }

@@ -154,9 +154,9 @@ __global__ __launch_bounds__(64, 2) void attn_decode_kernel(
   DecSmem<D>& sm = *reinterpret_cast<DecSmem<D>*>(smem_raw);
 
   const int s = blockIdx.z, kvh = blockIdx.y, sp = blockIdx.x;
-  const int t = cu_q[s];
-  if (cu_q[s + 1] - t != 1 || t < 0 || t >= n_tokens) return;
-  const int c = ctx_len[s], sl = slot[s];
+  // The sequence's scalars in one round trip (s < n_seqs by the grid).
+  const int t = cu_q[s], t1 = cu_q[s + 1], c = ctx_len[s], sl = slot[s];
+  if (t1 - t != 1 || t < 0 || t >= n_tokens) return;
   if (sl < 0 || sl >= n_slots || c < 0 || c + 1 > max_seq) return;
   const int k_begin = sp * split_keys;
   const int k_end = min(c + 1, k_begin + split_keys);
@@ -351,9 +351,8 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(
     const int32_t* __restrict__ ctx_len, const int32_t* __restrict__ slot, int n_slots,
     int max_seq, int Hq, int nsplit, int split_keys, int n_tokens) {
   const int s = blockIdx.x, qh = blockIdx.y, d = threadIdx.x;
-  const int t = cu_q[s];
-  if (cu_q[s + 1] - t != 1 || t < 0 || t >= n_tokens) return;
-  const int c = ctx_len[s], sl = slot[s];
+  const int t = cu_q[s], t1 = cu_q[s + 1], c = ctx_len[s], sl = slot[s];  // s < n_seqs
+  if (t1 - t != 1 || t < 0 || t >= n_tokens) return;
   if (sl < 0 || sl >= n_slots || c < 0 || c + 1 > max_seq) return;
   const int ns = min(cdiv(c + 1, split_keys), nsplit);  // never past the launched splits
   const float* pp = part + ((int64_t)t * Hq + qh) * nsplit * (D + 2);

@@ -52,11 +52,11 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   FaSmem<D>& sm = *reinterpret_cast<FaSmem<D>*>(smem_raw);
 
   const int s = blockIdx.z, qh = blockIdx.y;
-  const int q0 = cu_q[s], n = cu_q[s + 1] - q0;
+  // The sequence's scalars in one round trip (s < n_seqs by the grid).
+  const int q0 = cu_q[s], n = cu_q[s + 1] - q0, c = ctx_len[s], sl = slot[s];
   if (n <= 0 || (n == 1 && !include_single) || q0 < 0 || q0 + n > n_tokens) return;
   const int qt = (int)gridDim.x - 1 - (int)blockIdx.x;  // heavy (late) tiles first
   if (qt * kFaBQ >= n) return;
-  const int c = ctx_len[s], sl = slot[s];
   if (sl < 0 || sl >= n_slots || c < 0 || c + n > max_seq) return;
   const int kvh = (qh * Hkv) / Hq;
   const int64_t cache_off = ((int64_t)sl * Hkv + kvh) * max_seq * D;

@@ -840,6 +840,81 @@ __global__ __launch_bounds__(256) void splitk_epi_kernel(const float* __restrict
   }
 }
 
+// Split-K reduction fused with the residual add and the RMSNorm that follows
+// it (the O projection of a short batch): one workgroup per row sums the
+// planes in split order and adds the residual (x1, stored in bf16), then
+// normalises the stored row into y = x1 / sqrt(mean(x1^2) + eps) * g.
+constexpr int kNormRowThreads = 256;
+constexpr int kNormRowChunks = 8;  // 4-float chunks per thread: N <= 256 * 4 * 8
+
+__global__ __launch_bounds__(kNormRowThreads) void splitk_resid_norm_kernel(
+    const float* __restrict__ part, int splits, int M, int N, const bf16* __restrict__ resid,
+    int ldr, bf16* __restrict__ out, int ldo, const bf16* __restrict__ g, bf16* __restrict__ y,
+    float eps) {
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const int64_t MN = (int64_t)M * N;
+  const int nch = N / 4;
+  f32x4 v[kNormRowChunks];
+  float res[kNormRowChunks][4], gg[kNormRowChunks][4];
+  // Every operand of the row first (chunk indices clamped: no branch around
+  // the loads), then the ordered plane sums.
+#pragma unroll
+  for (int c = 0; c < kNormRowChunks; ++c) {
+    const int ch = min(tid + c * kNormRowThreads, nch - 1);
+    const bf16* rp = resid + (int64_t)row * ldr + ch * 4;
+    const bf16* gp = g + ch * 4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      res[c][e] = bf2f(rp[e]);
+      gg[c][e] = bf2f(gp[e]);
+    }
+    v[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int sp = 0; sp < splits; ++sp) {
+    f32x4 t[kNormRowChunks];
+#pragma unroll
+    for (int c = 0; c < kNormRowChunks; ++c) {
+      const int ch = min(tid + c * kNormRowThreads, nch - 1);
+      t[c] = *(const f32x4*)(part + sp * MN + (int64_t)row * N + ch * 4);
+    }
+#pragma unroll
+    for (int c = 0; c < kNormRowChunks; ++c) v[c] += t[c];
+  }
+  float ss = 0.f;
+  bf16 x1[kNormRowChunks][4];
+#pragma unroll
+  for (int c = 0; c < kNormRowChunks; ++c) {
+    const bool ok = tid + c * kNormRowThreads < nch;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x1[c][e] = f2bf(v[c][e] + res[c][e]);
+      const float f = bf2f(x1[c][e]);
+      if (ok) ss += f * f;
+    }
+  }
+  __shared__ float red[kNormRowThreads / 64];
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  ss = 0.f;
+#pragma unroll
+  for (int w = 0; w < kNormRowThreads / 64; ++w) ss += red[w];
+  const float r = 1.0f / sqrtf(ss / (float)N + eps);
+#pragma unroll
+  for (int c = 0; c < kNormRowChunks; ++c) {
+    const int ch = tid + c * kNormRowThreads;
+    if (ch >= nch) continue;
+    bf16x4 o, h;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[e] = x1[c][e];
+      h[e] = f2bf(bf2f(x1[c][e]) * r * gg[c][e]);
+    }
+    *(bf16x4*)(out + (int64_t)row * ldo + ch * 4) = o;
+    *(bf16x4*)(y + (int64_t)row * N + ch * 4) = h;
+  }
+}
+
 // Decode projections (M <= 128 rows).  The arithmetic intensity is ~M flop
 // per weight byte, so the weight stream from HBM sets the time: skinny
 // 64 x 64 tiles (two or four waves) give ~600 workgroups on the large
@@ -900,6 +975,30 @@ hipError_t launch_skinny(const void* A, int lda, const void* B, int ldb, int M, 
   if (splits == 1 && epi.kind == EPI_QKV) return launch_gemm(A, lda, B, ldb, M, N, K, epi, nullptr, s);
   if (M <= 64) return run_skinny<64, 2>(A, lda, B, ldb, M, N, K, epi, part, splits, s);
   return run_skinny<128, 4>(A, lda, B, ldb, M, N, K, epi, part, splits, s);
+}
+
+bool skinny_resid_norm_fused(int M, int N, int K) {
+  return M <= 128 && M > 0 && N % 4 == 0 && N <= kNormRowThreads * 4 * kNormRowChunks &&
+         skinny_splits(M, N, K, EPI_RESID) > 1;
+}
+
+hipError_t launch_skinny_resid_norm(const void* A, int lda, const void* B, int ldb, int M, int N,
+                                    int K, const void* resid, int ldr, void* out, int ldo,
+                                    const void* g, void* y, float eps, float* part, hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  const int splits = skinny_splits(M, N, K, EPI_RESID);
+  Epi pe{};
+  pe.kind = EPI_STORE_F32;
+  pe.out = part;
+  pe.ldo = N;
+  hipError_t e = M <= 64
+                     ? run_gemm<64, kSkinnyBN, 2, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits)
+                     : run_gemm<128, kSkinnyBN, 4, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
+  if (e != hipSuccess) return e;
+  splitk_resid_norm_kernel<<<M, kNormRowThreads, 0, s>>>(part, splits, M, N, (const bf16*)resid,
+                                                        ldr, (bf16*)out, ldo, (const bf16*)g,
+                                                        (bf16*)y, eps);
+  return hipGetLastError();
 }
 
 int gemm_planes_splits(int M, int N, int K) {

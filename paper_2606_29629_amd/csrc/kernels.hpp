@@ -74,6 +74,13 @@ hipError_t launch_gemm_planes(const void* A, int lda, const void* B, int ldb, in
 // Decode projections (M <= 128): skinny tiles, split-K for narrow N; fp32
 // partials in `part` (skinny_partial_bytes) reduced by an epilogue kernel.
 int skinny_splits(int M, int N, int K, int kind);
+// The O projection of a short batch fused with its residual add and the
+// following RMSNorm (split-K planes reduced row by row): used when this
+// returns true; out = x1 (bf16), y = RMSNorm(x1; g).
+bool skinny_resid_norm_fused(int M, int N, int K);
+hipError_t launch_skinny_resid_norm(const void* A, int lda, const void* B, int ldb, int M, int N,
+                                    int K, const void* resid, int ldr, void* out, int ldo,
+                                    const void* g, void* y, float eps, float* part, hipStream_t s);
 size_t skinny_partial_bytes(int M, int N, int K, int kind);
 hipError_t launch_skinny(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
                          const Epi& epi, float* part, hipStream_t s);

@@ -72,12 +72,16 @@ hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int
 }
 
 // Layer prologue, one wave per token t:
-//  * token map: the sequence s with cu_q[s] <= t < cu_q[s+1] (binary search
-//    over the non-decreasing offsets) gives the cache slot and row of t
-//    (-1 when out of range);
+//  * token map: the sequence holding t is the number of sequence ends
+//    cu_q[1 .. n_seqs] at or below t; the wave loads the ends 64 per lane
+//    group at once and counts them with ballots, so the map costs two memory
+//    round trips (ends, then the sequence's slot / prefix / start) however
+//    many sequences there are, instead of one per bisection step;
 //  * rotary table rope[t][i] = (cos, sin)(pos[t] * base^(-2i/D)), the angle
 //    formed in double precision, lane i < D/2;
 //  * RMSNorm of x[t] into y[t] (as rmsnorm_kernel).
+constexpr int kMapChunks = 4;  // sequence ends loaded per lane and round trip
+
 __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, int n_slots, int max_seq,
                                                        int half, double base,
                                                        int32_t* __restrict__ tok_slot,
@@ -90,7 +94,7 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, int n_slots, 
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= b.n_tokens) return;
-  // x and g loads first: their latency overlaps the map and the table.
+  // x, g and the position first: their latency overlaps the map.
   const bf16* xr = x + (int64_t)t * hidden;
   const int nchunk = hidden / 8;
   Pack8 v[kNormMaxChunks], gv[kNormMaxChunks];
@@ -102,22 +106,32 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, int n_slots, 
       gv[c].u = ldg16(g + ch * 8);
     }
   }
-  if (lane == 0) {
-    int lo = 0, hi = b.n_seqs;  // largest s with cu_q[s] <= t
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (b.cu_q[mid] <= t) lo = mid; else hi = mid;
+  const int pos = b.pos[t];
+  int sq = 0;
+  for (int j0 = 0; j0 < b.n_seqs; j0 += 64 * kMapChunks) {
+    int end[kMapChunks];
+#pragma unroll
+    for (int c = 0; c < kMapChunks; ++c) {
+      const int j = j0 + 64 * c + lane;
+      const int e = b.cu_q[min(j, b.n_seqs - 1) + 1];  // clamped: no branch around the load
+      end[c] = j < b.n_seqs ? e : INT32_MAX;
     }
-    const int sq = lo;
-    const int sl = b.slot[sq];
-    const int row = b.ctx_len[sq] + (t - b.cu_q[sq]);
-    const bool ok = sl >= 0 && sl < n_slots && row >= 0 && row < max_seq && t < b.cu_q[sq + 1];
+#pragma unroll
+    for (int c = 0; c < kMapChunks; ++c)
+      sq += __builtin_popcountll(__builtin_amdgcn_ballot_w64(end[c] <= t));
+  }
+  if (lane == 0) {
+    bool ok = sq < b.n_seqs;
+    const int sc = ok ? sq : 0;
+    const int q0 = b.cu_q[sc], q1 = b.cu_q[sc + 1], sl = b.slot[sc], c0 = b.ctx_len[sc];
+    const int row = c0 + (t - q0);
+    ok = ok && sl >= 0 && sl < n_slots && row >= 0 && row < max_seq && t >= q0 && t < q1;
     tok_slot[t] = ok ? sl : -1;
     tok_row[t] = ok ? row : -1;
   }
   if (lane < half) {
     const double inv_freq = pow(base, -2.0 * (double)lane / (double)(2 * half));
-    const double ang = (double)b.pos[t] * inv_freq;
+    const double ang = (double)pos * inv_freq;
     double sn, cs;
     sincos(ang, &sn, &cs);
     rope[(int64_t)t * half + lane] = make_float2((float)cs, (float)sn);

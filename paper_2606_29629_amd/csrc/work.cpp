@@ -105,10 +105,17 @@ tri_status tri_layer_work(const tri_layer_config* cfg, int32_t decode, int32_t n
         dec_tok * Hq * D * bf + dec_keys * Hkv * D * bf * 2 + part_elems * f32);
   a.add(ST_ATTN_COMBINE, 2.0 * dec_parts * Hq * D, part_elems * f32 + dec_tok * Hq * D * bf);
 
-  // O projection + residual.
-  a.add(ST_OPROJ, 2.0 * T * H * Hq * D, H * Hq * D * bf + T * Hq * D * bf + 2.0 * T * H * bf);
-  // RMSNorm(x1; mlp_norm).
-  a.add(ST_NORM2, 4.0 * T * H, 2.0 * T * H * bf + H * bf);
+  // O projection + residual, then RMSNorm(x1; mlp_norm) -- one stage for a
+  // short batch, whose split-K reduction applies the norm (x1 then never
+  // re-read).
+  const double o_flops = 2.0 * T * H * Hq * D, o_bytes = H * Hq * D * bf + T * Hq * D * bf +
+                                                         2.0 * T * H * bf;
+  if (skinny_resid_norm_fused((int)T, cfg->hidden, cfg->n_q_heads * cfg->head_dim)) {
+    a.add(ST_OPROJ, o_flops + 4.0 * T * H, o_bytes + T * H * bf + H * bf);
+  } else {
+    a.add(ST_OPROJ, o_flops, o_bytes);
+    a.add(ST_NORM2, 4.0 * T * H, 2.0 * T * H * bf + H * bf);
+  }
 
   if (!moe) {
     const double F = cfg->ffn_dim;
