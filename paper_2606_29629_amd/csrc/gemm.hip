@@ -163,10 +163,14 @@ struct Mainloop {
         buffer_load_lds16(rb, &sm.b[buf][(wv + NW * (p - A_BLK)) * 8 * kBK],
                           b_off[p - A_BLK] | kill, kb);
     };
+    // B (weight rows) as the MFMA's row operand and A (token rows) as its
+    // column operand: accumulator block (i, j) holds C^T, so a lane owns one
+    // token row and four consecutive output columns per element group, and
+    // the epilogues move 8 or 16 contiguous bytes per lane.
     auto mfma = [&](int slot, int g) {
       const int i = g / NI, j = g % NI;
       acc[i][j] =
-          __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][i], fb[slot][j], acc[i][j], 0, 0, 0);
+          __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][j], fa[slot][i], acc[i][j], 0, 0, 0);
     };
     constexpr int NMF = MI * NI, NRD = MI + NI, NLD = A_BLK + B_BLK;
     constexpr int NG = NMF > NRD ? NMF : NRD;
@@ -210,133 +214,144 @@ struct Mainloop {
   }
 };
 
-// Accumulator element r of block (i, j): row 32i + 8(r/4) + 4(lane/32) + r%4,
-// column 32j + lane%32 of the wave sub-tile.  row0 = output row of the wave's
-// first accumulator row (including 4 * (lane / 32)); rows >= row_lim are
-// not written.  The residual of a whole 32-row block row is loaded before any
-// of its sums is stored, so the loads are in flight together instead of each
-// waiting behind the previous store; out-of-range rows and columns load a
-// clamped (valid, unused) address rather than branching around the load.
+// Accumulator block (i, j) of a wave holds C^T: element e of lane l is
+// output row 32 i + l % 32 and output column 32 j + 8 (e / 4) + 4 (l / 32)
+// + e % 4 of the wave sub-tile, so elements 4q .. 4q + 3 are four consecutive
+// columns.  row0 = output row of the lane (including l % 32); col0 = output
+// column of the lane's first element (including 4 (l / 32)).  Rows >= row_lim
+// and column groups >= N are not written (N is a multiple of 4).  Operands
+// of a lane's row (residual) are loaded for a whole block before any store,
+// at clamped addresses, so no load waits behind a store.
 template <int MI, int NI, int EK>
 __device__ __forceinline__ void plain_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                                int row0, int row_lim, int col0, int N) {
   const bf16* __restrict__ resid = (const bf16*)epi.resid;
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
-    float res[NI][16];
+    const int row = row0 + 32 * i;
+    const int rc = min(row, row_lim - 1);
+    bf16x4 res[NI][4];
     if constexpr (EK == EPI_RESID) {
 #pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        const int col = min(col0 + 32 * j, N - 1);
+      for (int j = 0; j < NI; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = min(row0 + 32 * i + 8 * (r >> 2) + (r & 3), row_lim - 1);
-          res[j][r] = bf2f(resid[(int64_t)row * epi.ldr + col]);
+        for (int q = 0; q < 4; ++q) {
+          const int col = min(col0 + 32 * j + 8 * q, N - 4);
+          res[j][q] = *(const bf16x4*)(resid + (int64_t)rc * epi.ldr + col);
         }
-      }
     }
+    if (row >= row_lim) continue;
 #pragma unroll
-    for (int j = 0; j < NI; ++j) {
-      const int col = col0 + 32 * j;
-      if (col >= N) continue;
+    for (int j = 0; j < NI; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
-        if (row >= row_lim) continue;
-        float v = acc[i][j][r];
+      for (int q = 0; q < 4; ++q) {
+        const int col = col0 + 32 * j + 8 * q;
+        if (col >= N) continue;
         if constexpr (EK == EPI_STORE_F32) {
-          ((float*)epi.out)[(int64_t)row * epi.ldo + col] = v;
+          *(f32x4*)((float*)epi.out + (int64_t)row * epi.ldo + col) =
+              f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                    acc[i][j][4 * q + 3]};
         } else {
-          if constexpr (EK == EPI_RESID) v += res[j][r];
-          ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(v);
+          bf16x4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float v = acc[i][j][4 * q + e];
+            if constexpr (EK == EPI_RESID) v += bf2f(res[j][q][e]);
+            o[e] = f2bf(v);
+          }
+          *(bf16x4*)((bf16*)epi.out + (int64_t)row * epi.ldo + col) = o;
         }
       }
-    }
   }
 }
 
 // SwiGLU: blocks j < NI/2 hold gate, j + NI/2 the matching up; f0 = output
-// column (intermediate index) of block 0 for this lane.
+// column (intermediate index) of the lane's first element in block 0.
 template <int MI, int NI>
 __device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                                 int row0, int row_lim, int f0) {
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+  for (int i = 0; i < MI; ++i) {
+    const int row = row0 + 32 * i;
+    if (row >= row_lim) continue;
 #pragma unroll
-    for (int j = 0; j < NI / 2; ++j) {
-      const int f = f0 + 32 * j;
-      if (f >= epi.ffn) continue;
+    for (int j = 0; j < NI / 2; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
-        if (row >= row_lim) continue;
-        const float gt = acc[i][j][r], up = acc[i][j + NI / 2][r];
-        ((bf16*)epi.out)[(int64_t)row * epi.ldo + f] = f2bf(silu(gt) * up);
+      for (int q = 0; q < 4; ++q) {
+        const int f = f0 + 32 * j + 8 * q;
+        if (f >= epi.ffn) continue;
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float gt = acc[i][j][4 * q + e], up = acc[i][j + NI / 2][4 * q + e];
+          o[e] = f2bf(silu(gt) * up);
+        }
+        *(bf16x4*)((bf16*)epi.out + (int64_t)row * epi.ldo + f) = o;
       }
-    }
+  }
 }
 
-// q/k/v split + bias + rotary embedding + KV-cache write on the accumulators.
-// HB = 32-column blocks per half head (D / 64): block j (first half of a head)
-// pairs with block j + HB (second half), same lane, same element.  For each
-// 32-row block the rotary factors (and, for k/v heads, the tokens' cache slot
-// and row) are loaded before any store, so those loads overlap; rows past M
-// load row M - 1 (valid, unused) rather than branching around the load.
-// One 32-row block pair (first-half block j, second-half block j + HB) of a
-// q (KIND 0), k (1) or v (2) head.
+// One (token block i, first-half block j) of a q (KIND 0), k (1) or v (2)
+// head: the lane's token row, head-dim values d + 8 q + e (q, e < 4) of the
+// first half and the same plus D/2 from block j + HB.
 template <int KIND, int MI, int NI, int HB>
 __device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi& epi, int i,
-                                          int j, int row0, int M, int head, int d, float b1,
-                                          float b2) {
+                                          int j, int row0, int M, int head, int d,
+                                          const float (&b1)[4][4], const float (&b2)[4][4]) {
   constexpr int D = HB * 64, half = D / 2;
   const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
-  const float2* __restrict__ rope = epi.rope;
-  const int32_t* __restrict__ tok_slot = epi.tok_slot;
-  const int32_t* __restrict__ tok_row = epi.tok_row;
-  float2 cs[16];
-  int sl[16], tr[16];
+  const int row = row0 + 32 * i;
+  const int rc = min(row, M - 1);
+  f32x4 cs[4][2];  // (cos, sin) of d + 8 q + e: [q][0] = e 0..1, [q][1] = e 2..3
+  int sl = 0, tr = 0;
+  if constexpr (KIND != 2) {
+    const float2* __restrict__ rp = epi.rope + (int64_t)rc * half + d;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int rc = min(row0 + 32 * i + 8 * (r >> 2) + (r & 3), M - 1);
-    if constexpr (KIND != 2) cs[r] = rope[(int64_t)rc * half + d];
-    if constexpr (KIND != 0) {
-      sl[r] = tok_slot[rc];
-      tr[r] = tok_row[rc];
+    for (int q = 0; q < 4; ++q) {
+      cs[q][0] = *(const f32x4*)(rp + 8 * q);
+      cs[q][1] = *(const f32x4*)(rp + 8 * q + 2);
     }
   }
-  const int kvh = KIND == 1 ? head - Hq : head - Hq - Hkv;
-  bf16* base = (bf16*)(KIND == 0 ? epi.q : (KIND == 1 ? epi.kc : epi.vc));
+  if constexpr (KIND != 0) {
+    sl = epi.tok_slot[rc];
+    tr = epi.tok_row[rc];
+  }
+  if (row >= M) return;
+  bf16* p;
+  if constexpr (KIND == 0) {
+    p = (bf16*)epi.q + ((int64_t)row * Hq + head) * D + d;
+  } else {
+    if (sl < 0) return;
+    const int kvh = KIND == 1 ? head - Hq : head - Hq - Hkv;
+    p = (bf16*)(KIND == 1 ? epi.kc : epi.vc) + (((int64_t)sl * Hkv + kvh) * epi.max_seq + tr) * D + d;
+  }
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int row = row0 + 32 * i + 8 * (r >> 2) + (r & 3);
-    float x1 = acc[i][j][r] + b1, x2 = acc[i][j + HB][r] + b2;
-    if constexpr (KIND != 2) {
-      const float y1 = x1 * cs[r].x - x2 * cs[r].y;
-      const float y2 = x2 * cs[r].x + x1 * cs[r].y;
-      x1 = y1;
-      x2 = y2;
+  for (int q = 0; q < 4; ++q) {
+    bf16x4 o1, o2;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float x1 = acc[i][j][4 * q + e] + b1[q][e], x2 = acc[i][j + HB][4 * q + e] + b2[q][e];
+      if constexpr (KIND != 2) {
+        const float c = cs[q][e >> 1][2 * (e & 1)], sn = cs[q][e >> 1][2 * (e & 1) + 1];
+        const float y1 = x1 * c - x2 * sn;
+        const float y2 = x2 * c + x1 * sn;
+        x1 = y1;
+        x2 = y2;
+      }
+      o1[e] = f2bf(x1);
+      o2[e] = f2bf(x2);
     }
-    int64_t off;
-    bool ok = row < M;
-    if constexpr (KIND == 0) {
-      off = ((int64_t)row * Hq + head) * D + d;
-    } else {
-      ok = ok && sl[r] >= 0;
-      off = (((int64_t)sl[r] * Hkv + kvh) * epi.max_seq + tr[r]) * D + d;
-    }
-    if (ok) {
-      base[off] = f2bf(x1);
-      base[off + half] = f2bf(x2);
-    }
+    *(bf16x4*)(p + 8 * q) = o1;
+    *(bf16x4*)(p + 8 * q + half) = o2;
   }
 }
 
 // q/k/v split + bias + rotary embedding + KV-cache write on the accumulators.
 // HB = 32-column blocks per half head (D / 64): block j (first half of a head)
-// pairs with block j + HB (second half), same lane, same element.  For each
-// 32-row block the rotary factors (and, for k/v heads, the tokens' cache slot
-// and row) are loaded before any store, so those loads overlap; rows past M
-// load row M - 1 (valid, unused) rather than branching around the load.
+// pairs with block j + HB (second half), same lane, same element.  The
+// rotary factors (four (cos, sin) pairs per element group, 32 contiguous
+// bytes) and, for k/v heads, the token's cache slot and row are loaded before
+// the stores.
 template <int MI, int NI, int HB>
 __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                              int row0, int col0, int M, int N) {
@@ -345,14 +360,17 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
 #pragma unroll
   for (int j = 0; j < NI; ++j) {
     if ((j / HB) & 1) continue;
-    const int col = col0 + 32 * j;  // first-half column
+    const int col = col0 + 32 * j;  // first-half column of the lane's element 0
     if (col >= N) continue;
     const int head = col / D, d = col % D;
-    float b1 = 0.f, b2 = 0.f;
-    if (epi.bias) {
-      b1 = bf2f(((const bf16*)epi.bias)[col]);
-      b2 = bf2f(((const bf16*)epi.bias)[col + half]);
-    }
+    float b1[4][4], b2[4][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        b1[q][e] = epi.bias ? bf2f(((const bf16*)epi.bias)[col + 8 * q + e]) : 0.f;
+        b2[q][e] = epi.bias ? bf2f(((const bf16*)epi.bias)[col + 8 * q + e + half]) : 0.f;
+      }
     // the head, hence its kind, is uniform across the wave
     const int kind = __builtin_amdgcn_readfirstlane(head < Hq ? 0 : (head < Hq + Hkv ? 1 : 2));
 #pragma unroll
@@ -428,22 +446,22 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
     Epi e{};
     e.out = tail + (int64_t)u * BM * BN;
     e.ldo = BN;
-    plain_epilogue<MI, NI, EPI_STORE_F32>(acc, e, wm * WM + 4 * lg, BM, wn * WN + lr, BN);
+    plain_epilogue<MI, NI, EPI_STORE_F32>(acc, e, wm * WM + lr, BM, wn * WN + 4 * lg, BN);
     return;
   }
-  const int row0 = tm * BM + wm * WM + 4 * lg;
+  const int row0 = tm * BM + wm * WM + lr;
   if constexpr (EK == EPI_STORE_F32) {
     Epi e = epi;
     e.out = (float*)epi.out + (int64_t)blockIdx.y * M * epi.ldo;
-    plain_epilogue<MI, NI, EK>(acc, e, row0, M, tn * BN + wn * WN + lr, N);
+    plain_epilogue<MI, NI, EK>(acc, e, row0, M, tn * BN + wn * WN + 4 * lg, N);
   } else if constexpr (EK == EPI_STORE || EK == EPI_RESID) {
-    plain_epilogue<MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + lr, N);
+    plain_epilogue<MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + 4 * lg, N);
   } else if constexpr (EK == EPI_SWIGLU) {
-    swiglu_epilogue<MI, NI>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + lr);
+    swiglu_epilogue<MI, NI>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
   } else if (epi.head_dim == 128) {
-    qkv_epilogue<MI, NI, 2>(acc, epi, row0, tn * BN + wn * WN + lr, M, N);
+    qkv_epilogue<MI, NI, 2>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
   } else {
-    qkv_epilogue<MI, NI, 1>(acc, epi, row0, tn * BN + wn * WN + lr, M, N);
+    qkv_epilogue<MI, NI, 1>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
   }
 }
 
@@ -512,11 +530,11 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
   ML::run(sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
 
   const int lr = lane & 31, lg = lane >> 5;
-  const int row0 = p0 + wm * WM + 4 * lg;
+  const int row0 = p0 + wm * WM + lr;
   if constexpr (EK == EPI_SWIGLU)
-    swiglu_epilogue<MI, NI>(acc, epi, row0, p_end, tn * (BN / 2) + wn * (WN / 2) + lr);
+    swiglu_epilogue<MI, NI>(acc, epi, row0, p_end, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
   else
-    plain_epilogue<MI, NI, EK>(acc, epi, row0, p_end, tn * BN + wn * WN + lr, N);
+    plain_epilogue<MI, NI, EK>(acc, epi, row0, p_end, tn * BN + wn * WN + 4 * lg, N);
 }
 
 template <typename Kern>
