@@ -177,28 +177,47 @@ hipError_t launch_moe_route_bf16(const void* h, const void* w_router, int T, int
 }
 
 // One workgroup per expert: rank of every pair routed to it, in pair order.
+// The pairs are scanned kCountUnroll x 256 at a time: the loads of a batch
+// are issued together and one barrier per batch publishes the waves' counts.
+constexpr int kCountUnroll = 16;
+
 __global__ __launch_bounds__(256) void moe_count_kernel(const int32_t* __restrict__ idx,
                                                         int n_pairs, int32_t* __restrict__ rank,
                                                         int32_t* __restrict__ counts) {
-  __shared__ int wsum[4];
+  __shared__ int wsum[2][kCountUnroll][4];
   const int e = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int base = 0;
-  for (int p0 = 0; p0 < n_pairs; p0 += 256) {
-    const int p = p0 + tid;
-    const bool f = p < n_pairs && idx[p] == e;
-    const unsigned long long m = __ballot(f);
-    const int within = __popcll(m & ((1ull << lane) - 1ull));
-    if (lane == 0) wsum[wave] = __popcll(m);
-    __syncthreads();
-    int pre = 0, tot = 0;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  int base = 0, buf = 0;
+  for (int p0 = 0; p0 < n_pairs; p0 += 256 * kCountUnroll, buf ^= 1) {
+    bool f[kCountUnroll];
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      pre += w < wave ? wsum[w] : 0;
-      tot += wsum[w];
+    for (int u = 0; u < kCountUnroll; ++u) {
+      const int p = p0 + 256 * u + tid;
+      const int v = idx[min(p, n_pairs - 1)];  // clamped: no branch around the load
+      f[u] = p < n_pairs && v == e;
     }
-    if (f) rank[p] = base + pre + within;
-    base += tot;
+    int within[kCountUnroll];
+#pragma unroll
+    for (int u = 0; u < kCountUnroll; ++u) {
+      const unsigned long long m = __ballot(f[u]);
+      within[u] = __popcll(m & below);
+      if (lane == 0) wsum[buf][u][wave] = __popcll(m);
+    }
+    // double-buffered counts: one barrier per batch suffices
     __syncthreads();
+    int run = base;
+#pragma unroll
+    for (int u = 0; u < kCountUnroll; ++u) {
+      int pre = 0, tot = 0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        pre += w < wave ? wsum[buf][u][w] : 0;
+        tot += wsum[buf][u][w];
+      }
+      if (f[u]) rank[p0 + 256 * u + tid] = run + pre + within[u];
+      run += tot;
+    }
+    base = run;
   }
   if (tid == 0) counts[e] = base;
 }
@@ -210,18 +229,21 @@ __global__ __launch_bounds__(256) void moe_scatter_kernel(
     int32_t* __restrict__ inv, int32_t* __restrict__ seg, int32_t* __restrict__ tile_off) {
   __shared__ int off[257], toff[257];
   const int tid = threadIdx.x;
-  if (tid == 0) {
-    int s = 0, t = 0;
-    for (int e = 0; e < E; ++e) {
-      off[e] = s;
-      toff[e] = t;
-      s += counts[e];
-      t += cdiv(counts[e], bm);
-    }
-    off[E] = s;
-    toff[E] = t;
-  }
+  // exclusive scans of the counts and tile counts over the E <= 256 experts:
+  // one thread per expert, Hillis-Steele in LDS
+  const int c = tid < E ? counts[tid] : 0;
+  off[tid + 1] = c;
+  toff[tid + 1] = cdiv(c, bm);
+  if (tid == 0) off[0] = toff[0] = 0;
   __syncthreads();
+  for (int d = 1; d < 256; d <<= 1) {
+    const int a = tid + 1 - d >= 1 ? off[tid + 1 - d] : 0;
+    const int b = tid + 1 - d >= 1 ? toff[tid + 1 - d] : 0;
+    __syncthreads();
+    off[tid + 1] += a;
+    toff[tid + 1] += b;
+    __syncthreads();
+  }
   if (blockIdx.x == 0)
     for (int i = tid; i <= E; i += 256) {
       seg[i] = off[i];
