@@ -101,14 +101,29 @@ typedef struct {
   const void* w_router;  /* MoE [E, H]; NULL for a dense layer                     */
 } tri_layer_weights;
 
-/* KV cache: K and V each [n_slots, Hkv, max_seq, D] bfloat16 (device).  Keys
- * are stored after the rotary embedding.  Row r of a slot holds the token at
- * position r of the sequence occupying that slot.                              */
+/* KV cache (device, bfloat16).  Keys are stored after the rotary embedding.
+ * Row r of a slot holds the token at position r of the sequence occupying
+ * that slot.  Two layouts:
+ *  - contiguous (block_table == NULL): K and V each [n_slots, Hkv, max_seq, D];
+ *  - paged, the fixed-size cache blocks of the PagedAttention memory manager
+ *    under the serving framework of Section II-A: K and V are pools
+ *    [n_blocks, Hkv, block_size, D], and row r of slot s lives in block
+ *    block_table[s * (max_seq / block_size) + r / block_size] at row
+ *    r % block_size.  block_size is a multiple of 64 that divides max_seq;
+ *    block_table is device int32 [n_slots, max_seq / block_size], 4-byte
+ *    aligned, and may leave entries that no row of the batch uses unset.
+ *    An entry outside [0, n_blocks) is never dereferenced: its rows read as
+ *    zero and writes to it are dropped (the sequence's results are then
+ *    unspecified).  The layer reads and writes only the blocks the batch's
+ *    rows map to.                                                               */
 typedef struct {
   void* k;
   void* v;
-  int32_t n_slots;
-  int32_t max_seq;
+  int32_t n_slots;              /* sequences (block-table rows when paged)       */
+  int32_t max_seq;              /* logical rows per sequence                     */
+  const int32_t* block_table;   /* NULL: contiguous                              */
+  int32_t block_size;           /* paged: rows per block; else ignored           */
+  int32_t n_blocks;             /* paged: blocks in each pool; else ignored      */
 } tri_kv_cache;
 
 /* A ragged batch (one scheduler step).  Host scalars size the launches; the

@@ -3,13 +3,15 @@
 The compute path is libtri.so (hand-written HIP kernels for gfx950 behind the
 C ABI in include/tri.h); this package is its thin ctypes binding.
 """
-from ._lib import (DeviceBatch, LayerConfig, Profile, TriError, Work, kvcache_append,
+from ._lib import (DeviceBatch, LayerConfig, PagedCache, Profile, TriError, Work, kv_struct,
+                   kvcache_append,
                    layer_decode, layer_work, phase_intensity, profile_enable, profile_read,
                    work_dict, work_sum,
                    layer_prefill, lib, make_config, moe_route, status_string, workspace_layout,
                    workspace_size)
 
-__all__ = ["DeviceBatch", "LayerConfig", "Profile", "TriError", "Work", "kvcache_append",
+__all__ = ["DeviceBatch", "LayerConfig", "PagedCache", "Profile", "TriError", "Work", "kv_struct",
+           "kvcache_append",
            "layer_decode", "layer_work", "phase_intensity", "work_dict", "work_sum",
            "layer_prefill", "lib", "profile_enable", "profile_read", "make_config", "moe_route", "status_string",
            "workspace_layout", "workspace_size"]

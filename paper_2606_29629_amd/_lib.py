@@ -36,7 +36,8 @@ class LayerWeights(ctypes.Structure):
 
 class KVCache(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("n_slots", ctypes.c_int32),
-                ("max_seq", ctypes.c_int32)]
+                ("max_seq", ctypes.c_int32), ("block_table", ctypes.c_void_p),
+                ("block_size", ctypes.c_int32), ("n_blocks", ctypes.c_int32)]
 
 
 class BatchStruct(ctypes.Structure):
@@ -199,6 +200,30 @@ def workspace_layout(cfg: LayerConfig, batch: DeviceBatch) -> WorkspaceMap:
     return m
 
 
+class PagedCache:
+    """A paged KV cache: K and V pools [n_blocks, Hkv, block_size, D] (bf16) and
+    a device int32 block table [n_slots, max_seq / block_size]."""
+
+    def __init__(self, k_pool, v_pool, block_table, max_seq: int):
+        self.k, self.v, self.block_table = k_pool, v_pool, block_table
+        self.n_slots = int(block_table.shape[0])
+        self.max_seq = int(max_seq)
+        self.block_size = int(k_pool.shape[2])
+        self.n_blocks = int(k_pool.shape[0])
+
+    def __getitem__(self, i):
+        return (self.k, self.v)[i]
+
+
+def kv_struct(cache) -> KVCache:
+    """KVCache for a contiguous (k, v) pair [n_slots, Hkv, max_seq, D] or a PagedCache."""
+    if isinstance(cache, PagedCache):
+        return KVCache(_ptr(cache.k), _ptr(cache.v), cache.n_slots, cache.max_seq,
+                       _ptr(cache.block_table), cache.block_size, cache.n_blocks)
+    return KVCache(_ptr(cache[0]), _ptr(cache[1]), int(cache[0].shape[0]),
+                   int(cache[0].shape[2]), None, 0, 0)
+
+
 def _layer(fn_name, cfg, w, cache, batch, x, out, workspace, route_idx, route_w, stream):
     import torch
     if out is None:
@@ -207,7 +232,7 @@ def _layer(fn_name, cfg, w, cache, batch, x, out, workspace, route_idx, route_w,
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     ws = weights_struct(w)
-    kc = KVCache(_ptr(cache[0]), _ptr(cache[1]), int(cache[0].shape[0]), int(cache[0].shape[2]))
+    kc = kv_struct(cache)
     b = batch.struct()
     st = getattr(lib(), fn_name)(ctypes.byref(cfg), ctypes.byref(ws), ctypes.byref(kc),
                                  ctypes.byref(b), _ptr(x), _ptr(out), _ptr(route_idx),
@@ -232,7 +257,7 @@ def layer_decode(cfg, w, cache, batch, x, out=None, workspace=None, route_idx=No
 
 
 def kvcache_append(cfg, cache, batch, k_new, v_new, stream=None) -> None:
-    kc = KVCache(_ptr(cache[0]), _ptr(cache[1]), int(cache[0].shape[0]), int(cache[0].shape[2]))
+    kc = kv_struct(cache)
     b = batch.struct()
     _check(lib().tri_kvcache_append(ctypes.byref(cfg), ctypes.byref(kc), ctypes.byref(b),
                                     _ptr(k_new), _ptr(v_new), _stream(stream)),

@@ -91,6 +91,31 @@ size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
   return p;
 }
 
+// Cache shape checks shared by the layer and the append: logical sizes, and
+// for a paged cache the block table, block size and pool.
+tri_status check_cache(const tri_kv_cache* c) {
+  if (!c) return TRI_ERR_NULL;
+  if (!c->k || !c->v) return TRI_ERR_NULL;
+  if (c->n_slots <= 0 || c->max_seq <= 0) return TRI_ERR_SHAPE;
+  if (c->block_table) {
+    if (c->block_size <= 0 || c->n_blocks <= 0) return TRI_ERR_SHAPE;
+    if (c->block_size % 64 != 0) return TRI_ERR_UNSUPPORTED;
+    if (c->max_seq % c->block_size != 0) return TRI_ERR_SHAPE;
+    if (((uintptr_t)c->block_table & 3u) != 0) return TRI_ERR_ALIGN;
+  }
+  return TRI_OK;
+}
+
+KvDev kv_dev(const tri_kv_cache* c) {
+  KvDev kv{};
+  kv.n_slots = c->n_slots;
+  kv.max_seq = c->max_seq;
+  kv.table = c->block_table;
+  kv.block_size = c->block_table ? c->block_size : 0;
+  kv.n_blocks = c->block_table ? c->n_blocks : 0;
+  return kv;
+}
+
 Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
   const size_t T = (size_t)b->n_tokens, H = c->hidden, D = c->head_dim;
   const bool moe = is_moe(c);
@@ -197,14 +222,13 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   if (decode && (b->n_tokens != b->n_seqs || b->max_q_len > 1)) return TRI_ERR_SHAPE;
   if (b->n_tokens == 0) return TRI_OK;
   if (!x_in || !x_out || !ws || !b->cu_q || !b->ctx_len || !b->slot || !b->pos) return TRI_ERR_NULL;
-  if (!cache->k || !cache->v) return TRI_ERR_NULL;
+  if ((st = check_cache(cache)) != TRI_OK) return st;
   if (!w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up || !w->w_down)
     return TRI_ERR_NULL;
   const bool moe = is_moe(cfg);
   if (moe && !w->w_router) return TRI_ERR_NULL;
   const bool bias = (cfg->flags & TRI_F_QKV_BIAS) != 0;
   if (bias && !w->b_qkv) return TRI_ERR_NULL;
-  if (cache->n_slots <= 0 || cache->max_seq <= 0) return TRI_ERR_SHAPE;
   if (b->max_ctx_len >= cache->max_seq || b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
   if (decode && (int64_t)b->max_ctx_len + 1 > cache->max_seq) return TRI_ERR_RANGE;
   const void* ptrs[] = {x_in, x_out, ws, cache->k, cache->v, w->attn_norm, w->w_qkv, w->w_o,
@@ -227,6 +251,7 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   const int Nqkv = (Hq + 2 * Hkv) * D;
   BatchDev bd{b->cu_q, b->ctx_len, b->slot, b->pos, b->n_seqs, b->n_tokens, b->max_q_len,
               b->max_ctx_len};
+  const KvDev kv = kv_dev(cache);
   int32_t* tok_slot = at<int32_t>(ws, L.tok_slot);
   int32_t* tok_row = at<int32_t>(ws, L.tok_row);
   float2* rope = at<float2>(ws, L.rope);
@@ -241,8 +266,8 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   {
     // token map + rotary table + pre-attention RMSNorm
     StageTimer t_(ST_PROLOGUE, s);
-    TRI_HIP(launch_prologue(bd, cache->n_slots, cache->max_seq, D, cfg->rope_base, tok_slot,
-                            tok_row, rope, x_in, w->attn_norm, h, H, cfg->rms_eps, s));
+    TRI_HIP(launch_prologue(bd, kv, D, cfg->rope_base, tok_slot, tok_row, rope, x_in,
+                            w->attn_norm, h, H, cfg->rms_eps, s));
   }
   Epi e{};
   e.kind = EPI_QKV;
@@ -256,25 +281,22 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   e.n_q_heads = Hq;
   e.n_kv_heads = Hkv;
   e.head_dim = D;
-  e.max_seq = cache->max_seq;
+  e.max_seq = kv.panel_rows();
   {
     StageTimer t_(ST_QKV, s);
     if ((st = run_linear(h, H, w->w_qkv, T, Nqkv, H, e, part, s)) != TRI_OK) return st;
   }
   if (!decode && b->max_q_len > 1) {
     StageTimer t_(ST_ATTN_PREFILL, s);
-    TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, cache->n_slots, cache->max_seq,
-                                Hq, Hkv, D, 0, s));
+    TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, kv, Hq, Hkv, D, 0, s));
   }
   {
     StageTimer t_(ST_ATTN_DECODE, s);
-    TRI_HIP(launch_attn_decode_split(q, cache->k, cache->v, part, bd, cache->n_slots,
-                                     cache->max_seq, Hq, Hkv, D, s));
+    TRI_HIP(launch_attn_decode_split(q, cache->k, cache->v, part, bd, kv, Hq, Hkv, D, s));
   }
   {
     StageTimer t_(ST_ATTN_COMBINE, s);
-    TRI_HIP(launch_attn_decode_combine(part, attn, bd, cache->n_slots, cache->max_seq, Hq, Hkv, D,
-                                       s));
+    TRI_HIP(launch_attn_decode_combine(part, attn, bd, kv, Hq, Hkv, D, s));
   }
   e = Epi{};
   e.kind = EPI_RESID;
@@ -426,9 +448,8 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
   tri_status st = check_batch_scalars(b);
   if (st != TRI_OK) return st;
   if (b->n_tokens == 0) return TRI_OK;
-  if (!k_new || !v_new || !cache->k || !cache->v || !b->cu_q || !b->ctx_len || !b->slot)
-    return TRI_ERR_NULL;
-  if (cache->n_slots <= 0 || cache->max_seq <= 0) return TRI_ERR_SHAPE;
+  if (!k_new || !v_new || !b->cu_q || !b->ctx_len || !b->slot) return TRI_ERR_NULL;
+  if ((st = check_cache(cache)) != TRI_OK) return st;
   if (b->max_ctx_len >= cache->max_seq || b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
   const void* ptrs[] = {k_new, v_new, cache->k, cache->v};
   for (const void* p : ptrs)
@@ -436,7 +457,7 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
   BatchDev bd{b->cu_q, b->ctx_len, b->slot, b->pos, b->n_seqs, b->n_tokens, b->max_q_len,
               b->max_ctx_len};
   StageTimer t_(ST_APPEND, (hipStream_t)stream);
-  TRI_HIP(launch_kv_append_direct(bd, cache->n_slots, cache->max_seq, cfg->n_kv_heads,
+  TRI_HIP(launch_kv_append_direct(bd, kv_dev(cache), cfg->n_kv_heads,
                                   cfg->head_dim, k_new, v_new, cache->k, cache->v,
                                   (hipStream_t)stream));
   return TRI_OK;

@@ -53,15 +53,22 @@ static int decode_waves_per_cu(int head_dim, int group) {
 // wave then streams from launch to finish with no second round), but no
 // split shorter than kDecMinSplit keys; the split is a multiple of the
 // 32-key tile.
-int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv, int head_dim, int group) {
+int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv, int head_dim, int group,
+                           int max_split) {
   if (max_kv < 1) max_kv = 1;
   const int64_t pairs = (int64_t)(n_seqs > 0 ? n_seqs : 1) * (n_kv_heads > 0 ? n_kv_heads : 1);
   const int64_t resident = (int64_t)decode_waves_per_cu(head_dim, group) * cu_count();
   int64_t ns = resident / pairs;
   if (ns < 1) ns = 1;
   if (ns > cdiv(max_kv, kDecMinSplit)) ns = cdiv(max_kv, kDecMinSplit);
-  return cdiv(cdiv(max_kv, (int)ns), kDecTile) * kDecTile;
+  int split = cdiv(cdiv(max_kv, (int)ns), kDecTile) * kDecTile;
+  if (max_split > 0 && split > max_split) split = max_split / kDecTile * kDecTile;
+  return split;
 }
+
+// A split of a paged cache spans at most 64 blocks (one per lane of its
+// block-id register): splits of up to 62 blocks.
+int attn_decode_max_split(const KvDev& kv) { return kv.table ? 62 * kv.block_size : 0; }
 
 size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv) {
   const int ns = cdiv(max_kv < 1 ? 1 : max_kv, kDecMinSplit);  // bound for every split size
@@ -139,12 +146,12 @@ __device__ __forceinline__ void lds_read_tr16_group(const uint32_t (&a)[2 * DB],
   }
 }
 
-template <int D>
+template <int D, bool PAGED>
 __global__ __launch_bounds__(64, 2) void attn_decode_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
     float* __restrict__ part, const int32_t* __restrict__ cu_q,
-    const int32_t* __restrict__ ctx_len, const int32_t* __restrict__ slot, int n_slots,
-    int max_seq, int Hq, int Hkv, int nsplit, int split_keys, float scale_log2e, int n_tokens) {
+    const int32_t* __restrict__ ctx_len, const int32_t* __restrict__ slot, KvDev kv, int Hq,
+    int Hkv, int nsplit, int split_keys, float scale_log2e, int n_tokens) {
   constexpr int DC = D / 8;                  // 16-byte chunks per row
   constexpr int TB = kDecTile * D * 2;       // bytes per K (or V) tile
   constexpr int BLK = TB / 1024;             // 1 KB loads per V tile
@@ -157,7 +164,7 @@ __global__ __launch_bounds__(64, 2) void attn_decode_kernel(
   // The sequence's scalars in one round trip (s < n_seqs by the grid).
   const int t = cu_q[s], t1 = cu_q[s + 1], c = ctx_len[s], sl = slot[s];
   if (t1 - t != 1 || t < 0 || t >= n_tokens) return;
-  if (sl < 0 || sl >= n_slots || c < 0 || c + 1 > max_seq) return;
+  if (sl < 0 || sl >= kv.n_slots || c < 0 || c + 1 > kv.max_seq) return;
   const int k_begin = sp * split_keys;
   const int k_end = min(c + 1, k_begin + split_keys);
   if (k_begin >= k_end) return;
@@ -167,12 +174,37 @@ __global__ __launch_bounds__(64, 2) void attn_decode_kernel(
 
   const int lane = threadIdx.x;
   const int r = lane & 31, g = lane >> 5;
-  const int64_t cache_off = ((int64_t)sl * Hkv + kvh) * max_seq * D;
-  // Rows at or past k_end read as zero.
-  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(Kc + cache_off), (short)0, k_end * D * 2, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(Vc + cache_off), (short)0, k_end * D * 2, 0x00020000);
+  // Paged cache: lane j holds the pool block of the split's j-th block (the
+  // split spans at most 64 blocks), -1 for an entry outside the pool.
+  const int prows = PAGED ? kv.block_size : kv.max_seq;
+  const int jb0 = PAGED ? k_begin / kv.block_size : 0;
+  int tbl = -1;
+  if (PAGED) {
+    const int nblk = (k_end - 1) / kv.block_size - jb0 + 1;
+    if (lane < nblk) {
+      const int blk = kv.table[(int64_t)sl * kv.blocks_per_slot() + jb0 + lane];
+      tbl = (blk >= 0 && blk < kv.n_blocks) ? blk : -1;
+    }
+  }
+  // Buffer descriptor of tile i's rows of one cache operand: keys past the
+  // sequence, tiles past the split and blocks outside the pool read as zero.
+  auto tile_rsrc = [&](const bf16* base, int i) {
+    const int key0 = k_begin + kDecTile * i;
+    int panel = sl, prow = key0, rows = 0;
+    if (i < nt) {
+      rows = min(kDecTile, k_end - key0);
+      if (PAGED) {
+        const int j = key0 / kv.block_size;
+        panel = __builtin_amdgcn_readlane(tbl, j - jb0);
+        prow = key0 - j * kv.block_size;
+        if (panel < 0) rows = 0;
+      }
+    }
+    if (rows == 0) panel = prow = 0;
+    return __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(base + (((int64_t)panel * Hkv + kvh) * prows + prow) * D), (short)0,
+        rows * D * 2, 0x00020000);
+  };
   // V: lane l of 1 KB block b fills tile row b (64 / DC) + l / DC, physical
   // chunk l % DC = logical chunk kv_chunk(l % DC, row) (an involution).
   uint32_t ld_off[BLK];
@@ -185,28 +217,21 @@ __global__ __launch_bounds__(64, 2) void attn_decode_kernel(
   uint32_t k_off[DS];
 #pragma unroll
   for (int k = 0; k < DS; ++k) k_off[k] = (uint32_t)((r * D + (2 * k + g) * 8) * 2);
-  // Tile i = keys k_begin + 32 i ...; tiles past the split are issued out of
-  // range (zero fill, no traffic) to keep the load count uniform.
-  auto tile_base = [&](int i, uint32_t& kill) {
-    kill = i < nt ? 0u : 0x80000000u;
-    return (uint32_t)(k_begin + kDecTile * (i < nt ? i : 0)) * D * 2;
-  };
+  // Tile i = keys k_begin + 32 i ...; tiles past the split are issued with an
+  // empty descriptor (zero fill, no traffic) to keep the load count uniform.
   auto issue_v = [&](int i) {
-    uint32_t kill;
-    const uint32_t kb = tile_base(i, kill);
+    const __amdgpu_buffer_rsrc_t rv = tile_rsrc(Vc, i);
     const int st = i % kDecStages;
 #pragma unroll
-    for (int j = 0; j < BLK; ++j)
-      buffer_load_lds16(rv, &sm.v[st][j * 512], (ld_off[j] | kill) + kb, 0);
+    for (int j = 0; j < BLK; ++j) buffer_load_lds16(rv, &sm.v[st][j * 512], ld_off[j], 0);
   };
   bf16x8 kreg[2][DS];  // K of tile i in slot i % 2
   auto issue_k = [&](auto slot, int i) {
-    uint32_t kill;
-    const uint32_t kb = tile_base(i, kill);
+    const __amdgpu_buffer_rsrc_t rk = tile_rsrc(Kc, i);
 #pragma unroll
     for (int k = 0; k < DS; ++k)
-      kreg[decltype(slot)::value][k] = __builtin_bit_cast(
-          bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, (k_off[k] | kill) + kb, 0, 0));
+      kreg[decltype(slot)::value][k] =
+          __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, k_off[k], 0, 0));
   };
   // Q of the group's heads, staged once in LDS after the V ring ([grp][D],
   // chunks swizzled like the K/V tiles so the per-tile fragment reads are
@@ -382,38 +407,43 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(
   O[((int64_t)t * Hq + qh) * D + d] = f2bf(o / Lsum);
 }
 
-template <int D>
+template <int D, bool PAGED>
 static hipError_t run_decode(const void* q, const void* kc, const void* vc, float* part,
-                             const BatchDev& b, int n_slots, int max_seq, int Hq, int Hkv,
+                             const BatchDev& b, const KvDev& kv, int Hq, int Hkv,
                              hipStream_t s) {
   const int max_kv = b.max_ctx_len + 1;
-  const int split = attn_decode_split_keys(b.n_seqs, Hkv, max_kv, D, Hq / Hkv);
+  const int split =
+      attn_decode_split_keys(b.n_seqs, Hkv, max_kv, D, Hq / Hkv, attn_decode_max_split(kv));
   const int nsplit = cdiv(max_kv, split);
   const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
   dim3 grid(nsplit, Hkv, b.n_seqs);
   const size_t smem = sizeof(DecSmem<D>) + (size_t)cdiv(Hq / Hkv, 512 / D) * 1024;
-  attn_decode_kernel<D><<<grid, 64, smem, s>>>(
-      (const bf16*)q, (const bf16*)kc, (const bf16*)vc, part, b.cu_q, b.ctx_len, b.slot, n_slots,
-      max_seq, Hq, Hkv, nsplit, split, scale_log2e, b.n_tokens);
+  attn_decode_kernel<D, PAGED><<<grid, 64, smem, s>>>(
+      (const bf16*)q, (const bf16*)kc, (const bf16*)vc, part, b.cu_q, b.ctx_len, b.slot, kv, Hq,
+      Hkv, nsplit, split, scale_log2e, b.n_tokens);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_decode_split(const void* q, const void* kc, const void* vc, float* part,
-                                    const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
+                                    const BatchDev& b, const KvDev& kv, int n_q_heads,
                                     int n_kv_heads, int head_dim, hipStream_t s) {
   if (b.n_seqs == 0) return hipSuccess;
+  const bool paged = kv.table != nullptr;
   if (head_dim == 128)
-    return run_decode<128>(q, kc, vc, part, b, n_slots, max_seq, n_q_heads, n_kv_heads, s);
-  return run_decode<64>(q, kc, vc, part, b, n_slots, max_seq, n_q_heads, n_kv_heads, s);
+    return paged ? run_decode<128, true>(q, kc, vc, part, b, kv, n_q_heads, n_kv_heads, s)
+                 : run_decode<128, false>(q, kc, vc, part, b, kv, n_q_heads, n_kv_heads, s);
+  return paged ? run_decode<64, true>(q, kc, vc, part, b, kv, n_q_heads, n_kv_heads, s)
+               : run_decode<64, false>(q, kc, vc, part, b, kv, n_q_heads, n_kv_heads, s);
 }
 
 hipError_t launch_attn_decode_combine(const float* part, void* out, const BatchDev& b,
-                                      int n_slots, int max_seq, int n_q_heads, int n_kv_heads,
+                                      const KvDev& kv, int n_q_heads, int n_kv_heads,
                                       int head_dim, hipStream_t s) {
   if (b.n_seqs == 0) return hipSuccess;
+  const int n_slots = kv.n_slots, max_seq = kv.max_seq;
   const int max_kv = b.max_ctx_len + 1;
   const int split = attn_decode_split_keys(b.n_seqs, n_kv_heads, max_kv, head_dim,
-                                           n_q_heads / n_kv_heads);
+                                           n_q_heads / n_kv_heads, attn_decode_max_split(kv));
   const int nsplit = cdiv(max_kv, split);
   dim3 cgrid(b.n_seqs, n_q_heads);
   if (head_dim == 128)

@@ -37,12 +37,12 @@ struct FaSmem {
   bf16 v[2][kFaBK * D];  // [key][d], chunks swizzled by kv_chunk
 };
 
-template <int D>
+template <int D, bool PAGED>
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
     bf16* __restrict__ O, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ ctx_len,
-    const int32_t* __restrict__ slot, int n_slots, int max_seq, int Hq, int Hkv,
-    float scale_log2e, int include_single, int n_tokens) {
+    const int32_t* __restrict__ slot, KvDev kv, int Hq, int Hkv, float scale_log2e,
+    int include_single, int n_tokens) {
   constexpr int DC = D / 8;                     // 16-byte chunks per row
   constexpr int ROWS_PER_KB = 64 / DC;          // tile rows filled by one 1 KB wave load
   constexpr int BLK = kFaBK / ROWS_PER_KB / 4;  // 1 KB loads per wave per operand and tile
@@ -57,9 +57,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   if (n <= 0 || (n == 1 && !include_single) || q0 < 0 || q0 + n > n_tokens) return;
   const int qt = (int)gridDim.x - 1 - (int)blockIdx.x;  // heavy (late) tiles first
   if (qt * kFaBQ >= n) return;
-  if (sl < 0 || sl >= n_slots || c < 0 || c + n > max_seq) return;
+  if (sl < 0 || sl >= kv.n_slots || c < 0 || c + n > kv.max_seq) return;
   const int kvh = (qh * Hkv) / Hq;
-  const int64_t cache_off = ((int64_t)sl * Hkv + kvh) * max_seq * D;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -67,13 +66,25 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   const int kv_len = c + min(n, (qt + 1) * kFaBQ);
   const int nkt = cdiv(kv_len, kFaBK);
 
-  // The whole offset goes in the per-lane operand so that the range check
-  // (offset >= kv_len rows -> zero) covers it.
-  const uint32_t kv_bytes = (uint32_t)kv_len * D * 2;
-  const __amdgpu_buffer_rsrc_t rk =
-      __builtin_amdgcn_make_buffer_rsrc((void*)(Kc + cache_off), (short)0, kv_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rv =
-      __builtin_amdgcn_make_buffer_rsrc((void*)(Vc + cache_off), (short)0, kv_bytes, 0x00020000);
+  // Tile kt's rows live in one cache panel (the slot, or a pool block of a
+  // multiple of 64 rows); the block ids come from the table one tile ahead.
+  const int prows = PAGED ? kv.block_size : kv.max_seq;
+  auto panel_of = [&](int kt) {
+    if (!PAGED || kt >= nkt) return sl;
+    const int blk = kv.table[(int64_t)sl * kv.blocks_per_slot() + kt * kFaBK / kv.block_size];
+    return (blk >= 0 && blk < kv.n_blocks) ? blk : -1;
+  };
+  // Descriptor of tile kt's rows of one operand: rows past the visible range
+  // (and a block outside the pool) read as zero through the range check.
+  auto tile_rsrc = [&](const bf16* base, int kt, int panel) {
+    const int key0 = kt * kFaBK;
+    int rows = min(kFaBK, kv_len - key0), prow = key0;
+    if (PAGED) prow = key0 - (key0 / kv.block_size) * kv.block_size;
+    if (panel < 0) rows = panel = prow = 0;
+    return __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(base + (((int64_t)panel * Hkv + kvh) * prows + prow) * D), (short)0,
+        rows * D * 2, 0x00020000);
+  };
   // Lane l of a 1 KB wave load fills physical chunk l % DC of tile row
   // l / DC of its block, i.e. logical chunk kv_chunk(l % DC, row) (the
   // swizzle is an involution).
@@ -83,13 +94,14 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     const int row = (wave + 4 * j) * ROWS_PER_KB + lane / DC;
     ld_off[j] = (uint32_t)((row * D + kv_chunk<D>(lane % DC, row) * 8) * 2);
   }
-  auto gload = [&](int kt, int buf) {
-    const uint32_t kb = (uint32_t)kt * kFaBK * D * 2;
+  auto gload = [&](int kt, int buf, int panel) {
+    const __amdgpu_buffer_rsrc_t rk = tile_rsrc(Kc, kt, panel);
+    const __amdgpu_buffer_rsrc_t rv = tile_rsrc(Vc, kt, panel);
 #pragma unroll
     for (int j = 0; j < BLK; ++j) {
       const int blk = (wave + 4 * j) * ROWS_PER_KB * D;
-      buffer_load_lds16(rk, &sm.k[buf][blk], ld_off[j] + kb, 0);
-      buffer_load_lds16(rv, &sm.v[buf][blk], ld_off[j] + kb, 0);
+      buffer_load_lds16(rk, &sm.k[buf][blk], ld_off[j], 0);
+      buffer_load_lds16(rv, &sm.v[buf][blk], ld_off[j], 0);
     }
   };
 
@@ -117,12 +129,14 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   float m_run = -INFINITY, l_run = 0.f;  // running max in raw score units
   const float slack_raw = kSoftmaxSlack / scale_log2e;
 
-  gload(0, 0);
+  gload(0, 0, panel_of(0));
+  int next_panel = panel_of(1);
   for (int kt = 0; kt < nkt; ++kt) {
     const int buf = kt & 1;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();  // tile kt is in LDS; every wave is done with tile kt - 1
-    if (kt + 1 < nkt) gload(kt + 1, buf ^ 1);
+    if (kt + 1 < nkt) gload(kt + 1, buf ^ 1, next_panel);
+    next_panel = panel_of(kt + 2);
     const int key0 = kt * kFaBK;
     if (key0 > wave_qmin + 31) continue;  // no key of this tile is visible to this wave
     // S^T = K Q^T for two 32-key blocks: the two MFMA chains interleaved,
@@ -237,35 +251,36 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     }
 }
 
-template <int D>
+template <int D, bool PAGED>
 static hipError_t run_fa(const void* q, const void* kc, const void* vc, void* out,
-                         const BatchDev& b, int n_slots, int max_seq, int Hq, int Hkv,
+                         const BatchDev& b, const KvDev& kv, int Hq, int Hkv,
                          int include_single, hipStream_t s) {
   const size_t smem = sizeof(FaSmem<D>);
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_prefill_kernel<D>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_prefill_kernel<D, PAGED>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
     attr = true;
   }
   dim3 grid(cdiv(b.max_q_len, kFaBQ), Hq, b.n_seqs);
   const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  attn_prefill_kernel<D><<<grid, 256, smem, s>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vc,
-                                                 (bf16*)out, b.cu_q, b.ctx_len, b.slot, n_slots,
-                                                 max_seq, Hq, Hkv, scale_log2e, include_single, b.n_tokens);
+  attn_prefill_kernel<D, PAGED><<<grid, 256, smem, s>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vc,
+                                                 (bf16*)out, b.cu_q, b.ctx_len, b.slot, kv, Hq,
+                                                 Hkv, scale_log2e, include_single, b.n_tokens);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, void* out,
-                               const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
+                               const BatchDev& b, const KvDev& kv, int n_q_heads,
                                int n_kv_heads, int head_dim, int include_single, hipStream_t s) {
   if (b.n_seqs == 0 || b.max_q_len == 0) return hipSuccess;
+  const bool paged = kv.table != nullptr;
   if (head_dim == 128)
-    return run_fa<128>(q, kc, vc, out, b, n_slots, max_seq, n_q_heads, n_kv_heads,
-                       include_single, s);
-  return run_fa<64>(q, kc, vc, out, b, n_slots, max_seq, n_q_heads, n_kv_heads, include_single,
-                    s);
+    return paged ? run_fa<128, true>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, s)
+                 : run_fa<128, false>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, s);
+  return paged ? run_fa<64, true>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, s)
+               : run_fa<64, false>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, s);
 }
 
 }  // namespace tri

@@ -14,6 +14,33 @@ struct BatchDev {
   int n_seqs, n_tokens, max_q_len, max_ctx_len;
 };
 
+// KV-cache addressing.  Contiguous (table == nullptr): K and V are
+// [n_slots, Hkv, max_seq, D].  Paged: K and V are pools
+// [n_blocks, Hkv, block_size, D] and logical row r of slot s lives in block
+// table[s * (max_seq / block_size) + r / block_size] at row r % block_size.
+// A panel is a slot (contiguous) or a block (paged) of panel_rows() rows;
+// element (panel, kv head, row, d) is at ((panel Hkv + head) panel_rows + row) D + d.
+struct KvDev {
+  int n_slots, max_seq;     // logical: sequences and rows per sequence
+  const int32_t* table;     // paged block table (device) or nullptr
+  int block_size, n_blocks;
+  __host__ __device__ int panel_rows() const { return table ? block_size : max_seq; }
+  __host__ __device__ int blocks_per_slot() const { return table ? max_seq / block_size : 1; }
+};
+
+// Panel holding logical row `row` of slot `sl` (both in range), and the row
+// within it; -1 when the block table entry is not a block of the pool.
+__device__ __forceinline__ int kv_panel(const KvDev& kv, int sl, int row, int& prow) {
+  if (!kv.table) {
+    prow = row;
+    return sl;
+  }
+  const int j = row / kv.block_size;
+  prow = row - j * kv.block_size;
+  const int blk = kv.table[(int64_t)sl * kv.blocks_per_slot() + j];
+  return (blk >= 0 && blk < kv.n_blocks) ? blk : -1;
+}
+
 // Epilogue applied to C = A B^T (fp32 accumulators) by the GEMM kernels.
 enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_STORE_F32 = 4 };
 
@@ -27,18 +54,18 @@ struct Epi {
   // QKV: columns are q heads, then k heads, then v heads (head_dim each)
   const void* bias;   // nullable, [(Hq + 2 Hkv) D]
   void* q;            // bf16 [M, Hq, D]
-  void* kc;           // cache K [n_slots, Hkv, max_seq, D]
+  void* kc;           // cache K panels [*, Hkv, max_seq, D] (max_seq = panel rows)
   void* vc;           // cache V
-  const int32_t* tok_slot;  // [M] cache slot of each token, -1 = skip the cache write
-  const int32_t* tok_row;   // [M] cache row of each token
+  const int32_t* tok_slot;  // [M] cache panel of each token, -1 = skip the cache write
+  const int32_t* tok_row;   // [M] row of each token within its panel
   const float2* rope;       // [M, D/2] (cos, sin)
   int n_q_heads, n_kv_heads, head_dim, max_seq;
 };
 
-// Layer prologue: per-token map (slot and cache row of every token, -1 when
-// out of range), the rotary table rope[t][i] = (cos, sin)(pos[t] *
+// Layer prologue: per-token map (cache panel and row within it of every
+// token, -1 when out of range), the rotary table rope[t][i] = (cos, sin)(pos[t] *
 // base^(-2i/D)) (angle in double precision), and y = RMSNorm(x) * g.
-hipError_t launch_prologue(const BatchDev& b, int n_slots, int max_seq, int head_dim,
+hipError_t launch_prologue(const BatchDev& b, const KvDev& kv, int head_dim,
                            float rope_base, int32_t* tok_slot, int32_t* tok_row, float2* rope,
                            const void* x, const void* g, void* y, int hidden, float eps,
                            hipStream_t s);
@@ -47,14 +74,10 @@ hipError_t launch_prologue(const BatchDev& b, int n_slots, int max_seq, int head
 hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int rows,
                           int hidden, float eps, hipStream_t s);
 
-// cache[slot][h][row][:] = src[t][h][:] for every token with a valid map entry.
-hipError_t launch_kv_append(const void* k_new, const void* v_new, void* kc, void* vc,
-                            const int32_t* tok_slot, const int32_t* tok_row, int n_tokens,
-                            int n_kv_heads, int head_dim, int max_seq, hipStream_t s);
-
-// The same append for a batch given only by its device arrays (the sequence
-// of each token is found by binary search over cu_q).
-hipError_t launch_kv_append_direct(const BatchDev& b, int n_slots, int max_seq, int n_kv_heads,
+// KV append for a batch given by its device arrays: cache row ctx_len[s] + i
+// of slot slot[s] (through the block table when paged) <- row t of k_new /
+// v_new (the sequence of each token is found by binary search over cu_q).
+hipError_t launch_kv_append_direct(const BatchDev& b, const KvDev& kv, int n_kv_heads,
                                    int head_dim, const void* k_new, const void* v_new, void* kc,
                                    void* vc, hipStream_t s);
 
@@ -88,19 +111,23 @@ hipError_t launch_skinny(const void* A, int lda, const void* B, int ldb, int M, 
 // Causal flash attention for sequences with q_len > 1 (or all when
 // include_single != 0).
 hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, void* out,
-                               const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
+                               const BatchDev& b, const KvDev& kv, int n_q_heads,
                                int n_kv_heads, int head_dim, int include_single, hipStream_t s);
 
 // Split-KV attention for sequences with q_len == 1, plus the combine.
-int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv, int head_dim, int group);
+// Keys per split (a multiple of 32); max_split > 0 caps it.
+int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv, int head_dim, int group,
+                           int max_split);
+// The cap the split-KV kernel needs for this cache (0 = none).
+int attn_decode_max_split(const KvDev& kv);
 // Compute units of the current device (256 when it cannot be queried).
 int cu_count();
 size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv);
 hipError_t launch_attn_decode_split(const void* q, const void* kc, const void* vc, float* part,
-                                    const BatchDev& b, int n_slots, int max_seq, int n_q_heads,
+                                    const BatchDev& b, const KvDev& kv, int n_q_heads,
                                     int n_kv_heads, int head_dim, hipStream_t s);
 hipError_t launch_attn_decode_combine(const float* part, void* out, const BatchDev& b,
-                                      int n_slots, int max_seq, int n_q_heads, int n_kv_heads,
+                                      const KvDev& kv, int n_q_heads, int n_kv_heads,
                                       int head_dim, hipStream_t s);
 
 // Mixture of experts.  Grouped GEMM over experts: rows [seg[e], seg[e+1]) of

@@ -82,8 +82,8 @@ hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int
 //  * RMSNorm of x[t] into y[t] (as rmsnorm_kernel).
 constexpr int kMapChunks = 4;  // sequence ends loaded per lane and round trip
 
-__global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, int n_slots, int max_seq,
-                                                       int half, double base,
+__global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, KvDev kv, int half,
+                                                       double base,
                                                        int32_t* __restrict__ tok_slot,
                                                        int32_t* __restrict__ tok_row,
                                                        float2* __restrict__ rope,
@@ -125,9 +125,11 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, int n_slots, 
     const int sc = ok ? sq : 0;
     const int q0 = b.cu_q[sc], q1 = b.cu_q[sc + 1], sl = b.slot[sc], c0 = b.ctx_len[sc];
     const int row = c0 + (t - q0);
-    ok = ok && sl >= 0 && sl < n_slots && row >= 0 && row < max_seq && t >= q0 && t < q1;
-    tok_slot[t] = ok ? sl : -1;
-    tok_row[t] = ok ? row : -1;
+    ok = ok && sl >= 0 && sl < kv.n_slots && row >= 0 && row < kv.max_seq && t >= q0 && t < q1;
+    int prow = -1;
+    const int panel = ok ? kv_panel(kv, sl, row, prow) : -1;
+    tok_slot[t] = panel;
+    tok_row[t] = panel >= 0 ? prow : -1;
   }
   if (lane < half) {
     const double inv_freq = pow(base, -2.0 * (double)lane / (double)(2 * half));
@@ -162,49 +164,18 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, int n_slots, 
   }
 }
 
-hipError_t launch_prologue(const BatchDev& b, int n_slots, int max_seq, int head_dim,
-                           float rope_base, int32_t* tok_slot, int32_t* tok_row, float2* rope,
-                           const void* x, const void* g, void* y, int hidden, float eps,
-                           hipStream_t s) {
+hipError_t launch_prologue(const BatchDev& b, const KvDev& kv, int head_dim, float rope_base,
+                           int32_t* tok_slot, int32_t* tok_row, float2* rope, const void* x,
+                           const void* g, void* y, int hidden, float eps, hipStream_t s) {
   if (b.n_tokens == 0) return hipSuccess;
   prologue_kernel<<<cdiv(b.n_tokens, 4), 256, 0, s>>>(
-      b, n_slots, max_seq, head_dim / 2, (double)rope_base, tok_slot, tok_row, rope,
+      b, kv, head_dim / 2, (double)rope_base, tok_slot, tok_row, rope,
       (const bf16*)x, (const bf16*)g, (bf16*)y, hidden, eps);
   return hipGetLastError();
 }
 
 // One thread per 16-byte chunk of a new K/V row.
-__global__ void kv_append_kernel(const bf16* __restrict__ kn, const bf16* __restrict__ vn,
-                                 bf16* __restrict__ kc, bf16* __restrict__ vc,
-                                 const int32_t* __restrict__ tok_slot,
-                                 const int32_t* __restrict__ tok_row, int n_tokens, int hkv,
-                                 int d, int max_seq) {
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int cpr = d / 8;  // chunks per row
-  if (gid >= (int64_t)n_tokens * hkv * cpr) return;
-  const int t = (int)(gid / (hkv * cpr));
-  const int rem = (int)(gid - (int64_t)t * hkv * cpr);
-  const int h = rem / cpr, c = rem - h * cpr;
-  const int sl = tok_slot[t];
-  if (sl < 0) return;
-  const int64_t dst = (((int64_t)sl * hkv + h) * max_seq + tok_row[t]) * d + c * 8;
-  const int64_t src = ((int64_t)t * hkv + h) * d + c * 8;
-  stg16(kc + dst, ldg16(kn + src));
-  stg16(vc + dst, ldg16(vn + src));
-}
-
-hipError_t launch_kv_append(const void* k_new, const void* v_new, void* kc, void* vc,
-                            const int32_t* tok_slot, const int32_t* tok_row, int n_tokens,
-                            int n_kv_heads, int head_dim, int max_seq, hipStream_t s) {
-  const int64_t n = (int64_t)n_tokens * n_kv_heads * (head_dim / 8);
-  if (n == 0) return hipSuccess;
-  kv_append_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(
-      (const bf16*)k_new, (const bf16*)v_new, (bf16*)kc, (bf16*)vc, tok_slot, tok_row, n_tokens,
-      n_kv_heads, head_dim, max_seq);
-  return hipGetLastError();
-}
-
-__global__ void kv_append_direct_kernel(BatchDev b, int n_slots, int max_seq, int hkv, int d,
+__global__ void kv_append_direct_kernel(BatchDev b, KvDev kv, int hkv, int d,
                                         const bf16* __restrict__ kn, const bf16* __restrict__ vn,
                                         bf16* __restrict__ kc, bf16* __restrict__ vc) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -220,21 +191,24 @@ __global__ void kv_append_direct_kernel(BatchDev b, int n_slots, int max_seq, in
   }
   const int sl = b.slot[lo];
   const int row = b.ctx_len[lo] + (t - b.cu_q[lo]);
-  if (sl < 0 || sl >= n_slots || row < 0 || row >= max_seq || t >= b.cu_q[lo + 1]) return;
-  const int64_t dst = (((int64_t)sl * hkv + h) * max_seq + row) * d + c * 8;
+  if (sl < 0 || sl >= kv.n_slots || row < 0 || row >= kv.max_seq || t >= b.cu_q[lo + 1]) return;
+  int prow;
+  const int panel = kv_panel(kv, sl, row, prow);
+  if (panel < 0) return;
+  const int64_t dst = (((int64_t)panel * hkv + h) * kv.panel_rows() + prow) * d + c * 8;
   const int64_t src = ((int64_t)t * hkv + h) * d + c * 8;
   stg16(kc + dst, ldg16(kn + src));
   stg16(vc + dst, ldg16(vn + src));
 }
 
-hipError_t launch_kv_append_direct(const BatchDev& b, int n_slots, int max_seq, int n_kv_heads,
+hipError_t launch_kv_append_direct(const BatchDev& b, const KvDev& kv, int n_kv_heads,
                                    int head_dim, const void* k_new, const void* v_new, void* kc,
                                    void* vc, hipStream_t s) {
   const int64_t n = (int64_t)b.n_tokens * n_kv_heads * (head_dim / 8);
   if (n == 0 || b.n_seqs == 0) return hipSuccess;
   kv_append_direct_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(
-      b, n_slots, max_seq, n_kv_heads, head_dim, (const bf16*)k_new, (const bf16*)v_new,
-      (bf16*)kc, (bf16*)vc);
+      b, kv, n_kv_heads, head_dim, (const bf16*)k_new, (const bf16*)v_new, (bf16*)kc,
+      (bf16*)vc);
   return hipGetLastError();
 }
 

@@ -77,7 +77,7 @@ tri_status tri_layer_work(const tri_layer_config* cfg, int32_t decode, int32_t n
   // Attention: sequences with several new tokens take the causal flash path
   // (prefill entry point only), single-token sequences the split-KV path.
   const int split = attn_decode_split_keys(n_seqs, cfg->n_kv_heads, max_ctx + 1, cfg->head_dim,
-                                           cfg->n_q_heads / cfg->n_kv_heads);
+                                           cfg->n_q_heads / cfg->n_kv_heads, 0);
   bool flash = !decode && max_q > 1;
   double fl_pairs = 0, fl_tok = 0, fl_rows = 0;
   double dec_keys = 0, dec_tok = 0, dec_parts = 0;

@@ -109,7 +109,7 @@ def call(lib, fn="tri_layer_prefill", c=None, w=None, kv=None, b=None, x=FAKE + 
          out=FAKE + (2 << 20), ws=FAKE + (3 << 20), ws_bytes=1 << 30):
     c = cfg() if c is None else c
     w = weights() if w is None else w
-    kv = T.KVCache(FAKE + (4 << 20), FAKE + (5 << 20), 1, 64) if kv is None else kv
+    kv = T.KVCache(FAKE + (4 << 20), FAKE + (5 << 20), 1, 64, None, 0, 0) if kv is None else kv
     b = batch() if b is None else b
     return getattr(lib, fn)(ctypes.byref(c), ctypes.byref(w), ctypes.byref(kv), ctypes.byref(b),
                             x, out, None, None, ws, ws_bytes, None)
@@ -150,7 +150,7 @@ def test_batch_checks(lib):
     assert call(lib, b=batch(max_ctx=64)) == T.TRI_ERR_RANGE               # no row left
     assert call(lib, b=batch(n_seqs=2, n_tokens=65, max_q=65)) == T.TRI_ERR_RANGE
     assert call(lib, fn="tri_layer_decode", b=batch(n_seqs=1, n_tokens=1, max_q=1, max_ctx=64)) == T.TRI_ERR_RANGE
-    assert call(lib, kv=T.KVCache(FAKE, FAKE + 256, 0, 64)) == T.TRI_ERR_SHAPE
+    assert call(lib, kv=T.KVCache(FAKE, FAKE + 256, 0, 64, None, 0, 0)) == T.TRI_ERR_SHAPE
     # decode needs one token per sequence
     assert call(lib, fn="tri_layer_decode", b=batch(n_seqs=2, n_tokens=4, max_q=2)) == T.TRI_ERR_SHAPE
 
@@ -191,7 +191,7 @@ def test_workspace_size_and_layout(lib):
 
 def test_kvcache_append_and_route_validation(lib):
     c = cfg()
-    kv = T.KVCache(FAKE, FAKE + 4096, 1, 64)
+    kv = T.KVCache(FAKE, FAKE + 4096, 1, 64, None, 0, 0)
     b = batch(max_ctx=64)
     assert lib.tri_kvcache_append(ctypes.byref(c), ctypes.byref(kv), ctypes.byref(b), FAKE,
                                   FAKE, None) == T.TRI_ERR_RANGE
@@ -211,3 +211,18 @@ def test_status_strings(lib):
     for s in range(-8, 1):
         assert T.status_string(s) and T.status_string(s) != "unknown status"
     assert T.status_string(-99) == "unknown status"
+
+
+def test_paged_cache_validation(lib):
+    tab = FAKE + (6 << 20)
+    ok = T.KVCache(FAKE + (4 << 20), FAKE + (5 << 20), 1, 128, tab, 64, 4)
+    assert call(lib, kv=ok, ws_bytes=0) == T.TRI_ERR_WORKSPACE  # passes the cache checks
+    assert call(lib, kv=T.KVCache(FAKE, FAKE + 256, 1, 128, tab, 32, 4)) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, kv=T.KVCache(FAKE, FAKE + 256, 1, 96, tab, 64, 4)) == T.TRI_ERR_SHAPE
+    assert call(lib, kv=T.KVCache(FAKE, FAKE + 256, 1, 128, tab, 64, 0)) == T.TRI_ERR_SHAPE
+    assert call(lib, kv=T.KVCache(FAKE, FAKE + 256, 1, 128, tab + 2, 64, 4)) == T.TRI_ERR_ALIGN
+    b = batch()
+    kn = FAKE + (7 << 20)
+    assert lib.tri_kvcache_append(ctypes.byref(cfg()), ctypes.byref(
+        T.KVCache(FAKE, FAKE + 256, 1, 128, tab, 48, 4)), ctypes.byref(b), kn, kn + 4096,
+        None) == T.TRI_ERR_UNSUPPORTED
