@@ -349,9 +349,50 @@ def run_decode(args, tri):
     }
     if energy is not None:
         res["energy"] = energy_json(energy, steps * wl.batch.n_seqs)
+    res["paged"] = paged_decode(tri, dl, cache, batches, xs, out, ws, reps, stream)
     del dl, cache, xs, out, ws
     torch.cuda.empty_cache()
     return res, phase
+
+
+def paged_decode(tri, dl, cache, batches, xs, out, ws, reps, stream, block_size=64):
+    """The same decode sweep on a paged copy of the cache (64-row blocks in a
+    shuffled pool): step time and attention time."""
+    import torch
+    from paper_2606_29629_amd.workload import paged_from_contiguous
+    k, v = cache
+    pad = (-k.shape[2]) % block_size
+    if pad:
+        k = torch.nn.functional.pad(k, (0, 0, 0, pad))
+        v = torch.nn.functional.pad(v, (0, 0, 0, pad))
+    pc = paged_from_contiguous(k, v, block_size, seed=7, fill=0.0)
+    del k, v
+    steps = len(batches)
+
+    def sweep():
+        for s in range(steps):
+            tri.layer_decode(dl.cfg, dl.w, pc, batches[s], xs[s], out=out, workspace=ws)
+
+    sweep()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        sweep()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / (reps * steps)
+    tri.profile_enable(True)
+    sweep()
+    torch.cuda.synchronize()
+    prof = tri.profile_read()
+    tri.profile_enable(False)
+    res = {"block_size": block_size, "ms_per_step": ms,
+           "tokens_per_s": batches[0].n_seqs / (ms / 1e3),
+           "attn_decode_ms": prof["attn_decode"]["total_ms"] / steps}
+    del pc
+    torch.cuda.empty_cache()
+    return res
 
 
 def run_secondary(args, tri, name):
