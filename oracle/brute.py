@@ -8,8 +8,9 @@ It exists to pin the vectorised oracle (a dropped term, a wrong sign, a
 transposed operand or a wrong head mapping there disagrees with this).
 
 Readings are the same as in ``oracle/layer.py`` (pre-norm Qwen2-family layer,
-rotate-half rotary embedding, consecutive GQA grouping, SwiGLU, top-k softmax
-routing with ties to the lower index).
+optional per-head q/k RMSNorm before the rotation, rotate-half rotary
+embedding, consecutive GQA grouping, SwiGLU, top-k softmax routing with ties
+to the lower index).
 """
 from __future__ import annotations
 
@@ -61,8 +62,13 @@ def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
             qkv = _matvec(w["w_qkv"], h)
             if w.get("b_qkv") is not None:
                 qkv = [qkv[j] + w["b_qkv"][j] for j in range(len(qkv))]
-            qh = [[S(v) for v in rotate(qkv[j * D:(j + 1) * D], p)] for j in range(Hq)]
-            kh = [[S(v) for v in rotate(qkv[(Hq + j) * D:(Hq + j + 1) * D], p)] for j in range(Hkv)]
+            qpre = [qkv[j * D:(j + 1) * D] for j in range(Hq)]
+            kpre = [qkv[(Hq + j) * D:(Hq + j + 1) * D] for j in range(Hkv)]
+            if getattr(cfg, "qk_norm", False):   # per-head RMSNorm before the rotation
+                qpre = [norm(vec, w["q_norm"]) for vec in qpre]
+                kpre = [norm(vec, w["k_norm"]) for vec in kpre]
+            qh = [[S(v) for v in rotate(qpre[j], p)] for j in range(Hq)]
+            kh = [[S(v) for v in rotate(kpre[j], p)] for j in range(Hkv)]
             vh = [[S(v) for v in qkv[(Hq + Hkv + j) * D:(Hq + Hkv + j + 1) * D]] for j in range(Hkv)]
             toks.append((s, p, qh, kh, vh))
             k_rows.append(kh)

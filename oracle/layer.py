@@ -20,6 +20,10 @@ fix is a declared reading:
   * grouped-query attention with consecutive grouping (query head j reads KV
     head floor(j * Hkv / Hq)), scale 1/sqrt(D), causal over cache rows
     0 .. ctx_len + i, keys stored after rotation;
+  * optional per-head query/key normalisation (the Qwen3-family variant of
+    the layer, ``cfg.qk_norm``): before the rotation every head of q and of k
+    is RMS-normalised over its D values with gains q_norm / k_norm [D] and
+    the layer's eps;
   * SwiGLU  a = silu(h W_g^T) * (h W_u^T),  silu(z) = z / (1 + exp(-z));
   * MoE: softmax over all expert logits, top-k by logit (descending, ties to
     the lower expert index), weights renormalised over the chosen k, no shared
@@ -157,7 +161,8 @@ def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: n
     """One decoder-layer forward over a ragged batch.
 
     cfg      object with hidden, n_q_heads, n_kv_heads, head_dim, ffn_dim,
-             n_experts, top_k, rms_eps, rope_base, moe_renorm.
+             n_experts, top_k, rms_eps, rope_base, moe_renorm (and optionally
+             qk_norm, with weights q_norm / k_norm).
     w        weights as float arrays, row-major [out, in] (see module docstring).
     cache_k, cache_v   [n_slots, Hkv, max_seq, D]; rows below a sequence's
              ctx_len are its cached (rotated) keys / values.  Not modified.
@@ -195,8 +200,13 @@ def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: n
     if w.get("b_qkv") is not None:
         qkv = qkv + _as(w["b_qkv"], dtype)
     ang = rope_angles(pos, D, cfg.rope_base)
-    q = st(rope(qkv[:, :Hq * D].reshape(T, Hq, D), ang))
-    k_new = st(rope(qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D), ang))
+    q_pre = qkv[:, :Hq * D].reshape(T, Hq, D)
+    k_pre = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D)
+    if getattr(cfg, "qk_norm", False):
+        q_pre = rmsnorm(q_pre, _as(w["q_norm"], dtype), cfg.rms_eps)
+        k_pre = rmsnorm(k_pre, _as(w["k_norm"], dtype), cfg.rms_eps)
+    q = st(rope(q_pre, ang))
+    k_new = st(rope(k_pre, ang))
     v_new = st(qkv[:, (Hq + Hkv) * D:].reshape(T, Hkv, D))
 
     # Causal attention per sequence over its cached prefix plus its new rows.

@@ -38,6 +38,8 @@ TID_X_DECODE0 = 9          # step s uses TID_X_DECODE0 + s
 TID_CACHE_K = 100
 TID_CACHE_V = 101
 TID_KV_LENGTHS = 102
+TID_Q_NORM = 103
+TID_K_NORM = 104
 
 
 @dataclasses.dataclass(frozen=True)
@@ -54,6 +56,7 @@ class LayerConfig:
     rope_base: float = 1e6
     qkv_bias: bool = False
     moe_renorm: bool = True
+    qk_norm: bool = False         # per-head RMSNorm of q and k before the rotation
 
     @property
     def moe(self) -> bool:
@@ -109,6 +112,9 @@ def make_weights(cfg: LayerConfig, seed: int = 0, w_std: float = 0.02,
         w["b_qkv"] = normal_bf16(seed, TID_B_QKV, (cfg.qkv_rows,), w_std * 10)
     w["w_o"] = normal_bf16(seed, TID_W_O, (H, cfg.n_q_heads * D), w_std)
     w["mlp_norm"] = normal_bf16(seed, TID_MLP_NORM, (H,), gain_std, 1.0)
+    if cfg.qk_norm:
+        w["q_norm"] = normal_bf16(seed, TID_Q_NORM, (D,), gain_std, 1.0)
+        w["k_norm"] = normal_bf16(seed, TID_K_NORM, (D,), gain_std, 1.0)
     if cfg.moe:
         E, Fe = cfg.n_experts, cfg.expert_ffn_dim
         w["w_gate_up"] = normal_bf16(seed, TID_W_GATE_UP, (E, 2 * Fe, H), w_std)

@@ -152,10 +152,12 @@ def _lists(a):
     return np.asarray(a, dtype=np.float64).tolist()
 
 
-@pytest.mark.parametrize("cfg,bias", [(TINY, False), (TINY, True), (TINY_MOE, False)])
-def test_oracle_matches_brute_force(cfg, bias):
+@pytest.mark.parametrize("cfg,bias,qkn", [(TINY, False, False), (TINY, True, False),
+                                          (TINY_MOE, False, False), (TINY, True, True),
+                                          (TINY_MOE, False, True)])
+def test_oracle_matches_brute_force(cfg, bias, qkn):
     import dataclasses
-    cfg = dataclasses.replace(cfg, qkv_bias=bias)
+    cfg = dataclasses.replace(cfg, qkv_bias=bias, qk_norm=qkn)
     b = B([2, 0, 1], [3, 0, 5], [4, 3, 1])       # ragged: a chunk with prefix, a prefill, a decode
     w, ck, cv, x = setup(cfg, b, 3, 8)
     r = L.layer_forward(cfg, w, ck, cv, b, x)
@@ -395,3 +397,42 @@ def test_bf16_storage_matches_brute_force_with_bit_rounding(cfg):
                                                store=bit_round)
     assert np.allclose(r["k_new"], np.array(kr), rtol=1e-12, atol=1e-12)
     assert np.allclose(r["out"], np.array(out), rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------ q/k norm variant --
+
+def test_qk_norm_unit_gains_give_unit_rms_heads():
+    """With unit gains and eps = 0 every head of q and k has RMS exactly 1
+    before the rotation, hence after it (the rotation preserves pair norms)."""
+    import dataclasses
+    cfg = dataclasses.replace(TINY, qk_norm=True, rms_eps=0.0)
+    b = B([0, 1], [2, 0], [3, 4])
+    w, ck, cv, x = setup(cfg, b, 2, 8)
+    w["q_norm"] = np.ones(cfg.head_dim)
+    w["k_norm"] = np.ones(cfg.head_dim)
+    r = L.layer_forward(cfg, w, ck, cv, b, x)
+    assert np.allclose(np.mean(r["q"] ** 2, axis=-1), 1.0, rtol=1e-13)
+    assert np.allclose(np.mean(r["k_new"] ** 2, axis=-1), 1.0, rtol=1e-13)
+
+
+def test_qk_norm_makes_the_layer_invariant_to_query_and_key_scale():
+    """Scaling the q (or k) rows of W_qkv by a positive factor per head leaves
+    the layer unchanged with eps = 0; without the norm it does not."""
+    import dataclasses
+    b = B([0, 1], [0, 0], [5, 3])
+    for qkn in (True, False):
+        cfg = dataclasses.replace(TINY, qk_norm=qkn, rms_eps=0.0)
+        w, ck, cv, x = setup(cfg, b, 2, 8)
+        ck[:] = 0.0
+        cv[:] = 0.0   # no cached prefix: every key comes from the scaled projection
+        r0 = L.layer_forward(cfg, w, ck, cv, b, x)
+        w2 = dict(w)
+        w2["w_qkv"] = w["w_qkv"].copy()
+        D, Hq, Hkv = cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
+        for j, a in enumerate([0.5, 3.0, 1.7, 0.9]):           # q heads
+            w2["w_qkv"][j * D:(j + 1) * D] *= a
+        for j, a in enumerate([2.5, 0.4]):                     # k heads
+            w2["w_qkv"][(Hq + j) * D:(Hq + j + 1) * D] *= a
+        r1 = L.layer_forward(cfg, w2, ck, cv, b, x)
+        same = np.allclose(r1["out"], r0["out"], rtol=1e-12, atol=1e-12)
+        assert same == qkn
