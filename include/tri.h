@@ -10,7 +10,8 @@
  * library computes one decoder layer for such a step:
  *
  *   h   = RMSNorm(x; attn_norm)                      y = x / sqrt(mean(x^2)+eps) * g
- *   q,k,v = h W_qkv^T (+ b_qkv), rotary embedding on q and k at each token's
+ *   q,k,v = h W_qkv^T (+ b_qkv), optionally each q and k head RMS-normalised
+ *         (TRI_F_QK_NORM), rotary embedding on q and k at each token's
  *         position (rotate-half pairs (i, i+D/2), angle pos * base^(-2i/D)
  *         formed in double precision), k and v appended to the cache
  *   o   = causal grouped-query softmax attention over the cache (query head j
@@ -70,7 +71,10 @@ enum {
   TRI_F_QKV_BIAS = 1,   /* add b_qkv after the q/k/v projection                   */
   TRI_F_MOE = 2,        /* mixture-of-experts FFN instead of the dense SwiGLU      */
   TRI_F_MOE_RENORM = 4, /* renormalise the top-k routing weights to sum to 1       */
-  TRI_F_ALL = 7
+  TRI_F_QK_NORM = 8,    /* per-head RMSNorm of q and k (gains q_norm, k_norm, eps
+                           rms_eps) after the projection, before the rotation: the
+                           Qwen3-family variant of the layer                         */
+  TRI_F_ALL = 15
 };
 
 typedef struct {
@@ -99,6 +103,8 @@ typedef struct {
                             MoE   [E, 2Fe, H] (same split per expert)             */
   const void* w_down;    /* dense [H, F]; MoE [E, H, Fe]                           */
   const void* w_router;  /* MoE [E, H]; NULL for a dense layer                     */
+  const void* q_norm;    /* [D]; required iff TRI_F_QK_NORM, else ignored          */
+  const void* k_norm;    /* [D]; required iff TRI_F_QK_NORM, else ignored          */
 } tri_layer_weights;
 
 /* KV cache (device, bfloat16).  Keys are stored after the rotary embedding.

@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(HERE, "libtri.so")
 TRI_OK, TRI_ERR_NULL, TRI_ERR_SHAPE, TRI_ERR_UNSUPPORTED = 0, -1, -2, -3
 TRI_ERR_RANGE, TRI_ERR_ALIGN, TRI_ERR_WORKSPACE, TRI_ERR_HIP, TRI_ERR_ALIAS = -4, -5, -6, -7, -8
 TRI_BF16, TRI_F32 = 0, 1
-TRI_F_QKV_BIAS, TRI_F_MOE, TRI_F_MOE_RENORM = 1, 2, 4
+TRI_F_QKV_BIAS, TRI_F_MOE, TRI_F_MOE_RENORM, TRI_F_QK_NORM = 1, 2, 4, 8
 
 
 class LayerConfig(ctypes.Structure):
@@ -31,7 +31,7 @@ class LayerConfig(ctypes.Structure):
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("attn_norm", "w_qkv", "b_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down",
-                 "w_router")]
+                 "w_router", "q_norm", "k_norm")]
 
 
 class KVCache(ctypes.Structure):
@@ -123,6 +123,8 @@ def make_config(cfg) -> LayerConfig:
     flags = 0
     if getattr(cfg, "qkv_bias", False):
         flags |= TRI_F_QKV_BIAS
+    if getattr(cfg, "qk_norm", False):
+        flags |= TRI_F_QK_NORM
     n_exp = int(getattr(cfg, "n_experts", 0) or 0)
     if n_exp > 0:
         flags |= TRI_F_MOE
@@ -181,7 +183,7 @@ class DeviceBatch:
 def weights_struct(w: Dict[str, object]) -> LayerWeights:
     return LayerWeights(*[_ptr(w.get(n)) for n in
                           ("attn_norm", "w_qkv", "b_qkv", "w_o", "mlp_norm", "w_gate_up",
-                           "w_down", "w_router")])
+                           "w_down", "w_router", "q_norm", "k_norm")])
 
 
 def workspace_size(cfg: LayerConfig, batch: DeviceBatch) -> int:

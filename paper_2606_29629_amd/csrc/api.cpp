@@ -229,6 +229,8 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   if (moe && !w->w_router) return TRI_ERR_NULL;
   const bool bias = (cfg->flags & TRI_F_QKV_BIAS) != 0;
   if (bias && !w->b_qkv) return TRI_ERR_NULL;
+  const bool qk_norm = (cfg->flags & TRI_F_QK_NORM) != 0;
+  if (qk_norm && (!w->q_norm || !w->k_norm)) return TRI_ERR_NULL;
   if (b->max_ctx_len >= cache->max_seq || b->max_q_len > cache->max_seq) return TRI_ERR_RANGE;
   if (decode && (int64_t)b->max_ctx_len + 1 > cache->max_seq) return TRI_ERR_RANGE;
   const void* ptrs[] = {x_in, x_out, ws, cache->k, cache->v, w->attn_norm, w->w_qkv, w->w_o,
@@ -236,6 +238,7 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   for (const void* p : ptrs)
     if (!aligned16(p)) return TRI_ERR_ALIGN;
   if (bias && !aligned16(w->b_qkv)) return TRI_ERR_ALIGN;
+  if (qk_norm && (!aligned16(w->q_norm) || !aligned16(w->k_norm))) return TRI_ERR_ALIGN;
   if (moe && !aligned16(w->w_router)) return TRI_ERR_ALIGN;
   if (((uintptr_t)ws & (kAlign - 1)) != 0) return TRI_ERR_ALIGN;
   const Layout L = layout_of(cfg, b);
@@ -278,6 +281,9 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   e.tok_slot = tok_slot;
   e.tok_row = tok_row;
   e.rope = rope;
+  e.q_norm = qk_norm ? w->q_norm : nullptr;
+  e.k_norm = qk_norm ? w->k_norm : nullptr;
+  e.eps = cfg->rms_eps;
   e.n_q_heads = Hq;
   e.n_kv_heads = Hkv;
   e.head_dim = D;

@@ -34,6 +34,9 @@ namespace tri {
 constexpr int kBK = 64;
 constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
+// Template-only epilogue kind: EPI_QKV with the per-head q/k RMSNorm (the
+// Epi still says EPI_QKV; its q_norm pointer selects this instantiation).
+constexpr int EPI_QKV_NORM = 5;
 
 // LDS has 64 banks of 4 bytes (a 256-byte window).  A tile row is 128 bytes,
 // so rows r and r+1 share a window; a ds_read_b128 phase of 16 lanes reads the
@@ -382,6 +385,84 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
   }
 }
 
+// The q/k/v epilogue with the per-head RMSNorm of q and k.  The sum of
+// squares over a head needs every value of a (token, head) before any can be
+// stored, more registers than the accumulator tile leaves free, so this
+// epilogue goes through LDS (free once every wave is past the mainloop and
+// its last loads have landed): 32 rows of the wave's tile at a time, each
+// wave in its own 32 x WC fp32 region, 16-byte chunks stored at chunk
+// c ^ row (conflict-free column writes and row reads).  Then lane l takes
+// rotary pair l of each row (WC / 2 = 64 pairs): a head's pairs are an
+// aligned group of D / 2 lanes, its sum of squares a group sum; the bias,
+// gains and the lane's column stay fixed across rows.
+template <int MI, int NI>
+__device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
+                                                  char* smem, int wv, int lane, int wrow0,
+                                                  int wcol0, int M, int N) {
+  constexpr int WC = NI * 32;
+  static_assert(WC == 128, "one rotary pair per lane and row");
+  const int lr = lane & 31, lg = lane >> 5;
+  const int D = epi.head_dim, half = D / 2;
+  const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
+  const int hw = lane / half, d = lane % half;  // head within the wave's columns, pair
+  const int c1 = hw * D + d, c2 = c1 + half;     // first / second value's wave column
+  const int col = min(wcol0 + c1, N - half - 1); // (a head past N stores nothing)
+  const bool col_ok = wcol0 + c1 < N;
+  const int head = col / D;
+  const int kind = head < Hq ? 0 : (head < Hq + Hkv ? 1 : 2);
+  const float b1 = epi.bias ? bf2f(((const bf16*)epi.bias)[col]) : 0.f;
+  const float b2 = epi.bias ? bf2f(((const bf16*)epi.bias)[col + half]) : 0.f;
+  const bf16* gp = (const bf16*)(kind == 0 ? epi.q_norm : epi.k_norm);
+  const float g1 = kind == 2 ? 1.f : bf2f(gp[d]);
+  const float g2 = kind == 2 ? 1.f : bf2f(gp[d + half]);
+  const int kvh = kind == 1 ? head - Hq : head - Hq - Hkv;
+  bf16* const cache = (bf16*)(kind == 1 ? epi.kc : epi.vc);
+
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  float* __restrict__ buf = (float*)smem + wv * 32 * WC;
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+    // the accumulators' element group (j, q) is row lr, columns 32 j + 8 q + 4 lg .. + 3
+#pragma unroll
+    for (int j = 0; j < NI; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *(f32x4*)&buf[lr * WC + (((8 * j + 2 * q + lg) ^ lr) << 2)] =
+            f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+    const int rbase = wrow0 + 32 * i;
+#pragma unroll 4
+    for (int t = 0; t < 32; ++t) {
+      const int row = rbase + t;  // uniform
+      if (row >= M) break;
+      float x1 = buf[t * WC + (((c1 >> 2) ^ t) << 2) + (c1 & 3)] + b1;
+      float x2 = buf[t * WC + (((c2 >> 2) ^ t) << 2) + (c2 & 3)] + b2;
+      const float ss = group_sum(x1 * x1 + x2 * x2, half);
+      const float2 cs = epi.rope[(int64_t)row * half + d];
+      if (kind != 2) {
+        const float r = 1.0f / sqrtf(ss / (float)D + epi.eps);
+        x1 *= r * g1;
+        x2 *= r * g2;
+        const float y1 = x1 * cs.x - x2 * cs.y;
+        const float y2 = x2 * cs.x + x1 * cs.y;
+        x1 = y1;
+        x2 = y2;
+      }
+      bf16* dst = nullptr;
+      if (kind == 0) {
+        dst = (bf16*)epi.q + ((int64_t)row * Hq + head) * D + d;
+      } else {
+        const int sl = epi.tok_slot[row];
+        if (sl >= 0) dst = cache + (((int64_t)sl * Hkv + kvh) * epi.max_seq + epi.tok_row[row]) * D + d;
+      }
+      if (col_ok && dst) {
+        dst[0] = f2bf(x1);
+        dst[half] = f2bf(x2);
+      }
+    }
+  }
+}
+
 template <int BM, int BN, int WGM, int WGN, int EK>
 __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __restrict__ A, int lda,
                                                    const bf16* __restrict__ B, int ldb, int M,
@@ -458,6 +539,11 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
     plain_epilogue<MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + 4 * lg, N);
   } else if constexpr (EK == EPI_SWIGLU) {
     swiglu_epilogue<MI, NI>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
+  } else if constexpr (EK == EPI_QKV_NORM) {
+    static_assert(NW * 32 * WN * sizeof(float) <= sizeof(GemmSmem<BM, BN>),
+                  "the epilogue's row blocks must fit the mainloop's LDS");
+    qkv_norm_epilogue<MI, NI>(acc, epi, smem_raw, wv, lane, tm * BM + wm * WM, tn * BN + wn * WN,
+                              M, N);
   } else if (epi.head_dim == 128) {
     qkv_epilogue<MI, NI, 2>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
   } else {
@@ -677,24 +763,43 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
     }
   float2 cs[kTailPer];
   int sl[kTailPer], tr[kTailPer];
-  float b1[kTailPer], b2[kTailPer];
+  float b1[kTailPer], b2[kTailPer], g1[kTailPer], g2[kTailPer];
 #pragma unroll
   for (int q = 0; q < kTailPer; ++q) {
     const int row = min(tm * BM + rr[q], M - 1), col = min(tn * BN + cc[q], N - 1);
-    const int d = col % Dh;
+    const int head = col / Dh, d = col % Dh;
     cs[q] = epi.rope[(int64_t)row * half + d];
     sl[q] = epi.tok_slot[row];
     tr[q] = epi.tok_row[row];
     b1[q] = epi.bias ? bf2f(((const bf16*)epi.bias)[col]) : 0.f;
     b2[q] = epi.bias ? bf2f(((const bf16*)epi.bias)[col + half]) : 0.f;
+    const bf16* gp = (const bf16*)(head < Hq ? epi.q_norm : epi.k_norm);
+    const bool n = epi.q_norm && head < Hq + Hkv;
+    g1[q] = n ? bf2f(gp[d]) : 1.f;
+    g2[q] = n ? bf2f(gp[d + half]) : 1.f;
+  }
+  // Per-head RMSNorm of q and k: a head's rotary pairs are `half` consecutive
+  // elements, an aligned group of lanes, so its sum of squares is a group sum.
+  float rs[kTailPer];
+#pragma unroll
+  for (int q = 0; q < kTailPer; ++q) {
+    x1[q] += b1[q];
+    x2[q] += b2[q];
+    rs[q] = 1.f;
+    if (epi.q_norm) {
+      const float ss = group_sum(x1[q] * x1[q] + x2[q] * x2[q], half);
+      rs[q] = 1.0f / sqrtf(ss / (float)Dh + epi.eps);
+    }
   }
 #pragma unroll
   for (int q = 0; q < kTailPer; ++q) {
     const int row = tm * BM + rr[q], col = tn * BN + cc[q];
     if (e0 + 256 * q >= BM * (BN / 2) || row >= M || col >= N) continue;
     const int head = col / Dh, d = col % Dh;
-    float y1 = x1[q] + b1[q], y2 = x2[q] + b2[q];
+    float y1 = x1[q], y2 = x2[q];
     if (head < Hq + Hkv) {
+      y1 *= rs[q] * g1[q];
+      y2 *= rs[q] * g2[q];
       const float r1 = y1 * cs[q].x - y2 * cs[q].y;
       const float r2 = y2 * cs[q].x + y1 * cs[q].y;
       y1 = r1;
@@ -732,7 +837,7 @@ static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, 
       (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, K, epi, tiles_m, tiles_n, full, t, tail);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int elems = EK == EPI_QKV ? BM * BN / 2 : BM * BN;
+  const int elems = EK == EPI_QKV || EK == EPI_QKV_NORM ? BM * BN / 2 : BM * BN;
   tail_epi_kernel<BM, BN><<<dim3(cdiv(elems, kTailChunk), n_tail), 256, 0, s>>>(
       tail, t, full, tiles_m, tiles_n, M, N, epi);
   return hipGetLastError();
@@ -746,7 +851,10 @@ hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, in
     case EPI_RESID: return run_gemm_tail<256, 256, 4, 2, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, tail, s);
     case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU>(A, lda, B, ldb, M, N, K, epi, s);
     case EPI_STORE_F32: return run_gemm_tail<256, 256, 4, 2, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, epi, tail, s);
-    default: return run_gemm_tail<256, 256, 4, 2, EPI_QKV>(A, lda, B, ldb, M, N, K, epi, tail, s);
+    default:
+      if (epi.q_norm)
+        return run_gemm_tail<256, 256, 4, 2, EPI_QKV_NORM>(A, lda, B, ldb, M, N, K, epi, tail, s);
+      return run_gemm_tail<256, 256, 4, 2, EPI_QKV>(A, lda, B, ldb, M, N, K, epi, tail, s);
   }
 }
 
@@ -826,8 +934,11 @@ __global__ __launch_bounds__(256) void splitk_epi_kernel(const float* __restrict
     const int D = epi.head_dim, half = D / 2;
     const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
     const int pairs = (Hq + 2 * Hkv) * half;
-    if (gid >= (int64_t)M * pairs) return;
-    const int row = (int)(gid / pairs), p = (int)(gid % pairs);
+    // lanes past the end compute on a clamped pair (their group is whole:
+    // M pairs is a multiple of half) and store nothing
+    const bool live = gid < (int64_t)M * pairs;
+    const int64_t g = live ? gid : (int64_t)M * pairs - 1;
+    const int row = (int)(g / pairs), p = (int)(g % pairs);
     const int head = p / half, d = p % half;
     const int col = head * D + d;
     float x1 = sum(row, col), x2 = sum(row, col + half);
@@ -835,6 +946,18 @@ __global__ __launch_bounds__(256) void splitk_epi_kernel(const float* __restrict
       x1 += bf2f(((const bf16*)epi.bias)[col]);
       x2 += bf2f(((const bf16*)epi.bias)[col + half]);
     }
+    if (epi.q_norm) {
+      // per-head RMSNorm of q and k: a head's pairs are an aligned group of
+      // `half` lanes (D / 2 = 32 or 64)
+      const float ss = group_sum(x1 * x1 + x2 * x2, half);
+      if (head < Hq + Hkv) {
+        const bf16* gp = (const bf16*)(head < Hq ? epi.q_norm : epi.k_norm);
+        const float r = 1.0f / sqrtf(ss / (float)D + epi.eps);
+        x1 *= r * bf2f(gp[d]);
+        x2 *= r * bf2f(gp[d + half]);
+      }
+    }
+    if (!live) return;
     if (head < Hq + Hkv) {
       const float2 cs = epi.rope[(int64_t)row * half + d];
       const float y1 = x1 * cs.x - x2 * cs.y;

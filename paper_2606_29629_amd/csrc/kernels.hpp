@@ -59,8 +59,22 @@ struct Epi {
   const int32_t* tok_slot;  // [M] cache panel of each token, -1 = skip the cache write
   const int32_t* tok_row;   // [M] row of each token within its panel
   const float2* rope;       // [M, D/2] (cos, sin)
+  const void* q_norm;       // nullable [D] bf16: per-head RMSNorm gains of q (and k_norm of k)
+  const void* k_norm;
+  float eps;                // their epsilon
   int n_q_heads, n_kv_heads, head_dim, max_seq;
 };
+
+// Sum over aligned groups of `half` lanes (32 or 64).
+__device__ __forceinline__ float group_sum(float v, int half) {
+  v += __shfl_xor(v, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  v += __shfl_xor(v, 4, 64);
+  v += __shfl_xor(v, 8, 64);
+  v += __shfl_xor(v, 16, 64);
+  if (half == 64) v += __shfl_xor(v, 32, 64);
+  return v;
+}
 
 // Layer prologue: per-token map (cache panel and row within it of every
 // token, -1 when out of range), the rotary table rope[t][i] = (cos, sin)(pos[t] *

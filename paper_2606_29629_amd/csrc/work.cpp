@@ -66,12 +66,19 @@ tri_status tri_layer_work(const tri_layer_config* cfg, int32_t decode, int32_t n
   // scaled product, two multiply-adds per element.
   a.add(ST_PROLOGUE, 4.0 * T * H, T * H * bf + H * bf + T * H * bf + rope_table + token_map);
 
-  // q/k/v projection, rotary embedding, cache write.
+  // q/k/v projection, optional per-head q/k RMSNorm (sum of squares and the
+  // scaled product, two multiply-adds per q and k element), rotary
+  // embedding, cache write.
   {
     double bytes = Nqkv * H * bf + T * H * bf + rope_table + token_map + T * Hq * D * bf +
                    T * 2.0 * Hkv * D * bf;
+    double flops = 2.0 * T * Nqkv * H;
     if (cfg->flags & TRI_F_QKV_BIAS) bytes += Nqkv * bf;
-    a.add(ST_QKV, 2.0 * T * Nqkv * H, bytes);
+    if (cfg->flags & TRI_F_QK_NORM) {
+      bytes += 2.0 * D * bf;
+      flops += 4.0 * T * (Hq + Hkv) * D;
+    }
+    a.add(ST_QKV, flops, bytes);
   }
 
   // Attention: sequences with several new tokens take the causal flash path

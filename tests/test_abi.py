@@ -99,7 +99,7 @@ def batch(n_seqs=1, n_tokens=4, max_q=4, max_ctx=0, ptr=FAKE):
 
 
 def weights(ptr=FAKE):
-    w = T.LayerWeights(*[ptr + 4096 * i for i in range(8)])
+    w = T.LayerWeights(*[ptr + 4096 * i for i in range(10)])
     w.b_qkv = None
     w.w_router = None
     return w
@@ -129,6 +129,15 @@ def test_null_and_unsupported(lib):
     assert call(lib, w=T.LayerWeights()) == T.TRI_ERR_NULL
     assert call(lib, x=None) == T.TRI_ERR_NULL
     assert call(lib, c=cfg(flags=T.TRI_F_QKV_BIAS)) == T.TRI_ERR_NULL    # bias flag, no bias
+    for name in ("q_norm", "k_norm"):                                      # q/k norm gains
+        w = weights()
+        setattr(w, name, None)
+        assert call(lib, c=cfg(flags=T.TRI_F_QK_NORM), w=w) == T.TRI_ERR_NULL
+        setattr(w, name, FAKE + 2)
+        assert call(lib, c=cfg(flags=T.TRI_F_QK_NORM), w=w) == T.TRI_ERR_ALIGN
+        w = weights()
+        setattr(w, name, None)                                             # ignored without the flag
+        assert call(lib, w=w, ws_bytes=1024) == T.TRI_ERR_WORKSPACE
     bb = batch()
     bb.cu_q = None
     assert call(lib, b=bb) == T.TRI_ERR_NULL

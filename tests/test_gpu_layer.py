@@ -176,8 +176,13 @@ def stage_parity(cs, ws, rows, x_bits=None, label=""):
     if "b_qkv" in w:
         hq = hq + w["b_qkv"]
     ang = OL.rope_angles(b.pos[rows], D, cfg.rope_base)
-    assert_rounded(q, OL.rope(hq[:, :Hq * D].reshape(-1, Hq, D), ang), f"{label} q")
-    k_ref = OL.rope(hq[:, Hq * D:(Hq + Hkv) * D].reshape(-1, Hkv, D), ang)
+    q_pre = hq[:, :Hq * D].reshape(-1, Hq, D)
+    k_pre = hq[:, Hq * D:(Hq + Hkv) * D].reshape(-1, Hkv, D)
+    if getattr(cfg, "qk_norm", False):
+        q_pre = OL.rmsnorm(q_pre, w["q_norm"], cfg.rms_eps)
+        k_pre = OL.rmsnorm(k_pre, w["k_norm"], cfg.rms_eps)
+    assert_rounded(q, OL.rope(q_pre, ang), f"{label} q")
+    k_ref = OL.rope(k_pre, ang)
     v_ref = hq[:, (Hq + Hkv) * D:].reshape(-1, Hkv, D)
     assert_rounded(kc[sidx, :, crow], k_ref, f"{label} k cache rows")
     assert_rounded(vc[sidx, :, crow], v_ref, f"{label} v cache rows")

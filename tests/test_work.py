@@ -54,6 +54,25 @@ def test_dense_prefill_flops(lib):
     assert not any(k.startswith("moe_") for k in s)
 
 
+def test_qk_norm_adds_its_elementwise_work(lib):
+    """The per-head q/k RMSNorm: two multiply-adds per q and k element and
+    the two D-long gain vectors; nothing else changes."""
+    import dataclasses
+    wl = workload("dense_prefill")
+    b = wl.batch
+    plain = stages(T.layer_work(T.make_config(wl.cfg), False, b.q_len, b.ctx_len))
+    cfg = dataclasses.replace(wl.cfg, qk_norm=True)
+    normed = stages(T.layer_work(T.make_config(cfg), False, b.q_len, b.ctx_len))
+    n_tok = int(b.q_len.sum())
+    # 16384 tokens x (28 + 4) heads x 128 x 4
+    assert normed["qkv_rope"]["flops"] - plain["qkv_rope"]["flops"] == 16384 * 32 * 128 * 4
+    assert n_tok == 16384
+    assert normed["qkv_rope"]["bytes"] - plain["qkv_rope"]["bytes"] == 2 * 128 * 2
+    for k in plain:
+        if k != "qkv_rope":
+            assert normed[k] == plain[k]
+
+
 def test_dense_decode_bytes(lib):
     w = work("dense_decode")
     s = stages(w)
