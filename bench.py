@@ -11,7 +11,8 @@ region.  One JSON line is printed.  The decode workload (batch 64, KV 4096,
 32 steps) is timed as a secondary result in the same line.
 
 Phases: for each workload (dense prefill, dense decode, MoE prefill, MoE
-decode, mixed) the line carries the per-stage arithmetic intensity (the
+decode, mixed, and the dense and MoE prefills with the per-head q/k RMSNorm
+of the Qwen3-family attention block) the line carries the per-stage arithmetic intensity (the
 library's work model: algorithmic flops over compulsory HBM bytes), the
 phase's time-weighted intensity of Eq. 5 (weights: the stage times measured
 in the profiled repetition), achieved TFLOP/s and GB/s per stage, and the
@@ -550,7 +551,7 @@ def main(argv=None):
         res["decode"], phases["dense_decode"] = run_decode(args, tri)
     if not args.no_secondary:
         res["secondary"] = []
-        for n in ("moe_prefill", "moe_decode", "mixed"):
+        for n in ("moe_prefill", "moe_decode", "mixed", "dense_prefill_qkn", "moe_prefill_qkn"):
             r, phases[n] = run_secondary(args, tri, n)
             res["secondary"].append(r)
     res["phases"] = phases

@@ -391,32 +391,43 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
 // epilogue goes through LDS (free once every wave is past the mainloop and
 // its last loads have landed): 32 rows of the wave's tile at a time, each
 // wave in its own 32 x WC fp32 region, 16-byte chunks stored at chunk
-// c ^ row (conflict-free column writes and row reads).  Then lane l takes
-// rotary pair l of each row (WC / 2 = 64 pairs): a head's pairs are an
-// aligned group of D / 2 lanes, its sum of squares a group sum; the bias,
-// gains and the lane's column stay fixed across rows.
+// c ^ row (conflict-free column writes and row reads).  Then each lane takes
+// four consecutive rotary pairs of a row: 16 lanes cover a row's WC / 2 = 64
+// pairs, a pass covers 4 rows, and a head's pairs are an aligned group of
+// D / 8 lanes, its sum of squares a group sum.  The lane's columns, bias and
+// gains stay fixed across rows.
 template <int MI, int NI>
 __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                                   char* smem, int wv, int lane, int wrow0,
                                                   int wcol0, int M, int N) {
   constexpr int WC = NI * 32;
-  static_assert(WC == 128, "one rotary pair per lane and row");
+  static_assert(WC == 128, "16 lanes per row of the wave's columns");
   const int lr = lane & 31, lg = lane >> 5;
   const int D = epi.head_dim, half = D / 2;
   const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
-  const int hw = lane / half, d = lane % half;  // head within the wave's columns, pair
-  const int c1 = hw * D + d, c2 = c1 + half;     // first / second value's wave column
-  const int col = min(wcol0 + c1, N - half - 1); // (a head past N stores nothing)
-  const bool col_ok = wcol0 + c1 < N;
+  const int rl = lane >> 4;                       // row within a 4-row pass
+  const int p0 = 4 * (lane & 15);                 // first of the lane's 4 pairs
+  const int hw = p0 / half, d = p0 % half;        // head within the wave's columns
+  const int c1 = hw * D + d, c2 = c1 + half;      // wave columns of the 4 first / second values
+  const bool col_ok = wcol0 + c1 < N;             // whole heads: N is a multiple of D
+  const int col = col_ok ? wcol0 + c1 : 0;
   const int head = col / D;
   const int kind = head < Hq ? 0 : (head < Hq + Hkv ? 1 : 2);
-  const float b1 = epi.bias ? bf2f(((const bf16*)epi.bias)[col]) : 0.f;
-  const float b2 = epi.bias ? bf2f(((const bf16*)epi.bias)[col + half]) : 0.f;
-  const bf16* gp = (const bf16*)(kind == 0 ? epi.q_norm : epi.k_norm);
-  const float g1 = kind == 2 ? 1.f : bf2f(gp[d]);
-  const float g2 = kind == 2 ? 1.f : bf2f(gp[d + half]);
+  float b1[4], b2[4], g1[4], g2[4];
+  {
+    const bf16* bp = (const bf16*)epi.bias;
+    const bf16* gp = (const bf16*)(kind == 0 ? epi.q_norm : epi.k_norm);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      b1[e] = bp ? bf2f(bp[col + e]) : 0.f;
+      b2[e] = bp ? bf2f(bp[col + half + e]) : 0.f;
+      g1[e] = kind == 2 ? 1.f : bf2f(gp[d + e]);
+      g2[e] = kind == 2 ? 1.f : bf2f(gp[d + half + e]);
+    }
+  }
   const int kvh = kind == 1 ? head - Hq : head - Hq - Hkv;
   bf16* const cache = (bf16*)(kind == 1 ? epi.kc : epi.vc);
+  const float inv_d = 1.0f / (float)D;
 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
@@ -431,33 +442,64 @@ __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], c
         *(f32x4*)&buf[lr * WC + (((8 * j + 2 * q + lg) ^ lr) << 2)] =
             f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
     const int rbase = wrow0 + 32 * i;
-#pragma unroll 4
-    for (int t = 0; t < 32; ++t) {
-      const int row = rbase + t;  // uniform
-      if (row >= M) break;
-      float x1 = buf[t * WC + (((c1 >> 2) ^ t) << 2) + (c1 & 3)] + b1;
-      float x2 = buf[t * WC + (((c2 >> 2) ^ t) << 2) + (c2 & 3)] + b2;
-      const float ss = group_sum(x1 * x1 + x2 * x2, half);
-      const float2 cs = epi.rope[(int64_t)row * half + d];
-      if (kind != 2) {
-        const float r = 1.0f / sqrtf(ss / (float)D + epi.eps);
-        x1 *= r * g1;
-        x2 *= r * g2;
-        const float y1 = x1 * cs.x - x2 * cs.y;
-        const float y2 = x2 * cs.x + x1 * cs.y;
-        x1 = y1;
-        x2 = y2;
+    // two passes (8 rows) at a time: the rotary factors, cache slots and rows
+    // are loaded before the first store (a store could alias a later load)
+    for (int t0 = 0; t0 < 32; t0 += 8) {
+      if (rbase + t0 >= M) break;  // uniform
+      f32x4 cs[2][2];              // (cos, sin) of pairs d .. d + 3: [pass][0] = 0..1, [1] = 2..3
+      int sl[2], tr[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int rc = min(rbase + t0 + 4 * u + rl, M - 1);
+        const float2* rp = epi.rope + (int64_t)rc * half + d;
+        cs[u][0] = *(const f32x4*)rp;
+        cs[u][1] = *(const f32x4*)(rp + 2);
+        sl[u] = epi.tok_slot[rc];
+        tr[u] = epi.tok_row[rc];
       }
-      bf16* dst = nullptr;
-      if (kind == 0) {
-        dst = (bf16*)epi.q + ((int64_t)row * Hq + head) * D + d;
-      } else {
-        const int sl = epi.tok_slot[row];
-        if (sl >= 0) dst = cache + (((int64_t)sl * Hkv + kvh) * epi.max_seq + epi.tok_row[row]) * D + d;
-      }
-      if (col_ok && dst) {
-        dst[0] = f2bf(x1);
-        dst[half] = f2bf(x2);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int t = t0 + 4 * u + rl, row = rbase + t;
+        const f32x4 v1 = *(const f32x4*)&buf[t * WC + (((c1 >> 2) ^ t) << 2)];
+        const f32x4 v2 = *(const f32x4*)&buf[t * WC + (((c2 >> 2) ^ t) << 2)];
+        float x1[4], x2[4], ss = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x1[e] = v1[e] + b1[e];
+          x2[e] = v2[e] + b2[e];
+          ss += x1[e] * x1[e] + x2[e] * x2[e];
+        }
+        // sum over the head's D / 8 lanes (8 or 16, aligned)
+        ss += __shfl_xor(ss, 1, 64);
+        ss += __shfl_xor(ss, 2, 64);
+        ss += __shfl_xor(ss, 4, 64);
+        if (half == 64) ss += __shfl_xor(ss, 8, 64);
+        bf16x4 o1, o2;
+        const float r = 1.0f / sqrtf(ss * inv_d + epi.eps);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float y1 = x1[e], y2 = x2[e];
+          if (kind != 2) {
+            y1 *= r * g1[e];
+            y2 *= r * g2[e];
+            const float c = cs[u][e >> 1][2 * (e & 1)], sn = cs[u][e >> 1][2 * (e & 1) + 1];
+            const float z1 = y1 * c - y2 * sn;
+            const float z2 = y2 * c + y1 * sn;
+            y1 = z1;
+            y2 = z2;
+          }
+          o1[e] = f2bf(y1);
+          o2[e] = f2bf(y2);
+        }
+        bf16* dst = nullptr;
+        if (kind == 0)
+          dst = (bf16*)epi.q + ((int64_t)row * Hq + head) * D + d;
+        else if (sl[u] >= 0)
+          dst = cache + (((int64_t)sl[u] * Hkv + kvh) * epi.max_seq + tr[u]) * D + d;
+        if (row < M && col_ok && dst) {
+          *(bf16x4*)dst = o1;
+          *(bf16x4*)(dst + half) = o2;
+        }
       }
     }
   }

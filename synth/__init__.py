@@ -223,10 +223,18 @@ def workload(name: str, seed: int = 0) -> Workload:
                         Batch(np.arange(33, dtype=np.int32), np.concatenate([_ints(6144), lens]),
                               np.concatenate([_ints(512), np.ones(32, np.int32)])),
                         cache_prefilled=True, seed=seed)
+    if name in ("dense_prefill_qkn", "moe_prefill_qkn"):
+        # the same prefills with the per-head q/k RMSNorm of the Qwen3-family
+        # attention block (the MoE one then has the Qwen3-30B-A3B layer shape)
+        base = workload(name[:-4], seed)
+        return dataclasses.replace(
+            base, name=name, cfg=dataclasses.replace(base.cfg, qk_norm=True),
+            description=base.description + ", per-head q/k RMSNorm")
     raise KeyError(name)
 
 
-WORKLOADS = ("tiny", "dense_prefill", "dense_decode", "moe_prefill", "moe_decode", "mixed")
+WORKLOADS = ("tiny", "dense_prefill", "dense_decode", "moe_prefill", "moe_decode", "mixed",
+             "dense_prefill_qkn", "moe_prefill_qkn")
 
 
 def make_x(cfg: LayerConfig, n_tokens: int, seed: int = 0, step: Optional[int] = None) -> np.ndarray:
