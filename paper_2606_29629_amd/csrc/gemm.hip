@@ -70,10 +70,10 @@ __device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n,
   tile_of_id(xcd_id(bid, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int S = 2>
 struct GemmSmem {
-  bf16 a[2][BM * kBK];
-  bf16 b[2][BN * kBK];
+  bf16 a[S][BM * kBK];
+  bf16 b[S][BN * kBK];
 };
 
 // B-tile row -> weight row.  For SwiGLU each wave's N sub-tile holds WN/2 gate
@@ -93,14 +93,17 @@ __device__ __forceinline__ int b_row_of(int kind, int tn, int nt, int ffn) {
 // swz(row, lane % 8) of this lane's row in each of its 1 KB LDS blocks (at or
 // beyond the buffer size for rows that must read as zero).
 //
-// Schedule of k-tile t (4 k-steps of 16): the fragments of k-step s + 1 are
-// read from LDS while the MFMAs of step s run.  Before the MFMAs of the last
-// step, each wave waits for its loads of tile t + 1, one barrier makes tile
-// t + 1 visible and retires every read of tile t, the loads of tile t + 2 go
-// into tile t's buffer and the first fragments of tile t + 1 are read -- all
-// under the last step's MFMAs, so the barrier costs no matrix-core time beyond
-// the skew between waves.
-template <int BM, int BN, int WGM, int WGN>
+// S LDS stages, tiles loaded S - 1 ahead.  Schedule of k-tile t (4 k-steps
+// of 16): the fragments of k-step s + 1 are read from LDS while the MFMAs of
+// step s run.  Before the MFMAs of the last step, each wave waits for its
+// loads of tile t + 1 (those of tiles t + 2 .. t + S - 1 may stay in flight),
+// one barrier makes tile t + 1 visible and retires every read of tile t, the
+// loads of tile t + S go into tile t's buffer and the first fragments of tile
+// t + 1 are read -- all under the last step's MFMAs, so the barrier costs no
+// matrix-core time beyond the skew between waves.  Compute-bound tiles use
+// S = 2; the decode projections, bound by the weight stream, use more stages
+// for more bytes in flight per CU.
+template <int BM, int BN, int WGM, int WGN, int S = 2>
 struct Mainloop {
   static constexpr int NT = WGM * WGN * 64;
   static constexpr int NW = NT / 64;
@@ -109,7 +112,7 @@ struct Mainloop {
   static constexpr int A_BLK = BM / 8 / NW, B_BLK = BN / 8 / NW;  // 1 KB blocks per wave
   static constexpr int KSTEPS = kBK / 16;
 
-  __device__ __forceinline__ static void run(GemmSmem<BM, BN>& sm, __amdgpu_buffer_rsrc_t ra,
+  __device__ __forceinline__ static void run(GemmSmem<BM, BN, S>& sm, __amdgpu_buffer_rsrc_t ra,
                                              const uint32_t (&a_off)[A_BLK],
                                              __amdgpu_buffer_rsrc_t rb,
                                              const uint32_t (&b_off)[B_BLK], int K, int wv,
@@ -179,20 +182,18 @@ struct Mainloop {
     constexpr int NG = NMF > NRD ? NMF : NRD;
     constexpr int NGL = NG > NLD ? NG : NLD;
     const int KT = K / kBK;
-    gload(0, 0, 0);
-    if (KT > 1) {
-      gload(1, 1, 0);
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NLD) : "memory");  // tile 0 landed
-    } else {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    }
+    static_assert((S - 1) * NLD < 64, "vmcnt counts up to 63");
+#pragma unroll
+    for (int t = 0; t < S; ++t) gload(t, t, t < KT ? 0u : 0x80000000u);
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((S - 1) * NLD) : "memory");  // tile 0 landed
     __syncthreads();
     lload(0, 0, 0);
+    int buf = 0;
     // The issue order is spelled out: one MFMA, then one LDS read for the next
     // k-step (and on the last step one or more tile loads), fenced so the
     // compiler keeps it.
     for (int kt = 0; kt < KT; ++kt) {
-      const int buf = kt & 1;
+      const int nbuf = buf + 1 == S ? 0 : buf + 1;
 #pragma unroll
       for (int ks = 0; ks + 1 < KSTEPS; ++ks) {
 #pragma unroll
@@ -203,16 +204,18 @@ struct Mainloop {
         }
       }
       constexpr int last = (KSTEPS - 1) & 1;
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's tile t + 1 loads
+      // this wave's tile t + 1 loads
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"((S - 2) * NLD) : "memory");
       __syncthreads();
-      const uint32_t kill = kt + 2 < KT ? 0u : 0x80000000u;
+      const uint32_t kill = kt + S < KT ? 0u : 0x80000000u;
 #pragma unroll
       for (int g = 0; g < NGL; ++g) {
         if (g < NMF) mfma(last, g);
-        if (g < NLD) gpiece(kt + 2, buf, kill, g);
-        if (g < NRD) lread(buf ^ 1, 0, last ^ 1, g);  // stale but in-range on the last tile
+        if (g < NLD) gpiece(kt + S, buf, kill, g);
+        if (g < NRD) lread(nbuf, 0, last ^ 1, g);  // stale but in-range on the last tile
         __builtin_amdgcn_sched_barrier(0);
       }
+      buf = nbuf;
     }
   }
 };
@@ -505,16 +508,16 @@ __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], c
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int EK>
+template <int BM, int BN, int WGM, int WGN, int EK, int S = 2>
 __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __restrict__ A, int lda,
                                                    const bf16* __restrict__ B, int ldb, int M,
                                                    int N, int K, int kc, Epi epi,
                                                    int tiles_m, int tiles_n, int full,
                                                    int tsplit, float* __restrict__ tail) {
-  using ML = Mainloop<BM, BN, WGM, WGN>;
+  using ML = Mainloop<BM, BN, WGM, WGN, S>;
   constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
   extern __shared__ __align__(16) char smem_raw[];
-  GemmSmem<BM, BN>& sm = *reinterpret_cast<GemmSmem<BM, BN>*>(smem_raw);
+  GemmSmem<BM, BN, S>& sm = *reinterpret_cast<GemmSmem<BM, BN, S>*>(smem_raw);
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -676,17 +679,17 @@ static hipError_t opt_in_lds(Kern k, size_t smem, bool& done) {
 
 // splits > 1 only with EPI_STORE_F32 (plane z of epi.out holds split z); K
 // must then be a multiple of 64 * splits.
-template <int BM, int BN, int WGM, int WGN, int EK>
+template <int BM, int BN, int WGM, int WGN, int EK, int S = 2>
 static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
                            const Epi& epi, hipStream_t s, int splits = 1) {
   const int tiles_m = cdiv(M, BM);
   const int tiles_n = EK == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
-  const size_t smem = sizeof(GemmSmem<BM, BN>);
+  const size_t smem = sizeof(GemmSmem<BM, BN, S>);
   static bool attr_set = false;
-  hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK>, smem, attr_set);
+  hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK, S>, smem, attr_set);
   if (e != hipSuccess) return e;
   const int kc = K / splits;
-  gemm_kernel<BM, BN, WGM, WGN, EK><<<dim3(tiles_m * tiles_n, splits), WGM * WGN * 64, smem, s>>>(
+  gemm_kernel<BM, BN, WGM, WGN, EK, S><<<dim3(tiles_m * tiles_n, splits), WGM * WGN * 64, smem, s>>>(
       (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, kc, epi, tiles_m, tiles_n,
       tiles_m * tiles_n, 1, nullptr);
   return hipGetLastError();
@@ -1103,20 +1106,38 @@ __global__ __launch_bounds__(kNormRowThreads) void splitk_resid_norm_kernel(
 // 64 x 64 tiles (two or four waves) give ~600 workgroups on the large
 // projections -- every one resident at once, each a short run of weight rows,
 // which keeps the HBM pages streaming -- and split-K multiplies the
-// workgroups of the narrow projections until ~400 are in flight.  Without a
-// split the epilogue is fused; with one, fp32 partial planes go to the
-// workspace and splitk_epi_kernel finishes.  q/k/v always splits (its fused
-// epilogue needs a whole head per wave).
+// workgroups of the narrow projections until ~200 are in flight (~400 for
+// q/k/v, whose K is short).  Without a split the epilogue is fused; with one,
+// fp32 partial planes go to the workspace and splitk_epi_kernel finishes.
+// q/k/v always splits (its fused epilogue needs a whole head per wave).  The
+// split runs of up to two workgroups per CU keep four k-tiles in LDS (three
+// in flight), the rest two.
 constexpr int kSkinnyBN = 64;
 
 static int skinny_bm(int M) { return M <= 64 ? 64 : 128; }
 
 int skinny_splits(int M, int N, int K, int kind) {
   const int tiles = cdiv(M, skinny_bm(M)) * cdiv(N, kSkinnyBN);
+  const int target = kind == EPI_QKV ? 400 : 200;
   int s = 1;
-  while ((tiles * s < 400 || (kind == EPI_QKV && s == 1)) && s < 16 && K % (kBK * 2 * s) == 0)
+  while ((tiles * s < target || (kind == EPI_QKV && s == 1)) && s < 16 &&
+         K % (kBK * 2 * s) == 0)
     s *= 2;
   return s;
+}
+
+// fp32 partial planes [splits][M][N] of a short batch.
+static hipError_t run_skinny_planes(const void* A, int lda, const void* B, int ldb, int M, int N,
+                                    int K, float* part, int splits, int kind, hipStream_t s) {
+  Epi pe{};
+  pe.kind = EPI_STORE_F32;
+  pe.out = part;
+  pe.ldo = N;
+  if (M > 64)
+    return run_gemm<128, kSkinnyBN, 4, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
+  if (kind != EPI_QKV && cdiv(N, kSkinnyBN) * splits <= 2 * cu_count())
+    return run_gemm<64, kSkinnyBN, 2, 1, EPI_STORE_F32, 4>(A, lda, B, ldb, M, N, K, pe, s, splits);
+  return run_gemm<64, kSkinnyBN, 2, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
 }
 
 size_t skinny_partial_bytes(int M, int N, int K, int kind) {
@@ -1137,11 +1158,7 @@ static hipError_t run_skinny(const void* A, int lda, const void* B, int ldb, int
       default: return hipErrorInvalidValue;
     }
   }
-  Epi pe{};
-  pe.kind = EPI_STORE_F32;
-  pe.out = part;
-  pe.ldo = N;
-  hipError_t e = run_gemm<BM, kSkinnyBN, WGM, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
+  hipError_t e = run_skinny_planes(A, lda, B, ldb, M, N, K, part, splits, epi.kind, s);
   if (e != hipSuccess) return e;
   int64_t n_out;
   if (epi.kind == EPI_SWIGLU) n_out = (int64_t)M * epi.ffn;
@@ -1170,13 +1187,7 @@ hipError_t launch_skinny_resid_norm(const void* A, int lda, const void* B, int l
                                     const void* g, void* y, float eps, float* part, hipStream_t s) {
   if (M == 0) return hipSuccess;
   const int splits = skinny_splits(M, N, K, EPI_RESID);
-  Epi pe{};
-  pe.kind = EPI_STORE_F32;
-  pe.out = part;
-  pe.ldo = N;
-  hipError_t e = M <= 64
-                     ? run_gemm<64, kSkinnyBN, 2, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits)
-                     : run_gemm<128, kSkinnyBN, 4, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
+  hipError_t e = run_skinny_planes(A, lda, B, ldb, M, N, K, part, splits, EPI_RESID, s);
   if (e != hipSuccess) return e;
   splitk_resid_norm_kernel<<<M, kNormRowThreads, 0, s>>>(part, splits, M, N, (const bf16*)resid,
                                                         ldr, (bf16*)out, ldo, (const bf16*)g,
