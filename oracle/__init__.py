@@ -11,8 +11,8 @@ with the HIP path; both receive their inputs from the seeded generators in
   pins ``oracle.layer``.
 """
 from .layer import (attention, kvcache_append, layer_forward, moe_ffn, moe_route, rmsnorm,
-                    rope, rope_angles, round_bf16, silu, softmax, swiglu, topk_lower_index)
+                    rope, rope_angles, rope_angles_sections, round_bf16, silu, softmax, swiglu, topk_lower_index)
 from .brute import layer_brute
 
 __all__ = ["attention", "kvcache_append", "layer_forward", "moe_ffn", "moe_route", "rmsnorm",
-           "rope", "rope_angles", "round_bf16", "silu", "softmax", "swiglu", "topk_lower_index", "layer_brute"]
+           "rope", "rope_angles", "rope_angles_sections", "round_bf16", "silu", "softmax", "swiglu", "topk_lower_index", "layer_brute"]

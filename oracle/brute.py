@@ -25,11 +25,14 @@ def _matvec(wmat, vec):
 
 def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
                 ctx_lens: List[int], q_lens: List[int], x: List[List[float]],
-                forced_routes: Optional[List[List[int]]] = None, store=None):
+                forced_routes: Optional[List[List[int]]] = None, store=None,
+                pos3: Optional[List[List[int]]] = None):
     """Arguments are nested Python lists of floats (cache_k[slot][h][row][d]).
     ``store`` (scalar -> scalar), if given, is applied to every activation value
     at the storage points: h, q, k, v, attention output, x1, h2, the SwiGLU
-    activation and the output.
+    activation and the output.  ``pos3`` ([token][3] temporal, height, width
+    ids) replaces the one-dimensional positions when ``cfg.mrope_section``
+    is set.
     Returns (out rows, k_new, v_new, route_idx, route_w)."""
     S = (lambda v: v) if store is None else store
     H, Hq, Hkv, D = cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
@@ -42,11 +45,19 @@ def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
         r = 1.0 / math.sqrt(ms + eps)
         return [vec[i] * r * gain[i] for i in range(len(vec))]
 
+    sections = getattr(cfg, "mrope_section", None)
+
     def rotate(vec, p):
+        # p: the position, or the token's (temporal, height, width) ids
         half = D // 2
         res = [0.0] * D
         for i in range(half):
-            theta = p * math.pow(cfg.rope_base, -2.0 * i / D)
+            if sections:
+                k = 0 if i < sections[0] else (1 if i < sections[0] + sections[1] else 2)
+                pi = p[k]
+            else:
+                pi = p
+            theta = pi * math.pow(cfg.rope_base, -2.0 * i / D)
             c, s = math.cos(theta), math.sin(theta)
             res[i] = vec[i] * c - vec[i + half] * s
             res[i + half] = vec[i + half] * c + vec[i] * s
@@ -58,6 +69,7 @@ def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
     for s in range(len(slots)):
         for i in range(q_lens[s]):
             p = ctx_lens[s] + i
+            rp = pos3[t] if sections else p     # rotary position(s) of the token
             h = [S(v) for v in norm(x[t], w["attn_norm"])]
             qkv = _matvec(w["w_qkv"], h)
             if w.get("b_qkv") is not None:
@@ -67,8 +79,8 @@ def layer_brute(cfg, w: Dict[str, list], cache_k, cache_v, slots: List[int],
             if getattr(cfg, "qk_norm", False):   # per-head RMSNorm before the rotation
                 qpre = [norm(vec, w["q_norm"]) for vec in qpre]
                 kpre = [norm(vec, w["k_norm"]) for vec in kpre]
-            qh = [[S(v) for v in rotate(qpre[j], p)] for j in range(Hq)]
-            kh = [[S(v) for v in rotate(kpre[j], p)] for j in range(Hkv)]
+            qh = [[S(v) for v in rotate(qpre[j], rp)] for j in range(Hq)]
+            kh = [[S(v) for v in rotate(kpre[j], rp)] for j in range(Hkv)]
             vh = [[S(v) for v in qkv[(Hq + Hkv + j) * D:(Hq + Hkv + j + 1) * D]] for j in range(Hkv)]
             toks.append((s, p, qh, kh, vh))
             k_rows.append(kh)

@@ -24,6 +24,13 @@ fix is a declared reading:
     the layer, ``cfg.qk_norm``): before the rotation every head of q and of k
     is RMS-normalised over its D values with gains q_norm / k_norm [D] and
     the layer's eps;
+  * optional multi-section rotary positions (the multimodal rotary embedding
+    of the Qwen2-VL / Qwen2.5-Omni family, ``cfg.mrope_section`` = (s_t, s_h,
+    s_w), s_t + s_h + s_w = D/2): every token carries three position ids
+    (temporal, height, width; ``batch.pos3`` [3, T]) and rotary frequency i
+    takes its position from the section it falls in, frequencies
+    [0, s_t) the temporal id, [s_t, s_t + s_h) the height id, the rest the
+    width id.  With equal ids it is the one-dimensional embedding;
   * SwiGLU  a = silu(h W_g^T) * (h W_u^T),  silu(z) = z / (1 + exp(-z));
   * MoE: softmax over all expert logits, top-k by logit (descending, ties to
     the lower expert index), weights renormalised over the chosen k, no shared
@@ -67,6 +74,18 @@ def rope_angles(pos: np.ndarray, head_dim: int, base: float) -> np.ndarray:
     i = np.arange(head_dim // 2, dtype=np.float64)
     inv_freq = np.float64(base) ** (-2.0 * i / head_dim)
     return np.asarray(pos, dtype=np.float64)[:, None] * inv_freq[None, :]
+
+
+def rope_angles_sections(pos3: np.ndarray, head_dim: int, base: float, sections) -> np.ndarray:
+    """Multi-section rotary angles [n, D/2] in float64: frequency i of a token
+    uses position id pos3[k, token] of the section k that i falls in
+    (sections = (s_t, s_h, s_w) consecutive frequency counts)."""
+    i = np.arange(head_dim // 2, dtype=np.float64)
+    inv_freq = np.float64(base) ** (-2.0 * i / head_dim)
+    sec = np.repeat(np.arange(3), np.asarray(sections, dtype=np.int64))
+    assert sec.shape[0] == head_dim // 2, "sections must sum to D/2"
+    p = np.asarray(pos3, dtype=np.float64)[sec, :]          # [D/2, n]
+    return p.T * inv_freq[None, :]
 
 
 def rope(x: np.ndarray, angles: np.ndarray) -> np.ndarray:
@@ -199,7 +218,10 @@ def layer_forward(cfg, w: Dict[str, np.ndarray], cache_k: np.ndarray, cache_v: n
     qkv = h @ w_qkv.T
     if w.get("b_qkv") is not None:
         qkv = qkv + _as(w["b_qkv"], dtype)
-    ang = rope_angles(pos, D, cfg.rope_base)
+    if getattr(cfg, "mrope_section", None):
+        ang = rope_angles_sections(batch.pos3, D, cfg.rope_base, cfg.mrope_section)
+    else:
+        ang = rope_angles(pos, D, cfg.rope_base)
     q_pre = qkv[:, :Hq * D].reshape(T, Hq, D)
     k_pre = qkv[:, Hq * D:(Hq + Hkv) * D].reshape(T, Hkv, D)
     if getattr(cfg, "qk_norm", False):

@@ -20,7 +20,7 @@ workload descriptions.
 from __future__ import annotations
 
 import dataclasses
-from typing import Dict, List, Optional
+from typing import Dict, List, Optional, Tuple
 
 import numpy as np
 
@@ -57,6 +57,8 @@ class LayerConfig:
     qkv_bias: bool = False
     moe_renorm: bool = True
     qk_norm: bool = False         # per-head RMSNorm of q and k before the rotation
+    # multi-section rotary positions: (s_t, s_h, s_w) frequencies per section, sum D/2
+    mrope_section: Optional[Tuple[int, int, int]] = None
 
     @property
     def moe(self) -> bool:
@@ -133,10 +135,12 @@ def make_weights(cfg: LayerConfig, seed: int = 0, w_std: float = 0.02,
 class Batch:
     """A ragged batch: per sequence its cache slot, tokens already cached
     (``ctx_len``) and new tokens this call (``q_len``).  RoPE positions of the
-    new tokens are ``ctx_len + i``."""
+    new tokens are ``ctx_len + i``, or, for multi-section rotary positions,
+    the columns of ``pos3`` [3, T] (temporal, height, width ids)."""
     slot: np.ndarray      # int32 [n_seqs]
     ctx_len: np.ndarray   # int32 [n_seqs]
     q_len: np.ndarray     # int32 [n_seqs]
+    pos3: Optional[np.ndarray] = None   # int32 [3, T] or None
 
     @property
     def n_seqs(self) -> int:
@@ -155,10 +159,58 @@ class Batch:
         return np.concatenate([np.arange(c, c + q, dtype=np.int32)
                                for c, q in zip(self.ctx_len, self.q_len)]).astype(np.int32)
 
+    @property
+    def rope_pos(self) -> np.ndarray:
+        """The position array the layer reads: pos [T], or pos3 flattened [3 T]."""
+        return self.pos if self.pos3 is None else np.ascontiguousarray(self.pos3, np.int32).ravel()
+
     def advanced(self) -> "Batch":
-        """The batch after this call's tokens were appended (next decode step)."""
+        """The batch after this call's tokens were appended (next decode step).
+        With pos3, the next token of a sequence is text at one past the
+        largest id its tokens of this call used."""
+        nxt = None
+        if self.pos3 is not None:
+            cu = self.cu_q
+            nxt = np.stack([np.full(3, self.pos3[:, cu[i]:cu[i + 1]].max() + 1, np.int32)
+                            for i in range(self.n_seqs)], axis=1)
         return Batch(self.slot.copy(), (self.ctx_len + self.q_len).astype(np.int32),
-                     np.ones_like(self.q_len))
+                     np.ones_like(self.q_len), nxt)
+
+
+def mrope_positions(segments, start: int = 0):
+    """Multi-section position ids [3, n] (temporal, height, width) of a token
+    stream and the id after it.  segments: ("text", n) -- ids start .. start+n-1
+    on all three; ("image", gh, gw) -- gh x gw patches in row-major order,
+    temporal id start, height start + row, width start + col; ("video", gt,
+    gh, gw) -- gt frames of such patches, temporal id start + frame.  After an
+    image or video the next id is start + its largest extent."""
+    cols = []
+    for seg in segments:
+        kind = seg[0]
+        if kind == "text":
+            ids = np.arange(start, start + seg[1], dtype=np.int32)
+            cols.append(np.stack([ids, ids, ids]))
+            start += seg[1]
+        else:
+            gt, gh, gw = (1, seg[1], seg[2]) if kind == "image" else seg[1:4]
+            f, r, c = np.meshgrid(np.arange(gt), np.arange(gh), np.arange(gw), indexing="ij")
+            cols.append(np.stack([start + f.ravel(), start + r.ravel(), start + c.ravel()])
+                        .astype(np.int32))
+            start += max(gt, gh, gw)
+    out = np.concatenate(cols, axis=1) if cols else np.zeros((3, 0), np.int32)
+    return out.astype(np.int32), start
+
+
+def mrope_batch(slot, ctx_len, segments_per_seq) -> Batch:
+    """A Batch whose sequence s continues after ctx_len[s] cached text tokens
+    (ids 0 .. ctx_len[s]-1) with the given segments."""
+    pos, q = [], []
+    for c, segs in zip(ctx_len, segments_per_seq):
+        p3, _ = mrope_positions(segs, int(c))
+        pos.append(p3)
+        q.append(p3.shape[1])
+    return Batch(np.asarray(slot, np.int32), np.asarray(ctx_len, np.int32),
+                 np.asarray(q, np.int32), np.concatenate(pos, axis=1))
 
 
 @dataclasses.dataclass

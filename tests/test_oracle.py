@@ -436,3 +436,87 @@ def test_qk_norm_makes_the_layer_invariant_to_query_and_key_scale():
         r1 = L.layer_forward(cfg, w2, ck, cv, b, x)
         same = np.allclose(r1["out"], r0["out"], rtol=1e-12, atol=1e-12)
         assert same == qkn
+
+
+# ----------------------------------------------- multi-section rotary positions --
+
+def test_mrope_angles_hand_computed():
+    """D = 8 (four frequencies), base 100, sections (1, 2, 1), ids (t, h, w) =
+    (2, 5, 7): inverse frequencies 100^(-i/4) = 1, 10^-0.5, 0.1, 10^-1.5, so
+    the angles are 2 * 1, 5 * 10^-0.5, 5 * 0.1 and 7 * 10^-1.5."""
+    ang = L.rope_angles_sections(np.array([[2], [5], [7]]), 8, 100.0, (1, 2, 1))
+    want = [2.0, 1.5811388300841898, 0.5, 0.22135943621178655]
+    assert np.allclose(ang[0], want, rtol=1e-15, atol=0)
+
+
+def test_mrope_equal_ids_is_the_one_dimensional_layer():
+    """Three equal ids per token reduce the embedding to the 1-D one: the
+    layer output is bit-identical for any sections."""
+    import dataclasses
+    from synth import mrope_positions
+    b = B([1, 0], [3, 0], [4, 5])
+    pos = b.pos
+    b3 = Batch(b.slot, b.ctx_len, b.q_len, np.stack([pos, pos, pos]))
+    for sec in [(1, 2, 1), (4, 0, 0), (0, 0, 4), (2, 1, 1)]:
+        cfg = dataclasses.replace(TINY, mrope_section=sec)
+        w, ck, cv, x = setup(cfg, b, 2, 12)
+        r0 = L.layer_forward(TINY, w, ck, cv, b, x)
+        r1 = L.layer_forward(cfg, w, ck, cv, b3, x)
+        assert np.array_equal(r0["out"], r1["out"]) and np.array_equal(r0["k_new"], r1["k_new"])
+    # text segments of the position generator are equal ids
+    p3, nxt = mrope_positions([("text", 5)], 7)
+    assert np.array_equal(p3, np.tile(np.arange(7, 12), (3, 1))) and nxt == 12
+
+
+def test_mrope_single_section_ignores_the_other_ids():
+    """Sections (D/2, 0, 0): only the temporal id matters."""
+    import dataclasses
+    rng = np.random.default_rng(3)
+    b = B([0], [0], [6])
+    t = np.array([0, 0, 1, 1, 4, 9], np.int32)
+    b3 = Batch(b.slot, b.ctx_len, b.q_len, np.stack([t, rng.integers(0, 50, 6),
+                                                     rng.integers(0, 50, 6)]).astype(np.int32))
+    bt = Batch(b.slot, b.ctx_len, b.q_len, np.stack([t, t, t]))
+    cfg = dataclasses.replace(TINY, mrope_section=(4, 0, 0))
+    w, ck, cv, x = setup(cfg, b, 1, 8)
+    r0 = L.layer_forward(cfg, w, ck, cv, bt, x)
+    r1 = L.layer_forward(cfg, w, ck, cv, b3, x)
+    assert np.array_equal(r0["out"], r1["out"])
+
+
+def test_mrope_scores_depend_on_per_section_differences_only():
+    """Shifting every token's temporal, height and width ids by three
+    different constants leaves a fresh prefill unchanged: q.k after the
+    rotation depends only on the ids' differences, section by section."""
+    import dataclasses
+    from synth import mrope_batch
+    b = mrope_batch([0, 1], [0, 0], [[("text", 3), ("image", 2, 3), ("text", 2)],
+                                     [("video", 2, 2, 2), ("text", 1)]])
+    cfg = dataclasses.replace(TINY, mrope_section=(1, 2, 1))
+    w, ck, cv, x = setup(cfg, b, 2, 16)
+    r0 = L.layer_forward(cfg, w, ck, cv, b, x)
+    shifted = Batch(b.slot, b.ctx_len, b.q_len, b.pos3 + np.array([[5], [11], [2]], np.int32))
+    r1 = L.layer_forward(cfg, w, ck, cv, shifted, x)
+    assert np.allclose(r0["out"], r1["out"], rtol=1e-10, atol=1e-10)
+    assert not np.allclose(r0["k_new"], r1["k_new"])       # the keys themselves moved
+    # a shift of one section only, by different amounts per token, changes it
+    moved = Batch(b.slot, b.ctx_len, b.q_len,
+                  b.pos3 + np.array([[0], [1], [0]], np.int32) * np.arange(b.n_tokens)[None, :])
+    r2 = L.layer_forward(cfg, w, ck, cv, moved, x)
+    assert not np.allclose(r0["out"], r2["out"], rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("sec", [(1, 2, 1), (0, 3, 1), (2, 0, 2)])
+def test_mrope_oracle_matches_brute_force(sec):
+    import dataclasses
+    from synth import mrope_batch
+    b = mrope_batch([1, 0], [2, 0], [[("image", 2, 2), ("text", 1)], [("video", 2, 1, 2)]])
+    cfg = dataclasses.replace(TINY, mrope_section=sec)
+    w, ck, cv, x = setup(cfg, b, 2, 10)
+    r = L.layer_forward(cfg, w, ck, cv, b, x)
+    wl = {k: _lists(v) for k, v in w.items()}
+    out, kr, vr, _, _ = oracle.layer_brute(cfg, wl, _lists(ck), _lists(cv), b.slot.tolist(),
+                                           b.ctx_len.tolist(), b.q_len.tolist(), _lists(x),
+                                           pos3=b.pos3.T.tolist())
+    assert np.allclose(r["k_new"], np.array(kr), rtol=1e-12, atol=1e-12)
+    assert np.allclose(r["out"], np.array(out), rtol=1e-12, atol=1e-12)
