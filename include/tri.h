@@ -13,7 +13,9 @@
  *   q,k,v = h W_qkv^T (+ b_qkv), optionally each q and k head RMS-normalised
  *         (TRI_F_QK_NORM), rotary embedding on q and k at each token's
  *         position (rotate-half pairs (i, i+D/2), angle pos * base^(-2i/D)
- *         formed in double precision), k and v appended to the cache
+ *         formed in double precision; with TRI_F_MROPE frequency i takes the
+ *         temporal, height or width id of the token by its section), k and v
+ *         appended to the cache
  *   o   = causal grouped-query softmax attention over the cache (query head j
  *         reads KV head floor(j*Hkv/Hq)), scale 1/sqrt(D)
  *   x1  = x + o W_o^T
@@ -74,7 +76,14 @@ enum {
   TRI_F_QK_NORM = 8,    /* per-head RMSNorm of q and k (gains q_norm, k_norm, eps
                            rms_eps) after the projection, before the rotation: the
                            Qwen3-family variant of the layer                         */
-  TRI_F_ALL = 15
+  TRI_F_MROPE = 16,     /* multi-section rotary positions (the multimodal rotary
+                           embedding of the Qwen2-VL / Qwen2.5-Omni family): every
+                           token has three position ids (temporal, height, width;
+                           tri_batch.pos is then [3][n_tokens]) and rotary
+                           frequency i < mrope_section[0] takes the temporal id,
+                           i < mrope_section[0] + mrope_section[1] the height id,
+                           the rest the width id                                     */
+  TRI_F_ALL = 31
 };
 
 typedef struct {
@@ -90,6 +99,9 @@ typedef struct {
   float rope_base;        /* rotary base (> 0)                                      */
   int32_t dtype;          /* tri_dtype; only TRI_BF16 is implemented                */
   int32_t flags;          /* TRI_F_* bits                                           */
+  int32_t mrope_section[3]; /* TRI_F_MROPE: frequencies per section (temporal,
+                             height, width), each >= 0, summing to D/2
+                             (TRI_ERR_SHAPE otherwise); ignored without the flag   */
 } tri_layer_config;
 
 /* Device pointers to one layer's weights, row-major [out, in], bfloat16.       */
@@ -136,7 +148,9 @@ typedef struct {
  * arrays are device int32.  Sequence s owns new tokens cu_q[s] .. cu_q[s+1]-1
  * of x; its new token i is written to cache row ctx_len[s] + i of slot
  * slot[s] and attends to rows 0 .. ctx_len[s] + i.  pos[t] is the rotary
- * position of token t (normally ctx_len + i).  The caller guarantees
+ * position of token t (normally ctx_len + i); with TRI_F_MROPE, pos holds
+ * three planes, pos[k * n_tokens + t] being id k (temporal, height, width) of
+ * token t (for text tokens all three normally equal ctx_len + i).  The caller guarantees
  * ctx_len[s] + q_len[s] <= max_seq for every sequence; a sequence violating it
  * is skipped on the device (no access outside the cache).                     */
 typedef struct {
@@ -147,7 +161,7 @@ typedef struct {
   const int32_t* cu_q;    /* [n_seqs + 1], cu_q[0] = 0, non-decreasing             */
   const int32_t* ctx_len; /* [n_seqs]                                              */
   const int32_t* slot;    /* [n_seqs], distinct                                    */
-  const int32_t* pos;     /* [n_tokens]                                            */
+  const int32_t* pos;     /* [n_tokens], or [3][n_tokens] with TRI_F_MROPE         */
 } tri_batch;
 
 /* Byte offsets of the layer's intermediates inside the workspace (for

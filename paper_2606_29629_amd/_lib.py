@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(HERE, "libtri.so")
 TRI_OK, TRI_ERR_NULL, TRI_ERR_SHAPE, TRI_ERR_UNSUPPORTED = 0, -1, -2, -3
 TRI_ERR_RANGE, TRI_ERR_ALIGN, TRI_ERR_WORKSPACE, TRI_ERR_HIP, TRI_ERR_ALIAS = -4, -5, -6, -7, -8
 TRI_BF16, TRI_F32 = 0, 1
-TRI_F_QKV_BIAS, TRI_F_MOE, TRI_F_MOE_RENORM, TRI_F_QK_NORM = 1, 2, 4, 8
+TRI_F_QKV_BIAS, TRI_F_MOE, TRI_F_MOE_RENORM, TRI_F_QK_NORM, TRI_F_MROPE = 1, 2, 4, 8, 16
 
 
 class LayerConfig(ctypes.Structure):
@@ -25,7 +25,8 @@ class LayerConfig(ctypes.Structure):
                 ("ffn_dim", ctypes.c_int32), ("n_experts", ctypes.c_int32),
                 ("top_k", ctypes.c_int32), ("expert_ffn_dim", ctypes.c_int32),
                 ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float),
-                ("dtype", ctypes.c_int32), ("flags", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("mrope_section", ctypes.c_int32 * 3)]
 
 
 class LayerWeights(ctypes.Structure):
@@ -125,6 +126,9 @@ def make_config(cfg) -> LayerConfig:
         flags |= TRI_F_QKV_BIAS
     if getattr(cfg, "qk_norm", False):
         flags |= TRI_F_QK_NORM
+    sec = getattr(cfg, "mrope_section", None)
+    if sec:
+        flags |= TRI_F_MROPE
     n_exp = int(getattr(cfg, "n_experts", 0) or 0)
     if n_exp > 0:
         flags |= TRI_F_MOE
@@ -134,7 +138,8 @@ def make_config(cfg) -> LayerConfig:
                        int(cfg.head_dim), int(getattr(cfg, "ffn_dim", 0) or 0), n_exp,
                        int(getattr(cfg, "top_k", 0) or 0),
                        int(getattr(cfg, "expert_ffn_dim", 0) or 0), float(cfg.rms_eps),
-                       float(cfg.rope_base), TRI_BF16, flags)
+                       float(cfg.rope_base), TRI_BF16, flags,
+                       (ctypes.c_int32 * 3)(*(sec or (0, 0, 0))))
 
 
 def _ptr(t) -> Optional[int]:
@@ -152,15 +157,21 @@ class DeviceBatch:
     """A ragged batch: device int32 arrays plus the host scalars that size launches."""
 
     def __init__(self, slot: Sequence[int], ctx_len: Sequence[int], q_len: Sequence[int],
-                 device="cuda"):
+                 device="cuda", pos=None):
+        """pos: the rotary positions (default ctx_len + i per token), or the
+        three planes [3, n_tokens] of a TRI_F_MROPE layer."""
         import numpy as np
         import torch
         slot = np.asarray(slot, dtype=np.int32)
         ctx = np.asarray(ctx_len, dtype=np.int32)
         q = np.asarray(q_len, dtype=np.int32)
         cu = np.concatenate([[0], np.cumsum(q)]).astype(np.int32)
-        pos = (np.concatenate([np.arange(c, c + n) for c, n in zip(ctx, q)]).astype(np.int32)
-               if len(q) else np.zeros(0, np.int32))
+        if pos is not None:
+            pos = np.ascontiguousarray(pos, dtype=np.int32).ravel()
+        elif len(q):
+            pos = np.concatenate([np.arange(c, c + n) for c, n in zip(ctx, q)]).astype(np.int32)
+        else:
+            pos = np.zeros(0, np.int32)
         self.n_seqs, self.n_tokens = int(len(q)), int(cu[-1])
         self.max_q_len = int(q.max()) if len(q) else 0
         self.max_ctx_len = int(ctx.max()) if len(ctx) else 0

@@ -17,6 +17,14 @@ using namespace tri;
 
 namespace {
 bool is_moe(const tri_layer_config* c) { return (c->flags & TRI_F_MOE) != 0; }
+
+// Rotary frequency sections: frequency i < s0 reads position plane 0, i < s01
+// plane 1, the rest plane 2 (one plane, s0 = s01 = D/2, without TRI_F_MROPE).
+RopeSections rope_sections(const tri_layer_config* c) {
+  const int half = c->head_dim / 2;
+  if (!(c->flags & TRI_F_MROPE)) return {half, half};
+  return {c->mrope_section[0], c->mrope_section[0] + c->mrope_section[1]};
+}
 }  // namespace
 
 tri_status tri::check_config(const tri_layer_config* c) {
@@ -31,6 +39,11 @@ tri_status tri::check_config(const tri_layer_config* c) {
   if (c->n_q_heads / c->n_kv_heads > 32) return TRI_ERR_UNSUPPORTED;
   if ((int64_t)c->n_q_heads * c->head_dim % 64 != 0) return TRI_ERR_UNSUPPORTED;
   if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return TRI_ERR_RANGE;
+  if (c->flags & TRI_F_MROPE) {
+    const int32_t* m = c->mrope_section;
+    if (m[0] < 0 || m[1] < 0 || m[2] < 0 || (int64_t)m[0] + m[1] + m[2] != c->head_dim / 2)
+      return TRI_ERR_SHAPE;
+  }
   if (is_moe(c)) {
     if (c->n_experts < 1 || c->n_experts > 256) return TRI_ERR_UNSUPPORTED;
     if (c->top_k < 1 || c->top_k > c->n_experts || c->top_k > 16) return TRI_ERR_SHAPE;
@@ -269,8 +282,8 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   {
     // token map + rotary table + pre-attention RMSNorm
     StageTimer t_(ST_PROLOGUE, s);
-    TRI_HIP(launch_prologue(bd, kv, D, cfg->rope_base, tok_slot, tok_row, rope, x_in,
-                            w->attn_norm, h, H, cfg->rms_eps, s));
+    TRI_HIP(launch_prologue(bd, kv, D, cfg->rope_base, rope_sections(cfg), tok_slot, tok_row,
+                            rope, x_in, w->attn_norm, h, H, cfg->rms_eps, s));
   }
   Epi e{};
   e.kind = EPI_QKV;

@@ -76,11 +76,18 @@ __device__ __forceinline__ float group_sum(float v, int half) {
   return v;
 }
 
+// Rotary frequency sections: frequency i < s0 takes position plane 0
+// (pos[t]), i < s01 plane 1 (pos[T + t]), the rest plane 2 (pos[2 T + t]).
+struct RopeSections {
+  int s0, s01;
+};
+
 // Layer prologue: per-token map (cache panel and row within it of every
-// token, -1 when out of range), the rotary table rope[t][i] = (cos, sin)(pos[t] *
-// base^(-2i/D)) (angle in double precision), and y = RMSNorm(x) * g.
-hipError_t launch_prologue(const BatchDev& b, const KvDev& kv, int head_dim,
-                           float rope_base, int32_t* tok_slot, int32_t* tok_row, float2* rope,
+// token, -1 when out of range), the rotary table rope[t][i] = (cos, sin)(p *
+// base^(-2i/D)) with p the token's position in frequency i's section (angle in
+// double precision), and y = RMSNorm(x) * g.
+hipError_t launch_prologue(const BatchDev& b, const KvDev& kv, int head_dim, float rope_base,
+                           RopeSections sec, int32_t* tok_slot, int32_t* tok_row, float2* rope,
                            const void* x, const void* g, void* y, int hidden, float eps,
                            hipStream_t s);
 

@@ -77,13 +77,14 @@ hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int
 //    group at once and counts them with ballots, so the map costs two memory
 //    round trips (ends, then the sequence's slot / prefix / start) however
 //    many sequences there are, instead of one per bisection step;
-//  * rotary table rope[t][i] = (cos, sin)(pos[t] * base^(-2i/D)), the angle
-//    formed in double precision, lane i < D/2;
+//  * rotary table rope[t][i] = (cos, sin)(p * base^(-2i/D)), the angle
+//    formed in double precision, lane i < D/2, p = pos[k T + t] for the
+//    section k of frequency i (k = 0 for a one-plane position array);
 //  * RMSNorm of x[t] into y[t] (as rmsnorm_kernel).
 constexpr int kMapChunks = 4;  // sequence ends loaded per lane and round trip
 
 __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, KvDev kv, int half,
-                                                       double base,
+                                                       double base, RopeSections sec,
                                                        int32_t* __restrict__ tok_slot,
                                                        int32_t* __restrict__ tok_row,
                                                        float2* __restrict__ rope,
@@ -106,7 +107,8 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, KvDev kv, int
       gv[c].u = ldg16(g + ch * 8);
     }
   }
-  const int pos = b.pos[t];
+  const int plane = lane < sec.s0 ? 0 : (lane < sec.s01 ? 1 : 2);
+  const int pos = b.pos[(int64_t)(lane < half ? plane : 0) * b.n_tokens + t];
   int sq = 0;
   for (int j0 = 0; j0 < b.n_seqs; j0 += 64 * kMapChunks) {
     int end[kMapChunks];
@@ -165,11 +167,12 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, KvDev kv, int
 }
 
 hipError_t launch_prologue(const BatchDev& b, const KvDev& kv, int head_dim, float rope_base,
-                           int32_t* tok_slot, int32_t* tok_row, float2* rope, const void* x,
-                           const void* g, void* y, int hidden, float eps, hipStream_t s) {
+                           RopeSections sec, int32_t* tok_slot, int32_t* tok_row, float2* rope,
+                           const void* x, const void* g, void* y, int hidden, float eps,
+                           hipStream_t s) {
   if (b.n_tokens == 0) return hipSuccess;
   prologue_kernel<<<cdiv(b.n_tokens, 4), 256, 0, s>>>(
-      b, kv, head_dim / 2, (double)rope_base, tok_slot, tok_row, rope,
+      b, kv, head_dim / 2, (double)rope_base, sec, tok_slot, tok_row, rope,
       (const bf16*)x, (const bf16*)g, (bf16*)y, hidden, eps);
   return hipGetLastError();
 }

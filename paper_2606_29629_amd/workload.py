@@ -38,7 +38,9 @@ def device_cache(k_bits: np.ndarray, v_bits: np.ndarray, device="cuda"):
 
 def device_batch(batch, device="cuda") -> DeviceBatch:
     """DeviceBatch from any object with slot / ctx_len / q_len arrays."""
-    return DeviceBatch(batch.slot, batch.ctx_len, batch.q_len, device=device)
+    pos3 = getattr(batch, "pos3", None)
+    return DeviceBatch(batch.slot, batch.ctx_len, batch.q_len, device=device,
+                       pos=None if pos3 is None else pos3)
 
 
 def paged_from_contiguous(k, v, block_size: int, seed: int = 0, spare_blocks: int = 3,

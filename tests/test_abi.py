@@ -143,6 +143,21 @@ def test_null_and_unsupported(lib):
     assert call(lib, b=bb) == T.TRI_ERR_NULL
 
 
+def test_mrope_config_checks(lib):
+    def mc(sec):
+        c = cfg(flags=T.TRI_F_MROPE)
+        c.mrope_section[:] = sec
+        return c
+    assert call(lib, c=mc((8, 12, 12)), ws_bytes=1024) == T.TRI_ERR_WORKSPACE   # valid: D/2 = 32
+    assert call(lib, c=mc((32, 0, 0)), ws_bytes=1024) == T.TRI_ERR_WORKSPACE
+    assert call(lib, c=mc((8, 12, 11))) == T.TRI_ERR_SHAPE                     # sums to 31
+    assert call(lib, c=mc((-1, 21, 12))) == T.TRI_ERR_SHAPE
+    assert call(lib, c=mc((0, 0, 0))) == T.TRI_ERR_SHAPE
+    c = cfg()
+    c.mrope_section[:] = (1, 1, 1)                                              # ignored without the flag
+    assert call(lib, c=c, ws_bytes=1024) == T.TRI_ERR_WORKSPACE
+
+
 def test_moe_config_checks(lib):
     moe = dict(flags=T.TRI_F_MOE, n_experts=8, top_k=2, expert_ffn_dim=128, ffn_dim=0)
     assert call(lib, c=cfg(**dict(moe, top_k=9))) == T.TRI_ERR_SHAPE

@@ -175,7 +175,10 @@ def stage_parity(cs, ws, rows, x_bits=None, label=""):
     hq = h @ w["w_qkv"].T
     if "b_qkv" in w:
         hq = hq + w["b_qkv"]
-    ang = OL.rope_angles(b.pos[rows], D, cfg.rope_base)
+    if getattr(cfg, "mrope_section", None):
+        ang = OL.rope_angles_sections(b.pos3[:, rows], D, cfg.rope_base, cfg.mrope_section)
+    else:
+        ang = OL.rope_angles(b.pos[rows], D, cfg.rope_base)
     q_pre = hq[:, :Hq * D].reshape(-1, Hq, D)
     k_pre = hq[:, Hq * D:(Hq + Hkv) * D].reshape(-1, Hkv, D)
     if getattr(cfg, "qk_norm", False):
