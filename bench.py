@@ -472,6 +472,111 @@ def run_secondary(args, tri, name):
     return res, phase
 
 
+def ai_sweep(args, tri):
+    """Arithmetic-intensity sweep under the GPU's own clock management (the
+    paper's frequency-locked roofline, Section III-B, without clock control):
+    the 7B dense layer at token counts from one decode token to a 16384-token
+    prefill.  Per point: the layer's time-weighted A.I. (Eq. 5, from the work
+    model and the measured stage times), achieved TFLOP/s and GB/s, and the
+    shader clock and socket power over a 2 s loop after 1 s at the same load.  Then the throughput
+    models are fitted to the points: Eq. 1 with eta the published peak flops
+    per clock and beta fitted, and Eq. 3 with omega (gamma = 0: the clock is
+    not set, so its exponent cannot be separated)."""
+    import torch
+    from paper_2606_29629_amd.workload import DeviceLayer, device_batch, device_cache, to_device_bf16
+    from synth import Batch, layer_7b, make_cache, make_weights, make_x
+    cfg = layer_7b()
+    wb = make_weights(cfg, 0)
+    dl = DeviceLayer(cfg, wb)
+    points = []  # (label, decode, batch)
+    for B in (1, 4, 16, 64, 128):
+        points.append((f"decode B={B}, ctx 512", True,
+                       Batch(np.arange(B, dtype=np.int32), np.full(B, 512, np.int32),
+                             np.ones(B, np.int32))))
+    for n, L in ((1, 256), (1, 1024), (2, 2048), (8, 2048)):
+        points.append((f"prefill {n} x {L}", False,
+                       Batch(np.arange(n, dtype=np.int32), np.zeros(n, np.int32),
+                             np.full(n, L, np.int32))))
+    eta = PEAK_BF16_TFLOPS * 1e12 / 2.4e9   # flops per clock (published peak at 2.4 GHz)
+    out = []
+    for label, decode, b in points:
+        n_slots = b.n_seqs
+        kb, vb = make_cache(cfg, n_slots, int((b.ctx_len + b.q_len).max()) + 64, 0)
+        cache = device_cache(kb, vb)
+        del kb, vb
+        db = device_batch(b)
+        x = to_device_bf16(make_x(cfg, b.n_tokens, 0, step=0 if decode else None))
+        fn = tri.layer_decode if decode else tri.layer_prefill
+        o = torch.empty_like(x)
+        ws = torch.empty(tri.workspace_size(dl.cfg, db), dtype=torch.uint8, device="cuda")
+        call = lambda: fn(dl.cfg, dl.w, cache, db, x, out=o, workspace=ws)
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        reps = 20 if decode else 5
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        tri.profile_enable(True)
+        for _ in range(reps):
+            call()
+        torch.cuda.synchronize()
+        praw = tri.profile_read(raw=True)
+        tri.profile_enable(False)
+        w = tri.layer_work(dl.cfg, decode, b.q_len, b.ctx_len)
+        ai = tri.phase_intensity(w, praw)
+        flops = sum(w.flops[i] for i in range(w.n_stages))
+        byts = sum(w.bytes[i] for i in range(w.n_stages))
+        energy_loop(call, min_s=1.0)            # let clock and power settle at this load
+        en = energy_loop(call, min_s=2.0)
+        tel = en["telemetry"] if en else {}
+        pt = {"point": label, "tokens": b.n_tokens, "ms_per_call": ms, "ai_time_weighted": ai,
+              "ai_aggregate": flops / byts, "tflops": flops / (ms / 1e3) / 1e12,
+              "gbs": byts / (ms / 1e3) / 1e9, "gfxclk_mhz": tel.get("gfxclk_mhz"),
+              "socket_power_w": tel.get("socket_power_w"),
+              "board_power_w": en["avg_power_w"] if en else None,
+              "joules_per_token": en["joules_per_call"] / b.n_tokens if en else None}
+        out.append(pt)
+        print(json.dumps({"ai_sweep_point": pt}), file=sys.stderr, flush=True)
+        del cache, db, x, o, ws
+        torch.cuda.empty_cache()
+    # Fits.  Eq. 1: beta from the points whose Eq. 1 bound is the memory term.
+    fit = {"eta_flop_per_clock": eta}
+    have_f = [p for p in out if p["gfxclk_mhz"]]
+    if have_f:
+        ratios = sorted(p["tflops"] * 1e12 / p["ai_time_weighted"] for p in have_f
+                        if p["ai_time_weighted"] * 1 < 0.25 * eta * p["gfxclk_mhz"] * 1e6 /
+                        (PEAK_HBM_GBS * 1e9))
+        beta = ratios[len(ratios) // 2] if ratios else None
+        fit["eq1_beta_gbs"] = beta / 1e9 if beta else None
+        # Eq. 3 with gamma = 0: eta f A.I. / (A.I. + omega), fitted on the points
+        # past the ridge at their own clock (eta f / peak HBM bandwidth).
+        num = den = 0.0
+        for p in have_f:
+            f = p["gfxclk_mhz"] * 1e6
+            th = p["tflops"] * 1e12
+            if p["ai_time_weighted"] >= eta * f / (PEAK_HBM_GBS * 1e9):
+                c = eta * f * p["ai_time_weighted"] / th - p["ai_time_weighted"]
+                num += c
+                den += 1
+        fit["eq3_omega_flop_per_byte"] = num / den if den else None
+        for p in have_f:
+            f = p["gfxclk_mhz"] * 1e6
+            a = p["ai_time_weighted"]
+            p["eq1_tflops"] = min(eta * f, (beta or 0) * a) / 1e12
+            if fit["eq3_omega_flop_per_byte"] is not None:
+                p["eq3_tflops"] = min(eta * f * a / (a + fit["eq3_omega_flop_per_byte"]),
+                                      (beta or 0) * a) / 1e12
+    print(json.dumps({"ai_sweep": out, "fit": fit, "ridge_flop_per_byte":
+                      PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3,
+                      "layer": "7B dense (H 3584, 28/4 heads, D 128, F 18944), bf16"}))
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -484,6 +589,9 @@ def main(argv=None):
                     help="skip the MoE prefill / MoE decode / mixed-step context numbers")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 3 times (HBM counter calibration)")
+    ap.add_argument("--ai-sweep", action="store_true",
+                    help="only run the arithmetic-intensity sweep of the 7B layer (clock, power, "
+                         "Eq. 1 / Eq. 3 fits) and print it as one JSON line")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); "
@@ -502,6 +610,8 @@ def main(argv=None):
         return 0
     import paper_2606_29629_amd as tri
     from synth import make_cache, make_weights, make_x, workload
+    if args.ai_sweep:
+        return ai_sweep(args, tri)
 
     wl = workload("dense_prefill")
     wb = make_weights(wl.cfg, wl.seed)
