@@ -11,8 +11,9 @@ region.  One JSON line is printed.  The decode workload (batch 64, KV 4096,
 32 steps) is timed as a secondary result in the same line.
 
 Phases: for each workload (dense prefill, dense decode, MoE prefill, MoE
-decode, mixed, and the dense and MoE prefills with the per-head q/k RMSNorm
-of the Qwen3-family attention block) the line carries the per-stage arithmetic intensity (the
+decode, mixed, the dense and MoE prefills with the per-head q/k RMSNorm
+of the Qwen3-family attention block, and the dense prefill and decode with
+the q/k/v bias of the Qwen2 family) the line carries the per-stage arithmetic intensity (the
 library's work model: algorithmic flops over compulsory HBM bytes), the
 phase's time-weighted intensity of Eq. 5 (weights: the stage times measured
 in the profiled repetition), achieved TFLOP/s and GB/s per stage, and the
@@ -661,7 +662,8 @@ def main(argv=None):
         res["decode"], phases["dense_decode"] = run_decode(args, tri)
     if not args.no_secondary:
         res["secondary"] = []
-        for n in ("moe_prefill", "moe_decode", "mixed", "dense_prefill_qkn", "moe_prefill_qkn"):
+        for n in ("moe_prefill", "moe_decode", "mixed", "dense_prefill_qkn", "moe_prefill_qkn",
+                  "dense_prefill_bias", "dense_decode_bias"):
             r, phases[n] = run_secondary(args, tri, n)
             res["secondary"].append(r)
     res["phases"] = phases

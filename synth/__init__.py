@@ -275,6 +275,12 @@ def workload(name: str, seed: int = 0) -> Workload:
                         Batch(np.arange(33, dtype=np.int32), np.concatenate([_ints(6144), lens]),
                               np.concatenate([_ints(512), np.ones(32, np.int32)])),
                         cache_prefilled=True, seed=seed)
+    if name in ("dense_prefill_bias", "dense_decode_bias"):
+        # the 7B workloads with the q/k/v bias of the Qwen2 family (seeded, N(0, 0.2))
+        base = workload(name[:-5], seed)
+        return dataclasses.replace(
+            base, name=name, cfg=dataclasses.replace(base.cfg, qkv_bias=True),
+            description=base.description + ", q/k/v bias")
     if name in ("dense_prefill_qkn", "moe_prefill_qkn"):
         # the same prefills with the per-head q/k RMSNorm of the Qwen3-family
         # attention block (the MoE one then has the Qwen3-30B-A3B layer shape)
@@ -286,7 +292,7 @@ def workload(name: str, seed: int = 0) -> Workload:
 
 
 WORKLOADS = ("tiny", "dense_prefill", "dense_decode", "moe_prefill", "moe_decode", "mixed",
-             "dense_prefill_qkn", "moe_prefill_qkn")
+             "dense_prefill_qkn", "moe_prefill_qkn", "dense_prefill_bias", "dense_decode_bias")
 
 
 def make_x(cfg: LayerConfig, n_tokens: int, seed: int = 0, step: Optional[int] = None) -> np.ndarray:
