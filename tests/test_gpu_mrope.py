@@ -65,3 +65,43 @@ def test_mrope_7b_shape_prefill_and_decode():
         [("text", 1)],
         [("text", 3), ("video", 4, 3, 5)]])
     run_and_check(cfg, batch, 4, 640, "7B mrope", seed=5, decode_steps=2)
+
+
+def test_moe_layer_with_qk_norm_and_sections():
+    """The Qwen3-Omni Thinker's kind of layer: MoE FFN, per-head q/k RMSNorm
+    and multi-section positions together.  q and the written cache rows
+    against the reference from the GPU's own normalised input, the MoE stages
+    on identical inputs, then the end-to-end tolerance with the GPU's routes."""
+    from oracle import layer as OL
+    from paper_2606_29629_amd import _lib as T
+    from test_gpu_layer import assert_rounded, ws_view
+    from test_gpu_moe import TINY_MOE, MoECase, moe_stage_parity, routes_agree
+    cfg = dataclasses.replace(TINY_MOE, qk_norm=True, mrope_section=(10, 11, 11))
+    batch = mrope_batch([1, 0, 2], [0, 9, 30], [
+        [("text", 5), ("image", 4, 6), ("text", 7)],
+        [("video", 2, 3, 3)],
+        [("text", 1)]])
+    c = MoECase(cfg, batch, 3, 64, seed=8)
+    Tn, H, D, Hq, Hkv = batch.n_tokens, cfg.hidden, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
+    m = T.workspace_layout(c.dl.cfg, c.db)
+    w = {k: f64(v) for k, v in c.wb.items()}
+    h = to_host_f64(ws_view(c.ws, m.h, (Tn, H)))
+    q = to_host_f64(ws_view(c.ws, m.q, (Tn, Hq, D)))
+    hq = h @ w["w_qkv"].T
+    ang = OL.rope_angles_sections(batch.pos3, D, cfg.rope_base, cfg.mrope_section)
+    q_ref = OL.rope(OL.rmsnorm(hq[:, :Hq * D].reshape(Tn, Hq, D), w["q_norm"], cfg.rms_eps), ang)
+    k_ref = OL.rope(OL.rmsnorm(hq[:, Hq * D:(Hq + Hkv) * D].reshape(Tn, Hkv, D), w["k_norm"],
+                               cfg.rms_eps), ang)
+    assert_rounded(q, q_ref, "moe q")
+    k_cache = c.cache[0]
+    kr = np.concatenate([to_host_f64(k_cache[s, :, ct:ct + ql]).transpose(1, 0, 2)
+                         for s, ct, ql in zip(batch.slot, batch.ctx_len, batch.q_len)])
+    assert_rounded(kr, k_ref, "moe k cache rows")
+    moe_stage_parity(c, np.arange(Tn))
+    args = (cfg, w, f64(c.kb), f64(c.vb), batch, f64(c.xb))
+    ref = oracle.layer_forward(*args, storage="bf16")
+    gi = c.idx.cpu().numpy()
+    routes_agree(gi, ref["logits"], cfg.top_k, 2e-2)
+    forced = oracle.layer_forward(*args, storage="bf16", forced_routes=gi)
+    exact = oracle.layer_forward(*args, forced_routes=gi)
+    assert_close(to_host_f64(c.out), forced["out"], "moe qk-norm sections out", exact=exact["out"])
