@@ -209,7 +209,7 @@ def phase_report(tri, cfg, calls, decode, prof, reps, energy=None, tokens_per_ca
     return out
 
 
-def cpu_baseline(wl, wb, kb, vb, xb, budget_s=20.0):
+def cpu_baseline(wl, wb, kb, vb, xb, budget_s=12.0):
     """The CPU oracle (plain fp32 NumPy) on a bounded sample: whole sequences of
     the same workload, repeated until the time budget is used."""
     import oracle
@@ -230,7 +230,7 @@ def cpu_baseline(wl, wb, kb, vb, xb, budget_s=20.0):
         oracle.layer_forward(wl.cfg, w, kb, vb, sub, x, dtype=np.float32)
         n_tok += q
         reps += 1
-        if time.perf_counter() - t0 > budget_s / 2 or reps >= 4:
+        if time.perf_counter() - t0 >= budget_s:
             break
     dt = time.perf_counter() - t0
     return {"value": n_tok / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
