@@ -203,3 +203,21 @@ def test_moe_decode_full_size_sampled():
     forced = oracle.layer_forward(*args, storage="bf16", forced_routes=gi)
     exact = oracle.layer_forward(*args, forced_routes=gi)
     assert_close(to_host_f64(c.out)[pick], forced["out"], "MoE decode rows", exact=exact["out"])
+
+
+@pytest.mark.parametrize("n_tok", [600, 1000], ids=["128-row tiles", "256-row tiles"])
+def test_moe_grouped_tile_sizes(n_tok):
+    """The grouped expert GEMMs pick their tile rows from the mean rows per
+    expert: 1200 routed rows over 8 experts take 128-row tiles, 2000 take
+    256-row tiles (ragged: most experts end in a partial tile)."""
+    batch = B([0, 1], [0, 5], [n_tok - 100, 100])
+    c = MoECase(TINY_MOE, batch, 2, 1024, seed=9)
+    rows = np.array([0, 1, 255, 256, 257, n_tok - 101, n_tok - 100, n_tok - 1])
+    moe_stage_parity(c, rows)
+    w64 = {k: f64(v) for k, v in c.wb.items()}
+    args = (c.cfg, w64, f64(c.kb), f64(c.vb), batch, f64(c.xb))
+    gi = c.idx.cpu().numpy()
+    forced = oracle.layer_forward(*args, rows=rows, storage="bf16", forced_routes=gi)
+    exact = oracle.layer_forward(*args, rows=rows, forced_routes=gi)
+    assert_close(to_host_f64(c.out)[rows], forced["out"], f"MoE {n_tok} tokens rows",
+                 exact=exact["out"])
