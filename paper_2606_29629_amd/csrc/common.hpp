@@ -44,6 +44,17 @@ __device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t r, void
 }
 __device__ __forceinline__ void stg16(void* p, u32x4 v) { *(u32x4*)p = v; }
 
+// Sum over aligned groups of `half` lanes (32 or 64).
+__device__ __forceinline__ float group_sum(float v, int half) {
+  v += __shfl_xor(v, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  v += __shfl_xor(v, 4, 64);
+  v += __shfl_xor(v, 8, 64);
+  v += __shfl_xor(v, 16, 64);
+  if (half == 64) v += __shfl_xor(v, 32, 64);
+  return v;
+}
+
 // Wave-level reductions (wave64) through cross-lane shuffles.
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -65,17 +65,6 @@ struct Epi {
   int n_q_heads, n_kv_heads, head_dim, max_seq;
 };
 
-// Sum over aligned groups of `half` lanes (32 or 64).
-__device__ __forceinline__ float group_sum(float v, int half) {
-  v += __shfl_xor(v, 1, 64);
-  v += __shfl_xor(v, 2, 64);
-  v += __shfl_xor(v, 4, 64);
-  v += __shfl_xor(v, 8, 64);
-  v += __shfl_xor(v, 16, 64);
-  if (half == 64) v += __shfl_xor(v, 32, 64);
-  return v;
-}
-
 // Rotary frequency sections: frequency i < s0 takes position plane 0
 // (pos[t]), i < s01 plane 1 (pos[T + t]), the rest plane 2 (pos[2 T + t]).
 struct RopeSections {
