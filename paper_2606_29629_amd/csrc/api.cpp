@@ -85,6 +85,9 @@ size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
   const int T = b->n_tokens, H = c->hidden, D = c->head_dim;
   const int Nqkv = (c->n_q_heads + 2 * c->n_kv_heads) * D;
   size_t p = attn_decode_partial_bytes(T, c->n_q_heads, D, b->max_ctx_len + 1);
+  const size_t fa =
+      attn_prefill_partial_bytes(b->n_seqs, T, b->max_q_len, b->max_ctx_len, c->n_q_heads, D);
+  if (fa > p) p = fa;
   if (T > 0) {
     // Skinny-path partials; a larger batch reserves them for the largest
     // skinny batch, so that the size never shrinks as n_tokens grows.
@@ -307,7 +310,7 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   }
   if (!decode && b->max_q_len > 1) {
     StageTimer t_(ST_ATTN_PREFILL, s);
-    TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, kv, Hq, Hkv, D, 0, s));
+    TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, kv, Hq, Hkv, D, 0, part, s));
   }
   {
     StageTimer t_(ST_ATTN_DECODE, s);

@@ -37,12 +37,18 @@ struct FaSmem {
   bf16 v[2][kFaBK * D];  // [key][d], chunks swizzled by kv_chunk
 };
 
-template <int D, bool PAGED>
+// SPLIT: the key tiles of a query tile are dealt to `nsplit` workgroups
+// (blockIdx.z = sequence * nsplit + split), each writing its unnormalised
+// output with its running max (log2 units) and sum to `part`
+// [nsplit][n_tokens][Hq][D + 2]; attn_prefill_combine_kernel merges them.
+// Used when the batch has too few query tiles to fill the GPU (a chunk over
+// a long cached prefix).
+template <int D, bool PAGED, bool SPLIT>
 __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
     bf16* __restrict__ O, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ ctx_len,
     const int32_t* __restrict__ slot, KvDev kv, int Hq, int Hkv, float scale_log2e,
-    int include_single, int n_tokens) {
+    int include_single, int n_tokens, int nsplit, float* __restrict__ part) {
   constexpr int DC = D / 8;                     // 16-byte chunks per row
   constexpr int ROWS_PER_KB = 64 / DC;          // tile rows filled by one 1 KB wave load
   constexpr int BLK = kFaBK / ROWS_PER_KB / 4;  // 1 KB loads per wave per operand and tile
@@ -51,7 +57,8 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   extern __shared__ __align__(16) char smem_raw[];
   FaSmem<D>& sm = *reinterpret_cast<FaSmem<D>*>(smem_raw);
 
-  const int s = blockIdx.z, qh = blockIdx.y;
+  const int s = SPLIT ? (int)blockIdx.z / nsplit : (int)blockIdx.z, qh = blockIdx.y;
+  const int sp = SPLIT ? (int)blockIdx.z - s * nsplit : 0;
   // The sequence's scalars in one round trip (s < n_seqs by the grid).
   const int q0 = cu_q[s], n = cu_q[s + 1] - q0, c = ctx_len[s], sl = slot[s];
   if (n <= 0 || (n == 1 && !include_single) || q0 < 0 || q0 + n > n_tokens) return;
@@ -65,6 +72,10 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   const int lr = lane & 31, lg = lane >> 5;
   const int kv_len = c + min(n, (qt + 1) * kFaBQ);
   const int nkt = cdiv(kv_len, kFaBK);
+  // This workgroup's key tiles [kt_lo, kt_hi): all of them, or split sp's share.
+  const int tps = SPLIT ? cdiv(nkt, nsplit) : nkt;
+  const int kt_lo = sp * tps, kt_hi = min(nkt, kt_lo + tps);
+  if (kt_lo >= kt_hi) return;  // an empty split (the combine skips it)
 
   // Tile kt's rows live in one cache panel (the slot, or a pool block of a
   // multiple of 64 rows); the block ids come from the table one tile ahead.
@@ -129,13 +140,13 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   float m_run = -INFINITY, l_run = 0.f;  // running max in raw score units
   const float slack_raw = kSoftmaxSlack / scale_log2e;
 
-  gload(0, 0, panel_of(0));
-  int next_panel = panel_of(1);
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int buf = kt & 1;
+  gload(kt_lo, 0, panel_of(kt_lo));
+  int next_panel = panel_of(kt_lo + 1);
+  for (int kt = kt_lo; kt < kt_hi; ++kt) {
+    const int buf = (kt - kt_lo) & 1;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();  // tile kt is in LDS; every wave is done with tile kt - 1
-    if (kt + 1 < nkt) gload(kt + 1, buf ^ 1, next_panel);
+    if (kt + 1 < kt_hi) gload(kt + 1, buf ^ 1, next_panel);
     next_panel = panel_of(kt + 2);
     const int key0 = kt * kFaBK;
     if (key0 > wave_qmin + 31) continue;  // no key of this tile is visible to this wave
@@ -198,13 +209,17 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     const bool raise = mt > m_run + slack_raw;
     if (__builtin_amdgcn_ballot_w64(raise)) {
       const float m_new = raise ? mt : m_run;
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2e);
+      // (SPLIT: a lane that still has no finite max must not form -inf - -inf)
+      const float alpha = (SPLIT && !raise) ? 1.f
+                                            : __builtin_amdgcn_exp2f((m_run - m_new) * scale_log2e);
       m_run = m_new;
       l_run *= alpha;
 #pragma unroll
       for (int b = 0; b < DB; ++b) oacc[b] *= alpha;
     }
-    const float mc = m_run * scale_log2e;
+    // (SPLIT: a lane whose query precedes every key seen so far in this
+    // split still has no finite max; its weights are exp2(-inf) = 0.)
+    const float mc = (SPLIT && m_run == -INFINITY) ? 0.f : m_run * scale_log2e;
     bf16x8 pf[4], pl[4];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -237,6 +252,20 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (qi >= n) return;
+  if constexpr (SPLIT) {
+    float* pp = part + (((int64_t)sp * n_tokens + q0 + qi) * Hq + qh) * (D + 2);
+#pragma unroll
+    for (int b = 0; b < DB; ++b)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4)
+        *(f32x4*)(pp + 32 * b + 8 * r4 + 4 * lg) =
+            f32x4{oacc[b][4 * r4], oacc[b][4 * r4 + 1], oacc[b][4 * r4 + 2], oacc[b][4 * r4 + 3]};
+    if (lg == 0) {
+      pp[D] = m_run == -INFINITY ? -INFINITY : m_run * scale_log2e;
+      pp[D + 1] = l_tot;
+    }
+    return;
+  }
   const float inv = 1.0f / l_tot;
   bf16* op = O + ((int64_t)(q0 + qi) * Hq + qh) * D;
   // oacc[b] element r: d = 32b + 8(r/4) + 4lg + r%4  -> 4 consecutive d per (r/4).
@@ -251,36 +280,117 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     }
 }
 
-template <int D, bool PAGED>
+// Merge of the split partials of one (query tile, head): per query and
+// head, the splits' (max, sum, unnormalised output) folded in split order.
+// Same grid as the attention kernel without the split dimension; each thread
+// takes four consecutive d of one query per pass.
+template <int D>
+__global__ __launch_bounds__(256) void attn_prefill_combine_kernel(
+    const float* __restrict__ part, bf16* __restrict__ O, const int32_t* __restrict__ cu_q,
+    const int32_t* __restrict__ ctx_len, const int32_t* __restrict__ slot, KvDev kv, int Hq,
+    int include_single, int n_tokens, int nsplit) {
+  const int s = blockIdx.z, qh = blockIdx.y;
+  const int q0 = cu_q[s], n = cu_q[s + 1] - q0, c = ctx_len[s], sl = slot[s];
+  if (n <= 0 || (n == 1 && !include_single) || q0 < 0 || q0 + n > n_tokens) return;
+  const int qt = (int)gridDim.x - 1 - (int)blockIdx.x;
+  if (qt * kFaBQ >= n) return;
+  if (sl < 0 || sl >= kv.n_slots || c < 0 || c + n > kv.max_seq) return;
+  const int nkt = cdiv(c + min(n, (qt + 1) * kFaBQ), kFaBK);
+  const int tps = cdiv(nkt, nsplit);
+  const int ns = cdiv(nkt, tps);  // non-empty splits
+  constexpr int TPQ = D / 4;      // threads per query
+  const int d = 4 * ((int)threadIdx.x % TPQ);
+  const int64_t plane = (int64_t)n_tokens * Hq * (D + 2);
+  for (int qi = qt * kFaBQ + (int)threadIdx.x / TPQ; qi < min(n, (qt + 1) * kFaBQ);
+       qi += 256 / TPQ) {
+    const float* pp = part + ((int64_t)(q0 + qi) * Hq + qh) * (D + 2);
+    float M = -INFINITY, L = 0.f;
+    f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < ns; ++j) {
+      const float* pj = pp + j * plane;
+      const float m = pj[D], l = pj[D + 1];
+      const f32x4 a = *(const f32x4*)(pj + d);
+      if (m == -INFINITY) continue;  // no key of this split is visible to this query
+      const float Mn = fmaxf(M, m);
+      const float sc = exp2f(M - Mn), w = exp2f(m - Mn);
+      L = L * sc + l * w;
+      o = o * sc + a * w;
+      M = Mn;
+    }
+    const float inv = 1.0f / L;
+    bf16x4 o4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o4[e] = f2bf(o[e] * inv);
+    *(bf16x4*)(O + ((int64_t)(q0 + qi) * Hq + qh) * D + d) = o4;
+  }
+}
+
+// Key-range splits for a batch of n_tokens tokens: 1 when the query tiles
+// fill the GPU (two workgroups per CU); otherwise doubled (up to 8) until
+// they do, while every split keeps >= 8 key tiles of the longest key range.
+int attn_prefill_splits(int n_seqs, int n_tokens, int max_q_len, int max_ctx_len,
+                        int n_q_heads) {
+  const int64_t wgs = (int64_t)cdiv(n_tokens, kFaBQ) * n_q_heads;  // query tiles of the batch
+  const int max_tiles = cdiv(max_ctx_len + max_q_len, kFaBK);
+  int sp = 1;
+  while (sp < 8 && wgs * sp < 2 * cu_count() && max_tiles >= 16 * sp &&
+         (int64_t)n_seqs * sp * 2 <= 65535)  // the grid's z extent
+    sp *= 2;
+  return sp;
+}
+
+size_t attn_prefill_partial_bytes(int n_seqs, int n_tokens, int max_q_len, int max_ctx_len,
+                                  int n_q_heads, int head_dim) {
+  const int sp = attn_prefill_splits(n_seqs, n_tokens, max_q_len, max_ctx_len, n_q_heads);
+  return sp > 1 ? (size_t)sp * n_tokens * n_q_heads * (head_dim + 2) * sizeof(float) : 0;
+}
+
+template <int D, bool PAGED, bool SPLIT>
 static hipError_t run_fa(const void* q, const void* kc, const void* vc, void* out,
                          const BatchDev& b, const KvDev& kv, int Hq, int Hkv,
-                         int include_single, hipStream_t s) {
+                         int include_single, int nsplit, float* part, hipStream_t s) {
   const size_t smem = sizeof(FaSmem<D>);
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_prefill_kernel<D, PAGED>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_prefill_kernel<D, PAGED, SPLIT>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
     attr = true;
   }
-  dim3 grid(cdiv(b.max_q_len, kFaBQ), Hq, b.n_seqs);
+  dim3 grid(cdiv(b.max_q_len, kFaBQ), Hq, b.n_seqs * nsplit);
   const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  attn_prefill_kernel<D, PAGED><<<grid, 256, smem, s>>>((const bf16*)q, (const bf16*)kc, (const bf16*)vc,
-                                                 (bf16*)out, b.cu_q, b.ctx_len, b.slot, kv, Hq,
-                                                 Hkv, scale_log2e, include_single, b.n_tokens);
+  attn_prefill_kernel<D, PAGED, SPLIT><<<grid, 256, smem, s>>>(
+      (const bf16*)q, (const bf16*)kc, (const bf16*)vc, (bf16*)out, b.cu_q, b.ctx_len, b.slot, kv,
+      Hq, Hkv, scale_log2e, include_single, b.n_tokens, nsplit, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !SPLIT) return e;
+  dim3 cgrid(cdiv(b.max_q_len, kFaBQ), Hq, b.n_seqs);
+  attn_prefill_combine_kernel<D><<<cgrid, 256, 0, s>>>(part, (bf16*)out, b.cu_q, b.ctx_len, b.slot,
+                                                       kv, Hq, include_single, b.n_tokens, nsplit);
   return hipGetLastError();
+}
+
+template <int D, bool PAGED>
+static hipError_t run_fa_any(const void* q, const void* kc, const void* vc, void* out,
+                             const BatchDev& b, const KvDev& kv, int Hq, int Hkv,
+                             int include_single, float* part, hipStream_t s) {
+  const int sp = attn_prefill_splits(b.n_seqs, b.n_tokens, b.max_q_len, b.max_ctx_len, Hq);
+  if (sp > 1)
+    return run_fa<D, PAGED, true>(q, kc, vc, out, b, kv, Hq, Hkv, include_single, sp, part, s);
+  return run_fa<D, PAGED, false>(q, kc, vc, out, b, kv, Hq, Hkv, include_single, 1, nullptr, s);
 }
 
 hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, void* out,
                                const BatchDev& b, const KvDev& kv, int n_q_heads,
-                               int n_kv_heads, int head_dim, int include_single, hipStream_t s) {
+                               int n_kv_heads, int head_dim, int include_single, float* part,
+                               hipStream_t s) {
   if (b.n_seqs == 0 || b.max_q_len == 0) return hipSuccess;
   const bool paged = kv.table != nullptr;
   if (head_dim == 128)
-    return paged ? run_fa<128, true>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, s)
-                 : run_fa<128, false>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, s);
-  return paged ? run_fa<64, true>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, s)
-               : run_fa<64, false>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, s);
+    return paged ? run_fa_any<128, true>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, part, s)
+                 : run_fa_any<128, false>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, part, s);
+  return paged ? run_fa_any<64, true>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, part, s)
+               : run_fa_any<64, false>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, part, s);
 }
 
 }  // namespace tri

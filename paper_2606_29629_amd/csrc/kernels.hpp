@@ -119,10 +119,17 @@ hipError_t launch_skinny(const void* A, int lda, const void* B, int ldb, int M, 
                          const Epi& epi, float* part, hipStream_t s);
 
 // Causal flash attention for sequences with q_len > 1 (or all when
-// include_single != 0).
+// include_single != 0).  A batch with few query tiles but long key ranges
+// splits each query tile's keys over attn_prefill_splits() workgroups, whose
+// fp32 partials (attn_prefill_partial_bytes, in `part`) a second kernel merges.
+int attn_prefill_splits(int n_seqs, int n_tokens, int max_q_len, int max_ctx_len,
+                        int n_q_heads);
+size_t attn_prefill_partial_bytes(int n_seqs, int n_tokens, int max_q_len, int max_ctx_len,
+                                  int n_q_heads, int head_dim);
 hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, void* out,
                                const BatchDev& b, const KvDev& kv, int n_q_heads,
-                               int n_kv_heads, int head_dim, int include_single, hipStream_t s);
+                               int n_kv_heads, int head_dim, int include_single, float* part,
+                               hipStream_t s);
 
 // Split-KV attention for sequences with q_len == 1, plus the combine.
 // Keys per split (a multiple of 32); max_split > 0 caps it.
