@@ -22,6 +22,8 @@
 // 16 significant bits.  Softmax in the log2 domain: one FMA (scale and max)
 // and one v_exp_f32 per score; the running max is raised lazily (only past a
 // slack of 8), so the accumulators are rescaled on few tiles.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -30,12 +32,11 @@ namespace tri {
 constexpr int kFaBQ = 128;  // queries per workgroup
 constexpr int kFaBK = 64;   // keys per tile
 
-// K/V tile chunk swizzle: kv_chunk (common.hpp).
-template <int D>
-struct FaSmem {
-  bf16 k[2][kFaBK * D];  // [key][d], chunks swizzled by kv_chunk
-  bf16 v[2][kFaBK * D];  // [key][d], chunks swizzled by kv_chunk
-};
+// K/V tiles: four separate LDS arrays (K and V of buffers 0 and 1), [key][d]
+// with chunks swizzled by kv_chunk (common.hpp).  Separate arrays, and a loop
+// body instantiated per buffer, let the compiler see that reading one buffer
+// never aliases the direct-to-LDS fill of the other, so it waits for no fill
+// before a read.
 
 // SPLIT: the key tiles of a query tile are dealt to `nsplit` workgroups
 // (blockIdx.z = sequence * nsplit + split), each writing its unnormalised
@@ -54,8 +55,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   constexpr int BLK = kFaBK / ROWS_PER_KB / 4;  // 1 KB loads per wave per operand and tile
   constexpr int DS = D / 16;                    // MFMA k-steps over d
   constexpr int DB = D / 32;                    // 32-row d blocks of O^T
-  extern __shared__ __align__(16) char smem_raw[];
-  FaSmem<D>& sm = *reinterpret_cast<FaSmem<D>*>(smem_raw);
+  __shared__ __align__(16) bf16 sk0[kFaBK * D], sk1[kFaBK * D], sv0[kFaBK * D], sv1[kFaBK * D];
 
   const int s = SPLIT ? (int)blockIdx.z / nsplit : (int)blockIdx.z, qh = blockIdx.y;
   const int sp = SPLIT ? (int)blockIdx.z - s * nsplit : 0;
@@ -105,16 +105,20 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     const int row = (wave + 4 * j) * ROWS_PER_KB + lane / DC;
     ld_off[j] = (uint32_t)((row * D + kv_chunk<D>(lane % DC, row) * 8) * 2);
   }
-  auto gload = [&](int kt, int buf, int panel) {
+  auto gload = [&](int kt, auto buf, int panel) {
+    bf16* kd = buf ? sk1 : sk0;
+    bf16* vd = buf ? sv1 : sv0;
     const __amdgpu_buffer_rsrc_t rk = tile_rsrc(Kc, kt, panel);
     const __amdgpu_buffer_rsrc_t rv = tile_rsrc(Vc, kt, panel);
 #pragma unroll
     for (int j = 0; j < BLK; ++j) {
       const int blk = (wave + 4 * j) * ROWS_PER_KB * D;
-      buffer_load_lds16(rk, &sm.k[buf][blk], ld_off[j], 0);
-      buffer_load_lds16(rv, &sm.v[buf][blk], ld_off[j], 0);
+      buffer_load_lds16(rk, kd + blk, ld_off[j], 0);
+      buffer_load_lds16(rv, vd + blk, ld_off[j], 0);
     }
   };
+  using Buf0 = std::integral_constant<int, 0>;
+  using Buf1 = std::integral_constant<int, 1>;
 
   // This lane's query (clamped to a valid row; rows >= n are not written).
   const int qi = qt * kFaBQ + wave * 32 + lr;
@@ -140,42 +144,47 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   float m_run = -INFINITY, l_run = 0.f;  // running max in raw score units
   const float slack_raw = kSoftmaxSlack / scale_log2e;
 
-  gload(kt_lo, 0, panel_of(kt_lo));
+  gload(kt_lo, Buf0{}, panel_of(kt_lo));
   int next_panel = panel_of(kt_lo + 1);
-  for (int kt = kt_lo; kt < kt_hi; ++kt) {
-    const int buf = (kt - kt_lo) & 1;
+  // Key tile kt from buffer `buf` (tiles alternate between the buffers,
+  // the first in buffer 0).
+  auto step = [&](int kt, auto buf) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();  // tile kt is in LDS; every wave is done with tile kt - 1
-    if (kt + 1 < kt_hi) gload(kt + 1, buf ^ 1, next_panel);
+    if (kt + 1 < kt_hi) gload(kt + 1, std::integral_constant<int, 1 - buf>{}, next_panel);
     next_panel = panel_of(kt + 2);
+    const bf16* kb_lds = buf ? sk1 : sk0;
+    const bf16* vb = buf ? sv1 : sv0;
     const int key0 = kt * kFaBK;
-    if (key0 > wave_qmin + 31) continue;  // no key of this tile is visible to this wave
+    if (key0 > wave_qmin + 31) return;  // no key of this tile is visible to this wave
     // S^T = K Q^T for two 32-key blocks: the two MFMA chains interleaved,
-    // K fragments read one k-step ahead.
+    // K fragments read KLA k-steps ahead (a ring of KLA + 1), so no MFMA
+    // waits on the LDS read issued just before it.
+    constexpr int KLA = 3;
     f32x16 sacc[2] = {f32x16{0.f}, f32x16{0.f}};
-    bf16x8 kf[2][2];
+    bf16x8 kf[KLA + 1][2];
     auto kread = [&](int t, bf16x8 (&dst)[2]) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const int key = kb * 32 + lr;
-        dst[kb] = *(const bf16x8*)&sm.k[buf][key * D + kv_chunk<D>(2 * t + lg, key) * 8];
+        dst[kb] = *(const bf16x8*)&kb_lds[key * D + kv_chunk<D>(2 * t + lg, key) * 8];
       }
     };
-    kread(0, kf[0]);
-    // Matrix phases run at raised wave priority, so that the other wave on
-    // this SIMD fills the gaps with its softmax instead of competing.
-    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int t = 0; t < KLA && t < DS; ++t) kread(t, kf[t]);
+    // (the issue order is fenced: left alone, the compiler moves each read
+    // next to its MFMA to save registers, and every MFMA waits on LDS)
 #pragma unroll
     for (int t = 0; t < DS; ++t) {
-      if (t + 1 < DS) kread(t + 1, kf[(t + 1) & 1]);
+      if (t + KLA < DS) kread(t + KLA, kf[(t + KLA) % (KLA + 1)]);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t & 1][kb], qf[t], sacc[kb], 0, 0, 0);
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t % (KLA + 1)][kb], qf[t], sacc[kb],
+                                                           0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_s_setprio(0);
     // V^T fragments of a 16-key group (two transposing reads per d block),
     // the first group issued before the softmax.
-    const bf16* vb = sm.v[buf];
     union VFrag { s16x4 s[2]; bf16x8 h; };
     VFrag vf[2][DB];
     auto vread = [&](int g16, VFrag (&dst)[DB]) {
@@ -190,18 +199,22 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     vread(0, vf[0]);
     // Mask (raw scores; the scale is applied inside the exponent); element r
     // of block kb is key key0 + 32kb + (r%4) + 8(r/4) + 4lg.
-    const bool diag = key0 + kFaBK - 1 > wave_qmin;
+    // The mask is a wave-uniform branch: only the tiles crossing the
+    // diagonal pay for it.
+    if (key0 + kFaBK - 1 > wave_qmin) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + 32 * kb + (r & 3) + 8 * (r >> 2) + 4 * lg;
+          if (key > qpos) sacc[kb][r] = -INFINITY;
+        }
+    }
     float mt = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if (diag) {
-          const int key = key0 + 32 * kb + (r & 3) + 8 * (r >> 2) + 4 * lg;
-          if (key > qpos) sacc[kb][r] = -INFINITY;
-        }
-        mt = fmaxf(mt, sacc[kb][r]);
-      }
+      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[kb][r]);
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
     // Raise the running max (raw units) only past the slack; rescale when
     // any lane of the wave did.  m_run is finite after the first tile (key 0
@@ -236,7 +249,6 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     // O^T += V^T P^T over four 16-key groups: the hi MFMAs of the four d
     // blocks, then the lo ones (four independent chains), with the next
     // group's V fragments read meanwhile.
-    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int g16 = 0; g16 < 4; ++g16) {
       if (g16 + 1 < 4) vread(g16 + 1, vf[(g16 + 1) & 1]);
@@ -247,7 +259,10 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
       for (int bb = 0; bb < DB; ++bb)
         oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[g16 & 1][bb].h, pl[g16], oacc[bb], 0, 0, 0);
     }
-    __builtin_amdgcn_s_setprio(0);
+  };
+  for (int kt = kt_lo; kt < kt_hi; kt += 2) {
+    step(kt, Buf0{});
+    if (kt + 1 < kt_hi) step(kt + 1, Buf1{});
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -349,17 +364,9 @@ template <int D, bool PAGED, bool SPLIT>
 static hipError_t run_fa(const void* q, const void* kc, const void* vc, void* out,
                          const BatchDev& b, const KvDev& kv, int Hq, int Hkv,
                          int include_single, int nsplit, float* part, hipStream_t s) {
-  const size_t smem = sizeof(FaSmem<D>);
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_prefill_kernel<D, PAGED, SPLIT>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
   dim3 grid(cdiv(b.max_q_len, kFaBQ), Hq, b.n_seqs * nsplit);
   const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  attn_prefill_kernel<D, PAGED, SPLIT><<<grid, 256, smem, s>>>(
+  attn_prefill_kernel<D, PAGED, SPLIT><<<grid, 256, 0, s>>>(
       (const bf16*)q, (const bf16*)kc, (const bf16*)vc, (bf16*)out, b.cu_q, b.ctx_len, b.slot, kv,
       Hq, Hkv, scale_log2e, include_single, b.n_tokens, nsplit, part);
   hipError_t e = hipGetLastError();
