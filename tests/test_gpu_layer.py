@@ -277,6 +277,28 @@ def test_tiny_ragged_mixed_batch(bias):
     assert_close(vr, ref["v_new"], "ragged V")
 
 
+@pytest.mark.parametrize("q_lens", [[150, 0, 1, 0, 70, 0], [40, 0, 1, 0, 30, 0]],
+                         ids=["large", "short"])
+def test_empty_sequences_in_a_ragged_batch(q_lens):
+    # sequences with no new token inside and at the end of the batch (large:
+    # the 256 x 256 GEMM path; short: the split-K path of <= 128 tokens)
+    cfg = layer_c1()
+    batch = B([3, 0, 2, 1, 4, 5], [0, 40, 7, 0, 150, 10], q_lens)
+    cs = Case(cfg, batch, 6, 256, seed=9)
+    out, ws = cs.run()
+    ref = cs.oracle()
+    assert_close(to_host_f64(out), ref["out"], "empty-seq out", exact=cs.oracle(storage=None)["out"])
+    kr, vr = cs.cache_rows()
+    assert_close(kr, ref["k_new"], "empty-seq K")
+    assert_close(vr, ref["v_new"], "empty-seq V")
+    # the empty sequences' slots are untouched, bit for bit
+    k, v = cs.cache
+    for s, q in zip(batch.slot, batch.q_len):
+        if q == 0:
+            assert np.array_equal(to_host_f64(k[s]), f64(cs.kb[s])), f"slot {s} K changed"
+            assert np.array_equal(to_host_f64(v[s]), f64(cs.vb[s])), f"slot {s} V changed"
+
+
 # --------------------------------------------------------- 7B layer shapes --
 
 def test_7b_ragged_prefill_sampled_rows():
