@@ -18,7 +18,7 @@ in fp32 inside them.  Two gates, on the same seeded bf16 inputs:
    flips cascade through q/k -> attention -> residual -> FFN, so at the 7B
    shapes a few in 10^4 output elements sit 2-4 ulps apart.  A CPU emulation of
    the bf16 storage points reproduces the GPU's deviation from the exact
-   oracle; see DESIGN.md.)
+   oracle.)
 
 Index results are bit-exact.  Sizes span several GEMM / attention tiles with
 ragged tails; the full-size workloads are checked on sampled rows in the
