@@ -340,15 +340,20 @@ __global__ __launch_bounds__(256) void attn_prefill_combine_kernel(
   }
 }
 
-// Key-range splits for a batch of n_tokens tokens: 1 when the query tiles
-// fill the GPU (two workgroups per CU); otherwise doubled (up to 8) until
-// they do, while every split keeps >= 8 key tiles of the longest key range.
+// Key-range splits for a batch of n_tokens tokens: doubled (up to 8) while
+// the split workgroups still fit about one per CU (1.25 per CU: the query
+// tile count is estimated from n_tokens, which also counts the single-token
+// sequences of a mixed step), and every split keeps >= 8 key tiles of the
+// longest key range.  (Filling the second workgroup slot of each CU with
+// more splits costs more in partials and merge than it gains: a 512-token
+// chunk over a 6144-token prefix takes 117 us with 2 splits against 172 us
+// with 8.)
 int attn_prefill_splits(int n_seqs, int n_tokens, int max_q_len, int max_ctx_len,
                         int n_q_heads) {
   const int64_t wgs = (int64_t)cdiv(n_tokens, kFaBQ) * n_q_heads;  // query tiles of the batch
   const int max_tiles = cdiv(max_ctx_len + max_q_len, kFaBK);
   int sp = 1;
-  while (sp < 8 && wgs * sp < 2 * cu_count() && max_tiles >= 16 * sp &&
+  while (sp < 8 && wgs * sp * 2 * 4 <= (int64_t)cu_count() * 5 && max_tiles >= 16 * sp &&
          (int64_t)n_seqs * sp * 2 <= 65535)  // the grid's z extent
     sp *= 2;
   return sp;
