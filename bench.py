@@ -7,8 +7,10 @@ sequences x 2048 tokens (hidden 3584, 28/4 heads, head_dim 128, SwiGLU 18944),
 inputs seeded and already resident in HBM.  K timed steps are bracketed by
 torch.cuda.synchronize() and HIP events on the launch stream; per-stage
 durations come from the library's own HIP-event timers over the same timed
-region.  One JSON line is printed.  The decode workload (batch 64, KV 4096,
-32 steps) is timed as a secondary result in the same line.
+region.  The decode workload (batch 64, KV 4096, 32 steps) is timed as a
+secondary result.  The full record (per-stage times, phase intensities,
+secondary workloads) goes to stderr as one JSON line (and to --detail-out);
+the last stdout line is a compact JSON summary of at most 4 KB.
 
 Phases: for each workload (dense prefill, dense decode, MoE prefill, MoE
 decode, mixed, the dense and MoE prefills with the per-head q/k RMSNorm
@@ -41,6 +43,8 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 METRIC = "Thinker-layer prefill & decode tokens/s; % MFMA / HBM roofline; J/token"
+TRAFFIC_SOURCE = ("profiles/traffic.txt: rocprofv3 FETCH_SIZE / WRITE_SIZE per launch, "
+                  "copy-calibrated; null once the kernel source changed")
 
 
 def linear_params(cfg) -> int:
@@ -346,7 +350,8 @@ def run_decode(args, tri):
         "roofline": {"kernel": "attn_decode (split-KV partials; the LSE combine is a separate stage)",
                      "bound": "hbm",
                      "achieved": attn_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": attn_gbs / PEAK_HBM_GBS, "traffic": profiled_traffic("attn_decode")},
+                     "frac": attn_gbs / PEAK_HBM_GBS, "traffic": profiled_traffic("attn_decode"),
+                     "traffic_source": TRAFFIC_SOURCE},
         "stages_ms_per_step": {k: v["total_ms"] / (reps * steps) for k, v in prof.items() if v["launches"]},
     }
     if energy is not None:
@@ -475,7 +480,7 @@ def run_secondary(args, tri, name):
 
 def ai_sweep(args, tri):
     """Arithmetic-intensity sweep under the GPU's own clock management (the
-    paper's frequency-locked roofline, Section III-B, without clock control):
+    paper's frequency-locked roofline, Section II-C, without clock control):
     the 7B dense layer at token counts from one decode token to a 16384-token
     prefill.  Per point: the layer's time-weighted A.I. (Eq. 5, from the work
     model and the measured stage times), achieved TFLOP/s and GB/s, and the
@@ -590,6 +595,8 @@ def main(argv=None):
                     help="skip the MoE prefill / MoE decode / mixed-step context numbers")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy 3 times (HBM counter calibration)")
+    ap.add_argument("--detail-out", default=None,
+                    help="also write the full result record (phases, stages, secondary) here")
     ap.add_argument("--ai-sweep", action="store_true",
                     help="only run the arithmetic-intensity sweep of the 7B layer (clock, power, "
                          "Eq. 1 / Eq. 3 fits) and print it as one JSON line")
@@ -647,6 +654,7 @@ def main(argv=None):
         "roofline": {"kernel": "gate_up (fused SwiGLU GEMM)", "bound": "mfma", "achieved": gu_tflops,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": gu_tflops / PEAK_BF16_TFLOPS,
                      "traffic": profiled_traffic("gate_up"),
+                     "traffic_source": TRAFFIC_SOURCE,
                      "algorithmic_bytes": 2.0 * (T * wl.cfg.hidden + 2 * wl.cfg.ffn_dim * wl.cfg.hidden
                                                  + T * wl.cfg.ffn_dim)},
         "stages_ms_per_step": {k: v["total_ms"] / args.steps for k, v in prof.items() if v["launches"]},
@@ -670,8 +678,71 @@ def main(argv=None):
     if not args.no_cpu:
         from synth import bf16_to_f32
         res["cpu_baseline"] = cpu_baseline(wl, wb, bf16_to_f32(kb), bf16_to_f32(vb), xb)
-    print(json.dumps(res))
+    # Full detail (phases, per-stage data, secondary workloads) to stderr and,
+    # if asked, to a file; stdout ends with the compact summary line.
+    detail = json.dumps(res)
+    print(detail, file=sys.stderr, flush=True)
+    if args.detail_out:
+        with open(args.detail_out, "w") as f:
+            f.write(detail + "\n")
+    print(json.dumps(summary_line(res)))
     return 0
+
+
+def _r(v, sig=4):
+    """Round floats to `sig` significant digits (recursively) for the summary line."""
+    if isinstance(v, float):
+        return float(f"{v:.{sig}g}")
+    if isinstance(v, dict):
+        return {k: _r(x, sig) for k, x in v.items()}
+    if isinstance(v, list):
+        return [_r(x, sig) for x in v]
+    return v
+
+
+SUMMARY_MAX_BYTES = 4000
+
+
+def summary_line(res):
+    """The compact result line (<= 4 KB): the headline prefill metric with its
+    roofline, the decode result with its roofline, energy per token, the
+    secondary workloads' step times and the CPU baseline.  Per-stage data and
+    the phase intensities stay in the detail record."""
+    keys = ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+            "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+            "layer_tflops", "layer_mfma_frac", "roofline")
+    out = {k: res[k] for k in keys if k in res}
+    if res.get("energy"):
+        e = res["energy"]
+        out["energy"] = {"joules_per_token": e["joules_per_token"], "avg_power_w": e["avg_power_w"],
+                         "gfxclk_mhz": e["telemetry"].get("gfxclk_mhz")}
+    out["stages_ms_per_step"] = res.get("stages_ms_per_step")
+    d = res.get("decode")
+    if d:
+        dd = {k: d[k] for k in ("workload", "ms_per_step", "tokens_per_s", "hbm_frac_step",
+                                "roofline") if k in d}
+        if d.get("energy"):
+            dd["joules_per_token"] = d["energy"]["joules_per_token"]
+        if d.get("paged"):
+            dd["paged_ms_per_step"] = d["paged"]["ms_per_step"]
+        out["decode"] = dd
+    if res.get("secondary"):
+        sec = {}
+        for r in res["secondary"]:
+            e = r.get("energy")
+            sec[r["workload"].split(":")[0]] = {
+                "ms_per_step": r["ms_per_step"], "tokens_per_s": r["tokens_per_s"],
+                "joules_per_token": e["joules_per_token"] if e else None}
+        out["secondary"] = sec
+    if res.get("cpu_baseline"):
+        out["cpu_baseline"] = res["cpu_baseline"]
+    out = _r(out)
+    # stay within the size the driver keeps, dropping the least important parts
+    for drop in ("stages_ms_per_step", "secondary"):
+        if len(json.dumps(out)) <= SUMMARY_MAX_BYTES:
+            break
+        out.pop(drop, None)
+    return out
 
 
 if __name__ == "__main__":

@@ -254,7 +254,7 @@ tri_status tri_profile_enable(int32_t on);
 tri_status tri_profile_read(tri_profile* out);
 
 /* Algorithmic work of one layer call, stage by stage: the per-kernel
- * arithmetic intensity from which Section III-B forms the time-weighted
+ * arithmetic intensity from which Section III-C forms the time-weighted
  * intensity of a phase (Eq. 5).  Index i and name[i] are the stage of
  * tri_profile with the same index.  The counts follow the operations'
  * definitions, not the kernels' internals:
@@ -290,7 +290,7 @@ tri_status tri_layer_work(const tri_layer_config* cfg, int32_t decode, int32_t n
                           const int32_t* q_len, const int32_t* ctx_len,
                           const int32_t* expert_rows, tri_work* out);
 
-/* Time-weighted arithmetic intensity of a phase (Section III-B, Eq. 5):
+/* Time-weighted arithmetic intensity of a phase (Section III-C, Eq. 5):
  *   ai = sum_i d_i (flops_i / bytes_i) / sum_i d_i
  * over the stages i with work->runs[i] set, d_i = prof->total_ms[i]; stages
  * with d_i = 0, or with no work (flops and bytes both 0), drop out.  The work of several calls may be summed stage by

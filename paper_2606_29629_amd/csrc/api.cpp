@@ -84,7 +84,7 @@ struct Layout {
 size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
   const int T = b->n_tokens, H = c->hidden, D = c->head_dim;
   const int Nqkv = (c->n_q_heads + 2 * c->n_kv_heads) * D;
-  size_t p = attn_decode_partial_bytes(T, c->n_q_heads, D, b->max_ctx_len + 1);
+  size_t p = attn_decode_partial_bytes(b->n_seqs, c->n_q_heads, D, b->max_ctx_len + 1);
   const size_t fa =
       attn_prefill_partial_bytes(b->n_seqs, T, b->max_q_len, b->max_ctx_len, c->n_q_heads, D);
   if (fa > p) p = fa;
@@ -191,9 +191,9 @@ struct StageTimer {
   int stage;
   hipStream_t s;
   hipEvent_t a = nullptr, b = nullptr;
-  StageTimer(int st, hipStream_t str) : stage(st), s(str) {
+  StageTimer(int st, hipStream_t str, bool timed = true) : stage(st), s(str) {
     Profiler& p = prof();
-    if (!p.on) return;
+    if (!timed || !p.on) return;
     std::lock_guard<std::mutex> g(p.mu);
     a = p.get();
     b = p.get();
@@ -228,9 +228,14 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   return x < y + nb && y < x + na;
 }
 
-tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weights* w,
-                 const tri_kv_cache* cache, const tri_batch* b, const void* x_in, void* x_out,
-                 int32_t* route_idx, float* route_w, void* ws, size_t ws_bytes, void* stream) {
+}  // namespace
+
+// One layer call on the caller's workspace; `timed` = false keeps the call
+// free of profiling events (no event is created or recorded).
+tri_status tri::layer_call(bool decode, bool timed, const tri_layer_config* cfg,
+                           const tri_layer_weights* w, const tri_kv_cache* cache,
+                           const tri_batch* b, const void* x_in, void* x_out, int32_t* route_idx,
+                           float* route_w, void* ws, size_t ws_bytes, void* stream) {
   tri_status st = check_config(cfg);
   if (st != TRI_OK) return st;
   if (!w || !cache) return TRI_ERR_NULL;
@@ -284,7 +289,7 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
 
   {
     // token map + rotary table + pre-attention RMSNorm
-    StageTimer t_(ST_PROLOGUE, s);
+    StageTimer t_(ST_PROLOGUE, s, timed);
     TRI_HIP(launch_prologue(bd, kv, D, cfg->rope_base, rope_sections(cfg), tok_slot, tok_row,
                             rope, x_in, w->attn_norm, h, H, cfg->rms_eps, s));
   }
@@ -305,19 +310,21 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   e.head_dim = D;
   e.max_seq = kv.panel_rows();
   {
-    StageTimer t_(ST_QKV, s);
+    StageTimer t_(ST_QKV, s, timed);
     if ((st = run_linear(h, H, w->w_qkv, T, Nqkv, H, e, part, s)) != TRI_OK) return st;
   }
   if (!decode && b->max_q_len > 1) {
-    StageTimer t_(ST_ATTN_PREFILL, s);
+    StageTimer t_(ST_ATTN_PREFILL, s, timed);
     TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, kv, Hq, Hkv, D, 0, part, s));
   }
-  {
-    StageTimer t_(ST_ATTN_DECODE, s);
-    TRI_HIP(launch_attn_decode_split(q, cache->k, cache->v, part, bd, kv, Hq, Hkv, D, s));
-  }
-  {
-    StageTimer t_(ST_ATTN_COMBINE, s);
+  // Split-KV attention serves the single-token sequences; a batch in which
+  // every sequence has max_q_len > 1 tokens has none.
+  if (decode || b->max_q_len == 1 || (int64_t)b->n_seqs * b->max_q_len != b->n_tokens) {
+    {
+      StageTimer t_(ST_ATTN_DECODE, s, timed);
+      TRI_HIP(launch_attn_decode_split(q, cache->k, cache->v, part, bd, kv, Hq, Hkv, D, s));
+    }
+    StageTimer t_(ST_ATTN_COMBINE, s, timed);
     TRI_HIP(launch_attn_decode_combine(part, attn, bd, kv, Hq, Hkv, D, s));
   }
   e = Epi{};
@@ -329,15 +336,15 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   if (skinny_resid_norm_fused(T, H, Hq * D)) {
     // short batch: the O projection's split-K reduction also adds the
     // residual and applies the pre-MLP RMSNorm (no separate norm launch)
-    StageTimer t_(ST_OPROJ, s);
+    StageTimer t_(ST_OPROJ, s, timed);
     TRI_HIP(launch_skinny_resid_norm(attn, Hq * D, w->w_o, Hq * D, T, H, Hq * D, x_in, H, x1, H,
                                      w->mlp_norm, h2, cfg->rms_eps, part, s));
   } else {
     {
-      StageTimer t_(ST_OPROJ, s);
+      StageTimer t_(ST_OPROJ, s, timed);
       if ((st = run_linear(attn, Hq * D, w->w_o, T, H, Hq * D, e, part, s)) != TRI_OK) return st;
     }
-    StageTimer t_(ST_NORM2, s);
+    StageTimer t_(ST_NORM2, s, timed);
     TRI_HIP(launch_rmsnorm(x1, w->mlp_norm, h2, nullptr, T, H, cfg->rms_eps, s));
   }
 
@@ -348,7 +355,7 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
     e.ldo = F;
     e.ffn = F;
     {
-      StageTimer t_(ST_GATEUP, s);
+      StageTimer t_(ST_GATEUP, s, timed);
       if ((st = run_linear(h2, H, w->w_gate_up, T, 2 * F, H, e, part, s)) != TRI_OK) return st;
     }
     e = Epi{};
@@ -358,7 +365,7 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
     e.resid = x1;
     e.ldr = H;
     {
-      StageTimer t_(ST_DOWN, s);
+      StageTimer t_(ST_DOWN, s, timed);
       if ((st = run_linear(act, F, w->w_down, T, H, F, e, part, s)) != TRI_OK) return st;
     }
     return TRI_OK;
@@ -375,13 +382,13 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   int32_t* tile_off = at<int32_t>(ws, L.tile_off);
   float* y = at<float>(ws, L.y);
   {
-    StageTimer t_(ST_ROUTER, s);
+    StageTimer t_(ST_ROUTER, s, timed);
     TRI_HIP(launch_moe_route_bf16(h2, w->w_router, T, H, E, k,
                                   (cfg->flags & TRI_F_MOE_RENORM) ? 1 : 0,
                                   at<float>(ws, L.logits), idx, rw, s));
   }
   {
-    StageTimer t_(ST_MOE_PERMUTE, s);
+    StageTimer t_(ST_MOE_PERMUTE, s, timed);
     TRI_HIP(launch_moe_permute(idx, P, E, moe_tile_rows(P, E), at<int32_t>(ws, L.rank),
                                at<int32_t>(ws, L.counts), perm, inv, seg, tile_off, s));
   }
@@ -391,7 +398,7 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   e.ldo = Fe;
   e.ffn = Fe;
   {
-    StageTimer t_(ST_MOE_GATEUP, s);
+    StageTimer t_(ST_MOE_GATEUP, s, timed);
     TRI_HIP(launch_gemm_grouped(h2, H, T, perm, k, w->w_gate_up, (int64_t)2 * Fe * H, 2 * Fe, H,
                                 seg, tile_off, E, P, e, s));
   }
@@ -400,18 +407,18 @@ tri_status layer(bool decode, const tri_layer_config* cfg, const tri_layer_weigh
   e.out = y;
   e.ldo = H;
   {
-    StageTimer t_(ST_MOE_DOWN, s);
+    StageTimer t_(ST_MOE_DOWN, s, timed);
     TRI_HIP(launch_gemm_grouped(act, Fe, P, nullptr, k, w->w_down, (int64_t)H * Fe, H, Fe, seg,
                                 tile_off, E, P, e, s));
   }
   {
-    StageTimer t_(ST_MOE_COMBINE, s);
+    StageTimer t_(ST_MOE_COMBINE, s, timed);
     TRI_HIP(launch_moe_combine(x1, y, inv, rw, T, H, k, x_out, s));
   }
   return TRI_OK;
 }
 
-}  // namespace
+
 
 extern "C" {
 
@@ -447,16 +454,16 @@ tri_status tri_layer_prefill(const tri_layer_config* cfg, const tri_layer_weight
                              const tri_kv_cache* cache, const tri_batch* batch, const void* x_in,
                              void* x_out, int32_t* route_idx, float* route_w, void* workspace,
                              size_t workspace_bytes, void* stream) {
-  return layer(false, cfg, w, cache, batch, x_in, x_out, route_idx, route_w, workspace,
-               workspace_bytes, stream);
+  return layer_call(false, true, cfg, w, cache, batch, x_in, x_out, route_idx, route_w,
+                    workspace, workspace_bytes, stream);
 }
 
 tri_status tri_layer_decode(const tri_layer_config* cfg, const tri_layer_weights* w,
                             const tri_kv_cache* cache, const tri_batch* batch, const void* x_in,
                             void* x_out, int32_t* route_idx, float* route_w, void* workspace,
                             size_t workspace_bytes, void* stream) {
-  return layer(true, cfg, w, cache, batch, x_in, x_out, route_idx, route_w, workspace,
-               workspace_bytes, stream);
+  return layer_call(true, true, cfg, w, cache, batch, x_in, x_out, route_idx, route_w,
+                    workspace, workspace_bytes, stream);
 }
 
 tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* cache,

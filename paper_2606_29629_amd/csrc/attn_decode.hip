@@ -26,7 +26,7 @@
 // ds_read_b64_tr_b16 and P split into bf16 hi + lo parts (16 significant
 // bits).
 //
-// Output per (token, head, split): the unnormalised accumulator, the running
+// Output per (sequence, head, split): the unnormalised accumulator, the running
 // max m (log2 domain) and sum l; the combine kernel merges the splits:
 // M = max m_s, L = sum l_s 2^(m_s - M), o = sum acc_s 2^(m_s - M) / L.
 #include "common.hpp"
@@ -70,9 +70,11 @@ int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv, int head_dim,
 // block-id register): splits of up to 62 blocks.
 int attn_decode_max_split(const KvDev& kv) { return kv.table ? 62 * kv.block_size : 0; }
 
-size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv) {
+// Partials of one (sequence, query head, split): D accumulators, max and sum.
+// Indexed by sequence, so only the batch's sequences (not its tokens) count.
+size_t attn_decode_partial_bytes(int n_seqs, int n_q_heads, int head_dim, int max_kv) {
   const int ns = cdiv(max_kv < 1 ? 1 : max_kv, kDecMinSplit);  // bound for every split size
-  return (size_t)n_tokens * n_q_heads * ns * (head_dim + 2) * sizeof(float);
+  return (size_t)n_seqs * n_q_heads * ns * (head_dim + 2) * sizeof(float);
 }
 
 template <int D>
@@ -354,7 +356,7 @@ __global__ __launch_bounds__(64, 2) void attn_decode_kernel(
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (r >= grp) return;
-  float* pp = part + (((int64_t)t * Hq + qh0 + r) * nsplit + sp) * (D + 2);
+  float* pp = part + (((int64_t)s * Hq + qh0 + r) * nsplit + sp) * (D + 2);
   // oacc[b] element e: d = 32 b + 8 (e / 4) + 4 g + e % 4.
 #pragma unroll
   for (int b = 0; b < DB; ++b)
@@ -380,7 +382,7 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(
   if (t1 - t != 1 || t < 0 || t >= n_tokens) return;
   if (sl < 0 || sl >= n_slots || c < 0 || c + 1 > max_seq) return;
   const int ns = min(cdiv(c + 1, split_keys), nsplit);  // never past the launched splits
-  const float* pp = part + ((int64_t)t * Hq + qh) * nsplit * (D + 2);
+  const float* pp = part + ((int64_t)s * Hq + qh) * nsplit * (D + 2);
   // Splits in groups of 8: the group's (m, l, acc) loads are issued together,
   // then folded in split order into a running (M, L, o).
   float M = -INFINITY, Lsum = 0.f, o = 0.f;

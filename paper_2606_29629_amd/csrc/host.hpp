@@ -20,4 +20,12 @@ inline constexpr const char* kStageName[ST_COUNT] = {
 // Validates a layer config (TRI_OK, or the status the entry points return).
 tri_status check_config(const tri_layer_config* c);
 
+// The layer entry points' common body (tri_layer_prefill when decode is
+// false, tri_layer_decode when true) on a workspace of ws_bytes; with timed =
+// false no profiling event is created or recorded.
+tri_status layer_call(bool decode, bool timed, const tri_layer_config* cfg,
+                      const tri_layer_weights* w, const tri_kv_cache* cache, const tri_batch* b,
+                      const void* x_in, void* x_out, int32_t* route_idx, float* route_w, void* ws,
+                      size_t ws_bytes, void* stream);
+
 }  // namespace tri

@@ -139,7 +139,7 @@ int attn_decode_split_keys(int n_seqs, int n_kv_heads, int max_kv, int head_dim,
 int attn_decode_max_split(const KvDev& kv);
 // Compute units of the current device (256 when it cannot be queried).
 int cu_count();
-size_t attn_decode_partial_bytes(int n_tokens, int n_q_heads, int head_dim, int max_kv);
+size_t attn_decode_partial_bytes(int n_seqs, int n_q_heads, int head_dim, int max_kv);
 hipError_t launch_attn_decode_split(const void* q, const void* kc, const void* vc, float* part,
                                     const BatchDev& b, const KvDev& kv, int n_q_heads,
                                     int n_kv_heads, int head_dim, hipStream_t s);

@@ -1,5 +1,5 @@
 // Algorithmic work (flops, compulsory HBM bytes) of each stage of one layer
-// call, and the time-weighted phase intensity of Section III-B (Eq. 5) formed
+// call, and the time-weighted phase intensity of Section III-C (Eq. 5) formed
 // from it and the measured stage times.  Host code only.
 #include <stdint.h>
 

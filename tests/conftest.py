@@ -26,3 +26,17 @@ def pytest_collection_modifyitems(config, items):
     for it in items:
         if "gpu" in it.keywords:
             it.add_marker(skip)
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    """Counts of the end-to-end parity checks (GPU error against the exact
+    oracle, next to the CPU bf16-storage emulation's) for the run's log."""
+    try:
+        from parity import summary_lines
+    except Exception:  # pragma: no cover
+        return
+    lines = summary_lines()
+    if lines:
+        terminalreporter.write_sep("-", "end-to-end parity against the exact oracle")
+        for line in lines:
+            terminalreporter.write_line(line)

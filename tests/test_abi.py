@@ -213,6 +213,39 @@ def test_workspace_size_and_layout(lib):
     assert lib.tri_workspace_size(ctypes.byref(c), None, None) == T.TRI_ERR_NULL
 
 
+def test_workspace_of_long_chunked_prefill(lib):
+    """Chunked prefill over a long cached prefix: the workspace holds the
+    layer's activations plus scratch that grows with the number of sequences,
+    not with tokens x prefix (the split-KV partials serve single-token
+    sequences and are indexed by sequence)."""
+    H, Hq, Hkv, D, F = 3584, 28, 4, 128, 18944
+    c = cfg(hidden=H, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=D, ffn_dim=F)
+
+    def size(n_seqs, q, ctx, n_tokens=None):
+        n_tokens = n_seqs * q if n_tokens is None else n_tokens
+        b = batch(n_seqs=n_seqs, n_tokens=n_tokens, max_q=q, max_ctx=ctx)
+        s = ctypes.c_size_t()
+        assert lib.tri_workspace_size(ctypes.byref(c), ctypes.byref(b), ctypes.byref(s)) == 0
+        return s.value
+
+    def activations(t):
+        return t * (4 + 4 + (D // 2) * 8 + 3 * H * 2 + 2 * Hq * D * 2 + F * 2)
+
+    # scratch beyond the activations: the large GEMMs' tail-tile partials (one
+    # 256 x 256 fp32 tile per compute unit, 256 CUs without a device), which the
+    # split-KV partials share, plus 256-byte alignment of the regions
+    scratch = 256 * 256 * 256 * 4 + 20 * 256
+    for ctx in (8192, 30000):
+        t = 8 * 2048
+        assert size(8, 2048, ctx) <= activations(t) + scratch + 8 * Hq * 235 * (D + 2) * 4, ctx
+    assert size(8, 2048, 8192) <= activations(8 * 2048) + scratch
+    # the prefix adds only per-sequence partials: 8 x Hq x ceil(dctx / 128) x (D + 2) floats
+    grow = size(8, 2048, 30000) - size(8, 2048, 8192)
+    assert 0 <= grow <= 8 * Hq * -(-(30000 - 8192) // 128 + 1) * (D + 2) * 4 + 4096
+    # the mixed step's shape: a 512-token chunk at 6144 plus 32 decodes up to 8192
+    assert size(33, 512, 8192, n_tokens=544) <= activations(544) + scratch
+
+
 def test_kvcache_append_and_route_validation(lib):
     c = cfg()
     kv = T.KVCache(FAKE, FAKE + 4096, 1, 64, None, 0, 0)

@@ -13,7 +13,8 @@ from paper_2606_29629_amd.workload import (DeviceLayer, contiguous_from_paged, d
                                            paged_from_contiguous, to_device_bf16, to_host_f64)
 from paper_2606_29629_amd import _lib as T
 from synth import layer_7b, layer_c1, make_cache, make_weights, make_x
-from test_gpu_layer import B, Case, assert_close, check_down, f64, stage_parity
+from parity import strict_shape
+from test_gpu_layer import B, Case, assert_e2e, check_down, f64, stage_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -25,8 +26,8 @@ def run_case(cfg, batch, n_slots, max_seq, label, seed=0, e2e_rows=None):
     x1, act, w = stage_parity(cs, ws, rows, label=label)
     check_down(cs, out, x1, act, w, rows, label)
     ref = cs.oracle(rows=rows)
-    assert_close(to_host_f64(out)[rows], ref["out"], f"{label} out",
-                 exact=cs.oracle(rows=rows, storage=None)["out"])
+    assert_e2e(to_host_f64(out)[rows], cs.oracle(rows=rows, storage=None)["out"], f"{label} out",
+               emul=ref["out"], strict=strict_shape(cfg))
     return cs, out
 
 

@@ -10,15 +10,11 @@ in fp32 inside them.  Two gates, on the same seeded bf16 inputs:
    adjacent bf16 value (<= 1 ulp; a flip is possible when the exact value lies
    within fp32 error of a rounding boundary), and at most 1% of elements may
    be the adjacent one.
-2. End to end.  Against the oracle with the bf16 storage reading,
-   |gpu - ref| <= max(2e-2, 1e-2 |ref|) for >= 99.9% of elements and within 4x
-   that bound for all; against the exact float64 oracle the normwise error of
-   every row is <= 1e-2.  (Two correct bf16 computations whose fp32 sums differ
-   in the last bits round some intermediates to adjacent bf16 values; these
-   flips cascade through q/k -> attention -> residual -> FFN, so at the 7B
-   shapes a few in 10^4 output elements sit 2-4 ulps apart.  A CPU emulation of
-   the bf16 storage points reproduces the GPU's deviation from the exact
-   oracle.)
+2. End to end against the exact float64 oracle (tests/parity.py): at the tiny
+   shapes every element within max(2e-2, 1e-2 |r|); at the 7B shapes the
+   count of elements outside that bound and the largest error are held to
+   those of the CPU bf16-storage emulation on the same rows (plus a stated
+   margin); the normwise error of every row is also <= 1e-2.
 
 Index results are bit-exact.  Sizes span several GEMM / attention tiles with
 ragged tails; the full-size workloads are checked on sampled rows in the
@@ -34,31 +30,21 @@ from paper_2606_29629_amd.workload import (DeviceLayer, device_batch, device_cac
                                            to_device_bf16, to_host_f64)
 from synth import (Batch, LayerConfig, bf16_to_f32, layer_7b, layer_c1, make_cache,
                    make_weights, make_x, to_bf16_bits, workload)
+from parity import check_e2e
 
 pytestmark = pytest.mark.gpu
 
-ATOL, RTOL = 2e-2, 1e-2
 
-
-def assert_close(got, ref, what, atol=ATOL, rtol=RTOL, exact=None, norm_rtol=1e-2,
-                 min_frac=0.999, cap=4.0):
+def assert_e2e(got, exact, what, emul=None, strict=False, norm_rtol=1e-2):
+    """End-to-end check against the exact oracle (tests/parity.py), plus the
+    normwise error of every row."""
     got = np.asarray(got, np.float64)
-    ref = np.asarray(ref, np.float64)
-    assert got.shape == ref.shape, (what, got.shape, ref.shape)
-    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
-    if exact is not None:
-        exact = np.asarray(exact, np.float64).reshape(got.shape[0], -1)
-        g2 = got.reshape(got.shape[0], -1)
-        nrm = np.linalg.norm(g2 - exact, axis=1) / np.maximum(np.linalg.norm(exact, axis=1), 1e-30)
+    ex = np.asarray(exact, np.float64)
+    if got.ndim >= 2:
+        g2, e2 = got.reshape(got.shape[0], -1), ex.reshape(ex.shape[0], -1)
+        nrm = np.linalg.norm(g2 - e2, axis=1) / np.maximum(np.linalg.norm(e2, axis=1), 1e-30)
         assert nrm.max() <= norm_rtol, f"{what}: row normwise error vs exact oracle {nrm.max():.3g}"
-    err = np.abs(got - ref)
-    bound = np.maximum(atol, rtol * np.abs(ref))
-    frac_ok = np.mean(err <= bound)
-    worst = np.max(err / bound)
-    if frac_ok < min_frac or worst > cap:
-        i = np.unravel_index(np.argmax(err / bound), err.shape)
-        raise AssertionError(f"{what}: {np.sum(err > bound)}/{err.size} outside the bound "
-                             f"(worst {worst:.2f}x at {i}: gpu {got[i]:.6g} oracle {ref[i]:.6g})")
+    check_e2e(got, ex, what, emul=emul, strict=strict)
 
 
 def bf16_ordinal(a):
@@ -125,9 +111,13 @@ class Case:
                                     f64(self.xb if x_bits is None else x_bits), rows=rows,
                                     storage=storage)
 
+    def cache_view(self):
+        """The cache as contiguous (K, V) [n_slots, Hkv, max_seq, D] device tensors."""
+        return self.cache
+
     def cache_rows(self):
         """GPU cache rows written by this call, as [T, Hkv, D] (K and V)."""
-        k, v = self.cache
+        k, v = self.cache_view()
         ks, vs = [], []
         for s, c, q in zip(self.batch.slot, self.batch.ctx_len, self.batch.q_len):
             ks.append(to_host_f64(k[s, :, c:c + q]).transpose(1, 0, 2))
@@ -168,7 +158,8 @@ def stage_parity(cs, ws, rows, x_bits=None, label=""):
     crow = b.ctx_len[seq] + rows - b.cu_q[seq]
     slots, sidx = np.unique(b.slot[seq], return_inverse=True)
     st = torch.as_tensor(slots, device=ws.device)
-    kc, vc = to_host_f64(cs.cache[0][st]), to_host_f64(cs.cache[1][st])
+    kview, vview = cs.cache_view()
+    kc, vc = to_host_f64(kview[st]), to_host_f64(vview[st])
     # RMSNorm
     assert_rounded(h, OL.rmsnorm(x, w["attn_norm"], cfg.rms_eps), f"{label} rmsnorm_attn")
     # q/k/v projection + rotary + cache write
@@ -216,12 +207,11 @@ def test_tiny_prefill_then_16_decode_steps():
     wl = workload("tiny")
     cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
     out, _ = cs.run()
-    ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "tiny prefill out",
-                 exact=cs.oracle(storage=None)["out"])
+    ex = cs.oracle(storage=None)
+    assert_e2e(to_host_f64(out), ex["out"], "tiny prefill out", strict=True)
     kr, vr = cs.cache_rows()
-    assert_close(kr, ref["k_new"], "tiny prefill K rows")
-    assert_close(vr, ref["v_new"], "tiny prefill V rows")
+    assert_e2e(kr, ex["k_new"], "tiny prefill K rows", strict=True)
+    assert_e2e(vr, ex["v_new"], "tiny prefill V rows", strict=True)
     # decode: fresh N(0,1) input each step, oracle fed the GPU-written cache
     batch = wl.batch
     for step in range(wl.decode_steps):
@@ -230,14 +220,12 @@ def test_tiny_prefill_then_16_decode_steps():
         xb = make_x(wl.cfg, batch.n_tokens, wl.seed, step=step)
         k, v = cs.cache
         w64 = {kk: f64(vv) for kk, vv in cs.wb.items()}
-        ref = oracle.layer_forward(wl.cfg, w64, to_host_f64(k), to_host_f64(v), batch, f64(xb),
-                                   storage="bf16")
         ex = oracle.layer_forward(wl.cfg, w64, to_host_f64(k), to_host_f64(v), batch, f64(xb))
         out, _ = cs.run(decode=True, x=to_device_bf16(xb))
-        assert_close(to_host_f64(out), ref["out"], f"tiny decode step {step}", exact=ex["out"])
+        assert_e2e(to_host_f64(out), ex["out"], f"tiny decode step {step}", strict=True)
         kr, vr = cs.cache_rows()
-        assert_close(kr, ref["k_new"], f"tiny decode K row {step}")
-        assert_close(vr, ref["v_new"], f"tiny decode V row {step}")
+        assert_e2e(kr, ex["k_new"], f"tiny decode K row {step}", strict=True)
+        assert_e2e(vr, ex["v_new"], f"tiny decode V row {step}", strict=True)
 
 
 def test_tiny_intermediates():
@@ -245,15 +233,16 @@ def test_tiny_intermediates():
     batch = B([0, 1], [0, 5], [37, 20])
     cs = Case(cfg, batch, 2, 64)
     out, ws = cs.run()
-    ref = cs.oracle()
+    ex = cs.oracle(storage=None)
     m = T.workspace_layout(cs.dl.cfg, cs.db)
     Tn, H, D, Hq = batch.n_tokens, cfg.hidden, cfg.head_dim, cfg.n_q_heads
-    assert_close(to_host_f64(ws_view(ws, m.h, (Tn, H))), ref["h"], "h")
-    assert_close(to_host_f64(ws_view(ws, m.q, (Tn, Hq, D))), ref["q"], "q")
-    assert_close(to_host_f64(ws_view(ws, m.attn, (Tn, Hq * D))), ref["attn"], "attn")
-    assert_close(to_host_f64(ws_view(ws, m.x1, (Tn, H))), ref["x1"], "x1")
-    assert_close(to_host_f64(ws_view(ws, m.h2, (Tn, H))), ref["h2"], "h2")
-    assert_close(to_host_f64(out), ref["out"], "out", exact=cs.oracle(storage=None)["out"])
+    assert_e2e(to_host_f64(ws_view(ws, m.h, (Tn, H))), ex["h"], "tiny h", strict=True)
+    assert_e2e(to_host_f64(ws_view(ws, m.q, (Tn, Hq, D))), ex["q"], "tiny q", strict=True)
+    assert_e2e(to_host_f64(ws_view(ws, m.attn, (Tn, Hq * D))), ex["attn"], "tiny attn",
+               strict=True)
+    assert_e2e(to_host_f64(ws_view(ws, m.x1, (Tn, H))), ex["x1"], "tiny x1", strict=True)
+    assert_e2e(to_host_f64(ws_view(ws, m.h2, (Tn, H))), ex["h2"], "tiny h2", strict=True)
+    assert_e2e(to_host_f64(out), ex["out"], "tiny out", strict=True)
     rows = np.arange(batch.n_tokens)
     x1, act, w = stage_parity(cs, ws, rows, label="tiny")
     check_down(cs, out, x1, act, w, rows, "tiny")
@@ -270,11 +259,11 @@ def test_tiny_ragged_mixed_batch(bias):
     rows = np.arange(batch.n_tokens)
     x1, act, w = stage_parity(cs, ws, rows, label="ragged")
     check_down(cs, out, x1, act, w, rows, "ragged")
-    ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "ragged out", exact=cs.oracle(storage=None)["out"])
+    ex = cs.oracle(storage=None)
+    assert_e2e(to_host_f64(out), ex["out"], f"tiny ragged out (bias {bias})", strict=True)
     kr, vr = cs.cache_rows()
-    assert_close(kr, ref["k_new"], "ragged K")
-    assert_close(vr, ref["v_new"], "ragged V")
+    assert_e2e(kr, ex["k_new"], "tiny ragged K", strict=True)
+    assert_e2e(vr, ex["v_new"], "tiny ragged V", strict=True)
 
 
 @pytest.mark.parametrize("q_lens", [[150, 0, 1, 0, 70, 0], [40, 0, 1, 0, 30, 0]],
@@ -286,11 +275,11 @@ def test_empty_sequences_in_a_ragged_batch(q_lens):
     batch = B([3, 0, 2, 1, 4, 5], [0, 40, 7, 0, 150, 10], q_lens)
     cs = Case(cfg, batch, 6, 256, seed=9)
     out, ws = cs.run()
-    ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "empty-seq out", exact=cs.oracle(storage=None)["out"])
+    ex = cs.oracle(storage=None)
+    assert_e2e(to_host_f64(out), ex["out"], "tiny empty-seq out", strict=True)
     kr, vr = cs.cache_rows()
-    assert_close(kr, ref["k_new"], "empty-seq K")
-    assert_close(vr, ref["v_new"], "empty-seq V")
+    assert_e2e(kr, ex["k_new"], "tiny empty-seq K", strict=True)
+    assert_e2e(vr, ex["v_new"], "tiny empty-seq V", strict=True)
     # the empty sequences' slots are untouched, bit for bit
     k, v = cs.cache
     for s, q in zip(batch.slot, batch.q_len):
@@ -312,11 +301,11 @@ def test_7b_ragged_prefill_sampled_rows():
     x1, act, w = stage_parity(cs, ws, rows, label="7B ragged")
     check_down(cs, out, x1, act, w, rows, "7B ragged")
     ref = cs.oracle(rows=rows)
-    assert_close(to_host_f64(out)[rows], ref["out"], "7B ragged prefill rows",
-                 exact=cs.oracle(rows=rows, storage=None)["out"])
+    ex = cs.oracle(rows=rows, storage=None)
+    assert_e2e(to_host_f64(out)[rows], ex["out"], "7B ragged prefill rows", emul=ref["out"])
     kr, vr = cs.cache_rows()
-    assert_close(kr, ref["k_new"], "7B K rows")
-    assert_close(vr, ref["v_new"], "7B V rows")
+    assert_e2e(kr, ex["k_new"], "7B K rows", emul=ref["k_new"])
+    assert_e2e(vr, ex["v_new"], "7B V rows", emul=ref["v_new"])
 
 
 def test_7b_decode_step_all_rows():
@@ -329,10 +318,11 @@ def test_7b_decode_step_all_rows():
     x1, act, w = stage_parity(cs, ws, rows, label="7B decode")
     check_down(cs, out, x1, act, w, rows, "7B decode")
     ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "7B decode out", exact=cs.oracle(storage=None)["out"])
+    ex = cs.oracle(storage=None)
+    assert_e2e(to_host_f64(out), ex["out"], "7B decode out", emul=ref["out"])
     kr, vr = cs.cache_rows()
-    assert_close(kr, ref["k_new"], "7B decode K")
-    assert_close(vr, ref["v_new"], "7B decode V")
+    assert_e2e(kr, ex["k_new"], "7B decode K", emul=ref["k_new"])
+    assert_e2e(vr, ex["v_new"], "7B decode V", emul=ref["v_new"])
 
 
 def test_full_size_dense_prefill_sampled():
@@ -350,8 +340,8 @@ def test_full_size_dense_prefill_sampled():
     args = (wl.cfg, w, f64(cs.kb), f64(cs.vb), sub, f64(cs.xb[s * 2048:(s + 1) * 2048]))
     ref = oracle.layer_forward(*args, rows=local, storage="bf16")
     ex = oracle.layer_forward(*args, rows=local)
-    assert_close(to_host_f64(out)[s * 2048 + local], ref["out"], "full prefill sampled rows",
-                 exact=ex["out"])
+    assert_e2e(to_host_f64(out)[s * 2048 + local], ex["out"], "full prefill sampled rows",
+               emul=ref["out"])
 
 
 def test_full_size_dense_decode_sampled():
@@ -368,8 +358,8 @@ def test_full_size_dense_decode_sampled():
     args = (wl.cfg, w, f64(cs.kb[wl.batch.slot[pick]]), f64(cs.vb[wl.batch.slot[pick]]), sub,
             f64(cs.xb[pick]))
     ref = oracle.layer_forward(*args, storage="bf16")
-    assert_close(to_host_f64(out)[pick], ref["out"], "full decode sampled rows",
-                 exact=oracle.layer_forward(*args)["out"])
+    assert_e2e(to_host_f64(out)[pick], oracle.layer_forward(*args)["out"],
+               "full decode sampled rows", emul=ref["out"])
 
 
 # ------------------------------------------------------------- invariants --
@@ -438,7 +428,8 @@ def test_decode_equals_recompute():
     part.batch = B([0], [n], [1])
     part.db = device_batch(part.batch)
     out, _ = part.run(decode=True, x=full.x[n:n + 1].contiguous())
-    assert_close(to_host_f64(out)[0], ref_row, "decode vs recompute")
+    # both sides are the GPU: the strict bar against the recomputed row
+    check_e2e(to_host_f64(out)[0], ref_row, "tiny decode vs recompute", strict=True)
 
 
 def test_kvcache_append_and_canaries():
@@ -485,11 +476,11 @@ def test_full_size_mixed_step_sampled():
     args = (wl.cfg, w64, f64(cs.kb[wl.batch.slot[pick]]), f64(cs.vb[wl.batch.slot[pick]]), sub,
             f64(cs.xb[tok]))
     ref = oracle.layer_forward(*args, storage="bf16")
-    assert_close(to_host_f64(out)[tok], ref["out"], "mixed decode rows",
-                 exact=oracle.layer_forward(*args)["out"])
+    assert_e2e(to_host_f64(out)[tok], oracle.layer_forward(*args)["out"], "mixed decode rows",
+               emul=ref["out"])
     chunk = B([0], [wl.batch.ctx_len[0]], [512])
     args = (wl.cfg, w64, f64(cs.kb[:1]), f64(cs.vb[:1]), chunk, f64(cs.xb[:512]))
     local = np.array([0, 300, 511])
     ref = oracle.layer_forward(*args, rows=local, storage="bf16")
-    assert_close(to_host_f64(out)[local], ref["out"], "mixed chunk rows",
-                 exact=oracle.layer_forward(*args, rows=local)["out"])
+    assert_e2e(to_host_f64(out)[local], oracle.layer_forward(*args, rows=local)["out"],
+               "mixed chunk rows", emul=ref["out"])

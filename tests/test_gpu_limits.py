@@ -10,7 +10,8 @@ import pytest
 import oracle
 from paper_2606_29629_amd.workload import to_host_f64
 from synth import LayerConfig
-from test_gpu_layer import B, Case, assert_close, check_down, f64, stage_parity
+from parity import strict_shape
+from test_gpu_layer import B, Case, assert_e2e, check_down, f64, stage_parity
 from test_gpu_moe import MoECase, moe_stage_parity, routes_agree
 
 pytestmark = pytest.mark.gpu
@@ -28,8 +29,9 @@ def dense_case(cfg, batch, n_slots, max_seq, decode=False, seed=2):
     x1, act, w = stage_parity(cs, ws, rows, label=f"{cfg.hidden}/{cfg.n_q_heads}")
     check_down(cs, out, x1, act, w, rows, f"{cfg.hidden}/{cfg.n_q_heads}")
     ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], f"H{cfg.hidden} G{cfg.n_q_heads // cfg.n_kv_heads} out",
-                 exact=cs.oracle(storage=None)["out"])
+    assert_e2e(to_host_f64(out), cs.oracle(storage=None)["out"],
+               f"H{cfg.hidden} G{cfg.n_q_heads // cfg.n_kv_heads} out", emul=ref["out"],
+               strict=strict_shape(cfg))
 
 
 @pytest.mark.parametrize("cfg", [WIDE, NARROW_HEADS], ids=["H8192_D128_G32", "H512_D64_G32"])
@@ -63,4 +65,5 @@ def test_moe_256_experts_top16(decode):
     routes_agree(gi, ref["logits"], c.cfg.top_k, 2e-2)
     forced = oracle.layer_forward(*args, storage="bf16", forced_routes=gi)
     exact = oracle.layer_forward(*args, forced_routes=gi)
-    assert_close(to_host_f64(c.out), forced["out"], "max MoE out", exact=exact["out"])
+    assert_e2e(to_host_f64(c.out), exact["out"], "max MoE out", emul=forced["out"],
+               strict=strict_shape(c.cfg))

@@ -21,7 +21,8 @@ from paper_2606_29629_amd import _lib as T
 from paper_2606_29629_amd.workload import (DeviceLayer, device_batch, device_cache,
                                            to_device_bf16, to_host_f64)
 from synth import Batch, LayerConfig, bf16_to_f32, make_cache, make_weights, make_x, workload
-from test_gpu_layer import B, assert_close, assert_rounded, f64, ws_view
+from parity import strict_shape
+from test_gpu_layer import B, assert_e2e, assert_rounded, f64, ws_view
 
 pytestmark = pytest.mark.gpu
 
@@ -165,7 +166,8 @@ def test_tiny_moe_layer(decode):
     routes_agree(gi, ref["logits"], c.cfg.top_k, 2e-2)
     forced = oracle.layer_forward(*args, storage="bf16", forced_routes=gi)
     exact = oracle.layer_forward(*args, forced_routes=gi)
-    assert_close(to_host_f64(c.out), forced["out"], "tiny MoE out", exact=exact["out"])
+    assert_e2e(to_host_f64(c.out), exact["out"], f"tiny MoE out (decode {decode})",
+               emul=forced["out"], strict=True)
 
 
 def test_moe_prefill_full_size_sampled():
@@ -185,8 +187,8 @@ def test_moe_prefill_full_size_sampled():
     args = (wl.cfg, w64, f64(c.kb), f64(c.vb), sub, f64(c.xb[s * 1024:(s + 1) * 1024]))
     forced = oracle.layer_forward(*args, rows=local, storage="bf16", forced_routes=gi)
     exact = oracle.layer_forward(*args, rows=local, forced_routes=gi)
-    assert_close(to_host_f64(c.out)[s * 1024 + local], forced["out"], "MoE prefill rows",
-                 exact=exact["out"])
+    assert_e2e(to_host_f64(c.out)[s * 1024 + local], exact["out"], "MoE prefill rows",
+               emul=forced["out"])
 
 
 def test_moe_decode_full_size_sampled():
@@ -202,7 +204,7 @@ def test_moe_decode_full_size_sampled():
             f64(c.xb[pick]))
     forced = oracle.layer_forward(*args, storage="bf16", forced_routes=gi)
     exact = oracle.layer_forward(*args, forced_routes=gi)
-    assert_close(to_host_f64(c.out)[pick], forced["out"], "MoE decode rows", exact=exact["out"])
+    assert_e2e(to_host_f64(c.out)[pick], exact["out"], "MoE decode rows", emul=forced["out"])
 
 
 @pytest.mark.parametrize("n_tok", [600, 1000], ids=["128-row tiles", "256-row tiles"])
@@ -219,5 +221,5 @@ def test_moe_grouped_tile_sizes(n_tok):
     gi = c.idx.cpu().numpy()
     forced = oracle.layer_forward(*args, rows=rows, storage="bf16", forced_routes=gi)
     exact = oracle.layer_forward(*args, rows=rows, forced_routes=gi)
-    assert_close(to_host_f64(c.out)[rows], forced["out"], f"MoE {n_tok} tokens rows",
-                 exact=exact["out"])
+    assert_e2e(to_host_f64(c.out)[rows], exact["out"], f"tiny MoE {n_tok} tokens rows",
+               emul=forced["out"], strict=True)

@@ -17,7 +17,8 @@ import pytest
 import oracle
 from paper_2606_29629_amd.workload import device_batch, to_device_bf16, to_host_f64
 from synth import layer_7b, layer_c1, make_x, mrope_batch
-from test_gpu_layer import Case, assert_close, check_down, f64, stage_parity
+from parity import strict_shape
+from test_gpu_layer import Case, assert_e2e, check_down, f64, stage_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -29,10 +30,12 @@ def run_and_check(cfg, batch, n_slots, max_seq, label, seed=0, decode_steps=0):
     x1, act, w = stage_parity(cs, ws, rows, label=label)
     check_down(cs, out, x1, act, w, rows, label)
     ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], f"{label} out", exact=cs.oracle(storage=None)["out"])
+    ex = cs.oracle(storage=None)
+    strict = strict_shape(cfg)
+    assert_e2e(to_host_f64(out), ex["out"], f"{label} out", emul=ref["out"], strict=strict)
     kr, vr = cs.cache_rows()
-    assert_close(kr, ref["k_new"], f"{label} K rows")
-    assert_close(vr, ref["v_new"], f"{label} V rows")
+    assert_e2e(kr, ex["k_new"], f"{label} K rows", emul=ref["k_new"], strict=strict)
+    assert_e2e(vr, ex["v_new"], f"{label} V rows", emul=ref["v_new"], strict=strict)
     b = batch
     for step in range(decode_steps):
         b = b.advanced()
@@ -44,8 +47,8 @@ def run_and_check(cfg, batch, n_slots, max_seq, label, seed=0, decode_steps=0):
         w64 = {kk: f64(vv) for kk, vv in cs.wb.items()}
         args = (cfg, w64, to_host_f64(k), to_host_f64(v), b, f64(cs.xb))
         ref = oracle.layer_forward(*args, storage="bf16")
-        assert_close(to_host_f64(out), ref["out"], f"{label} decode {step} out",
-                     exact=oracle.layer_forward(*args)["out"])
+        assert_e2e(to_host_f64(out), oracle.layer_forward(*args)["out"],
+                   f"{label} decode {step} out", emul=ref["out"], strict=strict)
 
 
 def test_mrope_tiny_mixed_segments_then_decode():
@@ -104,4 +107,5 @@ def test_moe_layer_with_qk_norm_and_sections():
     routes_agree(gi, ref["logits"], cfg.top_k, 2e-2)
     forced = oracle.layer_forward(*args, storage="bf16", forced_routes=gi)
     exact = oracle.layer_forward(*args, forced_routes=gi)
-    assert_close(to_host_f64(c.out), forced["out"], "moe qk-norm sections out", exact=exact["out"])
+    assert_e2e(to_host_f64(c.out), exact["out"], "tiny moe qk-norm sections out",
+               emul=forced["out"], strict=True)

@@ -8,15 +8,22 @@ contiguous cache holding the same rows, and the rows it writes must land in
 the blocks the table names.  The pools hold spare blocks that no slot maps
 to, filled with NaN: a read of any of them would show in the outputs.
 
-The contiguous path itself is checked against the oracle in test_gpu_layer.py.
+The paged path is also checked against the oracle on its own (no contiguous
+cache in the process): per-kernel parity on identical inputs and the
+end-to-end bar, at the full decode launch (64 sequences at KV 4096) and at a
+7B ragged prefill whose chunk continues a cached prefix that ends mid-block,
+with 64- and 128-row blocks in a shuffled pool.
 """
 import numpy as np
 import pytest
 
+import oracle
 from paper_2606_29629_amd import _lib as T
 from paper_2606_29629_amd.workload import (DeviceLayer, contiguous_from_paged, device_batch,
-                                           device_cache, paged_from_contiguous, to_device_bf16)
-from synth import Batch, layer_7b, layer_c1, make_cache, make_weights, make_x
+                                           device_cache, paged_from_contiguous, to_device_bf16,
+                                           to_host_f64)
+from synth import Batch, layer_7b, layer_c1, make_cache, make_weights, make_x, workload
+from test_gpu_layer import Case, assert_e2e, check_down, f64, stage_parity
 
 pytestmark = pytest.mark.gpu
 
@@ -123,3 +130,64 @@ def test_paged_kvcache_append():
     kg, vg = contiguous_from_paged(paged)
     assert torch.equal(kg.view(torch.int16), cont[0].view(torch.int16))
     assert torch.equal(vg.view(torch.int16), cont[1].view(torch.int16))
+
+
+class PagedCase(Case):
+    """A Case whose layer calls see only a paged copy of the seeded cache
+    (blocks of `block_size` rows dealt to a shuffled pool with NaN spare
+    blocks); the contiguous device copy is dropped before any call."""
+
+    def __init__(self, cfg, batch, n_slots, max_seq, block_size, seed=0, x_step=None):
+        import torch
+        super().__init__(cfg, batch, n_slots, max_seq, seed=seed, x_step=x_step)
+        k, v = self.cache
+        self.cache = paged_from_contiguous(k, v, block_size, seed=seed + 23)
+        del k, v
+        torch.cuda.synchronize()
+
+    def cache_view(self):
+        return contiguous_from_paged(self.cache)
+
+
+@pytest.mark.parametrize("block_size", [64, 128])
+def test_paged_full_size_decode_against_oracle(block_size):
+    """The decode launch (64 sequences at KV 4096) on a paged cache only."""
+    wl = workload("dense_decode")
+    max_seq = -(-wl.max_seq // block_size) * block_size
+    cs = PagedCase(wl.cfg, wl.batch, wl.n_slots, max_seq, block_size)
+    out, ws = cs.run(decode=True)
+    pick = np.array([0, 3, 31, 40, 63])
+    label = f"paged bs{block_size} decode"
+    x1, act, w = stage_parity(cs, ws, pick, label=label)
+    check_down(cs, out, x1, act, w, pick, label)
+    sub = B(np.arange(len(pick)), wl.batch.ctx_len[pick], wl.batch.q_len[pick])
+    w64 = {k: f64(v) for k, v in cs.wb.items()}
+    args = (wl.cfg, w64, f64(cs.kb[wl.batch.slot[pick]]), f64(cs.vb[wl.batch.slot[pick]]), sub,
+            f64(cs.xb[pick]))
+    ref = oracle.layer_forward(*args, storage="bf16")
+    ex = oracle.layer_forward(*args)
+    assert_e2e(to_host_f64(out)[pick], ex["out"], f"{label} rows", emul=ref["out"])
+    # the rows written went to the blocks the table names
+    kr, vr = cs.cache_rows()
+    assert_e2e(kr[pick], ex["k_new"], f"{label} K rows", emul=ref["k_new"])
+    assert_e2e(vr[pick], ex["v_new"], f"{label} V rows", emul=ref["v_new"])
+
+
+@pytest.mark.parametrize("block_size", [64, 128])
+def test_paged_7b_ragged_prefill_against_oracle(block_size):
+    """A fresh prefill, a chunk whose cached prefix ends mid-block (130 rows),
+    a single-token sequence and a chunk crossing blocks, on a paged cache only."""
+    cfg = layer_7b()
+    batch = B([0, 2, 3, 1], [0, 130, 513, 64], [300, 200, 1, 65])
+    cs = PagedCase(cfg, batch, 4, 1024, block_size, seed=7)
+    out, ws = cs.run()
+    rows = np.array([0, 1, 127, 128, 299, 300, 301, 363, 364, 499, 500, 501, 564])
+    label = f"paged bs{block_size} ragged"
+    x1, act, w = stage_parity(cs, ws, rows, label=label)
+    check_down(cs, out, x1, act, w, rows, label)
+    ref = cs.oracle(rows=rows)
+    ex = cs.oracle(rows=rows, storage=None)
+    assert_e2e(to_host_f64(out)[rows], ex["out"], f"{label} rows", emul=ref["out"])
+    kr, vr = cs.cache_rows()
+    assert_e2e(kr, ex["k_new"], f"{label} K rows", emul=ref["k_new"])
+    assert_e2e(vr, ex["v_new"], f"{label} V rows", emul=ref["v_new"])

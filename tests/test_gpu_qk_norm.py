@@ -21,7 +21,8 @@ from oracle import layer as OL
 from paper_2606_29629_amd import _lib as T
 from paper_2606_29629_amd.workload import to_host_f64
 from synth import LayerConfig, layer_7b, layer_c1
-from test_gpu_layer import (B, Case, assert_close, assert_rounded, check_down, f64,
+from parity import strict_shape
+from test_gpu_layer import (B, Case, assert_e2e, assert_rounded, check_down, f64,
                             stage_parity, ws_view)
 
 pytestmark = pytest.mark.gpu
@@ -71,7 +72,8 @@ def end_to_end(cs, out, s, local, label):
     args = (cs.cfg, w, f64(cs.kb[[sl]]), f64(cs.vb[[sl]]), sub, f64(cs.xb[t0:t0 + ql]))
     ref = oracle.layer_forward(*args, rows=local, storage="bf16")
     ex = oracle.layer_forward(*args, rows=local)
-    assert_close(to_host_f64(out)[t0 + np.asarray(local)], ref["out"], label, exact=ex["out"])
+    assert_e2e(to_host_f64(out)[t0 + np.asarray(local)], ex["out"], label, emul=ref["out"],
+               strict=strict_shape(cs.cfg))
 
 
 @pytest.mark.parametrize("bias", [False, True])
@@ -85,12 +87,11 @@ def test_tiny_ragged_mixed(bias):
     rows = np.arange(batch.n_tokens)
     x1, act, w = stage_parity(cs, ws, rows, label="tiny qk-norm")
     check_down(cs, out, x1, act, w, rows, "tiny qk-norm")
-    ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "tiny qk-norm out",
-                 exact=cs.oracle(storage=None)["out"])
+    ex = cs.oracle(storage=None)
+    assert_e2e(to_host_f64(out), ex["out"], f"tiny qk-norm out (bias {bias})", strict=True)
     kr, vr = cs.cache_rows()
-    assert_close(kr, ref["k_new"], "tiny qk-norm K")
-    assert_close(vr, ref["v_new"], "tiny qk-norm V")
+    assert_e2e(kr, ex["k_new"], "tiny qk-norm K", strict=True)
+    assert_e2e(vr, ex["v_new"], "tiny qk-norm V", strict=True)
 
 
 @pytest.mark.parametrize("cfg", [qkn(layer_c1()), qkn(layer_7b(), True)], ids=["D64", "D128_bias"])
@@ -103,8 +104,8 @@ def test_short_batch_and_decode(cfg):
     x1, act, w = stage_parity(cs, ws, rows, label="short qk-norm")
     check_down(cs, out, x1, act, w, rows, "short qk-norm")
     ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "short qk-norm out",
-                 exact=cs.oracle(storage=None)["out"])
+    assert_e2e(to_host_f64(out), cs.oracle(storage=None)["out"], f"H{cfg.hidden} short qk-norm out",
+               emul=ref["out"], strict=strict_shape(cfg))
 
     cs = Case(cfg, B([0, 1, 2, 3], [1, 64, 129, 250], [1, 1, 1, 1]), 4, 256, seed=5, x_step=0)
     out, ws = cs.run(decode=True)
@@ -113,8 +114,8 @@ def test_short_batch_and_decode(cfg):
     x1, act, w = stage_parity(cs, ws, rows, label="decode qk-norm")
     check_down(cs, out, x1, act, w, rows, "decode qk-norm")
     ref = cs.oracle()
-    assert_close(to_host_f64(out), ref["out"], "decode qk-norm out",
-                 exact=cs.oracle(storage=None)["out"])
+    assert_e2e(to_host_f64(out), cs.oracle(storage=None)["out"],
+               f"H{cfg.hidden} decode qk-norm out", emul=ref["out"], strict=strict_shape(cfg))
 
 
 def test_7b_ragged_prefill():

@@ -1,5 +1,5 @@
 """Work model of the layer stages (tri_layer_work) and the time-weighted phase
-intensity of Section III-B, Eq. 5 (tri_phase_intensity).  Host code only:
+intensity of Section III-C, Eq. 5 (tri_phase_intensity).  Host code only:
 nothing here touches a GPU.
 
 The totals are pinned to the algorithmic flop and byte counts derived for the
