@@ -105,12 +105,15 @@ tri_status tri_layer_work(const tri_layer_config* cfg, int32_t decode, int32_t n
   if (flash)
     a.add(ST_ATTN_PREFILL, 4.0 * D * Hq * fl_pairs,
           fl_tok * Hq * D * bf * 2 + fl_rows * Hkv * D * bf * 2);
-  // The split-KV and merge stages are launched on every call (sequences that
-  // are not theirs exit at once).
-  const double part_elems = dec_parts * Hq * (D + 2);  // (m, l, acc[D]) per split
-  a.add(ST_ATTN_DECODE, 4.0 * D * Hq * dec_keys,
-        dec_tok * Hq * D * bf + dec_keys * Hkv * D * bf * 2 + part_elems * f32);
-  a.add(ST_ATTN_COMBINE, 2.0 * dec_parts * Hq * D, part_elems * f32 + dec_tok * Hq * D * bf);
+  // The split-KV and merge stages are launched unless every sequence has
+  // max_q > 1 new tokens (then none is theirs); sequences that are not theirs
+  // exit at once.
+  if (decode || max_q == 1 || (double)n_seqs * max_q != T) {
+    const double part_elems = dec_parts * Hq * (D + 2);  // (m, l, acc[D]) per split
+    a.add(ST_ATTN_DECODE, 4.0 * D * Hq * dec_keys,
+          dec_tok * Hq * D * bf + dec_keys * Hkv * D * bf * 2 + part_elems * f32);
+    a.add(ST_ATTN_COMBINE, 2.0 * dec_parts * Hq * D, part_elems * f32 + dec_tok * Hq * D * bf);
+  }
 
   // O projection + residual, then RMSNorm(x1; mlp_norm) -- one stage for a
   // short batch, whose split-K reduction applies the norm (x1 then never

@@ -49,8 +49,14 @@ def test_dense_prefill_flops(lib):
     assert sum(s[k]["flops"] for k in LINEAR) == pytest.approx(7.636e12, rel=2e-4)
     assert s["attn_prefill"]["flops"] == pytest.approx(0.2406e12, rel=2e-4)
     assert total(work("dense_prefill"), "flops") == pytest.approx(7.877e12, rel=5e-4)
-    # no single-token sequence: the split-KV stages launch but do nothing
-    assert s["attn_decode"]["flops"] == 0 and s["attn_combine"]["flops"] == 0
+    # every sequence has 2048 new tokens: the split-KV stages are not launched
+    assert "attn_decode" not in s and "attn_combine" not in s
+    # ragged prefill lengths (no single-token sequence either): launched, no work
+    from synth import Batch
+    rag = Batch(np.arange(2, dtype=np.int32), np.zeros(2, np.int32),
+                np.array([2048, 1000], np.int32))
+    sr = stages(work("dense_prefill", batch=rag))
+    assert sr["attn_decode"]["flops"] == 0 and sr["attn_combine"]["bytes"] == 0
     assert not any(k.startswith("moe_") for k in s)
 
 
@@ -166,9 +172,12 @@ def test_phase_intensity_eq5(lib):
     # time on a stage the call does not launch is ignored
     got = T.phase_intensity(w, prof({"gate_up": 3.0, "attn_prefill": 5.0}))
     assert got == pytest.approx(ai["gate_up"], rel=1e-12)
-    # a launched stage with no work (split-KV stages of an all-prefill batch)
-    # drops out whatever its time
-    wp = work("dense_prefill")
+    # a launched stage with no work (split-KV stages of a ragged all-prefill
+    # batch) drops out whatever its time
+    from synth import Batch
+    rag = Batch(np.arange(2, dtype=np.int32), np.zeros(2, np.int32),
+                np.array([2048, 1000], np.int32))
+    wp = work("dense_prefill", batch=rag)
     sp = stages(wp)
     assert sp["attn_decode"]["bytes"] == 0
     p = T.Profile()
