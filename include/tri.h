@@ -64,7 +64,9 @@ typedef enum {
   TRI_ERR_ALIGN = -5,       /* a device pointer is not 16-byte aligned            */
   TRI_ERR_WORKSPACE = -6,   /* workspace smaller than tri_workspace_size()        */
   TRI_ERR_HIP = -7,         /* a HIP launch failed                                */
-  TRI_ERR_ALIAS = -8        /* an output overlaps an input it must not overlap    */
+  TRI_ERR_ALIAS = -8,       /* an output overlaps an input it must not overlap    */
+  TRI_ERR_SCRATCH = -9      /* the call needs more than the library's fixed
+                               scratch (tri_layer_decode_noalloc)               */
 } tri_status;
 
 typedef enum { TRI_BF16 = 0, TRI_F32 = 1 } tri_dtype;
@@ -216,6 +218,26 @@ tri_status tri_layer_decode(const tri_layer_config* cfg, const tri_layer_weights
                             const void* x_in, void* x_out, int32_t* route_idx,
                             float* route_w, void* workspace, size_t workspace_bytes,
                             void* stream);
+
+/* The decode step of tri_layer_decode without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  The scratch lives
+ * in a fixed device array of TRI_NOALLOC_SCRATCH_BYTES inside the library,
+ * one per GPU, held until the process ends; the call itself allocates
+ * nothing (no hipMalloc, no allocating library routine, no profiling events).
+ * Same arguments and results as tri_layer_decode, minus the workspace.
+ * Errors: those of tri_layer_decode; TRI_ERR_SCRATCH, before any launch, when
+ * tri_workspace_size() of the batch exceeds TRI_NOALLOC_SCRATCH_BYTES (64 MiB:
+ * the 7B-class decode at batch 64 and KV 4096 needs 34 MiB, the 128-expert
+ * MoE decode at batch 128 and KV 2048 60 MiB); TRI_ERR_HIP if the scratch's
+ * device address cannot be obtained.  Calls on one GPU share its scratch:
+ * calls that overlap in time on one GPU (several streams or host threads)
+ * race and must be serialised by the caller.                                */
+#define TRI_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+tri_status tri_layer_decode_noalloc(const tri_layer_config* cfg, const tri_layer_weights* w,
+                                    const tri_kv_cache* cache, const tri_batch* batch,
+                                    const void* x_in, void* x_out, int32_t* route_idx,
+                                    float* route_w, void* stream);
 
 /* KV-cache append (the cache write of Section II-A's decode loop, done inside
  * the layer calls as well): for every new token t of sequence s,

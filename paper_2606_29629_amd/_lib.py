@@ -15,6 +15,8 @@ LIB_PATH = os.path.join(HERE, "libtri.so")
 
 TRI_OK, TRI_ERR_NULL, TRI_ERR_SHAPE, TRI_ERR_UNSUPPORTED = 0, -1, -2, -3
 TRI_ERR_RANGE, TRI_ERR_ALIGN, TRI_ERR_WORKSPACE, TRI_ERR_HIP, TRI_ERR_ALIAS = -4, -5, -6, -7, -8
+TRI_ERR_SCRATCH = -9
+NOALLOC_SCRATCH_BYTES = 64 << 20
 TRI_BF16, TRI_F32 = 0, 1
 TRI_F_QKV_BIAS, TRI_F_MOE, TRI_F_MOE_RENORM, TRI_F_QK_NORM, TRI_F_MROPE = 1, 2, 4, 8, 16
 
@@ -79,6 +81,8 @@ _FUNCS = {
                           + [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "tri_layer_decode": (ctypes.c_int, [ctypes.c_void_p] * 4 + [ctypes.c_void_p] * 4
                          + [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "tri_layer_decode_noalloc": (ctypes.c_int, [ctypes.c_void_p] * 4 + [ctypes.c_void_p] * 4
+                                 + [ctypes.c_void_p]),
     "tri_kvcache_append": (ctypes.c_int, [ctypes.c_void_p] * 6),
     "tri_moe_route": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
@@ -267,6 +271,23 @@ def layer_decode(cfg, w, cache, batch, x, out=None, workspace=None, route_idx=No
     """One decode step (one new token per sequence); returns (out, workspace)."""
     return _layer("tri_layer_decode", cfg, w, cache, batch, x, out, workspace, route_idx,
                   route_w, stream)
+
+
+def layer_decode_noalloc(cfg, w, cache, batch, x, out=None, route_idx=None, route_w=None,
+                         stream=None):
+    """One decode step on the library's fixed device scratch (no workspace;
+    tri_layer_decode_noalloc); returns out."""
+    import torch
+    if out is None:
+        out = torch.empty_like(x)
+    ws = weights_struct(w)
+    kc = kv_struct(cache)
+    b = batch.struct()
+    _check(lib().tri_layer_decode_noalloc(ctypes.byref(cfg), ctypes.byref(ws), ctypes.byref(kc),
+                                          ctypes.byref(b), _ptr(x), _ptr(out), _ptr(route_idx),
+                                          _ptr(route_w), _stream(stream)),
+           "tri_layer_decode_noalloc")
+    return out
 
 
 def kvcache_append(cfg, cache, batch, k_new, v_new, stream=None) -> None:

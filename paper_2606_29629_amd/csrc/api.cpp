@@ -556,6 +556,7 @@ const char* tri_status_string(tri_status s) {
     case TRI_ERR_WORKSPACE: return "workspace too small";
     case TRI_ERR_HIP: return "HIP launch failed";
     case TRI_ERR_ALIAS: return "output overlaps an input";
+    case TRI_ERR_SCRATCH: return "batch needs more than the fixed scratch of the no-allocation entry";
   }
   return "unknown status";
 }

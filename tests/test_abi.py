@@ -264,8 +264,28 @@ def test_kvcache_append_and_route_validation(lib):
     assert lib.tri_moe_route(ctypes.byref(m), FAKE, FAKE, -1, FAKE, FAKE, None) == T.TRI_ERR_SHAPE
 
 
+def test_noalloc_rejects_batches_beyond_its_scratch(lib):
+    """The no-allocation decode entry refuses, before touching any device, a
+    batch whose workspace would exceed its fixed scratch."""
+    c = cfg(hidden=3584, n_q_heads=28, n_kv_heads=4, head_dim=128, ffn_dim=18944)
+    b = batch(n_seqs=512, n_tokens=512, max_q=1, max_ctx=30000)
+    need = ctypes.c_size_t()
+    assert lib.tri_workspace_size(ctypes.byref(c), ctypes.byref(b), ctypes.byref(need)) == 0
+    assert need.value > T.NOALLOC_SCRATCH_BYTES
+    kv = T.KVCache(FAKE, FAKE + (1 << 30), 512, 30080, None, 0, 0)
+    w = weights()
+    st = lib.tri_layer_decode_noalloc(ctypes.byref(c), ctypes.byref(w), ctypes.byref(kv),
+                                      ctypes.byref(b), FAKE + (2 << 30), FAKE + (3 << 30), None,
+                                      None, None)
+    assert st == T.TRI_ERR_SCRATCH
+    # validation errors come first, as in tri_layer_decode
+    st = lib.tri_layer_decode_noalloc(None, ctypes.byref(w), ctypes.byref(kv), ctypes.byref(b),
+                                      FAKE, FAKE, None, None, None)
+    assert st == T.TRI_ERR_NULL
+
+
 def test_status_strings(lib):
-    for s in range(-8, 1):
+    for s in range(-9, 1):
         assert T.status_string(s) and T.status_string(s) != "unknown status"
     assert T.status_string(-99) == "unknown status"
 
