@@ -671,7 +671,7 @@ def main(argv=None):
     if not args.no_secondary:
         res["secondary"] = []
         for n in ("moe_prefill", "moe_decode", "mixed", "dense_prefill_qkn", "moe_prefill_qkn",
-                  "dense_prefill_bias", "dense_decode_bias"):
+                  "dense_prefill_bias", "dense_decode_bias", "talker_prefill", "talker_decode"):
             r, phases[n] = run_secondary(args, tri, n)
             res["secondary"].append(r)
     res["phases"] = phases

@@ -239,6 +239,14 @@ def layer_moe() -> LayerConfig:
                        n_experts=128, top_k=8, expert_ffn_dim=768)
 
 
+def layer_talker() -> LayerConfig:
+    """A Talker-shaped layer: the paper's Talker (Section II-A) is an
+    autoregressive transformer decoder whose shapes it does not give; the
+    reading here is a 0.5B-class dense decoder of the same model family
+    (hidden 896, 14 query / 2 KV heads of 64, SwiGLU 4864)."""
+    return LayerConfig(hidden=896, n_q_heads=14, n_kv_heads=2, head_dim=64, ffn_dim=4864)
+
+
 def _ints(*v) -> np.ndarray:
     return np.asarray(v, dtype=np.int32)
 
@@ -275,6 +283,17 @@ def workload(name: str, seed: int = 0) -> Workload:
                         Batch(np.arange(33, dtype=np.int32), np.concatenate([_ints(6144), lens]),
                               np.concatenate([_ints(512), np.ones(32, np.int32)])),
                         cache_prefilled=True, seed=seed)
+    if name == "talker_prefill":
+        return Workload(name, "Talker-shaped layer (H896, 14q/2kv heads, D64, F4864) prefill, "
+                        "8 x 512 tokens", layer_talker(), 8, 512,
+                        Batch(np.arange(8, dtype=np.int32), np.zeros(8, np.int32),
+                              np.full(8, 512, np.int32)), seed=seed)
+    if name == "talker_decode":
+        return Workload(name, "Talker-shaped layer decode, batch 64 streams, KV 1024, 32 steps",
+                        layer_talker(), 64, 1024 + 32,
+                        Batch(np.arange(64, dtype=np.int32), np.full(64, 1024, np.int32),
+                              np.ones(64, np.int32)),
+                        decode_steps=31, cache_prefilled=True, seed=seed)
     if name in ("dense_prefill_bias", "dense_decode_bias"):
         # the 7B workloads with the q/k/v bias of the Qwen2 family (seeded, N(0, 0.2))
         base = workload(name[:-5], seed)
@@ -292,7 +311,8 @@ def workload(name: str, seed: int = 0) -> Workload:
 
 
 WORKLOADS = ("tiny", "dense_prefill", "dense_decode", "moe_prefill", "moe_decode", "mixed",
-             "dense_prefill_qkn", "moe_prefill_qkn", "dense_prefill_bias", "dense_decode_bias")
+             "dense_prefill_qkn", "moe_prefill_qkn", "dense_prefill_bias", "dense_decode_bias",
+             "talker_prefill", "talker_decode")
 
 
 def make_x(cfg: LayerConfig, n_tokens: int, seed: int = 0, step: Optional[int] = None) -> np.ndarray:
