@@ -41,9 +41,17 @@
  *    the host.  Kernels never read or write outside the buffers described
  *    here: a token whose slot is >= n_slots or whose cache row is >= max_seq
  *    is skipped (its outputs are unspecified).
- *  - Element type: bfloat16 storage (TRI_BF16), float32 accumulation.
- *    Weights are row-major [out, in].  All device buffers must be 16-byte
- *    aligned.
+ *  - Element type ("storage type" below): bfloat16 (TRI_BF16, the serving
+ *    path) or float32 (TRI_F32, the tight-parity mode) for the weights, the
+ *    activations, the KV cache and the workspace intermediates, as
+ *    tri_layer_config.dtype says; arithmetic accumulates in float32 in both.
+ *    TRI_F32 runs the same kernels on fp32 storage: every projection on the
+ *    matrix cores over bf16 operand planes of the fp32 values (activations
+ *    split hi | lo | hi, weights hi | hi | lo, v = hi + lo with hi = bf16(v),
+ *    lo = bf16(v - hi)), which keeps each product to ~2^-16 relative, and
+ *    attention on the fp32 matrix instruction; it rebuilds the weight planes
+ *    in the workspace on every call and is not meant for speed.  Weights are
+ *    row-major [out, in].  All device buffers must be 16-byte aligned.
  */
 #ifndef TRI_H
 #define TRI_H
@@ -99,14 +107,14 @@ typedef struct {
   int32_t expert_ffn_dim; /* per-expert SwiGLU width (MoE only); multiple of 64     */
   float rms_eps;          /* RMSNorm epsilon (>= 0)                                 */
   float rope_base;        /* rotary base (> 0)                                      */
-  int32_t dtype;          /* tri_dtype; only TRI_BF16 is implemented                */
+  int32_t dtype;          /* tri_dtype: storage type of every tensor of the call    */
   int32_t flags;          /* TRI_F_* bits                                           */
   int32_t mrope_section[3]; /* TRI_F_MROPE: frequencies per section (temporal,
                              height, width), each >= 0, summing to D/2
                              (TRI_ERR_SHAPE otherwise); ignored without the flag   */
 } tri_layer_config;
 
-/* Device pointers to one layer's weights, row-major [out, in], bfloat16.       */
+/* Device pointers to one layer's weights, row-major [out, in], storage type.   */
 typedef struct {
   const void* attn_norm; /* [H]                                                    */
   const void* w_qkv;     /* [(Hq + 2 Hkv) D, H]: q heads, then k heads, then v     */
@@ -121,7 +129,7 @@ typedef struct {
   const void* k_norm;    /* [D]; required iff TRI_F_QK_NORM, else ignored          */
 } tri_layer_weights;
 
-/* KV cache (device, bfloat16).  Keys are stored after the rotary embedding.
+/* KV cache (device, storage type).  Keys are stored after the rotary embedding.
  * Row r of a slot holds the token at position r of the sequence occupying
  * that slot.  Two layouts:
  *  - contiguous (block_table == NULL): K and V each [n_slots, Hkv, max_seq, D];
@@ -167,15 +175,16 @@ typedef struct {
 } tri_batch;
 
 /* Byte offsets of the layer's intermediates inside the workspace (for
- * inspection after a call; contents are valid once the stream has finished).  */
+ * inspection after a call; contents are valid once the stream has finished).
+ * Element type of h .. act: the storage type.                                 */
 typedef struct {
-  size_t h;      /* [T, H]   bf16  RMSNorm(x)                                       */
-  size_t q;      /* [T, Hq, D] bf16  rotated queries                                */
-  size_t attn;   /* [T, Hq D] bf16  attention output                                */
-  size_t x1;     /* [T, H]   bf16  x + attn W_o^T                                   */
-  size_t h2;     /* [T, H]   bf16  RMSNorm(x1)                                      */
-  size_t act;    /* dense: [T, F] bf16 SwiGLU activation silu(g)*u;
-                    MoE: [T*top_k, Fe] bf16, rows in routed order                  */
+  size_t h;      /* [T, H]   RMSNorm(x)                                             */
+  size_t q;      /* [T, Hq, D] rotated queries                                      */
+  size_t attn;   /* [T, Hq D] attention output                                      */
+  size_t x1;     /* [T, H]   x + attn W_o^T                                         */
+  size_t h2;     /* [T, H]   RMSNorm(x1)                                            */
+  size_t act;    /* dense: [T, F] SwiGLU activation silu(g)*u;
+                    MoE: [T*top_k, Fe], rows in routed order                       */
   size_t perm;   /* MoE: [T*top_k] int32 routed order -> pair id t*top_k + j
                     (pairs grouped by expert, ascending pair id within an expert)   */
   size_t y;      /* MoE: [T*top_k, H] fp32 expert outputs, rows in routed order     */
@@ -195,8 +204,8 @@ tri_status tri_workspace_layout(const tri_layer_config* cfg, const tri_batch* ba
 
 /* One decoder layer over a ragged batch (prefill, chunked prefill with a
  * cached prefix, decode, or any mix: the mixed step of Section III-A1).
- *  x_in      device [T, H] bf16, token activations in batch order
- *  x_out     device [T, H] bf16, layer output; must not overlap x_in
+ *  x_in      device [T, H] storage type, token activations in batch order
+ *  x_out     device [T, H] storage type, layer output; must not overlap x_in
  *  route_idx device [T, top_k] int32 or NULL (MoE: chosen experts, descending
  *            logit, ties to the lower expert index)
  *  route_w   device [T, top_k] float or NULL (MoE: routing weights)
@@ -242,7 +251,7 @@ tri_status tri_layer_decode_noalloc(const tri_layer_config* cfg, const tri_layer
 /* KV-cache append (the cache write of Section II-A's decode loop, done inside
  * the layer calls as well): for every new token t of sequence s,
  *   k[slot[s]][h][ctx_len[s] + i][:] = k_new[t][h][:]   (same for v).
- *  k_new, v_new  device [T, Hkv, D] bf16.                                       */
+ *  k_new, v_new  device [T, Hkv, D], storage type.                              */
 tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* cache,
                               const tri_batch* batch, const void* k_new, const void* v_new,
                               void* stream);
@@ -250,10 +259,10 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
 /* MoE routing alone (test hook for bit-exact routing): logits = h2 W_r^T in
  * float32 (one fixed summation order per logit), softmax over all experts,
  * top_k by logit (descending, ties to the lower index), weights p[idx]
- * (renormalised if TRI_F_MOE_RENORM).  Inside the layer the router reads the
- * bf16 h2 (widened exactly to float32).
+ * (renormalised if TRI_F_MOE_RENORM).  Inside the layer the router reads h2
+ * in the storage type (bf16 widened exactly to float32, or float32).
  *  h2        device [n_tokens, H] float32
- *  w_router  device [E, H] bf16
+ *  w_router  device [E, H] storage type
  *  idx, w    device [n_tokens, top_k] int32 / float32                          */
 tri_status tri_moe_route(const tri_layer_config* cfg, const float* h2, const void* w_router,
                          int32_t n_tokens, int32_t* idx, float* w, void* stream);
@@ -286,10 +295,12 @@ tri_status tri_profile_read(tri_profile* out);
  *         (RMSNorm 4 per element, split merge 2 per partial element, MoE
  *         combine 2 per routed element).  Rotary, softmax and SwiGLU
  *         transcendentals are not counted.
- *  bytes  compulsory HBM traffic: every input a stage reads and every output
- *         it writes, once (weights, activations, the K/V rows attended, once
- *         per KV head, cache rows written, the split-KV partials passed from
- *         attn_decode to attn_combine).  On-chip re-reads are not counted.
+ *  bytes  compulsory HBM traffic in the storage type: every input a stage
+ *         reads and every output it writes, once (weights, activations, the
+ *         K/V rows attended, once per KV head, cache rows written, the
+ *         split-KV partials passed from attn_decode to attn_combine).
+ *         On-chip re-reads are not counted.  (The model follows the bf16
+ *         launch sequence; the fp32 mode's operand planes are not counted.)
  * Arguments (host memory):
  *  decode         1 for tri_layer_decode's launch sequence, 0 for
  *                 tri_layer_prefill's

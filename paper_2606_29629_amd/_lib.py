@@ -123,8 +123,10 @@ def _check(status: int, what: str) -> None:
         raise TriError(status, what)
 
 
-def make_config(cfg) -> LayerConfig:
-    """LayerConfig from any object with the layer's attribute names."""
+def make_config(cfg, f32: bool = False) -> LayerConfig:
+    """LayerConfig from any object with the layer's attribute names; f32
+    selects the fp32 storage mode (TRI_F32: fp32 weights, activations and
+    cache)."""
     flags = 0
     if getattr(cfg, "qkv_bias", False):
         flags |= TRI_F_QKV_BIAS
@@ -142,7 +144,7 @@ def make_config(cfg) -> LayerConfig:
                        int(cfg.head_dim), int(getattr(cfg, "ffn_dim", 0) or 0), n_exp,
                        int(getattr(cfg, "top_k", 0) or 0),
                        int(getattr(cfg, "expert_ffn_dim", 0) or 0), float(cfg.rms_eps),
-                       float(cfg.rope_base), TRI_BF16, flags,
+                       float(cfg.rope_base), TRI_F32 if f32 else TRI_BF16, flags,
                        (ctypes.c_int32 * 3)(*(sec or (0, 0, 0))))
 
 

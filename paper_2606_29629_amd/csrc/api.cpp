@@ -17,6 +17,7 @@ using namespace tri;
 
 namespace {
 bool is_moe(const tri_layer_config* c) { return (c->flags & TRI_F_MOE) != 0; }
+bool is_f32(const tri_layer_config* c) { return c->dtype == TRI_F32; }
 
 // Rotary frequency sections: frequency i < s0 reads position plane 0, i < s01
 // plane 1, the rest plane 2 (one plane, s0 = s01 = D/2, without TRI_F_MROPE).
@@ -29,7 +30,7 @@ RopeSections rope_sections(const tri_layer_config* c) {
 
 tri_status tri::check_config(const tri_layer_config* c) {
   if (!c) return TRI_ERR_NULL;
-  if (c->dtype != TRI_BF16) return TRI_ERR_UNSUPPORTED;
+  if (c->dtype != TRI_BF16 && c->dtype != TRI_F32) return TRI_ERR_UNSUPPORTED;
   if (c->flags & ~TRI_F_ALL) return TRI_ERR_UNSUPPORTED;
   if (c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0)
     return TRI_ERR_SHAPE;
@@ -78,6 +79,9 @@ struct Layout {
   size_t tok_slot, tok_row, rope, h, q, attn, x1, h2, act, part;
   // MoE (n_pairs = T * top_k)
   size_t route_idx, route_w, rank, counts, perm, inv, seg, tile_off, y, logits;
+  // fp32 storage: bf16 operand planes of the activations (one GEMM at a time)
+  // and of the weights (q/k/v, O, gate/up, down)
+  size_t a3, w_qkv3, w_o3, w_gu3, w_d3;
   size_t total;
 };
 
@@ -132,7 +136,53 @@ KvDev kv_dev(const tri_kv_cache* c) {
   return kv;
 }
 
+// fp32 storage: activations in fp32, every projection on bf16 operand planes
+// (split3: activations [hi | lo | hi], weights [hi | hi | lo], a 3K
+// contraction), attention through the flash kernel for every sequence (no
+// split-KV partials), the large GEMMs' tail partials.
+Layout layout_f32(const tri_layer_config* c, const tri_batch* b) {
+  const size_t T = (size_t)b->n_tokens, H = c->hidden, D = c->head_dim;
+  const size_t Hq = c->n_q_heads, Hkv = c->n_kv_heads;
+  const bool moe = is_moe(c);
+  const size_t P = moe ? T * c->top_k : 0, E = moe ? c->n_experts : 0;
+  const size_t F = moe ? (size_t)c->expert_ffn_dim : (size_t)c->ffn_dim;
+  const size_t act_rows = moe ? P : T;
+  const size_t Nqkv = (Hq + 2 * Hkv) * D;
+  const size_t f = 4, pl = 3 * 2;  // fp32 element; three bf16 planes per element
+  Layout l{};
+  size_t o = 0;
+  l.tok_slot = o; o += up(T * 4);
+  l.tok_row = o;  o += up(T * 4);
+  l.rope = o;     o += up(T * (D / 2) * 8);
+  l.h = o;        o += up(T * H * f);
+  l.q = o;        o += up(T * Hq * D * f);
+  l.attn = o;     o += up(T * Hq * D * f);
+  l.x1 = o;       o += up(T * H * f);
+  l.h2 = o;       o += up(T * H * f);
+  l.act = o;      o += up(act_rows * F * f);
+  l.part = o;     o += up(T > 0 ? gemm_tail_bytes() : 0);
+  l.route_idx = o; o += up(P * 4);
+  l.route_w = o;  o += up(P * 4);
+  l.rank = o;     o += up(P * 4);
+  l.counts = o;   o += up(E * 4);
+  l.perm = o;     o += up(P * 4);
+  l.inv = o;      o += up(P * 4);
+  l.seg = o;      o += up((E + 1) * 4);
+  l.tile_off = o; o += up((E + 1) * 4);
+  l.y = o;        o += up(P * H * 4);
+  const size_t a_cols = std::max(std::max(H, Hq * D), F);  // widest activation operand
+  l.a3 = o;       o += up(std::max(T, act_rows) * a_cols * pl);
+  l.w_qkv3 = o;   o += up(Nqkv * H * pl);
+  l.w_o3 = o;     o += up(H * Hq * D * pl);
+  const size_t experts = moe ? E : 1;
+  l.w_gu3 = o;    o += up(experts * 2 * F * H * pl);
+  l.w_d3 = o;     o += up(experts * H * F * pl);
+  l.total = o;
+  return l;
+}
+
 Layout layout_of(const tri_layer_config* c, const tri_batch* b) {
+  if (is_f32(c)) return layout_f32(c, b);
   const size_t T = (size_t)b->n_tokens, H = c->hidden, D = c->head_dim;
   const bool moe = is_moe(c);
   const size_t P = moe ? T * c->top_k : 0, E = moe ? c->n_experts : 0;
@@ -228,6 +278,169 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   return x < y + nb && y < x + na;
 }
 
+// The fp32 storage mode's launch sequence (arguments already validated): the
+// same stages on fp32 activations, cache and weights.  Every projection runs
+// the prefill GEMM on bf16 operand planes (activations [hi | lo | hi] against
+// weights [hi | hi | lo] over 3K: the products a_hi b_hi + a_lo b_hi + a_hi
+// b_lo, fp32 accumulation), with the same fused epilogues storing fp32; every
+// sequence's attention runs the flash kernel on the fp32 matrix instruction.
+// Used for tight parity, not for speed: the weight planes are rebuilt on
+// every call.
+tri_status layer_f32(const tri_layer_config* cfg, const tri_layer_weights* w,
+                     const tri_kv_cache* cache, const tri_batch* b, const void* x_in, void* x_out,
+                     int32_t* route_idx, float* route_w, void* ws, const Layout& L, bool timed,
+                     hipStream_t s) {
+  const int T = b->n_tokens, H = cfg->hidden, D = cfg->head_dim;
+  const int Hq = cfg->n_q_heads, Hkv = cfg->n_kv_heads, F = cfg->ffn_dim;
+  const int Nqkv = (Hq + 2 * Hkv) * D;
+  const bool moe = is_moe(cfg);
+  BatchDev bd{b->cu_q, b->ctx_len, b->slot, b->pos, b->n_seqs, b->n_tokens, b->max_q_len,
+              b->max_ctx_len};
+  const KvDev kv = kv_dev(cache);
+  int32_t* tok_slot = at<int32_t>(ws, L.tok_slot);
+  int32_t* tok_row = at<int32_t>(ws, L.tok_row);
+  float2* rope = at<float2>(ws, L.rope);
+  float* h = at<float>(ws, L.h);
+  float* q = at<float>(ws, L.q);
+  float* attn = at<float>(ws, L.attn);
+  float* x1 = at<float>(ws, L.x1);
+  float* h2 = at<float>(ws, L.h2);
+  float* act = at<float>(ws, L.act);
+  float* tail = at<float>(ws, L.part);
+  void* a3 = at<void>(ws, L.a3);
+  auto planes = [&](const void* src, int64_t rows, int cols, int pattern, void* dst) {
+    return launch_split3((const float*)src, cols, rows, cols, pattern, dst, s);
+  };
+  {
+    StageTimer t_(ST_PROLOGUE, s, timed);
+    TRI_HIP(launch_prologue(bd, kv, D, cfg->rope_base, rope_sections(cfg), tok_slot, tok_row,
+                            rope, x_in, w->attn_norm, h, H, cfg->rms_eps, s, true));
+  }
+  Epi e{};
+  e.f32 = 1;
+  e.kind = EPI_QKV;
+  e.bias = (cfg->flags & TRI_F_QKV_BIAS) ? w->b_qkv : nullptr;
+  e.q = q;
+  e.kc = cache->k;
+  e.vc = cache->v;
+  e.tok_slot = tok_slot;
+  e.tok_row = tok_row;
+  e.rope = rope;
+  e.q_norm = (cfg->flags & TRI_F_QK_NORM) ? w->q_norm : nullptr;
+  e.k_norm = (cfg->flags & TRI_F_QK_NORM) ? w->k_norm : nullptr;
+  e.eps = cfg->rms_eps;
+  e.n_q_heads = Hq;
+  e.n_kv_heads = Hkv;
+  e.head_dim = D;
+  e.max_seq = kv.panel_rows();
+  {
+    StageTimer t_(ST_QKV, s, timed);
+    TRI_HIP(planes(h, T, H, 0, a3));
+    TRI_HIP(planes(w->w_qkv, Nqkv, H, 1, at<void>(ws, L.w_qkv3)));
+    TRI_HIP(launch_gemm(a3, 3 * H, at<void>(ws, L.w_qkv3), 3 * H, T, Nqkv, 3 * H, e, tail, s));
+  }
+  {
+    StageTimer t_(ST_ATTN_PREFILL, s, timed);
+    TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, kv, Hq, Hkv, D, 1, nullptr, s,
+                                true));
+  }
+  e = Epi{};
+  e.f32 = 1;
+  e.kind = EPI_RESID;
+  e.out = x1;
+  e.ldo = H;
+  e.resid = x_in;
+  e.ldr = H;
+  {
+    StageTimer t_(ST_OPROJ, s, timed);
+    TRI_HIP(planes(attn, T, Hq * D, 0, a3));
+    TRI_HIP(planes(w->w_o, H, Hq * D, 1, at<void>(ws, L.w_o3)));
+    TRI_HIP(launch_gemm(a3, 3 * Hq * D, at<void>(ws, L.w_o3), 3 * Hq * D, T, H, 3 * Hq * D, e,
+                        tail, s));
+  }
+  {
+    StageTimer t_(ST_NORM2, s, timed);
+    TRI_HIP(launch_rmsnorm(x1, w->mlp_norm, h2, nullptr, T, H, cfg->rms_eps, s, true));
+  }
+  void* wgu3 = at<void>(ws, L.w_gu3);
+  void* wd3 = at<void>(ws, L.w_d3);
+  if (!moe) {
+    e = Epi{};
+    e.f32 = 1;
+    e.kind = EPI_SWIGLU;
+    e.out = act;
+    e.ldo = F;
+    e.ffn = F;
+    {
+      StageTimer t_(ST_GATEUP, s, timed);
+      TRI_HIP(planes(h2, T, H, 0, a3));
+      TRI_HIP(planes(w->w_gate_up, 2 * F, H, 1, wgu3));
+      TRI_HIP(launch_gemm(a3, 3 * H, wgu3, 3 * H, T, 2 * F, 3 * H, e, tail, s));
+    }
+    e = Epi{};
+    e.f32 = 1;
+    e.kind = EPI_RESID;
+    e.out = x_out;
+    e.ldo = H;
+    e.resid = x1;
+    e.ldr = H;
+    StageTimer t_(ST_DOWN, s, timed);
+    TRI_HIP(planes(act, T, F, 0, a3));
+    TRI_HIP(planes(w->w_down, H, F, 1, wd3));
+    TRI_HIP(launch_gemm(a3, 3 * F, wd3, 3 * F, T, H, 3 * F, e, tail, s));
+    return TRI_OK;
+  }
+  const int E = cfg->n_experts, k = cfg->top_k, Fe = cfg->expert_ffn_dim;
+  const int P = T * k;
+  int32_t* idx = route_idx ? route_idx : at<int32_t>(ws, L.route_idx);
+  float* rw = route_w ? route_w : at<float>(ws, L.route_w);
+  int32_t* perm = at<int32_t>(ws, L.perm);
+  int32_t* inv = at<int32_t>(ws, L.inv);
+  int32_t* seg = at<int32_t>(ws, L.seg);
+  int32_t* tile_off = at<int32_t>(ws, L.tile_off);
+  float* y = at<float>(ws, L.y);
+  {
+    StageTimer t_(ST_ROUTER, s, timed);
+    TRI_HIP(launch_moe_route_f32(h2, w->w_router, T, H, E, k,
+                                 (cfg->flags & TRI_F_MOE_RENORM) ? 1 : 0, idx, rw, s, true));
+  }
+  {
+    StageTimer t_(ST_MOE_PERMUTE, s, timed);
+    TRI_HIP(launch_moe_permute(idx, P, E, moe_tile_rows(P, E), at<int32_t>(ws, L.rank),
+                               at<int32_t>(ws, L.counts), perm, inv, seg, tile_off, s));
+  }
+  e = Epi{};
+  e.f32 = 1;
+  e.kind = EPI_SWIGLU;
+  e.out = act;
+  e.ldo = Fe;
+  e.ffn = Fe;
+  {
+    StageTimer t_(ST_MOE_GATEUP, s, timed);
+    TRI_HIP(planes(h2, T, H, 0, a3));
+    TRI_HIP(planes(w->w_gate_up, (int64_t)E * 2 * Fe, H, 1, wgu3));
+    TRI_HIP(launch_gemm_grouped(a3, 3 * H, T, perm, k, wgu3, (int64_t)2 * Fe * 3 * H, 2 * Fe,
+                                3 * H, seg, tile_off, E, P, e, s));
+  }
+  e = Epi{};
+  e.f32 = 1;
+  e.kind = EPI_STORE_F32;
+  e.out = y;
+  e.ldo = H;
+  {
+    StageTimer t_(ST_MOE_DOWN, s, timed);
+    TRI_HIP(planes(act, P, Fe, 0, a3));
+    TRI_HIP(planes(w->w_down, (int64_t)E * H, Fe, 1, wd3));
+    TRI_HIP(launch_gemm_grouped(a3, 3 * Fe, P, nullptr, k, wd3, (int64_t)H * 3 * Fe, H, 3 * Fe,
+                                seg, tile_off, E, P, e, s));
+  }
+  {
+    StageTimer t_(ST_MOE_COMBINE, s, timed);
+    TRI_HIP(launch_moe_combine(x1, y, inv, rw, T, H, k, x_out, s, true));
+  }
+  return TRI_OK;
+}
+
 }  // namespace
 
 // One layer call on the caller's workspace; `timed` = false keeps the call
@@ -264,10 +477,13 @@ tri_status tri::layer_call(bool decode, bool timed, const tri_layer_config* cfg,
   if (((uintptr_t)ws & (kAlign - 1)) != 0) return TRI_ERR_ALIGN;
   const Layout L = layout_of(cfg, b);
   if (ws_bytes < L.total) return TRI_ERR_WORKSPACE;
-  const size_t act_bytes = (size_t)b->n_tokens * cfg->hidden * 2;
+  const size_t act_bytes = (size_t)b->n_tokens * cfg->hidden * (is_f32(cfg) ? 4 : 2);
   if (overlaps(x_in, act_bytes, x_out, act_bytes)) return TRI_ERR_ALIAS;
   if (overlaps(ws, L.total, x_in, act_bytes) || overlaps(ws, L.total, x_out, act_bytes))
     return TRI_ERR_ALIAS;
+  if (is_f32(cfg))
+    return layer_f32(cfg, w, cache, b, x_in, x_out, route_idx, route_w, ws, L, timed,
+                     (hipStream_t)stream);
 
   hipStream_t s = (hipStream_t)stream;
   const int T = b->n_tokens, H = cfg->hidden, D = cfg->head_dim;
@@ -472,7 +688,7 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
   if (!cfg) return TRI_ERR_NULL;
   if (cfg->head_dim != 64 && cfg->head_dim != 128) return TRI_ERR_UNSUPPORTED;
   if (cfg->n_kv_heads <= 0) return TRI_ERR_SHAPE;
-  if (cfg->dtype != TRI_BF16) return TRI_ERR_UNSUPPORTED;
+  if (cfg->dtype != TRI_BF16 && cfg->dtype != TRI_F32) return TRI_ERR_UNSUPPORTED;
   if (!cache) return TRI_ERR_NULL;
   tri_status st = check_batch_scalars(b);
   if (st != TRI_OK) return st;
@@ -488,7 +704,7 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
   StageTimer t_(ST_APPEND, (hipStream_t)stream);
   TRI_HIP(launch_kv_append_direct(bd, kv_dev(cache), cfg->n_kv_heads,
                                   cfg->head_dim, k_new, v_new, cache->k, cache->v,
-                                  (hipStream_t)stream));
+                                  (hipStream_t)stream, is_f32(cfg)));
   return TRI_OK;
 }
 
@@ -504,7 +720,7 @@ tri_status tri_moe_route(const tri_layer_config* cfg, const float* h2, const voi
   StageTimer t_(ST_ROUTER, (hipStream_t)stream);
   TRI_HIP(launch_moe_route_f32(h2, w_router, n_tokens, cfg->hidden, cfg->n_experts, cfg->top_k,
                                (cfg->flags & TRI_F_MOE_RENORM) ? 1 : 0, idx, w,
-                               (hipStream_t)stream));
+                               (hipStream_t)stream, is_f32(cfg)));
   return TRI_OK;
 }
 

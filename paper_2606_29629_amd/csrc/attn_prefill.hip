@@ -22,6 +22,14 @@
 // 16 significant bits.  Softmax in the log2 domain: one FMA (scale and max)
 // and one v_exp_f32 per score; the running max is raised lazily (only past a
 // slack of 8), so the accumulators are rescaled on few tiles.
+//
+// fp32 storage (F32, the tight-parity mode): q, the cache and the output are
+// fp32, tiles hold fp32 rows, and both products run on the fp32 matrix
+// instruction v_mfma_f32_32x32x2_f32 with the same tiling, mask and online
+// softmax.  Its k-step t pairs head-dim values t (lanes 0..31) and
+// D/2 + t (lanes 32..63) for S^T = K Q^T, and keys 8 j + i and 8 j + 4 + i
+// for O^T = V^T P^T, the keys each lane's score accumulator holds, so P is
+// used in fp32 where it was computed.
 #include <type_traits>
 
 #include "common.hpp"
@@ -38,24 +46,38 @@ constexpr int kFaBK = 64;   // keys per tile
 // never aliases the direct-to-LDS fill of the other, so it waits for no fill
 // before a read.
 
+// fp32 tiles: physical 16-byte chunk of logical chunk c in row r (rows of 16
+// or 32 chunks): 16 consecutive rows read one logical chunk conflict-free.
+__device__ __forceinline__ int kv_chunk_f32(int c, int r) { return c ^ (r & 15); }
+
 // SPLIT: the key tiles of a query tile are dealt to `nsplit` workgroups
 // (blockIdx.z = sequence * nsplit + split), each writing its unnormalised
 // output with its running max (log2 units) and sum to `part`
 // [nsplit][n_tokens][Hq][D + 2]; attn_prefill_combine_kernel merges them.
 // Used when the batch has too few query tiles to fill the GPU (a chunk over
 // a long cached prefix).
-template <int D, bool PAGED, bool SPLIT>
-__global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
-    bf16* __restrict__ O, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ ctx_len,
+template <int D, bool PAGED, bool SPLIT, bool F32 = false>
+__global__ __launch_bounds__(256, F32 ? 1 : 2) void attn_prefill_kernel(
+    const void* __restrict__ Qv, const void* __restrict__ Kcv, const void* __restrict__ Vcv,
+    void* __restrict__ Ov, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ ctx_len,
     const int32_t* __restrict__ slot, KvDev kv, int Hq, int Hkv, float scale_log2e,
     int include_single, int n_tokens, int nsplit, float* __restrict__ part) {
-  constexpr int DC = D / 8;                     // 16-byte chunks per row
+  using E = typename Store<F32>::T;             // storage element of q, cache, output
+  constexpr int DC = D * (int)sizeof(E) / 16;   // 16-byte chunks per row
+  constexpr int EPC = 16 / (int)sizeof(E);      // elements per chunk
   constexpr int ROWS_PER_KB = 64 / DC;          // tile rows filled by one 1 KB wave load
   constexpr int BLK = kFaBK / ROWS_PER_KB / 4;  // 1 KB loads per wave per operand and tile
   constexpr int DS = D / 16;                    // MFMA k-steps over d
   constexpr int DB = D / 32;                    // 32-row d blocks of O^T
-  __shared__ __align__(16) bf16 sk0[kFaBK * D], sk1[kFaBK * D], sv0[kFaBK * D], sv1[kFaBK * D];
+  const E* __restrict__ Q = (const E*)Qv;
+  const E* __restrict__ Kc = (const E*)Kcv;
+  const E* __restrict__ Vc = (const E*)Vcv;
+  E* __restrict__ O = (E*)Ov;
+  __shared__ __align__(16) E sk0[kFaBK * D], sk1[kFaBK * D], sv0[kFaBK * D], sv1[kFaBK * D];
+  auto chunk_of = [](int c, int r) {
+    if constexpr (F32) return kv_chunk_f32(c, r);
+    else return kv_chunk<D>(c, r);
+  };
 
   const int s = SPLIT ? (int)blockIdx.z / nsplit : (int)blockIdx.z, qh = blockIdx.y;
   const int sp = SPLIT ? (int)blockIdx.z - s * nsplit : 0;
@@ -87,14 +109,14 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   };
   // Descriptor of tile kt's rows of one operand: rows past the visible range
   // (and a block outside the pool) read as zero through the range check.
-  auto tile_rsrc = [&](const bf16* base, int kt, int panel) {
+  auto tile_rsrc = [&](const E* base, int kt, int panel) {
     const int key0 = kt * kFaBK;
     int rows = min(kFaBK, kv_len - key0), prow = key0;
     if (PAGED) prow = key0 - (key0 / kv.block_size) * kv.block_size;
     if (panel < 0) rows = panel = prow = 0;
     return __builtin_amdgcn_make_buffer_rsrc(
         (void*)(base + (((int64_t)panel * Hkv + kvh) * prows + prow) * D), (short)0,
-        rows * D * 2, 0x00020000);
+        rows * D * (int)sizeof(E), 0x00020000);
   };
   // Lane l of a 1 KB wave load fills physical chunk l % DC of tile row
   // l / DC of its block, i.e. logical chunk kv_chunk(l % DC, row) (the
@@ -103,11 +125,11 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
 #pragma unroll
   for (int j = 0; j < BLK; ++j) {
     const int row = (wave + 4 * j) * ROWS_PER_KB + lane / DC;
-    ld_off[j] = (uint32_t)((row * D + kv_chunk<D>(lane % DC, row) * 8) * 2);
+    ld_off[j] = (uint32_t)((row * D + chunk_of(lane % DC, row) * EPC) * (int)sizeof(E));
   }
   auto gload = [&](int kt, auto buf, int panel) {
-    bf16* kd = buf ? sk1 : sk0;
-    bf16* vd = buf ? sv1 : sv0;
+    E* kd = buf ? sk1 : sk0;
+    E* vd = buf ? sv1 : sv0;
     const __amdgpu_buffer_rsrc_t rk = tile_rsrc(Kc, kt, panel);
     const __amdgpu_buffer_rsrc_t rv = tile_rsrc(Vc, kt, panel);
 #pragma unroll
@@ -125,9 +147,20 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   const int qrow = q0 + min(qi, n - 1);
   const int qpos = c + qi;                 // cache row of this query
   const int wave_qmin = c + qt * kFaBQ + wave * 32;
-  bf16x8 qf[DS];
-  {
-    const bf16* qp = Q + ((int64_t)qrow * Hq + qh) * D + 8 * lg;
+  // bf16: k-step t of lane (r, g) holds q values 16 t + 8 g .. + 7;
+  // fp32: q values g D/2 .. g D/2 + D/2 - 1, one per k-step.
+  bf16x8 qf[F32 ? 1 : DS];
+  float q32[F32 ? D / 2 : 1];
+  if constexpr (F32) {
+    const float* qp = (const float*)Q + ((int64_t)qrow * Hq + qh) * D + lg * (D / 2);
+#pragma unroll
+    for (int t = 0; t < D / 8; ++t) {
+      const f32x4 v = *(const f32x4*)(qp + 4 * t);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) q32[4 * t + e] = v[e];
+    }
+  } else {
+    const bf16* qp = (const bf16*)Q + ((int64_t)qrow * Hq + qh) * D + 8 * lg;
 #pragma unroll
     for (int t = 0; t < DS; ++t) qf[t] = *(const bf16x8*)(qp + 16 * t);
   }
@@ -148,55 +181,11 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
   int next_panel = panel_of(kt_lo + 1);
   // Key tile kt from buffer `buf` (tiles alternate between the buffers,
   // the first in buffer 0).
-  auto step = [&](int kt, auto buf) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();  // tile kt is in LDS; every wave is done with tile kt - 1
-    if (kt + 1 < kt_hi) gload(kt + 1, std::integral_constant<int, 1 - buf>{}, next_panel);
-    next_panel = panel_of(kt + 2);
-    const bf16* kb_lds = buf ? sk1 : sk0;
-    const bf16* vb = buf ? sv1 : sv0;
-    const int key0 = kt * kFaBK;
-    if (key0 > wave_qmin + 31) return;  // no key of this tile is visible to this wave
-    // S^T = K Q^T for two 32-key blocks: the two MFMA chains interleaved,
-    // K fragments read KLA k-steps ahead (a ring of KLA + 1), so no MFMA
-    // waits on the LDS read issued just before it.
-    constexpr int KLA = 3;
-    f32x16 sacc[2] = {f32x16{0.f}, f32x16{0.f}};
-    bf16x8 kf[KLA + 1][2];
-    auto kread = [&](int t, bf16x8 (&dst)[2]) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const int key = kb * 32 + lr;
-        dst[kb] = *(const bf16x8*)&kb_lds[key * D + kv_chunk<D>(2 * t + lg, key) * 8];
-      }
-    };
-#pragma unroll
-    for (int t = 0; t < KLA && t < DS; ++t) kread(t, kf[t]);
-    // (the issue order is fenced: left alone, the compiler moves each read
-    // next to its MFMA to save registers, and every MFMA waits on LDS)
-#pragma unroll
-    for (int t = 0; t < DS; ++t) {
-      if (t + KLA < DS) kread(t + KLA, kf[(t + KLA) % (KLA + 1)]);
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t % (KLA + 1)][kb], qf[t], sacc[kb],
-                                                           0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // V^T fragments of a 16-key group (two transposing reads per d block),
-    // the first group issued before the softmax.
-    union VFrag { s16x4 s[2]; bf16x8 h; };
-    VFrag vf[2][DB];
-    auto vread = [&](int g16, VFrag (&dst)[DB]) {
-      const int k1 = 16 * g16 + tr_key, k2 = k1 + 8;
-#pragma unroll
-      for (int bb = 0; bb < DB; ++bb) {
-        const int col = 32 * bb + tr_col;
-        dst[bb].s[0] = lds_read_tr16(vb + k1 * D + kv_chunk<D>(col >> 3, k1) * 8 + (col & 7));
-        dst[bb].s[1] = lds_read_tr16(vb + k2 * D + kv_chunk<D>(col >> 3, k2) * 8 + (col & 7));
-      }
-    };
-    vread(0, vf[0]);
+  // Causal mask, tile max and the lazily raised running max of one key tile's
+  // raw scores (both storage modes); returns the log2-domain offset of the
+  // exponent.  Element r of block kb is key key0 + 32 kb + (r % 4) + 8 (r / 4)
+  // + 4 lg.
+  auto softmax_update = [&](f32x16 (&sacc)[2], int key0) {
     // Mask (raw scores; the scale is applied inside the exponent); element r
     // of block kb is key key0 + 32kb + (r%4) + 8(r/4) + 4lg.
     // The mask is a wave-uniform branch: only the tiles crossing the
@@ -233,33 +222,138 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     // (SPLIT: a lane whose query precedes every key seen so far in this
     // split still has no finite max; its weights are exp2(-inf) = 0.)
     const float mc = (SPLIT && m_run == -INFINITY) ? 0.f : m_run * scale_log2e;
-    bf16x8 pf[4], pl[4];
+    return mc;
+  };
+  // fp32 storage: one key tile on the fp32 matrix instruction.  S^T = K Q^T
+  // (k-step t: head-dim values t and D/2 + t, K fragments four steps per
+  // 16-byte read), then O^T += V^T P^T over keys 8 j + 4 lg + i, whose
+  // weights are the lane's own score elements 4 j + i.
+  auto step_f32 = [&](const E* k_lds, const E* v_lds, int key0) {
+    if constexpr (F32) {
+      constexpr int QC = D / 8;  // 16-byte chunks of a half row
+      f32x16 sacc[2] = {f32x16{0.f}, f32x16{0.f}};
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int u = 0; u < QC; ++u) {
+        f32x4 kf[2];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        float p8[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          p8[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 * h + e], scale_log2e, -mc));
-          l_run += p8[e];
+        for (int kb = 0; kb < 2; ++kb) {
+          const int key = kb * 32 + lr;
+          kf[kb] = *(const f32x4*)&k_lds[key * D + kv_chunk_f32(lg * QC + u, key) * 4];
         }
-        split_hilo8(p8, pf[2 * kb + h], pl[2 * kb + h]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+            sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(kf[kb][e], q32[4 * u + e], sacc[kb],
+                                                            0, 0, 0);
       }
-    // O^T += V^T P^T over four 16-key groups: the hi MFMAs of the four d
-    // blocks, then the lo ones (four independent chains), with the next
-    // group's V fragments read meanwhile.
+      const float mc = softmax_update(sacc, key0);
+      float p[2][16];
 #pragma unroll
-    for (int g16 = 0; g16 < 4; ++g16) {
-      if (g16 + 1 < 4) vread(g16 + 1, vf[(g16 + 1) & 1]);
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int bb = 0; bb < DB; ++bb)
-        oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[g16 & 1][bb].h, pf[g16], oacc[bb], 0, 0, 0);
+        for (int r = 0; r < 16; ++r) {
+          p[kb][r] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][r], scale_log2e, -mc));
+          l_run += p[kb][r];
+        }
 #pragma unroll
-      for (int bb = 0; bb < DB; ++bb)
-        oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[g16 & 1][bb].h, pl[g16], oacc[bb], 0, 0, 0);
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = 32 * kb + 8 * j + 4 * lg + i;
+#pragma unroll
+            for (int bb = 0; bb < DB; ++bb) {
+              const int d = 32 * bb + lr;
+              const float vv = v_lds[key * D + kv_chunk_f32(d >> 2, key) * 4 + (d & 3)];
+              oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(vv, p[kb][4 * j + i], oacc[bb], 0,
+                                                              0, 0);
+            }
+          }
     }
   };
+  auto step = [&](int kt, auto buf) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // tile kt is in LDS; every wave is done with tile kt - 1
+    if (kt + 1 < kt_hi) gload(kt + 1, std::integral_constant<int, 1 - buf>{}, next_panel);
+    next_panel = panel_of(kt + 2);
+    const E* kb_lds = buf ? sk1 : sk0;
+    const E* vb = buf ? sv1 : sv0;
+    const int key0 = kt * kFaBK;
+    if (key0 > wave_qmin + 31) return;  // no key of this tile is visible to this wave
+    if constexpr (F32) {
+      step_f32(kb_lds, vb, key0);
+    } else {
+      // S^T = K Q^T for two 32-key blocks: the two MFMA chains interleaved,
+      // K fragments read KLA k-steps ahead (a ring of KLA + 1), so no MFMA
+      // waits on the LDS read issued just before it.
+      constexpr int KLA = 3;
+      f32x16 sacc[2] = {f32x16{0.f}, f32x16{0.f}};
+      bf16x8 kf[KLA + 1][2];
+      auto kread = [&](int t, bf16x8 (&dst)[2]) {
+  #pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const int key = kb * 32 + lr;
+          dst[kb] = *(const bf16x8*)&kb_lds[key * D + kv_chunk<D>(2 * t + lg, key) * 8];
+        }
+      };
+  #pragma unroll
+      for (int t = 0; t < KLA && t < DS; ++t) kread(t, kf[t]);
+      // (the issue order is fenced: left alone, the compiler moves each read
+      // next to its MFMA to save registers, and every MFMA waits on LDS)
+  #pragma unroll
+      for (int t = 0; t < DS; ++t) {
+        if (t + KLA < DS) kread(t + KLA, kf[(t + KLA) % (KLA + 1)]);
+  #pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t % (KLA + 1)][kb], qf[t], sacc[kb],
+                                                             0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // V^T fragments of a 16-key group (two transposing reads per d block),
+      // the first group issued before the softmax.
+      union VFrag { s16x4 s[2]; bf16x8 h; };
+      VFrag vf[2][DB];
+      auto vread = [&](int g16, VFrag (&dst)[DB]) {
+        const int k1 = 16 * g16 + tr_key, k2 = k1 + 8;
+  #pragma unroll
+        for (int bb = 0; bb < DB; ++bb) {
+          const int col = 32 * bb + tr_col;
+          dst[bb].s[0] = lds_read_tr16(vb + k1 * D + kv_chunk<D>(col >> 3, k1) * 8 + (col & 7));
+          dst[bb].s[1] = lds_read_tr16(vb + k2 * D + kv_chunk<D>(col >> 3, k2) * 8 + (col & 7));
+        }
+      };
+      vread(0, vf[0]);
+      const float mc = softmax_update(sacc, key0);
+      bf16x8 pf[4], pl[4];
+  #pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+  #pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          float p8[8];
+  #pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            p8[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 * h + e], scale_log2e, -mc));
+            l_run += p8[e];
+          }
+          split_hilo8(p8, pf[2 * kb + h], pl[2 * kb + h]);
+        }
+      // O^T += V^T P^T over four 16-key groups: the hi MFMAs of the four d
+      // blocks, then the lo ones (four independent chains), with the next
+      // group's V fragments read meanwhile.
+  #pragma unroll
+      for (int g16 = 0; g16 < 4; ++g16) {
+        if (g16 + 1 < 4) vread(g16 + 1, vf[(g16 + 1) & 1]);
+  #pragma unroll
+        for (int bb = 0; bb < DB; ++bb)
+          oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[g16 & 1][bb].h, pf[g16], oacc[bb], 0, 0, 0);
+  #pragma unroll
+        for (int bb = 0; bb < DB; ++bb)
+          oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[g16 & 1][bb].h, pl[g16], oacc[bb], 0, 0, 0);
+      }
+      }
+};
   for (int kt = kt_lo; kt < kt_hi; kt += 2) {
     step(kt, Buf0{});
     if (kt + 1 < kt_hi) step(kt + 1, Buf1{});
@@ -282,16 +376,17 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_kernel(
     return;
   }
   const float inv = 1.0f / l_tot;
-  bf16* op = O + ((int64_t)(q0 + qi) * Hq + qh) * D;
+  E* op = O + ((int64_t)(q0 + qi) * Hq + qh) * D;
+  typedef E E4 __attribute__((ext_vector_type(4)));
   // oacc[b] element r: d = 32b + 8(r/4) + 4lg + r%4  -> 4 consecutive d per (r/4).
 #pragma unroll
   for (int b = 0; b < DB; ++b)
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
-      bf16x4 o4;
+      E4 o4;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o4[e] = f2bf(oacc[b][4 * r4 + e] * inv);
-      *(bf16x4*)(op + 32 * b + 8 * r4 + 4 * lg) = o4;
+      for (int e = 0; e < 4; ++e) o4[e] = (E)(oacc[b][4 * r4 + e] * inv);
+      *(E4*)(op + 32 * b + 8 * r4 + 4 * lg) = o4;
     }
 }
 
@@ -365,15 +460,15 @@ size_t attn_prefill_partial_bytes(int n_seqs, int n_tokens, int max_q_len, int m
   return sp > 1 ? (size_t)sp * n_tokens * n_q_heads * (head_dim + 2) * sizeof(float) : 0;
 }
 
-template <int D, bool PAGED, bool SPLIT>
+template <int D, bool PAGED, bool SPLIT, bool F32 = false>
 static hipError_t run_fa(const void* q, const void* kc, const void* vc, void* out,
                          const BatchDev& b, const KvDev& kv, int Hq, int Hkv,
                          int include_single, int nsplit, float* part, hipStream_t s) {
   dim3 grid(cdiv(b.max_q_len, kFaBQ), Hq, b.n_seqs * nsplit);
   const float scale_log2e = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  attn_prefill_kernel<D, PAGED, SPLIT><<<grid, 256, 0, s>>>(
-      (const bf16*)q, (const bf16*)kc, (const bf16*)vc, (bf16*)out, b.cu_q, b.ctx_len, b.slot, kv,
-      Hq, Hkv, scale_log2e, include_single, b.n_tokens, nsplit, part);
+  attn_prefill_kernel<D, PAGED, SPLIT, F32><<<grid, 256, 0, s>>>(
+      q, kc, vc, out, b.cu_q, b.ctx_len, b.slot, kv, Hq, Hkv, scale_log2e, include_single,
+      b.n_tokens, nsplit, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !SPLIT) return e;
   dim3 cgrid(cdiv(b.max_q_len, kFaBQ), Hq, b.n_seqs);
@@ -395,9 +490,17 @@ static hipError_t run_fa_any(const void* q, const void* kc, const void* vc, void
 hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, void* out,
                                const BatchDev& b, const KvDev& kv, int n_q_heads,
                                int n_kv_heads, int head_dim, int include_single, float* part,
-                               hipStream_t s) {
+                               hipStream_t s, bool f32) {
   if (b.n_seqs == 0 || b.max_q_len == 0) return hipSuccess;
   const bool paged = kv.table != nullptr;
+  if (f32) {  // fp32 storage: no key-range split
+    const int H = n_q_heads, G = n_kv_heads, I = include_single;
+    if (head_dim == 128)
+      return paged ? run_fa<128, true, false, true>(q, kc, vc, out, b, kv, H, G, I, 1, nullptr, s)
+                   : run_fa<128, false, false, true>(q, kc, vc, out, b, kv, H, G, I, 1, nullptr, s);
+    return paged ? run_fa<64, true, false, true>(q, kc, vc, out, b, kv, H, G, I, 1, nullptr, s)
+                 : run_fa<64, false, false, true>(q, kc, vc, out, b, kv, H, G, I, 1, nullptr, s);
+  }
   if (head_dim == 128)
     return paged ? run_fa_any<128, true>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, part, s)
                  : run_fa_any<128, false>(q, kc, vc, out, b, kv, n_q_heads, n_kv_heads, include_single, part, s);

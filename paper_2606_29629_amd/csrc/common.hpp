@@ -129,6 +129,46 @@ __device__ __forceinline__ void split_hilo8(const float (&p)[8], bf16x8& hi, bf1
   lo = __builtin_bit_cast(bf16x8, l);
 }
 
+// Storage of the layer's tensors (activations, cache, norms, bias): bf16
+// (TRI_BF16) or fp32 (TRI_F32, the tight-parity mode).  Every load widens to
+// fp32 and every store rounds from fp32 (RNE for bf16).
+template <bool F32>
+struct Store;
+template <>
+struct Store<false> {
+  using T = bf16;
+  __device__ __forceinline__ static float ld(const void* p, int64_t i) {
+    return bf2f(((const bf16*)p)[i]);
+  }
+  __device__ __forceinline__ static void st(void* p, int64_t i, float v) {
+    ((bf16*)p)[i] = f2bf(v);
+  }
+  __device__ __forceinline__ static f32x4 ld4(const void* p, int64_t i) {
+    const bf16x4 v = *(const bf16x4*)((const bf16*)p + i);
+    return f32x4{bf2f(v[0]), bf2f(v[1]), bf2f(v[2]), bf2f(v[3])};
+  }
+  __device__ __forceinline__ static void st4(void* p, int64_t i, f32x4 v) {
+    bf16x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = f2bf(v[e]);
+    *(bf16x4*)((bf16*)p + i) = o;
+  }
+};
+template <>
+struct Store<true> {
+  using T = float;
+  __device__ __forceinline__ static float ld(const void* p, int64_t i) {
+    return ((const float*)p)[i];
+  }
+  __device__ __forceinline__ static void st(void* p, int64_t i, float v) { ((float*)p)[i] = v; }
+  __device__ __forceinline__ static f32x4 ld4(const void* p, int64_t i) {
+    return *(const f32x4*)((const float*)p + i);
+  }
+  __device__ __forceinline__ static void st4(void* p, int64_t i, f32x4 v) {
+    *(f32x4*)((float*)p + i) = v;
+  }
+};
+
 // Online softmax: the running max is only raised when a tile's max exceeds
 // it by more than this many log2 units; weights then stay below 2^8, and
 // the stale max cancels exactly in the final normalisation.

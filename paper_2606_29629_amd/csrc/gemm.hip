@@ -231,19 +231,22 @@ struct Mainloop {
 template <int MI, int NI, int EK>
 __device__ __forceinline__ void plain_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                                int row0, int row_lim, int col0, int N) {
-  const bf16* __restrict__ resid = (const bf16*)epi.resid;
+  constexpr int KIND = EK & kEpiKindMask;
+  using T = typename Store<(EK & kEpiF32) != 0>::T;
+  typedef T T4 __attribute__((ext_vector_type(4)));
+  const T* __restrict__ resid = (const T*)epi.resid;
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int row = row0 + 32 * i;
     const int rc = min(row, row_lim - 1);
-    bf16x4 res[NI][4];
-    if constexpr (EK == EPI_RESID) {
+    T4 res[NI][4];
+    if constexpr (KIND == EPI_RESID) {
 #pragma unroll
       for (int j = 0; j < NI; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int col = min(col0 + 32 * j + 8 * q, N - 4);
-          res[j][q] = *(const bf16x4*)(resid + (int64_t)rc * epi.ldr + col);
+          res[j][q] = *(const T4*)(resid + (int64_t)rc * epi.ldr + col);
         }
     }
     if (row >= row_lim) continue;
@@ -253,19 +256,19 @@ __device__ __forceinline__ void plain_epilogue(const f32x16 (&acc)[MI][NI], cons
       for (int q = 0; q < 4; ++q) {
         const int col = col0 + 32 * j + 8 * q;
         if (col >= N) continue;
-        if constexpr (EK == EPI_STORE_F32) {
+        if constexpr (KIND == EPI_STORE_F32) {
           *(f32x4*)((float*)epi.out + (int64_t)row * epi.ldo + col) =
               f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
                     acc[i][j][4 * q + 3]};
         } else {
-          bf16x4 o;
+          T4 o;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             float v = acc[i][j][4 * q + e];
-            if constexpr (EK == EPI_RESID) v += bf2f(res[j][q][e]);
-            o[e] = f2bf(v);
+            if constexpr (KIND == EPI_RESID) v += (float)res[j][q][e];
+            o[e] = (T)v;
           }
-          *(bf16x4*)((bf16*)epi.out + (int64_t)row * epi.ldo + col) = o;
+          *(T4*)((T*)epi.out + (int64_t)row * epi.ldo + col) = o;
         }
       }
   }
@@ -273,9 +276,11 @@ __device__ __forceinline__ void plain_epilogue(const f32x16 (&acc)[MI][NI], cons
 
 // SwiGLU: blocks j < NI/2 hold gate, j + NI/2 the matching up; f0 = output
 // column (intermediate index) of the lane's first element in block 0.
-template <int MI, int NI>
+template <int MI, int NI, bool F32>
 __device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                                 int row0, int row_lim, int f0) {
+  using T = typename Store<F32>::T;
+  typedef T T4 __attribute__((ext_vector_type(4)));
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int row = row0 + 32 * i;
@@ -286,13 +291,13 @@ __device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MI][NI], con
       for (int q = 0; q < 4; ++q) {
         const int f = f0 + 32 * j + 8 * q;
         if (f >= epi.ffn) continue;
-        bf16x4 o;
+        T4 o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float gt = acc[i][j][4 * q + e], up = acc[i][j + NI / 2][4 * q + e];
-          o[e] = f2bf(silu(gt) * up);
+          o[e] = (T)(silu(gt) * up);
         }
-        *(bf16x4*)((bf16*)epi.out + (int64_t)row * epi.ldo + f) = o;
+        *(T4*)((T*)epi.out + (int64_t)row * epi.ldo + f) = o;
       }
   }
 }
@@ -300,11 +305,13 @@ __device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MI][NI], con
 // One (token block i, first-half block j) of a q (KIND 0), k (1) or v (2)
 // head: the lane's token row, head-dim values d + 8 q + e (q, e < 4) of the
 // first half and the same plus D/2 from block j + HB.
-template <int KIND, int MI, int NI, int HB>
+template <int KIND, int MI, int NI, int HB, bool F32>
 __device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi& epi, int i,
                                           int j, int row0, int M, int head, int d,
                                           const float (&b1)[4][4], const float (&b2)[4][4]) {
   constexpr int D = HB * 64, half = D / 2;
+  using T = typename Store<F32>::T;
+  typedef T T4 __attribute__((ext_vector_type(4)));
   const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
   const int row = row0 + 32 * i;
   const int rc = min(row, M - 1);
@@ -323,17 +330,17 @@ __device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi
     tr = epi.tok_row[rc];
   }
   if (row >= M) return;
-  bf16* p;
+  T* p;
   if constexpr (KIND == 0) {
-    p = (bf16*)epi.q + ((int64_t)row * Hq + head) * D + d;
+    p = (T*)epi.q + ((int64_t)row * Hq + head) * D + d;
   } else {
     if (sl < 0) return;
     const int kvh = KIND == 1 ? head - Hq : head - Hq - Hkv;
-    p = (bf16*)(KIND == 1 ? epi.kc : epi.vc) + (((int64_t)sl * Hkv + kvh) * epi.max_seq + tr) * D + d;
+    p = (T*)(KIND == 1 ? epi.kc : epi.vc) + (((int64_t)sl * Hkv + kvh) * epi.max_seq + tr) * D + d;
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    bf16x4 o1, o2;
+    T4 o1, o2;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       float x1 = acc[i][j][4 * q + e] + b1[q][e], x2 = acc[i][j + HB][4 * q + e] + b2[q][e];
@@ -344,11 +351,11 @@ __device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi
         x1 = y1;
         x2 = y2;
       }
-      o1[e] = f2bf(x1);
-      o2[e] = f2bf(x2);
+      o1[e] = (T)x1;
+      o2[e] = (T)x2;
     }
-    *(bf16x4*)(p + 8 * q) = o1;
-    *(bf16x4*)(p + 8 * q + half) = o2;
+    *(T4*)(p + 8 * q) = o1;
+    *(T4*)(p + 8 * q + half) = o2;
   }
 }
 
@@ -358,9 +365,10 @@ __device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi
 // rotary factors (four (cos, sin) pairs per element group, 32 contiguous
 // bytes) and, for k/v heads, the token's cache slot and row are loaded before
 // the stores.
-template <int MI, int NI, int HB>
+template <int MI, int NI, int HB, bool F32>
 __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                              int row0, int col0, int M, int N) {
+  using St = Store<F32>;
   constexpr int D = HB * 64, half = D / 2;
   const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
 #pragma unroll
@@ -374,16 +382,16 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
     for (int q = 0; q < 4; ++q)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        b1[q][e] = epi.bias ? bf2f(((const bf16*)epi.bias)[col + 8 * q + e]) : 0.f;
-        b2[q][e] = epi.bias ? bf2f(((const bf16*)epi.bias)[col + 8 * q + e + half]) : 0.f;
+        b1[q][e] = epi.bias ? St::ld(epi.bias, col + 8 * q + e) : 0.f;
+        b2[q][e] = epi.bias ? St::ld(epi.bias, col + 8 * q + e + half) : 0.f;
       }
     // the head, hence its kind, is uniform across the wave
     const int kind = __builtin_amdgcn_readfirstlane(head < Hq ? 0 : (head < Hq + Hkv ? 1 : 2));
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
-      if (kind == 0) qkv_block<0, MI, NI, HB>(acc, epi, i, j, row0, M, head, d, b1, b2);
-      else if (kind == 1) qkv_block<1, MI, NI, HB>(acc, epi, i, j, row0, M, head, d, b1, b2);
-      else qkv_block<2, MI, NI, HB>(acc, epi, i, j, row0, M, head, d, b1, b2);
+      if (kind == 0) qkv_block<0, MI, NI, HB, F32>(acc, epi, i, j, row0, M, head, d, b1, b2);
+      else if (kind == 1) qkv_block<1, MI, NI, HB, F32>(acc, epi, i, j, row0, M, head, d, b1, b2);
+      else qkv_block<2, MI, NI, HB, F32>(acc, epi, i, j, row0, M, head, d, b1, b2);
     }
   }
 }
@@ -399,10 +407,13 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
 // pairs, a pass covers 4 rows, and a head's pairs are an aligned group of
 // D / 8 lanes, its sum of squares a group sum.  The lane's columns, bias and
 // gains stay fixed across rows.
-template <int MI, int NI>
+template <int MI, int NI, bool F32>
 __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
                                                   char* smem, int wv, int lane, int wrow0,
                                                   int wcol0, int M, int N) {
+  using St = Store<F32>;
+  using T = typename St::T;
+  typedef T T4 __attribute__((ext_vector_type(4)));
   constexpr int WC = NI * 32;
   static_assert(WC == 128, "16 lanes per row of the wave's columns");
   const int lr = lane & 31, lg = lane >> 5;
@@ -418,18 +429,18 @@ __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], c
   const int kind = head < Hq ? 0 : (head < Hq + Hkv ? 1 : 2);
   float b1[4], b2[4], g1[4], g2[4];
   {
-    const bf16* bp = (const bf16*)epi.bias;
-    const bf16* gp = (const bf16*)(kind == 0 ? epi.q_norm : epi.k_norm);
+    const void* bp = epi.bias;
+    const void* gp = kind == 0 ? epi.q_norm : epi.k_norm;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      b1[e] = bp ? bf2f(bp[col + e]) : 0.f;
-      b2[e] = bp ? bf2f(bp[col + half + e]) : 0.f;
-      g1[e] = kind == 2 ? 1.f : bf2f(gp[d + e]);
-      g2[e] = kind == 2 ? 1.f : bf2f(gp[d + half + e]);
+      b1[e] = bp ? St::ld(bp, col + e) : 0.f;
+      b2[e] = bp ? St::ld(bp, col + half + e) : 0.f;
+      g1[e] = kind == 2 ? 1.f : St::ld(gp, d + e);
+      g2[e] = kind == 2 ? 1.f : St::ld(gp, d + half + e);
     }
   }
   const int kvh = kind == 1 ? head - Hq : head - Hq - Hkv;
-  bf16* const cache = (bf16*)(kind == 1 ? epi.kc : epi.vc);
+  T* const cache = (T*)(kind == 1 ? epi.kc : epi.vc);
   const float inv_d = 1.0f / (float)D;
 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -477,7 +488,7 @@ __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], c
         ss += __shfl_xor(ss, 2, 64);
         ss += __shfl_xor(ss, 4, 64);
         if (half == 64) ss += __shfl_xor(ss, 8, 64);
-        bf16x4 o1, o2;
+        T4 o1, o2;
         const float r = 1.0f / sqrtf(ss * inv_d + epi.eps);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -491,17 +502,17 @@ __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], c
             y1 = z1;
             y2 = z2;
           }
-          o1[e] = f2bf(y1);
-          o2[e] = f2bf(y2);
+          o1[e] = (T)y1;
+          o2[e] = (T)y2;
         }
-        bf16* dst = nullptr;
+        T* dst = nullptr;
         if (kind == 0)
-          dst = (bf16*)epi.q + ((int64_t)row * Hq + head) * D + d;
+          dst = (T*)epi.q + ((int64_t)row * Hq + head) * D + d;
         else if (sl[u] >= 0)
           dst = cache + (((int64_t)sl[u] * Hkv + kvh) * epi.max_seq + tr[u]) * D + d;
         if (row < M && col_ok && dst) {
-          *(bf16x4*)dst = o1;
-          *(bf16x4*)(dst + half) = o2;
+          *(T4*)dst = o1;
+          *(T4*)(dst + half) = o2;
         }
       }
     }
@@ -516,6 +527,8 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
                                                    int tsplit, float* __restrict__ tail) {
   using ML = Mainloop<BM, BN, WGM, WGN, S>;
   constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
+  constexpr int KIND = EK & kEpiKindMask;
+  constexpr bool F32 = (EK & kEpiF32) != 0;
   extern __shared__ __align__(16) char smem_raw[];
   GemmSmem<BM, BN, S>& sm = *reinterpret_cast<GemmSmem<BM, BN, S>*>(smem_raw);
 
@@ -533,7 +546,7 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
     tile_of_id(full + u / tsplit, tiles_m, tiles_n, tm, tn);
     kc = K / tsplit;
   }
-  const int n_rows_b = EK == EPI_SWIGLU ? 2 * epi.ffn : N;
+  const int n_rows_b = KIND == EPI_SWIGLU ? 2 * epi.ffn : N;
   // Split-K (fp32 partial output only): split z covers k in [z kc, z kc + kc)
   // and writes plane z of the output.
   const int k0 = (u >= 0 ? u % tsplit : (int)blockIdx.y) * kc;
@@ -561,7 +574,7 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
 #pragma unroll
   for (int j = 0; j < ML::B_BLK; ++j) {
     const int tr = (wv + NW * j) * 8 + lrow;
-    const int gr = b_row_of<BN, WN>(EK, tn, tr, epi.ffn);
+    const int gr = b_row_of<BN, WN>(KIND, tn, tr, epi.ffn);
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
   f32x16 acc[MI][NI];
@@ -576,23 +589,23 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
     return;
   }
   const int row0 = tm * BM + wm * WM + lr;
-  if constexpr (EK == EPI_STORE_F32) {
+  if constexpr (KIND == EPI_STORE_F32) {
     Epi e = epi;
     e.out = (float*)epi.out + (int64_t)blockIdx.y * M * epi.ldo;
     plain_epilogue<MI, NI, EK>(acc, e, row0, M, tn * BN + wn * WN + 4 * lg, N);
-  } else if constexpr (EK == EPI_STORE || EK == EPI_RESID) {
+  } else if constexpr (KIND == EPI_STORE || KIND == EPI_RESID) {
     plain_epilogue<MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + 4 * lg, N);
-  } else if constexpr (EK == EPI_SWIGLU) {
-    swiglu_epilogue<MI, NI>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
-  } else if constexpr (EK == EPI_QKV_NORM) {
+  } else if constexpr (KIND == EPI_SWIGLU) {
+    swiglu_epilogue<MI, NI, F32>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
+  } else if constexpr (KIND == EPI_QKV_NORM) {
     static_assert(NW * 32 * WN * sizeof(float) <= sizeof(GemmSmem<BM, BN>),
                   "the epilogue's row blocks must fit the mainloop's LDS");
-    qkv_norm_epilogue<MI, NI>(acc, epi, smem_raw, wv, lane, tm * BM + wm * WM, tn * BN + wn * WN,
-                              M, N);
+    qkv_norm_epilogue<MI, NI, F32>(acc, epi, smem_raw, wv, lane, tm * BM + wm * WM,
+                                   tn * BN + wn * WN, M, N);
   } else if (epi.head_dim == 128) {
-    qkv_epilogue<MI, NI, 2>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
+    qkv_epilogue<MI, NI, 2, F32>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
   } else {
-    qkv_epilogue<MI, NI, 1>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
+    qkv_epilogue<MI, NI, 1, F32>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
   }
 }
 
@@ -609,6 +622,8 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
     int tiles_n, Epi epi) {
   using ML = Mainloop<BM, BN, WGM, WGN>;
   constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
+  constexpr int KIND = EK & kEpiKindMask;
+  constexpr bool F32 = (EK & kEpiF32) != 0;
   extern __shared__ __align__(16) char smem_raw[];
   GemmSmem<BM, BN>& sm = *reinterpret_cast<GemmSmem<BM, BN>*>(smem_raw);
 
@@ -630,7 +645,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
   const int e = lo;
   const int p0 = seg[e] + (mt - tile_off[e]) * BM;  // first routed row of this tile
   const int p_end = seg[e + 1];
-  const int n_rows_b = EK == EPI_SWIGLU ? 2 * epi.ffn : N;
+  const int n_rows_b = KIND == EPI_SWIGLU ? 2 * epi.ffn : N;
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -654,7 +669,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
 #pragma unroll
   for (int j = 0; j < ML::B_BLK; ++j) {
     const int tr = (wv + NW * j) * 8 + lrow;
-    const int gr = b_row_of<BN, WN>(EK, tn, tr, epi.ffn);
+    const int gr = b_row_of<BN, WN>(KIND, tn, tr, epi.ffn);
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * K + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
   f32x16 acc[MI][NI];
@@ -662,8 +677,8 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
 
   const int lr = lane & 31, lg = lane >> 5;
   const int row0 = p0 + wm * WM + lr;
-  if constexpr (EK == EPI_SWIGLU)
-    swiglu_epilogue<MI, NI>(acc, epi, row0, p_end, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
+  if constexpr (KIND == EPI_SWIGLU)
+    swiglu_epilogue<MI, NI, F32>(acc, epi, row0, p_end, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
   else
     plain_epilogue<MI, NI, EK>(acc, epi, row0, p_end, tn * BN + wn * WN + 4 * lg, N);
 }
@@ -683,7 +698,7 @@ template <int BM, int BN, int WGM, int WGN, int EK, int S = 2>
 static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
                            const Epi& epi, hipStream_t s, int splits = 1) {
   const int tiles_m = cdiv(M, BM);
-  const int tiles_n = EK == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
+  const int tiles_n = (EK & kEpiKindMask) == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
   const size_t smem = sizeof(GemmSmem<BM, BN, S>);
   static bool attr_set = false;
   hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK, S>, smem, attr_set);
@@ -742,10 +757,12 @@ size_t gemm_tail_bytes() { return (size_t)cu_count() * 256 * 256 * sizeof(float)
 constexpr int kTailChunk = 2048;
 constexpr int kTailPer = kTailChunk / 256;
 
-template <int BM, int BN>
+template <int BM, int BN, bool F32>
 __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__ tail, int tsplit,
                                                        int full, int tiles_m, int tiles_n, int M,
                                                        int N, Epi epi) {
+  using St = Store<F32>;
+  using T = typename St::T;
   const int j = blockIdx.y;
   int tm, tn;
   tile_of_id(full + j, tiles_m, tiles_n, tm, tn);
@@ -764,11 +781,10 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
       for (int q = 0; q < kTailPer; ++q) v[q] += tp[(int64_t)sp * BM * BN + idx[q]];
     float res[kTailPer];
     if (epi.kind == EPI_RESID) {
-      const bf16* __restrict__ rp = (const bf16*)epi.resid;
 #pragma unroll
       for (int q = 0; q < kTailPer; ++q) {
         const int row = min(tm * BM + idx[q] / BN, M - 1), col = min(tn * BN + idx[q] % BN, N - 1);
-        res[q] = bf2f(rp[(int64_t)row * epi.ldr + col]);
+        res[q] = St::ld(epi.resid, (int64_t)row * epi.ldr + col);
       }
     }
 #pragma unroll
@@ -780,7 +796,7 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
         ((float*)epi.out)[(int64_t)row * epi.ldo + col] = v[q];
       } else {
         const float o = epi.kind == EPI_RESID ? v[q] + res[q] : v[q];
-        ((bf16*)epi.out)[(int64_t)row * epi.ldo + col] = f2bf(o);
+        St::st(epi.out, (int64_t)row * epi.ldo + col, o);
       }
     }
     return;
@@ -816,12 +832,12 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
     cs[q] = epi.rope[(int64_t)row * half + d];
     sl[q] = epi.tok_slot[row];
     tr[q] = epi.tok_row[row];
-    b1[q] = epi.bias ? bf2f(((const bf16*)epi.bias)[col]) : 0.f;
-    b2[q] = epi.bias ? bf2f(((const bf16*)epi.bias)[col + half]) : 0.f;
-    const bf16* gp = (const bf16*)(head < Hq ? epi.q_norm : epi.k_norm);
+    b1[q] = epi.bias ? St::ld(epi.bias, col) : 0.f;
+    b2[q] = epi.bias ? St::ld(epi.bias, col + half) : 0.f;
+    const void* gp = head < Hq ? epi.q_norm : epi.k_norm;
     const bool n = epi.q_norm && head < Hq + Hkv;
-    g1[q] = n ? bf2f(gp[d]) : 1.f;
-    g2[q] = n ? bf2f(gp[d + half]) : 1.f;
+    g1[q] = n ? St::ld(gp, d) : 1.f;
+    g2[q] = n ? St::ld(gp, d + half) : 1.f;
   }
   // Per-head RMSNorm of q and k: a head's rotary pairs are `half` consecutive
   // elements, an aligned group of lanes, so its sum of squares is a group sum.
@@ -850,27 +866,28 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
       y1 = r1;
       y2 = r2;
     }
-    bf16* dst;
+    T* dst;
     if (head < Hq) {
-      dst = (bf16*)epi.q + ((int64_t)row * Hq + head) * Dh + d;
+      dst = (T*)epi.q + ((int64_t)row * Hq + head) * Dh + d;
     } else {
       if (sl[q] < 0) continue;
       const int kvh = head < Hq + Hkv ? head - Hq : head - Hq - Hkv;
-      bf16* cache = (bf16*)(head < Hq + Hkv ? epi.kc : epi.vc);
+      T* cache = (T*)(head < Hq + Hkv ? epi.kc : epi.vc);
       dst = cache + (((int64_t)sl[q] * Hkv + kvh) * epi.max_seq + tr[q]) * Dh + d;
     }
-    dst[0] = f2bf(y1);
-    dst[half] = f2bf(y2);
+    dst[0] = (T)y1;
+    dst[half] = (T)y2;
   }
 }
 
 template <int BM, int BN, int WGM, int WGN, int EK>
 static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, int M, int N,
                                 int K, const Epi& epi, float* tail, hipStream_t s) {
+  constexpr int KIND = EK & kEpiKindMask;
   const int tiles_m = cdiv(M, BM);
-  const int tiles_n = EK == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
+  const int tiles_n = KIND == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
   const int total = tiles_m * tiles_n;
-  const int t = tail ? tail_split(total, K, EK) : 1;
+  const int t = tail ? tail_split(total, K, KIND) : 1;
   if (t == 1) return run_gemm<BM, BN, WGM, WGN, EK>(A, lda, B, ldb, M, N, K, epi, s);
   const int n_tail = tail_tiles(total);
   const int full = total - n_tail;
@@ -882,8 +899,8 @@ static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, 
       (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, K, epi, tiles_m, tiles_n, full, t, tail);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int elems = EK == EPI_QKV || EK == EPI_QKV_NORM ? BM * BN / 2 : BM * BN;
-  tail_epi_kernel<BM, BN><<<dim3(cdiv(elems, kTailChunk), n_tail), 256, 0, s>>>(
+  const int elems = KIND == EPI_QKV || KIND == EPI_QKV_NORM ? BM * BN / 2 : BM * BN;
+  tail_epi_kernel<BM, BN, (EK & kEpiF32) != 0><<<dim3(cdiv(elems, kTailChunk), n_tail), 256, 0, s>>>(
       tail, t, full, tiles_m, tiles_n, M, N, epi);
   return hipGetLastError();
 }
@@ -891,6 +908,21 @@ static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, 
 hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
                        const Epi& epi, float* tail, hipStream_t s) {
   if (M == 0) return hipSuccess;
+  if (epi.f32) {
+    constexpr int F = kEpiF32;
+    switch (epi.kind) {
+      case EPI_RESID:
+        return run_gemm_tail<256, 256, 4, 2, EPI_RESID | F>(A, lda, B, ldb, M, N, K, epi, tail, s);
+      case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU | F>(A, lda, B, ldb, M, N, K, epi, s);
+      case EPI_STORE_F32:
+        return run_gemm_tail<256, 256, 4, 2, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, epi, tail, s);
+      case EPI_QKV:
+        if (epi.q_norm)
+          return run_gemm_tail<256, 256, 4, 2, EPI_QKV_NORM | F>(A, lda, B, ldb, M, N, K, epi, tail, s);
+        return run_gemm_tail<256, 256, 4, 2, EPI_QKV | F>(A, lda, B, ldb, M, N, K, epi, tail, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (epi.kind) {
     case EPI_STORE: return run_gemm_tail<256, 256, 4, 2, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, tail, s);
     case EPI_RESID: return run_gemm_tail<256, 256, 4, 2, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, tail, s);
@@ -917,7 +949,7 @@ static hipError_t run_grouped(const void* A, int lda, int a_rows, const int32_t*
                               const void* B, int64_t b_stride, int N, int K, const int32_t* seg,
                               const int32_t* tile_off, int n_experts, int max_tiles_m,
                               const Epi& epi, hipStream_t s) {
-  const int tiles_n = EK == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
+  const int tiles_n = (EK & kEpiKindMask) == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
   const size_t smem = sizeof(GemmSmem<BM, BN>);
   static bool attr_set = false;
   hipError_t e = opt_in_lds(gemm_grouped_kernel<BM, BN, WGM, WGN, EK>, smem, attr_set);
@@ -935,6 +967,17 @@ hipError_t launch_gemm_grouped(const void* A, int lda, int a_rows, const int32_t
   if (n_pairs == 0) return hipSuccess;
   const int bm = moe_tile_rows(n_pairs, n_experts);
   const int max_tiles_m = cdiv(n_pairs, bm) + n_experts;  // each expert adds <= 1 partial tile
+  if (epi.f32 && epi.kind == EPI_SWIGLU) {
+    constexpr int EK = EPI_SWIGLU | kEpiF32;
+    if (bm == 32)
+      return run_grouped<32, 256, 1, 4, EK>(A, lda, a_rows, perm, top_k, B, b_stride, N, K, seg,
+                                            tile_off, n_experts, max_tiles_m, epi, s);
+    if (bm == 256)
+      return run_grouped<256, 256, 4, 2, EK>(A, lda, a_rows, perm, top_k, B, b_stride, N, K, seg,
+                                             tile_off, n_experts, max_tiles_m, epi, s);
+    return run_grouped<128, 256, 2, 4, EK>(A, lda, a_rows, perm, top_k, B, b_stride, N, K, seg,
+                                           tile_off, n_experts, max_tiles_m, epi, s);
+  }
   if (bm == 32) {
     if (epi.kind == EPI_SWIGLU)
       return run_grouped<32, 256, 1, 4, EPI_SWIGLU>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,

@@ -43,12 +43,17 @@ __device__ __forceinline__ int kv_panel(const KvDev& kv, int sl, int row, int& p
 
 // Epilogue applied to C = A B^T (fp32 accumulators) by the GEMM kernels.
 enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_STORE_F32 = 4 };
+// Kernel-template epilogue ids: the kind in the low bits, kEpiF32 for fp32
+// storage of the epilogue's tensors (output, residual, q, cache, bias, gains).
+constexpr int kEpiKindMask = 15;
+constexpr int kEpiF32 = 16;
 
 struct Epi {
   int kind;
-  void* out;          // STORE / RESID / SWIGLU: bf16 [M, ldo]; STORE_F32: float [M, ldo]
+  int f32;            // 1: out, resid, q, cache, bias and gains are fp32 (fp32 storage mode)
+  void* out;          // STORE / RESID / SWIGLU: storage type [M, ldo]; STORE_F32: float
   int ldo;
-  const void* resid;  // RESID: bf16 [M, ldr]
+  const void* resid;  // RESID: storage type [M, ldr]
   int ldr;
   int ffn;            // SWIGLU: F; B rows [0,F) are gate, [F,2F) up; out has F cols
   // QKV: columns are q heads, then k heads, then v heads (head_dim each)
@@ -75,21 +80,30 @@ struct RopeSections {
 // token, -1 when out of range), the rotary table rope[t][i] = (cos, sin)(p *
 // base^(-2i/D)) with p the token's position in frequency i's section (angle in
 // double precision), and y = RMSNorm(x) * g.
+// x, g, y are bf16, or fp32 with f32 (the fp32 storage mode).
 hipError_t launch_prologue(const BatchDev& b, const KvDev& kv, int head_dim, float rope_base,
                            RopeSections sec, int32_t* tok_slot, int32_t* tok_row, float2* rope,
                            const void* x, const void* g, void* y, int hidden, float eps,
-                           hipStream_t s);
+                           hipStream_t s, bool f32 = false);
 
-// y = x / sqrt(mean(x^2) + eps) * g   (bf16 out, optional fp32 copy)
+// y = x / sqrt(mean(x^2) + eps) * g   (bf16 out with an optional fp32 copy, or
+// fp32 in and out with f32)
 hipError_t launch_rmsnorm(const void* x, const void* g, void* y, float* y32, int rows,
-                          int hidden, float eps, hipStream_t s);
+                          int hidden, float eps, hipStream_t s, bool f32 = false);
+
+// bf16 planes of an fp32 matrix [rows, cols] (row stride ld_in) for the
+// matrix cores: out [rows, 3 cols] = [hi | lo | hi] (pattern 0, activations)
+// or [hi | hi | lo] (pattern 1, weights), hi = bf16(v), lo = bf16(v - hi);
+// cols is a multiple of 4.
+hipError_t launch_split3(const float* in, int64_t ld_in, int64_t rows, int cols, int pattern,
+                         void* out, hipStream_t s);
 
 // KV append for a batch given by its device arrays: cache row ctx_len[s] + i
 // of slot slot[s] (through the block table when paged) <- row t of k_new /
 // v_new (the sequence of each token is found by binary search over cu_q).
 hipError_t launch_kv_append_direct(const BatchDev& b, const KvDev& kv, int n_kv_heads,
                                    int head_dim, const void* k_new, const void* v_new, void* kc,
-                                   void* vc, hipStream_t s);
+                                   void* vc, hipStream_t s, bool f32 = false);
 
 // Prefill GEMM (large M): C[M,N] = A[M,K] B[N,K]^T with the fused epilogue.
 // `tail` (gemm_tail_bytes, may be null) holds the fp32 partials of the tiles
@@ -126,10 +140,12 @@ int attn_prefill_splits(int n_seqs, int n_tokens, int max_q_len, int max_ctx_len
                         int n_q_heads);
 size_t attn_prefill_partial_bytes(int n_seqs, int n_tokens, int max_q_len, int max_ctx_len,
                                   int n_q_heads, int head_dim);
+// With f32 (the fp32 storage mode) q, the cache and out are fp32 and the key
+// range is not split.
 hipError_t launch_attn_prefill(const void* q, const void* kc, const void* vc, void* out,
                                const BatchDev& b, const KvDev& kv, int n_q_heads,
                                int n_kv_heads, int head_dim, int include_single, float* part,
-                               hipStream_t s);
+                               hipStream_t s, bool f32 = false);
 
 // Split-KV attention for sequences with q_len == 1, plus the combine.
 // Keys per split (a multiple of 32); max_split > 0 caps it.
@@ -156,15 +172,18 @@ hipError_t launch_gemm_grouped(const void* A, int lda, int a_rows, const int32_t
                                const void* B, int64_t b_stride, int N, int K, const int32_t* seg,
                                const int32_t* tile_off, int n_experts, int n_pairs,
                                const Epi& epi, hipStream_t s);
+// w_router bf16, or fp32 with w_f32 (the fp32 storage mode).
 hipError_t launch_moe_route_f32(const float* h32, const void* w_router, int T, int H, int E,
-                                int k, int renorm, int32_t* idx, float* w, hipStream_t s);
+                                int k, int renorm, int32_t* idx, float* w, hipStream_t s,
+                                bool w_f32 = false);
 size_t moe_route_planes_bytes(int T, int H, int E);
 hipError_t launch_moe_route_bf16(const void* h, const void* w_router, int T, int H, int E, int k,
                                  int renorm, float* planes, int32_t* idx, float* w, hipStream_t s);
 hipError_t launch_moe_permute(const int32_t* idx, int n_pairs, int E, int bm, int32_t* rank,
                               int32_t* counts, int32_t* perm, int32_t* inv, int32_t* seg,
                               int32_t* tile_off, hipStream_t s);
+// x1 and out bf16, or fp32 with f32.
 hipError_t launch_moe_combine(const void* x1, const float* y, const int32_t* inv, const float* w,
-                              int T, int H, int k, void* out, hipStream_t s);
+                              int T, int H, int k, void* out, hipStream_t s, bool f32 = false);
 
 }  // namespace tri

@@ -76,9 +76,25 @@ __device__ __forceinline__ void route_topk(const float (&vin)[4], int E, int k, 
   }
 }
 
-template <typename InT>
+// Eight router weights of one row as fp32 (bf16 or fp32 storage).
+__device__ __forceinline__ void load_w8(const bf16* p, float (&w)[8]) {
+  Pack8 v;
+  v.u = ldg16(p);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) w[q] = bf2f(v.e[q]);
+}
+__device__ __forceinline__ void load_w8(const float* p, float (&w)[8]) {
+  const f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    w[q] = a[q];
+    w[q + 4] = b[q];
+  }
+}
+
+template <typename InT, typename WT = bf16>
 __global__ __launch_bounds__(256) void moe_router_kernel(const InT* __restrict__ h,
-                                                         const bf16* __restrict__ wr, int T, int H,
+                                                         const WT* __restrict__ wr, int T, int H,
                                                          int E, int k, int renorm,
                                                          int32_t* __restrict__ idx_out,
                                                          float* __restrict__ w_out) {
@@ -99,15 +115,15 @@ __global__ __launch_bounds__(256) void moe_router_kernel(const InT* __restrict__
       }
       __syncthreads();
       if (e < E) {
-        const bf16* wrow = wr + (int64_t)e * H + hc;
+        const WT* wrow = wr + (int64_t)e * H + hc;
         for (int j = 0; j < hn; j += 8) {
-          Pack8 w8;
-          w8.u = ldg16(wrow + j);
+          float w8[8];
+          load_w8(wrow + j, w8);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float* hp = &hs[4 * tg + i][j];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) acc[i] = fmaf(bf2f(w8.e[q]), hp[q], acc[i]);
+            for (int q = 0; q < 8; ++q) acc[i] = fmaf(w8[q], hp[q], acc[i]);
           }
         }
       }
@@ -155,10 +171,15 @@ __global__ __launch_bounds__(256) void moe_topk_kernel(const float* __restrict__
 }
 
 hipError_t launch_moe_route_f32(const float* h32, const void* w_router, int T, int H, int E,
-                                int k, int renorm, int32_t* idx, float* w, hipStream_t s) {
+                                int k, int renorm, int32_t* idx, float* w, hipStream_t s,
+                                bool w_f32) {
   if (T == 0) return hipSuccess;
-  moe_router_kernel<float><<<cdiv(T, kRouteTok), 256, 0, s>>>(h32, (const bf16*)w_router, T, H, E,
-                                                               k, renorm, idx, w);
+  if (w_f32)
+    moe_router_kernel<float, float><<<cdiv(T, kRouteTok), 256, 0, s>>>(
+        h32, (const float*)w_router, T, H, E, k, renorm, idx, w);
+  else
+    moe_router_kernel<float><<<cdiv(T, kRouteTok), 256, 0, s>>>(h32, (const bf16*)w_router, T, H,
+                                                                 E, k, renorm, idx, w);
   return hipGetLastError();
 }
 
@@ -269,12 +290,14 @@ hipError_t launch_moe_permute(const int32_t* idx, int n_pairs, int E, int bm, in
   return hipGetLastError();
 }
 
-// out[t] = x1[t] + sum_j w[t][j] y[inv[t k + j]], 8 columns per thread.
-__global__ __launch_bounds__(256) void moe_combine_kernel(const bf16* __restrict__ x1,
+// out[t] = x1[t] + sum_j w[t][j] y[inv[t k + j]], 8 columns per thread; x1
+// and out in the storage type (bf16, or fp32 with F32).
+template <bool F32>
+__global__ __launch_bounds__(256) void moe_combine_kernel(const void* __restrict__ x1,
                                                           const float* __restrict__ y,
                                                           const int32_t* __restrict__ inv,
                                                           const float* __restrict__ w, int T,
-                                                          int H, int k, bf16* __restrict__ out) {
+                                                          int H, int k, void* __restrict__ out) {
   const int t = blockIdx.x;
   for (int c = threadIdx.x * 8; c < H; c += 256 * 8) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -288,18 +311,31 @@ __global__ __launch_bounds__(256) void moe_combine_kernel(const bf16* __restrict
         acc[q + 4] = fmaf(wj, b[q], acc[q + 4]);
       }
     }
-    Pack8 xv, o;
-    xv.u = ldg16(x1 + (int64_t)t * H + c);
+    const int64_t at = (int64_t)t * H + c;
+    if constexpr (F32) {
+      const f32x4 xa = *(const f32x4*)((const float*)x1 + at);
+      const f32x4 xb = *(const f32x4*)((const float*)x1 + at + 4);
+      *(f32x4*)((float*)out + at) = f32x4{xa[0] + acc[0], xa[1] + acc[1], xa[2] + acc[2],
+                                          xa[3] + acc[3]};
+      *(f32x4*)((float*)out + at + 4) = f32x4{xb[0] + acc[4], xb[1] + acc[5], xb[2] + acc[6],
+                                              xb[3] + acc[7]};
+    } else {
+      Pack8 xv, o;
+      xv.u = ldg16((const bf16*)x1 + at);
 #pragma unroll
-    for (int q = 0; q < 8; ++q) o.e[q] = f2bf(bf2f(xv.e[q]) + acc[q]);
-    stg16(out + (int64_t)t * H + c, o.u);
+      for (int q = 0; q < 8; ++q) o.e[q] = f2bf(bf2f(xv.e[q]) + acc[q]);
+      stg16((bf16*)out + at, o.u);
+    }
   }
 }
 
 hipError_t launch_moe_combine(const void* x1, const float* y, const int32_t* inv, const float* w,
-                              int T, int H, int k, void* out, hipStream_t s) {
+                              int T, int H, int k, void* out, hipStream_t s, bool f32) {
   if (T == 0) return hipSuccess;
-  moe_combine_kernel<<<T, 256, 0, s>>>((const bf16*)x1, y, inv, w, T, H, k, (bf16*)out);
+  if (f32)
+    moe_combine_kernel<true><<<T, 256, 0, s>>>(x1, y, inv, w, T, H, k, out);
+  else
+    moe_combine_kernel<false><<<T, 256, 0, s>>>(x1, y, inv, w, T, H, k, out);
   return hipGetLastError();
 }
 

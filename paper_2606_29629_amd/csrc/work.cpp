@@ -58,7 +58,8 @@ tri_status tri_layer_work(const tri_layer_config* cfg, int32_t decode, int32_t n
   Acc a{out};
   const double H = cfg->hidden, D = cfg->head_dim, Hq = cfg->n_q_heads, Hkv = cfg->n_kv_heads;
   const double Nqkv = (Hq + 2.0 * Hkv) * D;
-  const double bf = 2.0, f32 = 4.0, i32 = 4.0;
+  // bytes of one stored element (bf16, or fp32 in the fp32 storage mode)
+  const double bf = cfg->dtype == TRI_F32 ? 4.0 : 2.0, f32 = 4.0, i32 = 4.0;
   const double rope_table = T * (D / 2) * 8.0;  // (cos, sin) fp32 per token and pair
   const double token_map = T * 2 * i32;         // (slot, cache row) per token
 

@@ -17,6 +17,14 @@ def to_device_bf16(bits: np.ndarray, device="cuda"):
     return t.to(device).view(torch.bfloat16)
 
 
+def to_device_f32(bits: np.ndarray, device="cuda"):
+    """uint16 bfloat16 bit patterns -> torch.float32 tensor on `device` holding
+    the same values (exact widening; the fp32 storage mode's inputs)."""
+    import torch
+    f = (np.ascontiguousarray(bits).astype(np.uint32) << 16).view(np.float32)
+    return torch.from_numpy(f).to(device)
+
+
 def to_host_f64(t) -> np.ndarray:
     """torch bfloat16/float tensor -> float64 NumPy array (exact widening)."""
     import torch
@@ -24,16 +32,19 @@ def to_host_f64(t) -> np.ndarray:
 
 
 class DeviceLayer:
-    """Weights of one layer resident in HBM plus its C config struct."""
+    """Weights of one layer resident in HBM plus its C config struct (bf16
+    storage, or fp32 storage holding the same values with f32)."""
 
-    def __init__(self, cfg, weights_bits: Dict[str, np.ndarray], device="cuda"):
+    def __init__(self, cfg, weights_bits: Dict[str, np.ndarray], device="cuda", f32=False):
         self.cfg_py = cfg
-        self.cfg = make_config(cfg)
-        self.w = {k: to_device_bf16(v, device) for k, v in weights_bits.items()}
+        self.cfg = make_config(cfg, f32=f32)
+        to_dev = to_device_f32 if f32 else to_device_bf16
+        self.w = {k: to_dev(v, device) for k, v in weights_bits.items()}
 
 
-def device_cache(k_bits: np.ndarray, v_bits: np.ndarray, device="cuda"):
-    return to_device_bf16(k_bits, device), to_device_bf16(v_bits, device)
+def device_cache(k_bits: np.ndarray, v_bits: np.ndarray, device="cuda", f32=False):
+    to_dev = to_device_f32 if f32 else to_device_bf16
+    return to_dev(k_bits, device), to_dev(v_bits, device)
 
 
 def device_batch(batch, device="cuda") -> DeviceBatch:

@@ -14,6 +14,9 @@ read elementwise: element g of the GPU output passes against the exact
     worst_gpu <= worst_emul + 0.5                  (largest |g - r| / bound)
   With n_emul = 0 the first line is the strict bar.  Both counts are recorded
   and printed in the pytest terminal summary.
+
+The fp32 storage mode is held to 1e-4 / 1e-4 in the same form, strictly
+(tol=F32_TOL).
 """
 from __future__ import annotations
 
@@ -22,15 +25,16 @@ import math
 import numpy as np
 
 ATOL, RTOL = 2e-2, 1e-2
+F32_TOL = (1e-4, 1e-4)
 WORST_MARGIN = 0.5
 
 # (what, N, n_gpu, n_emul, worst_gpu, worst_emul, max_abs_gpu, strict) of every check
 RECORDS: list = []
 
 
-def _stats(got, exact):
+def _stats(got, exact, tol=(ATOL, RTOL)):
     err = np.abs(got - exact)
-    bound = np.maximum(ATOL, RTOL * np.abs(exact))
+    bound = np.maximum(tol[0], tol[1] * np.abs(exact))
     ratio = err / bound
     return int(np.sum(ratio > 1.0)), float(ratio.max(initial=0.0)), float(err.max(initial=0.0)), ratio
 
@@ -40,17 +44,17 @@ def count_margin(n_emul: int) -> int:
     return int(math.ceil(3.0 * math.sqrt(2.0 * n_emul)))
 
 
-def check_e2e(got, exact, what, emul=None, strict=False):
+def check_e2e(got, exact, what, emul=None, strict=False, tol=(ATOL, RTOL)):
     """Assert the end-to-end bar (see the module docstring) and record the counts."""
     got = np.asarray(got, np.float64)
     exact = np.asarray(exact, np.float64)
     assert got.shape == exact.shape, (what, got.shape, exact.shape)
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
-    n_g, w_g, a_g, ratio = _stats(got, exact)
+    n_g, w_g, a_g, ratio = _stats(got, exact, tol)
     if emul is not None:
         emul = np.asarray(emul, np.float64)
         assert emul.shape == exact.shape, (what, emul.shape, exact.shape)
-        n_e, w_e, _, _ = _stats(emul, exact)
+        n_e, w_e, _, _ = _stats(emul, exact, tol)
     else:
         n_e, w_e = None, None
     RECORDS.append((what, got.size, n_g, n_e, w_g, w_e, a_g, bool(strict)))
@@ -58,7 +62,8 @@ def check_e2e(got, exact, what, emul=None, strict=False):
     where = (f"worst {w_g:.3f}x the bound at {i}: gpu {got[i]:.6g} exact {exact[i]:.6g}"
              if ratio.size else "")
     if strict or emul is None:
-        assert n_g == 0, f"{what}: {n_g}/{got.size} elements outside max(2e-2, 1e-2|r|) ({where})"
+        assert n_g == 0, (f"{what}: {n_g}/{got.size} elements outside max({tol[0]:g}, "
+                          f"{tol[1]:g}|r|) ({where})")
         return
     lim = n_e + count_margin(n_e)
     assert n_g <= lim, (f"{what}: {n_g}/{got.size} outside the bound, bf16 emulation {n_e} "

@@ -119,7 +119,7 @@ def test_null_and_unsupported(lib):
     assert lib.tri_layer_prefill(None, None, None, None, None, None, None, None, None, 0,
                                  None) == T.TRI_ERR_NULL
     assert call(lib, c=cfg(head_dim=96)) == T.TRI_ERR_UNSUPPORTED
-    assert call(lib, c=cfg(dtype=T.TRI_F32)) == T.TRI_ERR_UNSUPPORTED
+    assert call(lib, c=cfg(dtype=2)) == T.TRI_ERR_UNSUPPORTED        # no such storage type
     assert call(lib, c=cfg(flags=64)) == T.TRI_ERR_UNSUPPORTED
     assert call(lib, c=cfg(hidden=200)) == T.TRI_ERR_UNSUPPORTED
     assert call(lib, c=cfg(ffn_dim=100)) == T.TRI_ERR_UNSUPPORTED
@@ -211,6 +211,27 @@ def test_workspace_size_and_layout(lib):
         sizes.append(s.value)
     assert sizes == sorted(sizes)
     assert lib.tri_workspace_size(ctypes.byref(c), None, None) == T.TRI_ERR_NULL
+
+
+def test_workspace_of_f32_storage(lib):
+    """fp32 storage: fp32 activations and the bf16 operand planes (three per
+    value) of every weight matrix and of the widest activation operand."""
+    H, Hq, Hkv, D, F = 256, 4, 2, 64, 1024
+    c = cfg(dtype=T.TRI_F32)
+    T_ = 40
+    b = batch(n_seqs=1, n_tokens=T_, max_q=T_, max_ctx=0)
+    s = ctypes.c_size_t()
+    assert lib.tri_workspace_size(ctypes.byref(c), ctypes.byref(b), ctypes.byref(s)) == 0
+    params = (Hq + 2 * Hkv) * D * H + H * Hq * D + 3 * F * H
+    acts = T_ * (3 * H + 2 * Hq * D + F) * 4
+    assert s.value >= params * 6 + acts + T_ * F * 6
+    m = T.WorkspaceMap()
+    assert lib.tri_workspace_layout(ctypes.byref(c), ctypes.byref(b), ctypes.byref(m)) == 0
+    assert m.x1 - m.attn == -(-T_ * Hq * D * 4 // 256) * 256      # attention output in fp32
+    sb = ctypes.c_size_t()
+    cb = cfg()
+    assert lib.tri_workspace_size(ctypes.byref(cb), ctypes.byref(b), ctypes.byref(sb)) == 0
+    assert s.value > sb.value
 
 
 def test_workspace_of_long_chunked_prefill(lib):
