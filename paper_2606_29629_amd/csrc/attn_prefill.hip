@@ -199,17 +199,17 @@ __global__ __launch_bounds__(256, F32 ? 1 : 2) void attn_prefill_kernel(
           if (key > qpos) sacc[kb][r] = -INFINITY;
         }
     }
-    float mt = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[kb][r]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
     // Raise the running max (raw units) only past the slack; rescale when
     // any lane of the wave did.  m_run is finite after the first tile (key 0
-    // is visible to every query).
-    const bool raise = mt > m_run + slack_raw;
-    if (__builtin_amdgcn_ballot_w64(raise)) {
+    // is visible to every query).  A query's scores sit in two lanes (lg = 0,
+    // 1): when neither half of any row passes the threshold, no row's max
+    // does, and the cross-lane exchange is skipped (the common case once
+    // the max has settled).
+    const float thr = m_run + slack_raw;
+    const float mh = tree_max32(sacc);
+    if (__builtin_amdgcn_ballot_w64(mh > thr)) {
+      const float mt = fmaxf(mh, __shfl_xor(mh, 32, 64));
+      const bool raise = mt > thr;
       const float m_new = raise ? mt : m_run;
       // (SPLIT: a lane that still has no finite max must not form -inf - -inf)
       const float alpha = (SPLIT && !raise) ? 1.f
@@ -252,10 +252,17 @@ __global__ __launch_bounds__(256, F32 ? 1 : 2) void attn_prefill_kernel(
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < 16; ++r)
           p[kb][r] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][r], scale_log2e, -mc));
-          l_run += p[kb][r];
-        }
+      float ls[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float v8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v8[e] = p[g >> 1][8 * (g & 1) + e];
+        ls[g] = tree_sum8(v8);
+      }
+      l_run += (ls[0] + ls[1]) + (ls[2] + ls[3]);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -327,18 +334,19 @@ __global__ __launch_bounds__(256, F32 ? 1 : 2) void attn_prefill_kernel(
       vread(0, vf[0]);
       const float mc = softmax_update(sacc, key0);
       bf16x8 pf[4], pl[4];
+      float ls[4];  // the tile's row sum in four tree-summed parts
   #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
   #pragma unroll
         for (int h = 0; h < 2; ++h) {
           float p8[8];
   #pragma unroll
-          for (int e = 0; e < 8; ++e) {
+          for (int e = 0; e < 8; ++e)
             p8[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][8 * h + e], scale_log2e, -mc));
-            l_run += p8[e];
-          }
+          ls[2 * kb + h] = tree_sum8(p8);
           split_hilo8(p8, pf[2 * kb + h], pl[2 * kb + h]);
         }
+      l_run += (ls[0] + ls[1]) + (ls[2] + ls[3]);
       // O^T += V^T P^T over four 16-key groups: the hi MFMAs of the four d
       // blocks, then the lo ones (four independent chains), with the next
       // group's V fragments read meanwhile.

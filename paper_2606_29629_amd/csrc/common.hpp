@@ -129,6 +129,32 @@ __device__ __forceinline__ void split_hilo8(const float (&p)[8], bf16x8& hi, bf1
   lo = __builtin_bit_cast(bf16x8, l);
 }
 
+// Balanced reductions of a lane's values.  A dependent VALU result takes tens
+// of cycles to come back, so a linear fold over n values is an n-deep
+// latency chain; a tree is log2(n) deep.
+__device__ __forceinline__ float tree_sum8(const float (&v)[8]) {
+  return ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
+}
+// max(a, b, c) as one instruction.  (The compiler quiets each operand of an
+// fmaxf first, one more instruction per operand of unknown origin; the
+// operands here are matrix-instruction results, never signalling NaNs.)
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float tree_max32(const f32x16 (&s)[2]) {
+  float m[11], n[4];
+#pragma unroll
+  for (int i = 0; i < 11; ++i) {
+    const int a = 3 * i, b = 3 * i + 1, c = i < 10 ? 3 * i + 2 : 31;
+    m[i] = max3f(s[a >> 4][a & 15], s[b >> 4][b & 15], s[c >> 4][c & 15]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) n[i] = max3f(m[3 * i], m[3 * i + 1], m[i < 3 ? 3 * i + 2 : 10]);
+  return max3f(max3f(n[0], n[1], n[2]), n[3], n[3]);
+}
+
 // Storage of the layer's tensors (activations, cache, norms, bias): bf16
 // (TRI_BF16) or fp32 (TRI_F32, the tight-parity mode).  Every load widens to
 // fp32 and every store rounds from fp32 (RNE for bf16).
