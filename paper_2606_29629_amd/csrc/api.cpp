@@ -85,13 +85,22 @@ struct Layout {
   size_t total;
 };
 
+// Bytes of the flash kernel's split partials, rounded up to the alignment
+// (none when no sequence has more than one token: no flash launch).
+size_t flash_part_bytes(const tri_layer_config* c, const tri_batch* b) {
+  if (b->max_q_len <= 1) return 0;
+  return up(attn_prefill_partial_bytes(b->n_seqs, b->n_tokens, b->max_q_len, b->max_ctx_len,
+                                       c->n_q_heads, c->head_dim));
+}
+
 size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
   const int T = b->n_tokens, H = c->hidden, D = c->head_dim;
   const int Nqkv = (c->n_q_heads + 2 * c->n_kv_heads) * D;
-  size_t p = attn_decode_partial_bytes(b->n_seqs, c->n_q_heads, D, b->max_ctx_len + 1);
-  const size_t fa =
-      attn_prefill_partial_bytes(b->n_seqs, T, b->max_q_len, b->max_ctx_len, c->n_q_heads, D);
-  if (fa > p) p = fa;
+  // A chunk's flash attention and the single-token sequences' split-KV
+  // attention may run at the same time (on two streams), so their partials
+  // sit side by side: the flash partials first, then the decode partials.
+  size_t p = flash_part_bytes(c, b) +
+             attn_decode_partial_bytes(b->n_seqs, c->n_q_heads, D, b->max_ctx_len + 1);
   if (T > 0) {
     // Skinny-path partials; a larger batch reserves them for the largest
     // skinny batch, so that the size never shrinks as n_tokens grows.
@@ -260,6 +269,49 @@ struct StageTimer {
 
 template <typename T>
 T* at(void* ws, size_t off) { return (T*)((char*)ws + off); }
+
+// A second stream per device, on which a mixed batch's split-KV attention
+// (the single-token sequences) runs beside the flash attention of its
+// multi-token sequences: both read the projected q and the cache, and they
+// write disjoint output rows and disjoint partials.  Created on first use
+// (default priority, non-blocking); the fork and join events are recorded and
+// waited on under the device's lock, so concurrent callers cannot pair one
+// caller's record with another's wait.
+struct SideStream {
+  std::mutex mu;
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool failed = false;  // creation failed once (e.g. under graph capture): run serially
+};
+constexpr int kMaxSideDevices = 64;
+SideStream* side_stream() {
+  static SideStream ss[kMaxSideDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxSideDevices) return nullptr;
+  return &ss[dev];
+}
+// With the device's lock held: makes sure the stream and events exist; false
+// means "run on the caller's stream".
+bool side_ready(SideStream& x) {
+  if (x.s) return true;
+  if (x.failed) return false;
+  hipStream_t st = nullptr;
+  hipEvent_t f = nullptr, j = nullptr;
+  if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) == hipSuccess &&
+      hipEventCreateWithFlags(&f, hipEventDisableTiming) == hipSuccess &&
+      hipEventCreateWithFlags(&j, hipEventDisableTiming) == hipSuccess) {
+    x.s = st;
+    x.fork = f;
+    x.join = j;
+    return true;
+  }
+  if (f) (void)hipEventDestroy(f);
+  if (st) (void)hipStreamDestroy(st);
+  (void)hipGetLastError();  // clear the failed call's error
+  x.failed = true;
+  return false;
+}
+
 
 #define TRI_HIP(expr)                              \
   do {                                             \
@@ -529,20 +581,43 @@ tri_status tri::layer_call(bool decode, bool timed, const tri_layer_config* cfg,
     StageTimer t_(ST_QKV, s, timed);
     if ((st = run_linear(h, H, w->w_qkv, T, Nqkv, H, e, part, s)) != TRI_OK) return st;
   }
-  if (!decode && b->max_q_len > 1) {
+  // Flash attention serves the multi-token sequences, split-KV attention the
+  // single-token ones (a batch in which every sequence has max_q_len > 1
+  // tokens has none).  When a batch has both, the split-KV kernels run on the
+  // side stream, overlapping the compute-bound flash kernel with the
+  // memory-bound decode attention.
+  const bool flash = !decode && b->max_q_len > 1;
+  const bool splitkv =
+      decode || b->max_q_len == 1 || (int64_t)b->n_seqs * b->max_q_len != b->n_tokens;
+  float* part_dec = (float*)((char*)part + flash_part_bytes(cfg, b));
+  hipStream_t sd = s;  // stream of the split-KV attention
+  SideStream* side = (flash && splitkv) ? side_stream() : nullptr;
+  std::unique_lock<std::mutex> side_lock;
+  if (side) {
+    side_lock = std::unique_lock<std::mutex>(side->mu);
+    if (side_ready(*side)) {
+      TRI_HIP(hipEventRecord(side->fork, s));
+      TRI_HIP(hipStreamWaitEvent(side->s, side->fork, 0));
+      sd = side->s;
+    }
+  }
+  if (splitkv) {
+    {
+      StageTimer t_(ST_ATTN_DECODE, sd, timed);
+      TRI_HIP(launch_attn_decode_split(q, cache->k, cache->v, part_dec, bd, kv, Hq, Hkv, D, sd));
+    }
+    StageTimer t_(ST_ATTN_COMBINE, sd, timed);
+    TRI_HIP(launch_attn_decode_combine(part_dec, attn, bd, kv, Hq, Hkv, D, sd));
+  }
+  if (flash) {
     StageTimer t_(ST_ATTN_PREFILL, s, timed);
     TRI_HIP(launch_attn_prefill(q, cache->k, cache->v, attn, bd, kv, Hq, Hkv, D, 0, part, s));
   }
-  // Split-KV attention serves the single-token sequences; a batch in which
-  // every sequence has max_q_len > 1 tokens has none.
-  if (decode || b->max_q_len == 1 || (int64_t)b->n_seqs * b->max_q_len != b->n_tokens) {
-    {
-      StageTimer t_(ST_ATTN_DECODE, s, timed);
-      TRI_HIP(launch_attn_decode_split(q, cache->k, cache->v, part, bd, kv, Hq, Hkv, D, s));
-    }
-    StageTimer t_(ST_ATTN_COMBINE, s, timed);
-    TRI_HIP(launch_attn_decode_combine(part, attn, bd, kv, Hq, Hkv, D, s));
+  if (sd != s) {
+    TRI_HIP(hipEventRecord(side->join, sd));
+    TRI_HIP(hipStreamWaitEvent(s, side->join, 0));
   }
+  if (side_lock.owns_lock()) side_lock.unlock();
   e = Epi{};
   e.kind = EPI_RESID;
   e.out = x1;

@@ -305,6 +305,27 @@ def test_noalloc_rejects_batches_beyond_its_scratch(lib):
     assert st == T.TRI_ERR_NULL
 
 
+def test_decode_batches_fit_the_noalloc_scratch(lib):
+    """The decode workloads fit the no-allocation entry's scratch: a batch
+    with no multi-token sequence reserves no flash-attention partials (they
+    sit beside the split-KV partials only when both kernels run)."""
+    dense = cfg(hidden=3584, n_q_heads=28, n_kv_heads=4, head_dim=128, ffn_dim=18944)
+    moe = cfg(hidden=2048, n_q_heads=32, n_kv_heads=4, head_dim=128, ffn_dim=768,
+              flags=T.TRI_F_MOE, n_experts=128, top_k=8, expert_ffn_dim=768)
+    for c, n, ctx in ((dense, 64, 4096), (moe, 128, 2048)):
+        need = ctypes.c_size_t()
+        b = batch(n_seqs=n, n_tokens=n, max_q=1, max_ctx=ctx)
+        assert lib.tri_workspace_size(ctypes.byref(c), ctypes.byref(b), ctypes.byref(need)) == 0
+        assert need.value <= T.NOALLOC_SCRATCH_BYTES, (n, ctx, need.value)
+    # a chunk beside decodes reserves both kinds of attention partials
+    b1 = batch(n_seqs=33, n_tokens=544, max_q=512, max_ctx=8192)
+    b2 = batch(n_seqs=1, n_tokens=512, max_q=512, max_ctx=8192)
+    s1, s2 = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.tri_workspace_size(ctypes.byref(dense), ctypes.byref(b1), ctypes.byref(s1)) == 0
+    assert lib.tri_workspace_size(ctypes.byref(dense), ctypes.byref(b2), ctypes.byref(s2)) == 0
+    assert s1.value >= s2.value
+
+
 def test_status_strings(lib):
     for s in range(-9, 1):
         assert T.status_string(s) and T.status_string(s) != "unknown status"
