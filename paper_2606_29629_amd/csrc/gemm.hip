@@ -923,6 +923,28 @@ hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, in
       default: return hipErrorInvalidValue;
     }
   }
+  // Mid-size M (a chunk of a few hundred tokens, the mixed step): when the
+  // 256 x 256 tiles would not fill one round of CUs, 128 x 128 tiles of four
+  // 32 x 128 waves with three LDS stages (two k-tiles in flight): a short
+  // k-tile of a small tile computes in less time than a load's round trip,
+  // so two stages leave such a GEMM bound by load latency.  The waves keep
+  // 128 columns (the q/k/v epilogue pairs rotary halves inside a wave).
+  // gate/up at M <= 640: 128 x 256 tiles with three stages (its 256-row
+  // tiles leave most of a third tile empty).  A long K (the down
+  // projection) keeps the 256 x 256 tail split.
+  if (epi.kind != EPI_SWIGLU && epi.kind != EPI_STORE_F32 && K <= 8192 &&
+      cdiv(M, 256) * cdiv(N, 256) < cu_count()) {
+    switch (epi.kind) {
+      case EPI_STORE: return run_gemm<128, 128, 4, 1, EPI_STORE, 3>(A, lda, B, ldb, M, N, K, epi, s);
+      case EPI_RESID: return run_gemm<128, 128, 4, 1, EPI_RESID, 3>(A, lda, B, ldb, M, N, K, epi, s);
+      default:
+        if (epi.q_norm)
+          return run_gemm<128, 128, 4, 1, EPI_QKV_NORM, 3>(A, lda, B, ldb, M, N, K, epi, s);
+        return run_gemm<128, 128, 4, 1, EPI_QKV, 3>(A, lda, B, ldb, M, N, K, epi, s);
+    }
+  }
+  if (epi.kind == EPI_SWIGLU && M <= 640)
+    return run_gemm<128, 256, 2, 4, EPI_SWIGLU, 3>(A, lda, B, ldb, M, N, K, epi, s);
   switch (epi.kind) {
     case EPI_STORE: return run_gemm_tail<256, 256, 4, 2, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, tail, s);
     case EPI_RESID: return run_gemm_tail<256, 256, 4, 2, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, tail, s);
