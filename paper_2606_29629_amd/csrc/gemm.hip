@@ -112,11 +112,19 @@ struct Mainloop {
   static constexpr int A_BLK = BM / 8 / NW, B_BLK = BN / 8 / NW;  // 1 KB blocks per wave
   static constexpr int KSTEPS = kBK / 16;
 
-  __device__ __forceinline__ static void run(GemmSmem<BM, BN, S>& sm, __amdgpu_buffer_rsrc_t ra,
-                                             const uint32_t (&a_off)[A_BLK],
-                                             __amdgpu_buffer_rsrc_t rb,
-                                             const uint32_t (&b_off)[B_BLK], int K, int wv,
-                                             int lane, f32x16 (&acc)[MI][NI]) {
+  // MA = the wave's row blocks that hold rows of the tile's valid range
+  // (compile-time, MA <= MI): blocks past it would only multiply zero rows,
+  // so the wave issues neither their MFMAs nor their A fragment reads (with
+  // MA = 0, no MFMA and no fragment read at all).  Its share of the tile
+  // loads and every barrier stay, so all waves keep the same barrier count.
+  template <int MA>
+  __device__ __forceinline__ static void run_rows(GemmSmem<BM, BN, S>& sm,
+                                                  __amdgpu_buffer_rsrc_t ra,
+                                                  const uint32_t (&a_off)[A_BLK],
+                                                  __amdgpu_buffer_rsrc_t rb,
+                                                  const uint32_t (&b_off)[B_BLK], int K, int wv,
+                                                  int lane, f32x16 (&acc)[MI][NI]) {
+    static_assert(MA >= 0 && MA <= MI, "active row blocks");
     const int wm = wv / WGN, wn = wv % WGN;
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -137,9 +145,10 @@ struct Mainloop {
     const int lr = lane & 31, lg = lane >> 5;
     bf16x8 fa[2][MI], fb[2][NI];
     auto lload = [&](int buf, int ks, int slot) {
+      if constexpr (MA == 0) return;
       const int ch = ks * 2 + lg;
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {
+      for (int i = 0; i < MA; ++i) {
         const int r = wm * WM + i * 32 + lr;
         fa[slot][i] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
       }
@@ -149,15 +158,15 @@ struct Mainloop {
         fb[slot][j] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
       }
     };
-    // Fragment f of a k-step: f < MI -> A block f, else B block f - MI.
+    // Fragment f of a k-step: f < MA -> A block f, else B block f - MA.
     auto lread = [&](int buf, int ks, int slot, int f) {
       const int ch = ks * 2 + lg;
-      if (f < MI) {
+      if (f < MA) {
         const int r = wm * WM + f * 32 + lr;
         fa[slot][f] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
       } else {
-        const int r = wn * WN + (f - MI) * 32 + lr;
-        fb[slot][f - MI] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
+        const int r = wn * WN + (f - MA) * 32 + lr;
+        fb[slot][f - MA] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
       }
     };
     // Load piece p of a tile: p < A_BLK -> A block p, else B block p - A_BLK.
@@ -178,7 +187,7 @@ struct Mainloop {
       acc[i][j] =
           __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][j], fa[slot][i], acc[i][j], 0, 0, 0);
     };
-    constexpr int NMF = MI * NI, NRD = MI + NI, NLD = A_BLK + B_BLK;
+    constexpr int NMF = MA * NI, NRD = MA > 0 ? MA + NI : 0, NLD = A_BLK + B_BLK;
     constexpr int NG = NMF > NRD ? NMF : NRD;
     constexpr int NGL = NG > NLD ? NG : NLD;
     const int KT = K / kBK;
@@ -216,6 +225,31 @@ struct Mainloop {
         __builtin_amdgcn_sched_barrier(0);
       }
       buf = nbuf;
+    }
+  }
+  __device__ __forceinline__ static void run(GemmSmem<BM, BN, S>& sm, __amdgpu_buffer_rsrc_t ra,
+                                             const uint32_t (&a_off)[A_BLK],
+                                             __amdgpu_buffer_rsrc_t rb,
+                                             const uint32_t (&b_off)[B_BLK], int K, int wv,
+                                             int lane, f32x16 (&acc)[MI][NI]) {
+    run_rows<MI>(sm, ra, a_off, rb, b_off, K, wv, lane, acc);
+  }
+  // The tile's first `rows` rows are valid: the wave runs the instantiation
+  // for its active row blocks (a wave-uniform choice).
+  template <int MA = MI>
+  __device__ __forceinline__ static void run_valid(int rows, GemmSmem<BM, BN, S>& sm,
+                                                   __amdgpu_buffer_rsrc_t ra,
+                                                   const uint32_t (&a_off)[A_BLK],
+                                                   __amdgpu_buffer_rsrc_t rb,
+                                                   const uint32_t (&b_off)[B_BLK], int K, int wv,
+                                                   int lane, f32x16 (&acc)[MI][NI]) {
+    const int wm = wv / WGN;
+    const int act = (rows - wm * WM + 31) / 32;  // row blocks holding valid rows
+    if constexpr (MA == 0) {
+      run_rows<0>(sm, ra, a_off, rb, b_off, K, wv, lane, acc);
+    } else {
+      if (act >= MA) run_rows<MA>(sm, ra, a_off, rb, b_off, K, wv, lane, acc);
+      else run_valid<MA - 1>(rows, sm, ra, a_off, rb, b_off, K, wv, lane, acc);
     }
   }
 };
@@ -544,7 +578,7 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
   } else {
     u = blockIdx.x - full;
     tile_of_id(full + u / tsplit, tiles_m, tiles_n, tm, tn);
-    kc = K / tsplit;
+    kc = cdiv(K / kBK, tsplit) * kBK;  // the last split takes the remainder
   }
   const int n_rows_b = KIND == EPI_SWIGLU ? 2 * epi.ffn : N;
   // Split-K (fp32 partial output only): split z covers k in [z kc, z kc + kc)
@@ -578,7 +612,7 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
   f32x16 acc[MI][NI];
-  ML::run(sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
+  ML::run_valid(M - tm * BM, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
 
   const int lr = lane & 31, lg = lane >> 5;
   if (u >= 0) {  // tail split: the tile's fp32 partial sums, [BM][BN]
@@ -673,7 +707,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * K + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
   f32x16 acc[MI][NI];
-  ML::run(sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
+  ML::run_valid(p_end - p0, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
 
   const int lr = lane & 31, lg = lane >> 5;
   const int row0 = p0 + wm * WM + lr;
@@ -738,9 +772,12 @@ static int tail_split(int total, int K, int kind) {
   const int G = cu_count();
   const int rem = tail_tiles(total);
   if (kind == EPI_SWIGLU || rem == 0) return 1;
+  // Split s covers k-tiles [s c, s c + c) with c = ceil(k-tiles / t), the
+  // last one the remainder: every split must keep at least one k-tile.
+  const int kt = K / kBK;
   int t = G / rem;
   if (t > 8) t = 8;
-  while (t > 1 && K % (kBK * t) != 0) --t;
+  while (t > 1 && (t - 1) * cdiv(kt, t) >= kt) --t;
   return t;
 }
 
