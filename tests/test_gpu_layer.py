@@ -308,6 +308,27 @@ def test_7b_ragged_prefill_sampled_rows():
     assert_e2e(vr, ex["v_new"], "7B V rows", emul=ref["v_new"])
 
 
+@pytest.mark.parametrize("n_tok", [129, 257, 640, 641, 1025])
+def test_7b_mid_size_prefill_gemm_paths(n_tok):
+    """Batches of a few hundred tokens take the mid-size GEMM tiles (128 x 128
+    with three stages for q/k/v and O, 128 x 256 for gate/up up to 640 rows),
+    skip the row blocks past the last valid row, and split the down
+    projection's K unevenly (1025 rows: three splits of 99, 99, 98 k-tiles).
+    Sampled rows on both sides of every tile boundary and the last rows."""
+    cfg = layer_7b()
+    batch = B([0, 1], [0, 100], [n_tok - 7, 7])
+    cs = Case(cfg, batch, 2, n_tok + 8, seed=7)
+    out, ws = cs.run()
+    rows = np.unique([r for r in (0, 1, 127, 128, 255, 256, 511, 512, 639, 640, 1023, 1024,
+                                  n_tok - 8, n_tok - 7, n_tok - 2, n_tok - 1)
+                     if 0 <= r < n_tok])
+    x1, act, w = stage_parity(cs, ws, rows, label=f"7B T={n_tok}")
+    check_down(cs, out, x1, act, w, rows, f"7B T={n_tok}")
+    ref = cs.oracle(rows=rows)
+    ex = cs.oracle(rows=rows, storage=None)
+    assert_e2e(to_host_f64(out)[rows], ex["out"], f"7B T={n_tok} rows", emul=ref["out"])
+
+
 def test_7b_decode_step_all_rows():
     cfg = layer_7b()
     ctx = [1, 63, 64, 127, 128, 129, 1000, 4095]
