@@ -256,6 +256,24 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
                               const tri_batch* batch, const void* k_new, const void* v_new,
                               void* stream);
 
+/* Plain projection C = A B^T on the layer's GEMM kernels: the matrix
+ * multiply of the Thinker's projections (Section II-A) and the synthetic
+ * kernel of the paper's roofline benchmark over arithmetic intensity
+ * (Section II-C, frequency-locked roofline benchmarking).
+ *  A [M, K], B [N, K] (the nn.Linear weight layout), C [M, N]: bf16,
+ *    row-major, device memory, 16-byte aligned; fp32 accumulation, C rounded
+ *    to nearest even.  M, N, K >= 1, K a multiple of 64, N a multiple of 4,
+ *    A and B each under 2 GiB; C overlaps neither operand.
+ *  workspace: device scratch of tri_linear_workspace_size bytes (split
+ *    partials; 256-byte aligned), or NULL when that size is 0.
+ *  stream: hipStream_t (NULL = default stream).
+ * Errors (before any launch): TRI_ERR_NULL, TRI_ERR_SHAPE, TRI_ERR_RANGE,
+ * TRI_ERR_ALIGN, TRI_ERR_WORKSPACE, TRI_ERR_ALIAS; TRI_ERR_HIP if a launch
+ * fails. */
+tri_status tri_linear_workspace_size(int32_t M, int32_t N, int32_t K, size_t* bytes);
+tri_status tri_linear(const void* A, const void* B, void* C, int32_t M, int32_t N, int32_t K,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
 /* MoE routing alone (test hook for bit-exact routing): logits = h2 W_r^T in
  * float32 (one fixed summation order per logit), softmax over all experts,
  * top_k by logit (descending, ties to the lower index), weights p[idx]

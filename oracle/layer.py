@@ -63,6 +63,13 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     return np.ldexp(np.rint(np.ldexp(m, 8)), e - 8).astype(x.dtype)
 
 
+def project(a: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """A projection y = a W^T with an nn.Linear weight W [out, in]: the
+    matrix multiply of the layer's q/k/v, O and MLP projections (Section
+    II-A) and of the roofline benchmark kernel (Section II-C)."""
+    return a @ w.T
+
+
 def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
     """RMSNorm over the last axis: x / sqrt(mean(x^2) + eps) * g."""
     ms = np.mean(x * x, axis=-1, keepdims=True)

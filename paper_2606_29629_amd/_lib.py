@@ -95,6 +95,9 @@ _FUNCS = {
                                       ctypes.c_void_p]),
     "tri_phase_intensity": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "tri_version": (ctypes.c_int32, []),
+    "tri_linear_workspace_size": (ctypes.c_int, [ctypes.c_int32] * 3 + [ctypes.c_void_p]),
+    "tri_linear": (ctypes.c_int, [ctypes.c_void_p] * 3 + [ctypes.c_int32] * 3
+                   + [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
 }
 
 
@@ -298,6 +301,29 @@ def kvcache_append(cfg, cache, batch, k_new, v_new, stream=None) -> None:
     _check(lib().tri_kvcache_append(ctypes.byref(cfg), ctypes.byref(kc), ctypes.byref(b),
                                     _ptr(k_new), _ptr(v_new), _stream(stream)),
            "tri_kvcache_append")
+
+
+def linear_workspace_size(M: int, N: int, K: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().tri_linear_workspace_size(int(M), int(N), int(K), ctypes.byref(n)),
+           "tri_linear_workspace_size")
+    return n.value
+
+
+def linear(a, b, out=None, workspace=None, stream=None):
+    """out = a @ b^T (bf16 [M, K] x bf16 [N, K] -> bf16 [M, N]) through tri_linear."""
+    import torch
+    M, K = a.shape
+    N = b.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    need = linear_workspace_size(M, N, K)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=a.device)
+    wb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().tri_linear(_ptr(a), _ptr(b), _ptr(out), M, N, K, _ptr(workspace), wb,
+                            _stream(stream)), "tri_linear")
+    return out
 
 
 def moe_route(cfg, h2_f32, w_router, idx, w, stream=None) -> None:

@@ -783,6 +783,34 @@ tri_status tri_kvcache_append(const tri_layer_config* cfg, const tri_kv_cache* c
   return TRI_OK;
 }
 
+tri_status tri_linear_workspace_size(int32_t M, int32_t N, int32_t K, size_t* bytes) {
+  if (!bytes) return TRI_ERR_NULL;
+  if (M <= 0 || N <= 0 || K <= 0 || K % 64 != 0 || N % 4 != 0) return TRI_ERR_SHAPE;
+  *bytes = M <= kSkinnyMaxRows ? skinny_partial_bytes(M, N, K, EPI_STORE) : gemm_tail_bytes();
+  return TRI_OK;
+}
+
+tri_status tri_linear(const void* A, const void* B, void* C, int32_t M, int32_t N, int32_t K,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  size_t need = 0;
+  tri_status st = tri_linear_workspace_size(M, N, K, &need);
+  if (st != TRI_OK) return st;
+  if (!A || !B || !C) return TRI_ERR_NULL;
+  if ((int64_t)M * K * 2 >= (int64_t)1 << 31 || (int64_t)N * K * 2 >= (int64_t)1 << 31)
+    return TRI_ERR_RANGE;  // 32-bit buffer ranges of the operand loads
+  if (!aligned16(A) || !aligned16(B) || !aligned16(C)) return TRI_ERR_ALIGN;
+  if (need > 0 && (!workspace || workspace_bytes < need)) return TRI_ERR_WORKSPACE;
+  if (need > 0 && ((uintptr_t)workspace % kAlign) != 0) return TRI_ERR_ALIGN;
+  if (overlaps(C, (size_t)M * N * 2, A, (size_t)M * K * 2) ||
+      overlaps(C, (size_t)M * N * 2, B, (size_t)N * K * 2))
+    return TRI_ERR_ALIAS;
+  Epi e{};
+  e.kind = EPI_STORE;
+  e.out = C;
+  e.ldo = N;
+  return run_linear(A, K, B, M, N, K, e, (float*)workspace, (hipStream_t)stream);
+}
+
 tri_status tri_moe_route(const tri_layer_config* cfg, const float* h2, const void* w_router,
                          int32_t n_tokens, int32_t* idx, float* w, void* stream) {
   tri_status st = check_config(cfg);

@@ -326,6 +326,37 @@ def test_decode_batches_fit_the_noalloc_scratch(lib):
     assert s1.value >= s2.value
 
 
+def test_linear_validation(lib):
+    """tri_linear checks shapes, pointers, alignment, ranges, workspace and
+    aliasing before any launch (fake device addresses: nothing runs)."""
+    ws = ctypes.c_size_t()
+    assert lib.tri_linear_workspace_size(64, 4096, 4096, ctypes.byref(ws)) == 0
+    assert ws.value > 0                       # short batch: split-K partials
+    big = ctypes.c_size_t()
+    assert lib.tri_linear_workspace_size(1024, 4096, 4096, ctypes.byref(big)) == 0
+    assert big.value == 256 * 256 * 256 * 4   # the large GEMMs' tail tiles
+    assert lib.tri_linear_workspace_size(8, 64, 100, ctypes.byref(ws)) == T.TRI_ERR_SHAPE
+    assert lib.tri_linear_workspace_size(8, 6, 64, ctypes.byref(ws)) == T.TRI_ERR_SHAPE
+    assert lib.tri_linear_workspace_size(0, 64, 64, ctypes.byref(ws)) == T.TRI_ERR_SHAPE
+    assert lib.tri_linear_workspace_size(8, 64, 64, None) == T.TRI_ERR_NULL
+    # Every call below must fail validation (the pointers are fake): the
+    # shape needs split-K partials, so a missing workspace is an error too.
+    A, B, C, W = FAKE, FAKE + (1 << 30), FAKE + (2 << 30), FAKE + (3 << 30)
+    M, N, K = 64, 4096, 4096
+    need = ctypes.c_size_t()
+    assert lib.tri_linear_workspace_size(M, N, K, ctypes.byref(need)) == 0 and need.value > 0
+    f = lib.tri_linear
+    ok_ws = need.value
+    assert f(None, B, C, M, N, K, W, ok_ws, None) == T.TRI_ERR_NULL
+    assert f(A + 8, B, C, M, N, K, W, ok_ws, None) == T.TRI_ERR_ALIGN
+    assert f(A, B, C, M, N, K, None, 0, None) == T.TRI_ERR_WORKSPACE
+    assert f(A, B, C, M, N, K, W, ok_ws - 1, None) == T.TRI_ERR_WORKSPACE
+    assert f(A, B, C, M, N, K, W + 16, ok_ws, None) == T.TRI_ERR_ALIGN
+    assert f(A, B, A, M, N, K, W, ok_ws, None) == T.TRI_ERR_ALIAS
+    assert f(A, B, C, 8, 1 << 20, 1024, W, 1 << 30, None) == T.TRI_ERR_RANGE
+    assert f(A, B, C, M, N, 96, W, ok_ws, None) == T.TRI_ERR_SHAPE
+
+
 def test_status_strings(lib):
     for s in range(-9, 1):
         assert T.status_string(s) and T.status_string(s) != "unknown status"

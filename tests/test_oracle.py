@@ -36,6 +36,23 @@ def B(slot, ctx, q):
 
 # --------------------------------------------------------------- P1 RMSNorm --
 
+def test_project_matches_scalar_sums():
+    """y[i, j] = sum_k a[i, k] w[j, k], written out as scalar loops on a tiny
+    integer case (exact in float64), and the identity weight."""
+    rng = np.random.default_rng(5)
+    a = rng.integers(-9, 10, (3, 5)).astype(np.float64)
+    w = rng.integers(-9, 10, (4, 5)).astype(np.float64)
+    y = L.project(a, w)
+    assert y.shape == (3, 4)
+    for i in range(3):
+        for j in range(4):
+            acc = 0.0
+            for k in range(5):
+                acc += a[i, k] * w[j, k]
+            assert y[i, j] == acc
+    assert np.array_equal(L.project(a, np.eye(5)), a)
+
+
 def test_rmsnorm_constant_vector():
     H, c, eps = 64, 3.0, 1e-6
     g = np.linspace(0.5, 1.5, H)
