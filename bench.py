@@ -478,6 +478,88 @@ def run_secondary(args, tri, name):
     return res, phase
 
 
+def fit_models(points, eta, ai_key):
+    """Fits of the throughput models of Section III-C to sweep points: Eq. 1
+    with eta the published peak flops per clock and beta the median of
+    throughput / A.I. over the points whose Eq. 1 bound is the memory term,
+    and Eq. 3 with omega (gamma = 0: the clock is not set, so its exponent
+    cannot be separated) on the points past the ridge at their own clock.
+    Adds each point's model predictions."""
+    fit = {"eta_flop_per_clock": eta}
+    have_f = [p for p in points if p.get("gfxclk_mhz")]
+    if not have_f:
+        return fit
+    ratios = sorted(p["tflops"] * 1e12 / p[ai_key] for p in have_f
+                    if p[ai_key] < 0.25 * eta * p["gfxclk_mhz"] * 1e6 / (PEAK_HBM_GBS * 1e9))
+    beta = ratios[len(ratios) // 2] if ratios else None
+    fit["eq1_beta_gbs"] = beta / 1e9 if beta else None
+    num = den = 0.0
+    for p in have_f:
+        f = p["gfxclk_mhz"] * 1e6
+        if p[ai_key] >= eta * f / (PEAK_HBM_GBS * 1e9):
+            num += eta * f * p[ai_key] / (p["tflops"] * 1e12) - p[ai_key]
+            den += 1
+    fit["eq3_omega_flop_per_byte"] = num / den if den else None
+    for p in have_f:
+        f = p["gfxclk_mhz"] * 1e6
+        a = p[ai_key]
+        p["eq1_tflops"] = min(eta * f, (beta or 0) * a) / 1e12
+        if fit["eq3_omega_flop_per_byte"] is not None:
+            p["eq3_tflops"] = min(eta * f * a / (a + fit["eq3_omega_flop_per_byte"]),
+                                  (beta or 0) * a) / 1e12
+    return fit
+
+
+def matmul_sweep(tri, eta):
+    """The paper's roofline benchmark kernel (Section II-C, frequency-locked
+    roofline benchmarking) without clock control: a matrix multiply C = A W^T
+    through tri_linear, W [N, K] = [65536, 4096] (512 MiB, past the 256 MB
+    Infinity Cache; K as in the layer's projections), swept over A.I. in
+    {1, 25, 50, 100, 200} flop/B by the row count M (A.I. = M N K / (M K + N K
+    + M N) for bf16 operands, so M = A.I. N K / (N K - A.I. (N + K))).  Per
+    point: time per call, TFLOP/s, GB/s, and the shader clock and socket
+    power over a 2 s loop after 1 s at the same load.  Synthetic normal
+    operands."""
+    import torch
+    K, N = 4096, 65536
+    g = torch.Generator(device="cuda").manual_seed(0)
+    w = (torch.randn((N, K), device="cuda", generator=g) * 0.02).to(torch.bfloat16)
+    out = []
+    for ai_target in (1, 25, 50, 100, 200):
+        M = max(1, round(ai_target * N * K / (N * K - ai_target * (N + K))))
+        a = torch.randn((M, K), device="cuda", generator=g).to(torch.bfloat16)
+        c = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+        need = tri.linear_workspace_size(M, N, K)
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device="cuda")
+        call = lambda: tri.linear(a, w, out=c, workspace=ws)
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        reps = 20
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        flops, byts = 2.0 * M * N * K, 2.0 * (M * K + N * K + M * N)
+        energy_loop(call, min_s=1.0)            # let clock and power settle at this load
+        en = energy_loop(call, min_s=2.0)
+        tel = en["telemetry"] if en else {}
+        pt = {"ai_target": ai_target, "rows": M, "ai": flops / byts, "ms_per_call": ms,
+              "tflops": flops / (ms / 1e3) / 1e12, "gbs": byts / (ms / 1e3) / 1e9,
+              "gfxclk_mhz": tel.get("gfxclk_mhz"), "socket_power_w": tel.get("socket_power_w"),
+              "board_power_w": en["avg_power_w"] if en else None,
+              "joules_per_tflop": en["joules_per_call"] / (flops / 1e12) if en else None}
+        out.append(pt)
+        print(json.dumps({"matmul_sweep_point": pt}), file=sys.stderr, flush=True)
+        del a, c, ws
+    del w
+    torch.cuda.empty_cache()
+    return out, fit_models(out, eta, "ai")
+
+
 def ai_sweep(args, tri):
     """Arithmetic-intensity sweep under the GPU's own clock management (the
     paper's frequency-locked roofline, Section II-C, without clock control):
@@ -550,35 +632,10 @@ def ai_sweep(args, tri):
         print(json.dumps({"ai_sweep_point": pt}), file=sys.stderr, flush=True)
         del cache, db, x, o, ws
         torch.cuda.empty_cache()
-    # Fits.  Eq. 1: beta from the points whose Eq. 1 bound is the memory term.
-    fit = {"eta_flop_per_clock": eta}
-    have_f = [p for p in out if p["gfxclk_mhz"]]
-    if have_f:
-        ratios = sorted(p["tflops"] * 1e12 / p["ai_time_weighted"] for p in have_f
-                        if p["ai_time_weighted"] * 1 < 0.25 * eta * p["gfxclk_mhz"] * 1e6 /
-                        (PEAK_HBM_GBS * 1e9))
-        beta = ratios[len(ratios) // 2] if ratios else None
-        fit["eq1_beta_gbs"] = beta / 1e9 if beta else None
-        # Eq. 3 with gamma = 0: eta f A.I. / (A.I. + omega), fitted on the points
-        # past the ridge at their own clock (eta f / peak HBM bandwidth).
-        num = den = 0.0
-        for p in have_f:
-            f = p["gfxclk_mhz"] * 1e6
-            th = p["tflops"] * 1e12
-            if p["ai_time_weighted"] >= eta * f / (PEAK_HBM_GBS * 1e9):
-                c = eta * f * p["ai_time_weighted"] / th - p["ai_time_weighted"]
-                num += c
-                den += 1
-        fit["eq3_omega_flop_per_byte"] = num / den if den else None
-        for p in have_f:
-            f = p["gfxclk_mhz"] * 1e6
-            a = p["ai_time_weighted"]
-            p["eq1_tflops"] = min(eta * f, (beta or 0) * a) / 1e12
-            if fit["eq3_omega_flop_per_byte"] is not None:
-                p["eq3_tflops"] = min(eta * f * a / (a + fit["eq3_omega_flop_per_byte"]),
-                                      (beta or 0) * a) / 1e12
-    print(json.dumps({"ai_sweep": out, "fit": fit, "ridge_flop_per_byte":
-                      PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3,
+    fit = fit_models(out, eta, "ai_time_weighted")
+    mm, mm_fit = matmul_sweep(tri, eta)
+    print(json.dumps({"ai_sweep": out, "fit": fit, "matmul_sweep": mm, "matmul_fit": mm_fit,
+                      "ridge_flop_per_byte": PEAK_BF16_TFLOPS / PEAK_HBM_GBS * 1e3,
                       "layer": "7B dense (H 3584, 28/4 heads, D 128, F 18944), bf16"}))
     return 0
 
@@ -598,7 +655,7 @@ def main(argv=None):
     ap.add_argument("--detail-out", default=None,
                     help="also write the full result record (phases, stages, secondary) here")
     ap.add_argument("--ai-sweep", action="store_true",
-                    help="only run the arithmetic-intensity sweep of the 7B layer (clock, power, "
+                    help="only run the arithmetic-intensity sweeps of the 7B layer and of the matrix-multiply kernel (clock, power, "
                          "Eq. 1 / Eq. 3 fits) and print it as one JSON line")
     args = ap.parse_args(argv)
     if args.gpus != 1:
