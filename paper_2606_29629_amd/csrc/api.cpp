@@ -284,17 +284,31 @@ struct SideStream {
   bool failed = false;  // creation failed once (e.g. under graph capture): run serially
 };
 constexpr int kMaxSideDevices = 64;
-SideStream* side_stream() {
+// The side stream of the current device, or nullptr (run on the caller's
+// stream) when the caller's stream belongs to another device.
+SideStream* side_stream(hipStream_t caller) {
   static SideStream ss[kMaxSideDevices];
-  int dev = -1;
+  int dev = -1, sdev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxSideDevices) return nullptr;
+  if (caller && (hipStreamGetDevice(caller, &sdev) != hipSuccess || sdev != dev)) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
   return &ss[dev];
 }
 // With the device's lock held: makes sure the stream and events exist; false
-// means "run on the caller's stream".
-bool side_ready(SideStream& x) {
+// means "run on the caller's stream".  No stream is created while the
+// caller's stream is being captured into a graph (creating one could
+// invalidate the capture); an existing side stream joins the capture through
+// the fork and join events.
+bool side_ready(SideStream& x, hipStream_t caller) {
   if (x.s) return true;
   if (x.failed) return false;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(caller, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) {
+    (void)hipGetLastError();
+    return false;
+  }
   hipStream_t st = nullptr;
   hipEvent_t f = nullptr, j = nullptr;
   if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) == hipSuccess &&
@@ -591,11 +605,11 @@ tri_status tri::layer_call(bool decode, bool timed, const tri_layer_config* cfg,
       decode || b->max_q_len == 1 || (int64_t)b->n_seqs * b->max_q_len != b->n_tokens;
   float* part_dec = (float*)((char*)part + flash_part_bytes(cfg, b));
   hipStream_t sd = s;  // stream of the split-KV attention
-  SideStream* side = (flash && splitkv) ? side_stream() : nullptr;
+  SideStream* side = (flash && splitkv) ? side_stream(s) : nullptr;
   std::unique_lock<std::mutex> side_lock;
   if (side) {
     side_lock = std::unique_lock<std::mutex>(side->mu);
-    if (side_ready(*side)) {
+    if (side_ready(*side, s)) {
       TRI_HIP(hipEventRecord(side->fork, s));
       TRI_HIP(hipStreamWaitEvent(side->s, side->fork, 0));
       sd = side->s;
