@@ -3,12 +3,17 @@
 // q/k/v split + rotary embedding + KV-cache write, fp32 store).
 //
 // Both operands are K-contiguous ("nn.Linear" weights [out, in] and row-major
-// activations), which is the native operand layout of v_mfma_f32_32x32x16_bf16:
-// lane l supplies row (l % 32) and 8 consecutive k of slice (l / 32).
+// activations), which is the native operand layout of the bf16 MFMAs with 8
+// values per lane: in v_mfma_f32_32x32x16_bf16 lane l supplies row l % 32 and
+// k 8 (l / 32) .. + 7, in v_mfma_f32_16x16x32_bf16 row l % 16 and k 8 (l / 16)
+// .. + 7.
 //
 // Tiling: BM x BN x 64 block tile, WGM x WGN waves (two waves per SIMD, so one
 // wave's LDS waits overlap the other's MFMAs), each wave a (BM/WGM) x (BN/WGN)
-// sub-tile of 32x32 MFMA blocks.  A and B tiles are staged through LDS, double
+// sub-tile of SH x SH MFMA blocks: 32x32x16 or 16x16x32 instructions (the
+// same flops per clock; the 16x16 form moves half the accumulator bytes per
+// flop through the register file, which lets the power-capped prefill GEMMs
+// hold a higher clock).  A and B tiles are staged through LDS, double
 // buffered, with 16-byte chunks XOR-swizzled (see swz) so that fragment reads
 // are free of bank conflicts.  Tiles move from HBM to LDS with
 // buffer_load_dwordx4 ... lds (no register staging); the loads of tile k+1
@@ -70,6 +75,59 @@ __device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n,
   tile_of_id(xcd_id(bid, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
 }
 
+// MFMA shape SH: SH x SH output blocks, KSTEP = 512 / SH of k per
+// instruction, the accumulator a 16- or 4-vector per lane.
+template <int SH>
+struct Mfma;
+template <>
+struct Mfma<32> {
+  using acc_t = f32x16;
+  static constexpr int KSTEP = 16;
+  __device__ __forceinline__ static acc_t mma(bf16x8 a, bf16x8 b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <>
+struct Mfma<16> {
+  using acc_t = f32x4;
+  static constexpr int KSTEP = 32;
+  __device__ __forceinline__ static acc_t mma(bf16x8 a, bf16x8 b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+// Accumulator geometry.  Block (i, j) of a wave holds C^T (the weight rows
+// are the MFMA's row operand): lane l owns token row SH i + l % SH and, in
+// each block, QN = SH * SH / 256 groups of four consecutive output columns,
+// group q at SH j + (256 / SH) q + 4 (l / SH).  The epilogues walk the G =
+// NI * QN groups of a row block: group g = QN j + q, column offset col(g)
+// (plus the lane's 4 (l / SH)), values grp(acc, i, g).
+template <int SH, int MI, int NI>
+struct AccGeo {
+  using acc_t = typename Mfma<SH>::acc_t;
+  static constexpr int QN = SH * SH / 256, G = NI * QN;
+  __device__ __forceinline__ static constexpr int col(int g) {
+    return SH * (g / QN) + (256 / SH) * (g % QN);
+  }
+  __device__ __forceinline__ static f32x4 grp(const acc_t (&acc)[MI][NI], int i, int g) {
+    if constexpr (SH == 32) {
+      const int j = g / 4, q = g % 4;
+      return f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                   acc[i][j][4 * q + 3]};
+    } else {
+      return acc[i][g];
+    }
+  }
+  __device__ __forceinline__ static int lane_row(int lane) { return lane % SH; }
+  __device__ __forceinline__ static int lane_col(int lane) { return 4 * (lane / SH); }
+};
+
+// MFMA shapes per tile family: the compute-bound prefill tiles (256 x 256,
+// the grouped expert tiles of 128 or 256 rows) and the mid-size-M tiles.  The
+// weight-streaming decode tiles keep 32 x 32 blocks.
+constexpr int kPrefillSH = 16;
+constexpr int kMidSH = 16;
+
 template <int BM, int BN, int S = 2>
 struct GemmSmem {
   bf16 a[S][BM * kBK];
@@ -93,24 +151,27 @@ __device__ __forceinline__ int b_row_of(int kind, int tn, int nt, int ffn) {
 // swz(row, lane % 8) of this lane's row in each of its 1 KB LDS blocks (at or
 // beyond the buffer size for rows that must read as zero).
 //
-// S LDS stages, tiles loaded S - 1 ahead.  Schedule of k-tile t (4 k-steps
-// of 16): the fragments of k-step s + 1 are read from LDS while the MFMAs of
-// step s run.  Before the MFMAs of the last step, each wave waits for its
-// loads of tile t + 1 (those of tiles t + 2 .. t + S - 1 may stay in flight),
-// one barrier makes tile t + 1 visible and retires every read of tile t, the
-// loads of tile t + S go into tile t's buffer and the first fragments of tile
-// t + 1 are read -- all under the last step's MFMAs, so the barrier costs no
-// matrix-core time beyond the skew between waves.  Compute-bound tiles use
-// S = 2; the decode projections, bound by the weight stream, use more stages
-// for more bytes in flight per CU.
-template <int BM, int BN, int WGM, int WGN, int S = 2>
+// S LDS stages, tiles loaded S - 1 ahead.  Schedule of k-tile t (KSTEPS
+// k-steps of one MFMA's depth): the fragments of k-step s + 1 are read from
+// LDS while the MFMAs of step s run.  Before the MFMAs of the last step, each
+// wave waits for its loads of tile t + 1 (those of tiles t + 2 .. t + S - 1
+// may stay in flight), one barrier makes tile t + 1 visible and retires every
+// read of tile t, the loads of tile t + S go into tile t's buffer and the
+// first fragments of tile t + 1 are read -- all under the last step's MFMAs,
+// so the barrier costs no matrix-core time beyond the skew between waves.
+// Compute-bound tiles use S = 2; the decode projections, bound by the weight
+// stream, use more stages for more bytes in flight per CU.
+template <int BM, int BN, int WGM, int WGN, int S = 2, int SH = 32>
 struct Mainloop {
+  using MF = Mfma<SH>;
+  using acc_t = typename MF::acc_t;
   static constexpr int NT = WGM * WGN * 64;
   static constexpr int NW = NT / 64;
   static constexpr int WM = BM / WGM, WN = BN / WGN;
-  static constexpr int MI = WM / 32, NI = WN / 32;
+  static constexpr int MI = WM / SH, NI = WN / SH;
   static constexpr int A_BLK = BM / 8 / NW, B_BLK = BN / 8 / NW;  // 1 KB blocks per wave
-  static constexpr int KSTEPS = kBK / 16;
+  static constexpr int KSTEPS = kBK / MF::KSTEP;
+  static_assert(WM % SH == 0 && WN % SH == 0, "wave tile of whole MFMA blocks");
 
   // MA = the wave's row blocks that hold rows of the tile's valid range
   // (compile-time, MA <= MI): blocks past it would only multiply zero rows,
@@ -123,13 +184,13 @@ struct Mainloop {
                                                   const uint32_t (&a_off)[A_BLK],
                                                   __amdgpu_buffer_rsrc_t rb,
                                                   const uint32_t (&b_off)[B_BLK], int K, int wv,
-                                                  int lane, f32x16 (&acc)[MI][NI]) {
+                                                  int lane, acc_t (&acc)[MI][NI]) {
     static_assert(MA >= 0 && MA <= MI, "active row blocks");
     const int wm = wv / WGN, wn = wv % WGN;
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{0.f};
+      for (int j = 0; j < NI; ++j) acc[i][j] = acc_t{0.f};
     // kill = 0x80000000 pushes every offset past the buffer's range, so the
     // load writes zeros instead of touching memory (used past the last tile,
     // keeping the schedule free of branches).
@@ -142,32 +203,42 @@ struct Mainloop {
       for (int j = 0; j < B_BLK; ++j)
         buffer_load_lds16(rb, &sm.b[buf][(wv + NW * j) * 8 * kBK], b_off[j] | kill, kb);
     };
-    const int lr = lane & 31, lg = lane >> 5;
+    // Fragment reads.  The lane reads row SH i + l % SH of a block and the
+    // 16-byte chunk ks * KSTEP / 8 + l / SH of the step.  The swizzle of a row
+    // depends on (row / 2) % 8 only, the same for rows r and r + SH i, so one
+    // byte address per operand and k-step serves every block and buffer
+    // (immediate offsets).
+    uint32_t a_base[KSTEPS], b_base[KSTEPS];
+    {
+      const int lr = lane % SH, lg = lane / SH;
+      const int ra0 = wm * WM + lr, rb0 = wn * WN + lr;
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+        const int ch = ks * (MF::KSTEP / 8) + lg;
+        a_base[ks] = (uint32_t)((ra0 * kBK + swz(ra0, ch) * 8) * 2);
+        b_base[ks] = (uint32_t)((rb0 * kBK + swz(rb0, ch) * 8) * 2);
+      }
+    }
+    const char* const lds_a = (const char*)&sm.a[0][0];
+    const char* const lds_b = (const char*)&sm.b[0][0];
+    auto rd_a = [&](int buf, int ks, int i) {
+      return *(const bf16x8*)(lds_a + a_base[ks] + (buf * BM * kBK + i * SH * kBK) * 2);
+    };
+    auto rd_b = [&](int buf, int ks, int j) {
+      return *(const bf16x8*)(lds_b + b_base[ks] + (buf * BN * kBK + j * SH * kBK) * 2);
+    };
     bf16x8 fa[2][MI], fb[2][NI];
     auto lload = [&](int buf, int ks, int slot) {
       if constexpr (MA == 0) return;
-      const int ch = ks * 2 + lg;
 #pragma unroll
-      for (int i = 0; i < MA; ++i) {
-        const int r = wm * WM + i * 32 + lr;
-        fa[slot][i] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
-      }
+      for (int i = 0; i < MA; ++i) fa[slot][i] = rd_a(buf, ks, i);
 #pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        const int r = wn * WN + j * 32 + lr;
-        fb[slot][j] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
-      }
+      for (int j = 0; j < NI; ++j) fb[slot][j] = rd_b(buf, ks, j);
     };
     // Fragment f of a k-step: f < MA -> A block f, else B block f - MA.
     auto lread = [&](int buf, int ks, int slot, int f) {
-      const int ch = ks * 2 + lg;
-      if (f < MA) {
-        const int r = wm * WM + f * 32 + lr;
-        fa[slot][f] = *(const bf16x8*)&sm.a[buf][r * kBK + swz(r, ch) * 8];
-      } else {
-        const int r = wn * WN + (f - MA) * 32 + lr;
-        fb[slot][f - MA] = *(const bf16x8*)&sm.b[buf][r * kBK + swz(r, ch) * 8];
-      }
+      if (f < MA) fa[slot][f] = rd_a(buf, ks, f);
+      else fb[slot][f - MA] = rd_b(buf, ks, f - MA);
     };
     // Load piece p of a tile: p < A_BLK -> A block p, else B block p - A_BLK.
     auto gpiece = [&](int kt, int buf, uint32_t kill, int p) {
@@ -180,12 +251,11 @@ struct Mainloop {
     };
     // B (weight rows) as the MFMA's row operand and A (token rows) as its
     // column operand: accumulator block (i, j) holds C^T, so a lane owns one
-    // token row and four consecutive output columns per element group, and
-    // the epilogues move 8 or 16 contiguous bytes per lane.
+    // token row and groups of four consecutive output columns, and the
+    // epilogues move 8 or 16 contiguous bytes per lane.
     auto mfma = [&](int slot, int g) {
       const int i = g / NI, j = g % NI;
-      acc[i][j] =
-          __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[slot][j], fa[slot][i], acc[i][j], 0, 0, 0);
+      acc[i][j] = MF::mma(fb[slot][j], fa[slot][i], acc[i][j]);
     };
     constexpr int NMF = MA * NI, NRD = MA > 0 ? MA + NI : 0, NLD = A_BLK + B_BLK;
     constexpr int NG = NMF > NRD ? NMF : NRD;
@@ -231,7 +301,7 @@ struct Mainloop {
                                              const uint32_t (&a_off)[A_BLK],
                                              __amdgpu_buffer_rsrc_t rb,
                                              const uint32_t (&b_off)[B_BLK], int K, int wv,
-                                             int lane, f32x16 (&acc)[MI][NI]) {
+                                             int lane, acc_t (&acc)[MI][NI]) {
     run_rows<MI>(sm, ra, a_off, rb, b_off, K, wv, lane, acc);
   }
   // The tile's first `rows` rows are valid: the wave runs the instantiation
@@ -242,9 +312,9 @@ struct Mainloop {
                                                    const uint32_t (&a_off)[A_BLK],
                                                    __amdgpu_buffer_rsrc_t rb,
                                                    const uint32_t (&b_off)[B_BLK], int K, int wv,
-                                                   int lane, f32x16 (&acc)[MI][NI]) {
+                                                   int lane, acc_t (&acc)[MI][NI]) {
     const int wm = wv / WGN;
-    const int act = (rows - wm * WM + 31) / 32;  // row blocks holding valid rows
+    const int act = (rows - wm * WM + SH - 1) / SH;  // row blocks holding valid rows
     if constexpr (MA == 0) {
       run_rows<0>(sm, ra, a_off, rb, b_off, K, wv, lane, acc);
     } else {
@@ -254,109 +324,108 @@ struct Mainloop {
   }
 };
 
-// Accumulator block (i, j) of a wave holds C^T: element e of lane l is
-// output row 32 i + l % 32 and output column 32 j + 8 (e / 4) + 4 (l / 32)
-// + e % 4 of the wave sub-tile, so elements 4q .. 4q + 3 are four consecutive
-// columns.  row0 = output row of the lane (including l % 32); col0 = output
-// column of the lane's first element (including 4 (l / 32)).  Rows >= row_lim
+// Epilogues.  The accumulators are read by column group (AccGeo): row0 =
+// output row of the lane in row block 0 (including l % SH); col0 = output
+// column of the lane's first group (including 4 (l / SH)).  Rows >= row_lim
 // and column groups >= N are not written (N is a multiple of 4).  Operands
-// of a lane's row (residual) are loaded for a whole block before any store,
-// at clamped addresses, so no load waits behind a store.
-template <int MI, int NI, int EK>
-__device__ __forceinline__ void plain_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
-                                               int row0, int row_lim, int col0, int N) {
+// of a lane's row (residual) are loaded for a whole row block before any
+// store, at clamped addresses, so no load waits behind a store.
+template <int SH, int MI, int NI, int EK>
+__device__ __forceinline__ void plain_epilogue(
+    const typename Mfma<SH>::acc_t (&acc)[MI][NI], const Epi& epi, int row0, int row_lim,
+    int col0, int N) {
+  using Geo = AccGeo<SH, MI, NI>;
+  constexpr int G = Geo::G;
   constexpr int KIND = EK & kEpiKindMask;
   using T = typename Store<(EK & kEpiF32) != 0>::T;
   typedef T T4 __attribute__((ext_vector_type(4)));
   const T* __restrict__ resid = (const T*)epi.resid;
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
-    const int row = row0 + 32 * i;
+    const int row = row0 + SH * i;
     const int rc = min(row, row_lim - 1);
-    T4 res[NI][4];
+    T4 res[G];
     if constexpr (KIND == EPI_RESID) {
 #pragma unroll
-      for (int j = 0; j < NI; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int col = min(col0 + 32 * j + 8 * q, N - 4);
-          res[j][q] = *(const T4*)(resid + (int64_t)rc * epi.ldr + col);
-        }
+      for (int g = 0; g < G; ++g) {
+        const int col = min(col0 + Geo::col(g), N - 4);
+        res[g] = *(const T4*)(resid + (int64_t)rc * epi.ldr + col);
+      }
     }
     if (row >= row_lim) continue;
 #pragma unroll
-    for (int j = 0; j < NI; ++j)
+    for (int g = 0; g < G; ++g) {
+      const int col = col0 + Geo::col(g);
+      if (col >= N) continue;
+      const f32x4 v = Geo::grp(acc, i, g);
+      if constexpr (KIND == EPI_STORE_F32) {
+        *(f32x4*)((float*)epi.out + (int64_t)row * epi.ldo + col) = v;
+      } else {
+        T4 o;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int col = col0 + 32 * j + 8 * q;
-        if (col >= N) continue;
-        if constexpr (KIND == EPI_STORE_F32) {
-          *(f32x4*)((float*)epi.out + (int64_t)row * epi.ldo + col) =
-              f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
-                    acc[i][j][4 * q + 3]};
-        } else {
-          T4 o;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float v = acc[i][j][4 * q + e];
-            if constexpr (KIND == EPI_RESID) v += (float)res[j][q][e];
-            o[e] = (T)v;
-          }
-          *(T4*)((T*)epi.out + (int64_t)row * epi.ldo + col) = o;
+        for (int e = 0; e < 4; ++e) {
+          float x = v[e];
+          if constexpr (KIND == EPI_RESID) x += (float)res[g][e];
+          o[e] = (T)x;
         }
+        *(T4*)((T*)epi.out + (int64_t)row * epi.ldo + col) = o;
       }
+    }
   }
 }
 
-// SwiGLU: blocks j < NI/2 hold gate, j + NI/2 the matching up; f0 = output
-// column (intermediate index) of the lane's first element in block 0.
-template <int MI, int NI, bool F32>
-__device__ __forceinline__ void swiglu_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
-                                                int row0, int row_lim, int f0) {
+// SwiGLU: the first half of a wave's columns holds gate rows, the second half
+// the matching up rows (b_row_of), so group g < G / 2 pairs with g + G / 2;
+// f0 = output column (intermediate index) of the lane's first group.
+template <int SH, int MI, int NI, bool F32>
+__device__ __forceinline__ void swiglu_epilogue(const typename Mfma<SH>::acc_t (&acc)[MI][NI],
+                                                const Epi& epi, int row0, int row_lim, int f0) {
+  using Geo = AccGeo<SH, MI, NI>;
+  constexpr int G = Geo::G;
   using T = typename Store<F32>::T;
   typedef T T4 __attribute__((ext_vector_type(4)));
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
-    const int row = row0 + 32 * i;
+    const int row = row0 + SH * i;
     if (row >= row_lim) continue;
 #pragma unroll
-    for (int j = 0; j < NI / 2; ++j)
+    for (int g = 0; g < G / 2; ++g) {
+      const int f = f0 + Geo::col(g);
+      if (f >= epi.ffn) continue;
+      const f32x4 gt = Geo::grp(acc, i, g), up = Geo::grp(acc, i, g + G / 2);
+      T4 o;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int f = f0 + 32 * j + 8 * q;
-        if (f >= epi.ffn) continue;
-        T4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float gt = acc[i][j][4 * q + e], up = acc[i][j + NI / 2][4 * q + e];
-          o[e] = (T)(silu(gt) * up);
-        }
-        *(T4*)((T*)epi.out + (int64_t)row * epi.ldo + f) = o;
-      }
+      for (int e = 0; e < 4; ++e) o[e] = (T)(silu(gt[e]) * up[e]);
+      *(T4*)((T*)epi.out + (int64_t)row * epi.ldo + f) = o;
+    }
   }
 }
 
-// One (token block i, first-half block j) of a q (KIND 0), k (1) or v (2)
-// head: the lane's token row, head-dim values d + 8 q + e (q, e < 4) of the
-// first half and the same plus D/2 from block j + HB.
-template <int KIND, int MI, int NI, int HB, bool F32>
-__device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi& epi, int i,
-                                          int j, int row0, int M, int head, int d,
-                                          const float (&b1)[4][4], const float (&b2)[4][4]) {
-  constexpr int D = HB * 64, half = D / 2;
+// QB consecutive first-half groups g0 .. g0 + QB - 1 of row block i, all in
+// one q (KIND 0), k (1) or v (2) head: the lane's token row, head-dim values
+// d + (col(g0 + u) - col(g0)) + e of the first half and the same plus D / 2
+// from group g0 + u + GH.
+template <int KIND, int SH, int MI, int NI, int GH, int QB, bool F32>
+__device__ __forceinline__ void qkv_block(const typename Mfma<SH>::acc_t (&acc)[MI][NI],
+                                          const Epi& epi, int i, int g0, int D, int row0, int M,
+                                          int head, int d, const float (&b1)[QB][4],
+                                          const float (&b2)[QB][4]) {
+  using Geo = AccGeo<SH, MI, NI>;
+  const int half = D / 2;
   using T = typename Store<F32>::T;
   typedef T T4 __attribute__((ext_vector_type(4)));
   const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
-  const int row = row0 + 32 * i;
+  const int row = row0 + SH * i;
   const int rc = min(row, M - 1);
-  f32x4 cs[4][2];  // (cos, sin) of d + 8 q + e: [q][0] = e 0..1, [q][1] = e 2..3
+  f32x4 cs[QB][2];  // (cos, sin) of the group's 4 values: [u][0] = e 0..1, [u][1] = e 2..3
   int sl = 0, tr = 0;
   if constexpr (KIND != 2) {
     const float2* __restrict__ rp = epi.rope + (int64_t)rc * half + d;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      cs[q][0] = *(const f32x4*)(rp + 8 * q);
-      cs[q][1] = *(const f32x4*)(rp + 8 * q + 2);
+    for (int u = 0; u < QB; ++u) {
+      const int dc = Geo::col(g0 + u) - Geo::col(g0);
+      cs[u][0] = *(const f32x4*)(rp + dc);
+      cs[u][1] = *(const f32x4*)(rp + dc + 2);
     }
   }
   if constexpr (KIND != 0) {
@@ -373,13 +442,15 @@ __device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi
     p = (T*)(KIND == 1 ? epi.kc : epi.vc) + (((int64_t)sl * Hkv + kvh) * epi.max_seq + tr) * D + d;
   }
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
+  for (int u = 0; u < QB; ++u) {
+    const int dc = Geo::col(g0 + u) - Geo::col(g0);
+    const f32x4 v1 = Geo::grp(acc, i, g0 + u), v2 = Geo::grp(acc, i, g0 + u + GH);
     T4 o1, o2;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      float x1 = acc[i][j][4 * q + e] + b1[q][e], x2 = acc[i][j + HB][4 * q + e] + b2[q][e];
+      float x1 = v1[e] + b1[u][e], x2 = v2[e] + b2[u][e];
       if constexpr (KIND != 2) {
-        const float c = cs[q][e >> 1][2 * (e & 1)], sn = cs[q][e >> 1][2 * (e & 1) + 1];
+        const float c = cs[u][e >> 1][2 * (e & 1)], sn = cs[u][e >> 1][2 * (e & 1) + 1];
         const float y1 = x1 * c - x2 * sn;
         const float y2 = x2 * c + x1 * sn;
         x1 = y1;
@@ -388,44 +459,53 @@ __device__ __forceinline__ void qkv_block(const f32x16 (&acc)[MI][NI], const Epi
       o1[e] = (T)x1;
       o2[e] = (T)x2;
     }
-    *(T4*)(p + 8 * q) = o1;
-    *(T4*)(p + 8 * q + half) = o2;
+    *(T4*)(p + dc) = o1;
+    *(T4*)(p + dc + half) = o2;
   }
 }
 
 // q/k/v split + bias + rotary embedding + KV-cache write on the accumulators.
-// HB = 32-column blocks per half head (D / 64): block j (first half of a head)
-// pairs with block j + HB (second half), same lane, same element.  The
-// rotary factors (four (cos, sin) pairs per element group, 32 contiguous
-// bytes) and, for k/v heads, the token's cache slot and row are loaded before
-// the stores.
-template <int MI, int NI, int HB, bool F32>
-__device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
-                                             int row0, int col0, int M, int N) {
+// HB = D / 64.  A half head is GH = D / 2 / SH * QN groups, so a first-half
+// group g pairs with g + GH (same lane, same element).  The groups are taken
+// QB at a time (QB <= GH, all in one half head): the rotary factors (four
+// (cos, sin) pairs per group, 32 contiguous bytes) and, for k/v heads, the
+// token's cache slot and row are loaded before the stores.
+template <int SH, int MI, int NI, int HB, bool F32>
+__device__ __forceinline__ void qkv_epilogue(const typename Mfma<SH>::acc_t (&acc)[MI][NI],
+                                             const Epi& epi, int row0, int col0, int M, int N) {
   using St = Store<F32>;
+  using Geo = AccGeo<SH, MI, NI>;
   constexpr int D = HB * 64, half = D / 2;
+  constexpr int GH = half / SH * Geo::QN;
+  constexpr int QB = GH < 4 ? GH : 4;
+  static_assert(GH % QB == 0 && Geo::G % (2 * GH) == 0, "whole heads per wave");
   const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
 #pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    if ((j / HB) & 1) continue;
-    const int col = col0 + 32 * j;  // first-half column of the lane's element 0
+  for (int g0 = 0; g0 < Geo::G; g0 += QB) {
+    if ((g0 / GH) & 1) continue;
+    const int col = col0 + Geo::col(g0);  // first-half column of the lane's first group
     if (col >= N) continue;
     const int head = col / D, d = col % D;
-    float b1[4][4], b2[4][4];
+    float b1[QB][4], b2[QB][4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+    for (int u = 0; u < QB; ++u) {
+      const int dc = Geo::col(g0 + u) - Geo::col(g0);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        b1[q][e] = epi.bias ? St::ld(epi.bias, col + 8 * q + e) : 0.f;
-        b2[q][e] = epi.bias ? St::ld(epi.bias, col + 8 * q + e + half) : 0.f;
+        b1[u][e] = epi.bias ? St::ld(epi.bias, col + dc + e) : 0.f;
+        b2[u][e] = epi.bias ? St::ld(epi.bias, col + dc + e + half) : 0.f;
       }
+    }
     // the head, hence its kind, is uniform across the wave
     const int kind = __builtin_amdgcn_readfirstlane(head < Hq ? 0 : (head < Hq + Hkv ? 1 : 2));
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
-      if (kind == 0) qkv_block<0, MI, NI, HB, F32>(acc, epi, i, j, row0, M, head, d, b1, b2);
-      else if (kind == 1) qkv_block<1, MI, NI, HB, F32>(acc, epi, i, j, row0, M, head, d, b1, b2);
-      else qkv_block<2, MI, NI, HB, F32>(acc, epi, i, j, row0, M, head, d, b1, b2);
+      if (kind == 0)
+        qkv_block<0, SH, MI, NI, GH, QB, F32>(acc, epi, i, g0, D, row0, M, head, d, b1, b2);
+      else if (kind == 1)
+        qkv_block<1, SH, MI, NI, GH, QB, F32>(acc, epi, i, g0, D, row0, M, head, d, b1, b2);
+      else
+        qkv_block<2, SH, MI, NI, GH, QB, F32>(acc, epi, i, g0, D, row0, M, head, d, b1, b2);
     }
   }
 }
@@ -434,23 +514,24 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[MI][NI], const 
 // squares over a head needs every value of a (token, head) before any can be
 // stored, more registers than the accumulator tile leaves free, so this
 // epilogue goes through LDS (free once every wave is past the mainloop and
-// its last loads have landed): 32 rows of the wave's tile at a time, each
-// wave in its own 32 x WC fp32 region, 16-byte chunks stored at chunk
-// c ^ row (conflict-free column writes and row reads).  Then each lane takes
+// its last loads have landed): one row block (SH rows) of the wave's tile at
+// a time, each wave in its own SH x WC fp32 region, 16-byte chunks stored at
+// chunk c ^ row (conflict-free column writes and row reads).  Then each lane takes
 // four consecutive rotary pairs of a row: 16 lanes cover a row's WC / 2 = 64
 // pairs, a pass covers 4 rows, and a head's pairs are an aligned group of
 // D / 8 lanes, its sum of squares a group sum.  The lane's columns, bias and
 // gains stay fixed across rows.
-template <int MI, int NI, bool F32>
-__device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], const Epi& epi,
-                                                  char* smem, int wv, int lane, int wrow0,
-                                                  int wcol0, int M, int N) {
+template <int SH, int MI, int NI, bool F32>
+__device__ __forceinline__ void qkv_norm_epilogue(const typename Mfma<SH>::acc_t (&acc)[MI][NI],
+                                                  const Epi& epi, char* smem, int wv, int lane,
+                                                  int wrow0, int wcol0, int M, int N) {
   using St = Store<F32>;
   using T = typename St::T;
+  using Geo = AccGeo<SH, MI, NI>;
   typedef T T4 __attribute__((ext_vector_type(4)));
-  constexpr int WC = NI * 32;
+  constexpr int WC = NI * SH;
   static_assert(WC == 128, "16 lanes per row of the wave's columns");
-  const int lr = lane & 31, lg = lane >> 5;
+  const int lr = Geo::lane_row(lane), lg = lane / SH;
   const int D = epi.head_dim, half = D / 2;
   const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
   const int rl = lane >> 4;                       // row within a 4-row pass
@@ -479,20 +560,17 @@ __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], c
 
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  float* __restrict__ buf = (float*)smem + wv * 32 * WC;
+  float* __restrict__ buf = (float*)smem + wv * SH * WC;
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
-    // the accumulators' element group (j, q) is row lr, columns 32 j + 8 q + 4 lg .. + 3
+    // group g of the row block is row lr, columns col(g) + 4 lg .. + 3
 #pragma unroll
-    for (int j = 0; j < NI; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *(f32x4*)&buf[lr * WC + (((8 * j + 2 * q + lg) ^ lr) << 2)] =
-            f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-    const int rbase = wrow0 + 32 * i;
+    for (int g = 0; g < Geo::G; ++g)
+      *(f32x4*)&buf[lr * WC + (((Geo::col(g) / 4 + lg) ^ lr) << 2)] = Geo::grp(acc, i, g);
+    const int rbase = wrow0 + SH * i;
     // two passes (8 rows) at a time: the rotary factors, cache slots and rows
     // are loaded before the first store (a store could alias a later load)
-    for (int t0 = 0; t0 < 32; t0 += 8) {
+    for (int t0 = 0; t0 < SH; t0 += 8) {
       if (rbase + t0 >= M) break;  // uniform
       f32x4 cs[2][2];              // (cos, sin) of pairs d .. d + 3: [pass][0] = 0..1, [1] = 2..3
       int sl[2], tr[2];
@@ -553,13 +631,14 @@ __device__ __forceinline__ void qkv_norm_epilogue(const f32x16 (&acc)[MI][NI], c
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int EK, int S = 2>
+template <int BM, int BN, int WGM, int WGN, int EK, int S = 2, int SH = 32>
 __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __restrict__ A, int lda,
                                                    const bf16* __restrict__ B, int ldb, int M,
                                                    int N, int K, int kc, Epi epi,
                                                    int tiles_m, int tiles_n, int full,
                                                    int tsplit, float* __restrict__ tail) {
-  using ML = Mainloop<BM, BN, WGM, WGN, S>;
+  using ML = Mainloop<BM, BN, WGM, WGN, S, SH>;
+  using Geo = AccGeo<SH, ML::MI, ML::NI>;
   constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
   constexpr int KIND = EK & kEpiKindMask;
   constexpr bool F32 = (EK & kEpiF32) != 0;
@@ -611,35 +690,35 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
     const int gr = b_row_of<BN, WN>(KIND, tn, tr, epi.ffn);
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
-  f32x16 acc[MI][NI];
+  typename ML::acc_t acc[MI][NI];
   ML::run_valid(M - tm * BM, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
 
-  const int lr = lane & 31, lg = lane >> 5;
+  const int lr = Geo::lane_row(lane), lc = Geo::lane_col(lane);
   if (u >= 0) {  // tail split: the tile's fp32 partial sums, [BM][BN]
     Epi e{};
     e.out = tail + (int64_t)u * BM * BN;
     e.ldo = BN;
-    plain_epilogue<MI, NI, EPI_STORE_F32>(acc, e, wm * WM + lr, BM, wn * WN + 4 * lg, BN);
+    plain_epilogue<SH, MI, NI, EPI_STORE_F32>(acc, e, wm * WM + lr, BM, wn * WN + lc, BN);
     return;
   }
   const int row0 = tm * BM + wm * WM + lr;
   if constexpr (KIND == EPI_STORE_F32) {
     Epi e = epi;
     e.out = (float*)epi.out + (int64_t)blockIdx.y * M * epi.ldo;
-    plain_epilogue<MI, NI, EK>(acc, e, row0, M, tn * BN + wn * WN + 4 * lg, N);
+    plain_epilogue<SH, MI, NI, EK>(acc, e, row0, M, tn * BN + wn * WN + lc, N);
   } else if constexpr (KIND == EPI_STORE || KIND == EPI_RESID) {
-    plain_epilogue<MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + 4 * lg, N);
+    plain_epilogue<SH, MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + lc, N);
   } else if constexpr (KIND == EPI_SWIGLU) {
-    swiglu_epilogue<MI, NI, F32>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
+    swiglu_epilogue<SH, MI, NI, F32>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + lc);
   } else if constexpr (KIND == EPI_QKV_NORM) {
-    static_assert(NW * 32 * WN * sizeof(float) <= sizeof(GemmSmem<BM, BN>),
+    static_assert(NW * SH * WN * sizeof(float) <= sizeof(GemmSmem<BM, BN>),
                   "the epilogue's row blocks must fit the mainloop's LDS");
-    qkv_norm_epilogue<MI, NI, F32>(acc, epi, smem_raw, wv, lane, tm * BM + wm * WM,
-                                   tn * BN + wn * WN, M, N);
+    qkv_norm_epilogue<SH, MI, NI, F32>(acc, epi, smem_raw, wv, lane, tm * BM + wm * WM,
+                                       tn * BN + wn * WN, M, N);
   } else if (epi.head_dim == 128) {
-    qkv_epilogue<MI, NI, 2, F32>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
+    qkv_epilogue<SH, MI, NI, 2, F32>(acc, epi, row0, tn * BN + wn * WN + lc, M, N);
   } else {
-    qkv_epilogue<MI, NI, 1, F32>(acc, epi, row0, tn * BN + wn * WN + 4 * lg, M, N);
+    qkv_epilogue<SH, MI, NI, 1, F32>(acc, epi, row0, tn * BN + wn * WN + lc, M, N);
   }
 }
 
@@ -648,13 +727,14 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
 // the gate/up pass (EPI_SWIGLU) A row p is token perm[p] / top_k of A; for the
 // down pass (EPI_STORE_F32) A row p is row p of A.  B of expert e starts at
 // B + e * b_stride elements.  Output row = routed position p.
-template <int BM, int BN, int WGM, int WGN, int EK>
+template <int BM, int BN, int WGM, int WGN, int EK, int SH = 32>
 __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
     const bf16* __restrict__ A, int lda, int a_rows, const int32_t* __restrict__ perm, int top_k,
     const bf16* __restrict__ B, int64_t b_stride, int N, int K,
     const int32_t* __restrict__ seg, const int32_t* __restrict__ tile_off, int n_experts,
     int tiles_n, Epi epi) {
-  using ML = Mainloop<BM, BN, WGM, WGN>;
+  using ML = Mainloop<BM, BN, WGM, WGN, 2, SH>;
+  using Geo = AccGeo<SH, ML::MI, ML::NI>;
   constexpr int NW = ML::NW, WM = ML::WM, WN = ML::WN, MI = ML::MI, NI = ML::NI;
   constexpr int KIND = EK & kEpiKindMask;
   constexpr bool F32 = (EK & kEpiF32) != 0;
@@ -706,15 +786,15 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
     const int gr = b_row_of<BN, WN>(KIND, tn, tr, epi.ffn);
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * K + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
-  f32x16 acc[MI][NI];
+  typename ML::acc_t acc[MI][NI];
   ML::run_valid(p_end - p0, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
 
-  const int lr = lane & 31, lg = lane >> 5;
+  const int lr = Geo::lane_row(lane), lc = Geo::lane_col(lane);
   const int row0 = p0 + wm * WM + lr;
   if constexpr (KIND == EPI_SWIGLU)
-    swiglu_epilogue<MI, NI, F32>(acc, epi, row0, p_end, tn * (BN / 2) + wn * (WN / 2) + 4 * lg);
+    swiglu_epilogue<SH, MI, NI, F32>(acc, epi, row0, p_end, tn * (BN / 2) + wn * (WN / 2) + lc);
   else
-    plain_epilogue<MI, NI, EK>(acc, epi, row0, p_end, tn * BN + wn * WN + 4 * lg, N);
+    plain_epilogue<SH, MI, NI, EK>(acc, epi, row0, p_end, tn * BN + wn * WN + lc, N);
 }
 
 template <typename Kern>
@@ -728,17 +808,17 @@ static hipError_t opt_in_lds(Kern k, size_t smem, bool& done) {
 
 // splits > 1 only with EPI_STORE_F32 (plane z of epi.out holds split z); K
 // must then be a multiple of 64 * splits.
-template <int BM, int BN, int WGM, int WGN, int EK, int S = 2>
+template <int BM, int BN, int WGM, int WGN, int EK, int S = 2, int SH = 32>
 static hipError_t run_gemm(const void* A, int lda, const void* B, int ldb, int M, int N, int K,
                            const Epi& epi, hipStream_t s, int splits = 1) {
   const int tiles_m = cdiv(M, BM);
   const int tiles_n = (EK & kEpiKindMask) == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
   const size_t smem = sizeof(GemmSmem<BM, BN, S>);
   static bool attr_set = false;
-  hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK, S>, smem, attr_set);
+  hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK, S, SH>, smem, attr_set);
   if (e != hipSuccess) return e;
   const int kc = K / splits;
-  gemm_kernel<BM, BN, WGM, WGN, EK, S><<<dim3(tiles_m * tiles_n, splits), WGM * WGN * 64, smem, s>>>(
+  gemm_kernel<BM, BN, WGM, WGN, EK, S, SH><<<dim3(tiles_m * tiles_n, splits), WGM * WGN * 64, smem, s>>>(
       (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, kc, epi, tiles_m, tiles_n,
       tiles_m * tiles_n, 1, nullptr);
   return hipGetLastError();
@@ -917,7 +997,7 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int EK>
+template <int BM, int BN, int WGM, int WGN, int EK, int SH = 32>
 static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, int M, int N,
                                 int K, const Epi& epi, float* tail, hipStream_t s) {
   constexpr int KIND = EK & kEpiKindMask;
@@ -925,14 +1005,14 @@ static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, 
   const int tiles_n = KIND == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
   const int total = tiles_m * tiles_n;
   const int t = tail ? tail_split(total, K, KIND) : 1;
-  if (t == 1) return run_gemm<BM, BN, WGM, WGN, EK>(A, lda, B, ldb, M, N, K, epi, s);
+  if (t == 1) return run_gemm<BM, BN, WGM, WGN, EK, 2, SH>(A, lda, B, ldb, M, N, K, epi, s);
   const int n_tail = tail_tiles(total);
   const int full = total - n_tail;
   const size_t smem = sizeof(GemmSmem<BM, BN>);
   static bool attr_set = false;
-  hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK>, smem, attr_set);
+  hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK, 2, SH>, smem, attr_set);
   if (e != hipSuccess) return e;
-  gemm_kernel<BM, BN, WGM, WGN, EK><<<full + n_tail * t, WGM * WGN * 64, smem, s>>>(
+  gemm_kernel<BM, BN, WGM, WGN, EK, 2, SH><<<full + n_tail * t, WGM * WGN * 64, smem, s>>>(
       (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, K, epi, tiles_m, tiles_n, full, t, tail);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -949,14 +1029,14 @@ hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, in
     constexpr int F = kEpiF32;
     switch (epi.kind) {
       case EPI_RESID:
-        return run_gemm_tail<256, 256, 4, 2, EPI_RESID | F>(A, lda, B, ldb, M, N, K, epi, tail, s);
-      case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU | F>(A, lda, B, ldb, M, N, K, epi, s);
+        return run_gemm_tail<256, 256, 4, 2, EPI_RESID | F, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
+      case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU | F, 2, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, s);
       case EPI_STORE_F32:
-        return run_gemm_tail<256, 256, 4, 2, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, epi, tail, s);
+        return run_gemm_tail<256, 256, 4, 2, EPI_STORE_F32, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
       case EPI_QKV:
         if (epi.q_norm)
-          return run_gemm_tail<256, 256, 4, 2, EPI_QKV_NORM | F>(A, lda, B, ldb, M, N, K, epi, tail, s);
-        return run_gemm_tail<256, 256, 4, 2, EPI_QKV | F>(A, lda, B, ldb, M, N, K, epi, tail, s);
+          return run_gemm_tail<256, 256, 4, 2, EPI_QKV_NORM | F, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
+        return run_gemm_tail<256, 256, 4, 2, EPI_QKV | F, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
       default: return hipErrorInvalidValue;
     }
   }
@@ -972,25 +1052,25 @@ hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, in
   if (epi.kind != EPI_SWIGLU && epi.kind != EPI_STORE_F32 && K <= 8192 &&
       cdiv(M, 256) * cdiv(N, 256) < cu_count()) {
     switch (epi.kind) {
-      case EPI_STORE: return run_gemm<128, 128, 4, 1, EPI_STORE, 3>(A, lda, B, ldb, M, N, K, epi, s);
-      case EPI_RESID: return run_gemm<128, 128, 4, 1, EPI_RESID, 3>(A, lda, B, ldb, M, N, K, epi, s);
+      case EPI_STORE: return run_gemm<128, 128, 4, 1, EPI_STORE, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
+      case EPI_RESID: return run_gemm<128, 128, 4, 1, EPI_RESID, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
       default:
         if (epi.q_norm)
-          return run_gemm<128, 128, 4, 1, EPI_QKV_NORM, 3>(A, lda, B, ldb, M, N, K, epi, s);
-        return run_gemm<128, 128, 4, 1, EPI_QKV, 3>(A, lda, B, ldb, M, N, K, epi, s);
+          return run_gemm<128, 128, 4, 1, EPI_QKV_NORM, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
+        return run_gemm<128, 128, 4, 1, EPI_QKV, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
     }
   }
   if (epi.kind == EPI_SWIGLU && M <= 640)
-    return run_gemm<128, 256, 2, 4, EPI_SWIGLU, 3>(A, lda, B, ldb, M, N, K, epi, s);
+    return run_gemm<128, 256, 2, 4, EPI_SWIGLU, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
   switch (epi.kind) {
-    case EPI_STORE: return run_gemm_tail<256, 256, 4, 2, EPI_STORE>(A, lda, B, ldb, M, N, K, epi, tail, s);
-    case EPI_RESID: return run_gemm_tail<256, 256, 4, 2, EPI_RESID>(A, lda, B, ldb, M, N, K, epi, tail, s);
-    case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU>(A, lda, B, ldb, M, N, K, epi, s);
-    case EPI_STORE_F32: return run_gemm_tail<256, 256, 4, 2, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, epi, tail, s);
+    case EPI_STORE: return run_gemm_tail<256, 256, 4, 2, EPI_STORE, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
+    case EPI_RESID: return run_gemm_tail<256, 256, 4, 2, EPI_RESID, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
+    case EPI_SWIGLU: return run_gemm<256, 256, 4, 2, EPI_SWIGLU, 2, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, s);
+    case EPI_STORE_F32: return run_gemm_tail<256, 256, 4, 2, EPI_STORE_F32, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
     default:
       if (epi.q_norm)
-        return run_gemm_tail<256, 256, 4, 2, EPI_QKV_NORM>(A, lda, B, ldb, M, N, K, epi, tail, s);
-      return run_gemm_tail<256, 256, 4, 2, EPI_QKV>(A, lda, B, ldb, M, N, K, epi, tail, s);
+        return run_gemm_tail<256, 256, 4, 2, EPI_QKV_NORM, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
+      return run_gemm_tail<256, 256, 4, 2, EPI_QKV, kPrefillSH>(A, lda, B, ldb, M, N, K, epi, tail, s);
   }
 }
 
@@ -1003,7 +1083,7 @@ int moe_tile_rows(int n_pairs, int n_experts) {
   return n_pairs >= 224 * n_experts ? 256 : 128;
 }
 
-template <int BM, int BN, int WGM, int WGN, int EK>
+template <int BM, int BN, int WGM, int WGN, int EK, int SH = 32>
 static hipError_t run_grouped(const void* A, int lda, int a_rows, const int32_t* perm, int top_k,
                               const void* B, int64_t b_stride, int N, int K, const int32_t* seg,
                               const int32_t* tile_off, int n_experts, int max_tiles_m,
@@ -1011,9 +1091,9 @@ static hipError_t run_grouped(const void* A, int lda, int a_rows, const int32_t*
   const int tiles_n = (EK & kEpiKindMask) == EPI_SWIGLU ? cdiv(epi.ffn, BN / 2) : cdiv(N, BN);
   const size_t smem = sizeof(GemmSmem<BM, BN>);
   static bool attr_set = false;
-  hipError_t e = opt_in_lds(gemm_grouped_kernel<BM, BN, WGM, WGN, EK>, smem, attr_set);
+  hipError_t e = opt_in_lds(gemm_grouped_kernel<BM, BN, WGM, WGN, EK, SH>, smem, attr_set);
   if (e != hipSuccess) return e;
-  gemm_grouped_kernel<BM, BN, WGM, WGN, EK><<<max_tiles_m * tiles_n, WGM * WGN * 64, smem, s>>>(
+  gemm_grouped_kernel<BM, BN, WGM, WGN, EK, SH><<<max_tiles_m * tiles_n, WGM * WGN * 64, smem, s>>>(
       (const bf16*)A, lda, a_rows, perm, top_k, (const bf16*)B, b_stride, N, K, seg, tile_off,
       n_experts, tiles_n, epi);
   return hipGetLastError();
@@ -1032,9 +1112,9 @@ hipError_t launch_gemm_grouped(const void* A, int lda, int a_rows, const int32_t
       return run_grouped<32, 256, 1, 4, EK>(A, lda, a_rows, perm, top_k, B, b_stride, N, K, seg,
                                             tile_off, n_experts, max_tiles_m, epi, s);
     if (bm == 256)
-      return run_grouped<256, 256, 4, 2, EK>(A, lda, a_rows, perm, top_k, B, b_stride, N, K, seg,
+      return run_grouped<256, 256, 4, 2, EK, kPrefillSH>(A, lda, a_rows, perm, top_k, B, b_stride, N, K, seg,
                                              tile_off, n_experts, max_tiles_m, epi, s);
-    return run_grouped<128, 256, 2, 4, EK>(A, lda, a_rows, perm, top_k, B, b_stride, N, K, seg,
+    return run_grouped<128, 256, 2, 4, EK, kPrefillSH>(A, lda, a_rows, perm, top_k, B, b_stride, N, K, seg,
                                            tile_off, n_experts, max_tiles_m, epi, s);
   }
   if (bm == 32) {
@@ -1046,16 +1126,16 @@ hipError_t launch_gemm_grouped(const void* A, int lda, int a_rows, const int32_t
   }
   if (bm == 256) {
     if (epi.kind == EPI_SWIGLU)
-      return run_grouped<256, 256, 4, 2, EPI_SWIGLU>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
+      return run_grouped<256, 256, 4, 2, EPI_SWIGLU, kPrefillSH>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
                                                       seg, tile_off, n_experts, max_tiles_m, epi, s);
-    return run_grouped<256, 256, 4, 2, EPI_STORE_F32>(A, lda, a_rows, perm, top_k, B, b_stride, N,
+    return run_grouped<256, 256, 4, 2, EPI_STORE_F32, kPrefillSH>(A, lda, a_rows, perm, top_k, B, b_stride, N,
                                                        K, seg, tile_off, n_experts, max_tiles_m, epi,
                                                        s);
   }
   if (epi.kind == EPI_SWIGLU)
-    return run_grouped<128, 256, 2, 4, EPI_SWIGLU>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
+    return run_grouped<128, 256, 2, 4, EPI_SWIGLU, kPrefillSH>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
                                                     seg, tile_off, n_experts, max_tiles_m, epi, s);
-  return run_grouped<128, 256, 2, 4, EPI_STORE_F32>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
+  return run_grouped<128, 256, 2, 4, EPI_STORE_F32, kPrefillSH>(A, lda, a_rows, perm, top_k, B, b_stride, N, K,
                                                      seg, tile_off, n_experts, max_tiles_m, epi, s);
 }
 
