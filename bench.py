@@ -140,13 +140,21 @@ def _mean(samples, key):
 
 def energy_loop(fn, min_s=2.0):
     """Joules per call of fn over a loop of at least min_s seconds (the counter
-    updates every few ms), with average board power and the clock, temperature
-    and power sampled while the GPU is busy; None without a counter."""
+    updates every few ms), after one second at the same load, with average
+    board power and the clock, temperature and power sampled while the GPU is
+    busy; None without a counter."""
     import torch
     meter = Energy()
     if meter.h is None:
         return None
+    # one second at the same load first: the metrics table (clock, socket
+    # power) lags a change of load, so the samples reflect the steady state
     torch.cuda.synchronize()
+    t_w = time.perf_counter()
+    while time.perf_counter() - t_w < 1.0:
+        for _ in range(4):
+            fn()
+        torch.cuda.synchronize()
     t0, j0, n = time.perf_counter(), meter.joules(), 0
     samples = []
     while True:
@@ -544,7 +552,6 @@ def matmul_sweep(tri, eta):
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / reps
         flops, byts = 2.0 * M * N * K, 2.0 * (M * K + N * K + M * N)
-        energy_loop(call, min_s=1.0)            # let clock and power settle at this load
         en = energy_loop(call, min_s=2.0)
         tel = en["telemetry"] if en else {}
         pt = {"ai_target": ai_target, "rows": M, "ai": flops / byts, "ms_per_call": ms,
@@ -619,7 +626,6 @@ def ai_sweep(args, tri):
         ai = tri.phase_intensity(w, praw)
         flops = sum(w.flops[i] for i in range(w.n_stages))
         byts = sum(w.bytes[i] for i in range(w.n_stages))
-        energy_loop(call, min_s=1.0)            # let clock and power settle at this load
         en = energy_loop(call, min_s=2.0)
         tel = en["telemetry"] if en else {}
         pt = {"point": label, "tokens": b.n_tokens, "ms_per_call": ms, "ai_time_weighted": ai,
