@@ -117,13 +117,18 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 // (RNE, packed in pairs), lo = bf16(p - hi) with the difference exact in
 // fp32; hi + lo keeps ~16 significant bits of p.  Six VALU instructions per
 // pair: two conversions, two unpacks (shift / mask) and two subtractions.
+// (The packed pair goes through an empty asm first: otherwise the compiler
+// rewrites the shift of its low half as a second conversion of p[2 i] alone
+// plus the shift, one more instruction per pair.)
 __device__ __forceinline__ void split_hilo8(const float (&p)[8], bf16x8& hi, bf16x8& lo) {
   u32x4 h, l;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    h[i] = pack_bf16x2(p[2 * i], p[2 * i + 1]);
-    l[i] = pack_bf16x2(p[2 * i] - __uint_as_float(h[i] << 16),
-                       p[2 * i + 1] - __uint_as_float(h[i] & 0xffff0000u));
+    uint32_t hv = pack_bf16x2(p[2 * i], p[2 * i + 1]);
+    asm("" : "+v"(hv));
+    h[i] = hv;
+    l[i] = pack_bf16x2(p[2 * i] - __uint_as_float(hv << 16),
+                       p[2 * i + 1] - __uint_as_float(hv & 0xffff0000u));
   }
   hi = __builtin_bit_cast(bf16x8, h);
   lo = __builtin_bit_cast(bf16x8, l);
