@@ -31,6 +31,8 @@
 // an upper bound on the tile count and surplus workgroups exit, so no count is
 // read back to the host; the real tiles are dealt to the XCDs in contiguous
 // shares so that an expert's M-tiles share its weights in one L2.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -147,6 +149,23 @@ __device__ __forceinline__ int b_row_of(int kind, int tn, int nt, int ffn) {
   return tn * BN + nt;
 }
 
+// Residual prefetch for the 256 x 256 residual epilogue.  The loads for the
+// two tiles past the last one (zeros otherwise) fetch instead the two 128-row
+// halves of the output tile's residual into the buffers they would fill: half
+// h into buffer (KT + h) % 2, its rows 0..63 in the A region, 64..127 in the B
+// region, row-major with 512-byte rows whose 16-byte chunks are stored at
+// chunk ^ (row % 16) (16 consecutive rows read one logical chunk without bank
+// conflicts).  Piece j of wave w in a region covers region rows 2 L and 2 L + 1,
+// L = w + 8 j; lane l writes position l % 32 of row 2 L + l / 32, so it fetches
+// logical chunk (l % 32) ^ ((2 w + l / 32) % 16) (the swizzle is an
+// involution).  Rows past M read as zero through the descriptor's range.
+struct ResPf {
+  __amdgpu_buffer_rsrc_t rsrc;  // residual of the tile's rows (rows past M out of range)
+  uint32_t voff;                // lane part: row l / 32 of the piece, source chunk
+  int ld_bytes;                 // residual row stride in bytes
+  bool on;
+};
+
 // The shared K loop.  a_off / b_off: byte offset (within the buffer) of chunk
 // swz(row, lane % 8) of this lane's row in each of its 1 KB LDS blocks (at or
 // beyond the buffer size for rows that must read as zero).
@@ -178,14 +197,17 @@ struct Mainloop {
   // so the wave issues neither their MFMAs nor their A fragment reads (with
   // MA = 0, no MFMA and no fragment read at all).  Its share of the tile
   // loads and every barrier stay, so all waves keep the same barrier count.
-  template <int MA>
+  template <int MA, bool RPF = false>
   __device__ __forceinline__ static void run_rows(GemmSmem<BM, BN, S>& sm,
                                                   __amdgpu_buffer_rsrc_t ra,
                                                   const uint32_t (&a_off)[A_BLK],
                                                   __amdgpu_buffer_rsrc_t rb,
                                                   const uint32_t (&b_off)[B_BLK], int K, int wv,
-                                                  int lane, acc_t (&acc)[MI][NI]) {
+                                                  int lane, acc_t (&acc)[MI][NI],
+                                                  const ResPf& rp) {
     static_assert(MA >= 0 && MA <= MI, "active row blocks");
+    static_assert(!RPF || (BM == 256 && BN == 256 && NW == 8 && S == 2),
+                  "residual prefetch: two 64-row regions of 32 pieces per buffer");
     const int wm = wv / WGN, wn = wv % WGN;
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -249,6 +271,14 @@ struct Mainloop {
         buffer_load_lds16(rb, &sm.b[buf][(wv + NW * (p - A_BLK)) * 8 * kBK],
                           b_off[p - A_BLK] | kill, kb);
     };
+    // Piece p of residual half h (ResPf): the LDS destination of tile piece p.
+    auto rpiece = [&](int h, int buf, int p) {
+      const int reg = p < A_BLK ? 0 : 1, j = p - reg * A_BLK;
+      const int row = 128 * h + 64 * reg + 2 * (wv + NW * j);
+      void* dst = reg ? (void*)&sm.b[buf][(wv + NW * j) * 8 * kBK]
+                      : (void*)&sm.a[buf][(wv + NW * j) * 8 * kBK];
+      buffer_load_lds16(rp.rsrc, dst, rp.voff, row * rp.ld_bytes);
+    };
     // B (weight rows) as the MFMA's row operand and A (token rows) as its
     // column operand: accumulator block (i, j) holds C^T, so a lane owns one
     // token row and groups of four consecutive output columns, and the
@@ -271,7 +301,7 @@ struct Mainloop {
     // The issue order is spelled out: one MFMA, then one LDS read for the next
     // k-step (and on the last step one or more tile loads), fenced so the
     // compiler keeps it.
-    for (int kt = 0; kt < KT; ++kt) {
+    auto ktile = [&](int kt, auto res) {
       const int nbuf = buf + 1 == S ? 0 : buf + 1;
 #pragma unroll
       for (int ks = 0; ks + 1 < KSTEPS; ++ks) {
@@ -290,36 +320,41 @@ struct Mainloop {
 #pragma unroll
       for (int g = 0; g < NGL; ++g) {
         if (g < NMF) mfma(last, g);
-        if (g < NLD) gpiece(kt + S, buf, kill, g);
+        if (g < NLD) {
+          if constexpr (decltype(res)::value) rpiece(kt + S - KT, buf, g);
+          else gpiece(kt + S, buf, kill, g);
+        }
         if (g < NRD) lread(nbuf, 0, last ^ 1, g);  // stale but in-range on the last tile
         __builtin_amdgcn_sched_barrier(0);
       }
       buf = nbuf;
+    };
+    // With the residual prefetch, the last S k-tiles (those whose tile + S
+    // does not exist) run in a loop of their own that loads residual halves.
+    const int kt_main = (RPF && rp.on) ? KT - S : KT;
+    int kt = 0;
+    for (; kt < kt_main; ++kt) ktile(kt, std::false_type{});
+    if constexpr (RPF) {
+      for (; kt < KT; ++kt) ktile(kt, std::true_type{});
     }
-  }
-  __device__ __forceinline__ static void run(GemmSmem<BM, BN, S>& sm, __amdgpu_buffer_rsrc_t ra,
-                                             const uint32_t (&a_off)[A_BLK],
-                                             __amdgpu_buffer_rsrc_t rb,
-                                             const uint32_t (&b_off)[B_BLK], int K, int wv,
-                                             int lane, acc_t (&acc)[MI][NI]) {
-    run_rows<MI>(sm, ra, a_off, rb, b_off, K, wv, lane, acc);
   }
   // The tile's first `rows` rows are valid: the wave runs the instantiation
   // for its active row blocks (a wave-uniform choice).
-  template <int MA = MI>
+  template <int MA = MI, bool RPF = false>
   __device__ __forceinline__ static void run_valid(int rows, GemmSmem<BM, BN, S>& sm,
                                                    __amdgpu_buffer_rsrc_t ra,
                                                    const uint32_t (&a_off)[A_BLK],
                                                    __amdgpu_buffer_rsrc_t rb,
                                                    const uint32_t (&b_off)[B_BLK], int K, int wv,
-                                                   int lane, acc_t (&acc)[MI][NI]) {
+                                                   int lane, acc_t (&acc)[MI][NI],
+                                                   const ResPf& rp = ResPf{}) {
     const int wm = wv / WGN;
     const int act = (rows - wm * WM + SH - 1) / SH;  // row blocks holding valid rows
     if constexpr (MA == 0) {
-      run_rows<0>(sm, ra, a_off, rb, b_off, K, wv, lane, acc);
+      run_rows<0, RPF>(sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp);
     } else {
-      if (act >= MA) run_rows<MA>(sm, ra, a_off, rb, b_off, K, wv, lane, acc);
-      else run_valid<MA - 1>(rows, sm, ra, a_off, rb, b_off, K, wv, lane, acc);
+      if (act >= MA) run_rows<MA, RPF>(sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp);
+      else run_valid<MA - 1, RPF>(rows, sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp);
     }
   }
 };
@@ -370,6 +405,43 @@ __device__ __forceinline__ void plain_epilogue(
         }
         *(T4*)((T*)epi.out + (int64_t)row * epi.ldo + col) = o;
       }
+    }
+  }
+}
+
+// The residual epilogue of a 256 x 256 tile whose residual was prefetched
+// into LDS (ResPf): tile-relative row tr / column tc of the lane's first group
+// (row0 - tile row0 and col0 - tile col0), kt_par = KT % 2.  The caller has
+// waited for the prefetch loads and passed a barrier.
+template <int SH, int MI, int NI>
+__device__ __forceinline__ void resid_lds_epilogue(
+    const typename Mfma<SH>::acc_t (&acc)[MI][NI], const Epi& epi, int row0, int row_lim,
+    int col0, int N, const char* smem, int kt_par, int tr, int tc) {
+  using Geo = AccGeo<SH, MI, NI>;
+  constexpr int G = Geo::G;
+  constexpr int kRegion = 256 * kBK * 2;  // bytes of one buffer's A (or B) region
+  typedef bf16 T4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+    const int row = row0 + SH * i, r = tr + SH * i;
+    const int h = r >> 7, reg = (r >> 6) & 1, rr = r & 63;
+    const char* rbase = smem + reg * 2 * kRegion + ((kt_par + h) & 1) * kRegion + rr * 512;
+    T4 res[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int c = tc + Geo::col(g);
+      res[g] = *(const T4*)(rbase + (((c >> 3) ^ (rr & 15)) << 4) + (c & 7) * 2);
+    }
+    if (row >= row_lim) continue;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int col = col0 + Geo::col(g);
+      if (col >= N) continue;
+      const f32x4 v = Geo::grp(acc, i, g);
+      T4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = (bf16)(v[e] + (float)res[g][e]);
+      *(T4*)((bf16*)epi.out + (int64_t)row * epi.ldo + col) = o;
     }
   }
 }
@@ -691,9 +763,27 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * ldb + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
   typename ML::acc_t acc[MI][NI];
-  ML::run_valid(M - tm * BM, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
-
   const int lr = Geo::lane_row(lane), lc = Geo::lane_col(lane);
+  // bf16 residual epilogue of a whole 256 x 256 tile: prefetch the residual
+  // into the LDS buffers freed by the last two k-tiles (ResPf)
+  constexpr bool kResPf = KIND == EPI_RESID && !F32 && BM == 256 && BN == 256 && S == 2 &&
+                          NW == 8;
+  ResPf rp{};
+  if constexpr (kResPf) {
+    if (u < 0 && K / kBK >= 2) {
+      const int rows_left = M - tm * BM;
+      rp.on = true;
+      rp.ld_bytes = epi.ldr * 2;
+      rp.rsrc = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)((const bf16*)epi.resid + (int64_t)tm * BM * epi.ldr + tn * BN), (short)0,
+          (int)((int64_t)rows_left * epi.ldr * 2), 0x00020000);
+      rp.voff = (uint32_t)((lane >> 5) * rp.ld_bytes +
+                           (((lane & 31) ^ ((2 * wv + (lane >> 5)) & 15)) << 4));
+    }
+  }
+  ML::template run_valid<MI, kResPf>(M - tm * BM, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane,
+                                     acc, rp);
+
   if (u >= 0) {  // tail split: the tile's fp32 partial sums, [BM][BN]
     Epi e{};
     e.out = tail + (int64_t)u * BM * BN;
@@ -707,6 +797,15 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
     e.out = (float*)epi.out + (int64_t)blockIdx.y * M * epi.ldo;
     plain_epilogue<SH, MI, NI, EK>(acc, e, row0, M, tn * BN + wn * WN + lc, N);
   } else if constexpr (KIND == EPI_STORE || KIND == EPI_RESID) {
+    if constexpr (kResPf) {
+      if (rp.on) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();  // every wave's residual pieces have landed
+        resid_lds_epilogue<SH, MI, NI>(acc, epi, row0, M, tn * BN + wn * WN + lc, N, smem_raw,
+                                       (K / kBK) & 1, wm * WM + lr, wn * WN + lc);
+        return;
+      }
+    }
     plain_epilogue<SH, MI, NI, EK>(acc, epi, row0, M, tn * BN + wn * WN + lc, N);
   } else if constexpr (KIND == EPI_SWIGLU) {
     swiglu_epilogue<SH, MI, NI, F32>(acc, epi, row0, M, tn * (BN / 2) + wn * (WN / 2) + lc);
