@@ -228,7 +228,9 @@ __global__ __launch_bounds__(256, F32 ? 1 : 2) void attn_prefill_kernel(
   // (k-step t: head-dim values t and D/2 + t, K fragments four steps per
   // 16-byte read), then O^T += V^T P^T over keys 8 j + 4 lg + i, whose
   // weights are the lane's own score elements 4 j + i.
-  auto step_f32 = [&](const E* k_lds, const E* v_lds, int key0) {
+  // (always inlined: called out of line, its captures, the accumulators
+  // among them, would live in private memory)
+  auto step_f32 = [&](const E* k_lds, const E* v_lds, int key0) __attribute__((always_inline)) {
     if constexpr (F32) {
       constexpr int QC = D / 8;  // 16-byte chunks of a half row
       f32x16 sacc[2] = {f32x16{0.f}, f32x16{0.f}};
@@ -263,17 +265,23 @@ __global__ __launch_bounds__(256, F32 ? 1 : 2) void attn_prefill_kernel(
         ls[g] = tree_sum8(v8);
       }
       l_run += (ls[0] + ls[1]) + (ls[2] + ls[3]);
+      // V element (key, d), key = 32 kb + 8 j + 4 lg + i, d = 32 bb + lr: as
+      // key % 16 = 8 (j % 2) + 4 lg + i, its swizzled chunk (d / 4) ^ (key % 16)
+      // is 8 (bb ^ (j % 2)) + ((lr / 4) ^ (4 lg + i)), so four lane offsets
+      // (one per i) plus compile-time constants address every read.
+      int v_off[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        v_off[i] = (4 * lg + i) * D + (((lr >> 2) ^ (4 * lg + i)) << 2) + (lr & 3);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int key = 32 * kb + 8 * j + 4 * lg + i;
 #pragma unroll
             for (int bb = 0; bb < DB; ++bb) {
-              const int d = 32 * bb + lr;
-              const float vv = v_lds[key * D + kv_chunk_f32(d >> 2, key) * 4 + (d & 3)];
+              const float vv = v_lds[v_off[i] + (32 * kb + 8 * j) * D + 32 * (bb ^ (j & 1))];
               oacc[bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(vv, p[kb][4 * j + i], oacc[bb], 0,
                                                               0, 0);
             }

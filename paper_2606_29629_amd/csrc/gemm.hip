@@ -768,18 +768,19 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
   // into the LDS buffers freed by the last two k-tiles (ResPf)
   constexpr bool kResPf = KIND == EPI_RESID && !F32 && BM == 256 && BN == 256 && S == 2 &&
                           NW == 8;
+  // The descriptor is built unconditionally (only `on` depends on the split):
+  // a descriptor assigned under a run-time branch ends up in private memory,
+  // and a kernel with a private segment slows every later dispatch on its
+  // queue.
   ResPf rp{};
   if constexpr (kResPf) {
-    if (u < 0 && K / kBK >= 2) {
-      const int rows_left = M - tm * BM;
-      rp.on = true;
-      rp.ld_bytes = epi.ldr * 2;
-      rp.rsrc = __builtin_amdgcn_make_buffer_rsrc(
-          (void*)((const bf16*)epi.resid + (int64_t)tm * BM * epi.ldr + tn * BN), (short)0,
-          (int)((int64_t)rows_left * epi.ldr * 2), 0x00020000);
-      rp.voff = (uint32_t)((lane >> 5) * rp.ld_bytes +
-                           (((lane & 31) ^ ((2 * wv + (lane >> 5)) & 15)) << 4));
-    }
+    const int ld_bytes = epi.ldr * 2;
+    rp = ResPf{__builtin_amdgcn_make_buffer_rsrc(
+                   (void*)((const bf16*)epi.resid + (int64_t)tm * BM * epi.ldr + tn * BN),
+                   (short)0, (int)((int64_t)(M - tm * BM) * ld_bytes), 0x00020000),
+               (uint32_t)((lane >> 5) * ld_bytes +
+                          (((lane & 31) ^ ((2 * wv + (lane >> 5)) & 15)) << 4)),
+               ld_bytes, u < 0 && K / kBK >= 2};
   }
   ML::template run_valid<MI, kResPf>(M - tm * BM, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane,
                                      acc, rp);
