@@ -19,6 +19,7 @@
 namespace tri {
 
 constexpr int kRouteTok = 8;     // tokens per router workgroup
+constexpr int kMaxPlanes = 16;   // split-K planes of the router logits, at most
 constexpr int kRouteChunk = 1024;  // hidden columns staged per pass
 
 template <typename InT>
@@ -27,15 +28,15 @@ __device__ __forceinline__ float to_f32(InT v) { return (float)v; }
 // Top-k of one token's logits (lane holds experts lane + 64 q, q < 4; -inf
 // past E) with ties to the lower expert index, then the softmax weights of the
 // chosen experts (over all experts, or renormalised over the k chosen).
-// Lanes < k write slot `lane` of idx / w.
+// Selection s is kept by lane s, which writes slot s of idx / w.
 __device__ __forceinline__ void route_topk(const float (&vin)[4], int E, int k, int renorm,
                                            int lane, int32_t* __restrict__ idx,
                                            float* __restrict__ w) {
-  float v[4], orig[4];
+  float v[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) v[q] = orig[q] = vin[q];
-  float top_v[16];
-  int top_i[16];
+  for (int q = 0; q < 4; ++q) v[q] = vin[q];
+  float my_v = -INFINITY;
+  int my_i = 0;
   for (int s = 0; s < k; ++s) {
     // this lane's best (highest value, then lowest expert index)
     float bv = v[0];
@@ -52,26 +53,24 @@ __device__ __forceinline__ void route_topk(const float (&vin)[4], int E, int k, 
       const int oi = __shfl_xor(bi, o, 64);
       if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
     }
-    top_v[s] = bv;
-    top_i[s] = bi;
+    if (lane == s) { my_v = bv; my_i = bi; }
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (lane + 64 * q == bi) v[q] = -INFINITY;
   }
-  const float m = top_v[0];
+  const float m = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                                __builtin_bit_cast(int, my_v)));
   float z = 0.f;
 #pragma unroll
   for (int q = 0; q < 4; ++q)
-    if (lane + 64 * q < E) z += expf(orig[q] - m);
+    if (lane + 64 * q < E) z += expf(vin[q] - m);
   z = wave_sum(z);
-  float zk = 0.f;
-  for (int s = 0; s < k; ++s) zk += expf(top_v[s] - m);
+  const float p = expf(my_v - m);
+  float zk = 0.f;  // the k chosen weights summed in selection order
+  for (int s = 0; s < k; ++s)
+    zk += __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p), s));
   if (lane < k) {
-    float p = 0.f;
-    int ii = 0;
-    for (int s = 0; s < k; ++s)
-      if (s == lane) { p = expf(top_v[s] - m); ii = top_i[s]; }
-    idx[lane] = ii;
+    idx[lane] = my_i;
     w[lane] = renorm ? p / zk : p / z;
   }
 }
@@ -158,14 +157,27 @@ __global__ __launch_bounds__(256) void moe_topk_kernel(const float* __restrict__
                                                        float* __restrict__ w_out) {
   const int lane = threadIdx.x & 63, t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
+  // Every plane's value is loaded before the ordered sum (S <= kMaxPlanes),
+  // so the loads are in flight together; planes past S and experts past E
+  // re-read an in-range address and are dropped.
+  const float* base = planes + (int64_t)t * E;
+  const int64_t plane = (int64_t)T * E;
+  float pv[4][kMaxPlanes];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = min(lane + 64 * q, E - 1);
+#pragma unroll
+    for (int sp = 0; sp < kMaxPlanes; ++sp)
+      pv[q][sp] = 64 * q < E ? base[min(sp, S - 1) * plane + e] : 0.f;  // (E is uniform)
+  }
   float v[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int e = lane + 64 * q;
     float a = 0.f;
-    if (e < E)
-      for (int sp = 0; sp < S; ++sp) a += planes[((int64_t)sp * T + t) * E + e];
-    v[q] = e < E ? a : -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < kMaxPlanes; ++sp)
+      if (sp < S) a += pv[q][sp];
+    v[q] = lane + 64 * q < E ? a : -INFINITY;
   }
   route_topk(v, E, k, renorm, lane, idx_out + (int64_t)t * k, w_out + (int64_t)t * k);
 }
@@ -191,6 +203,7 @@ hipError_t launch_moe_route_bf16(const void* h, const void* w_router, int T, int
                                  int renorm, float* planes, int32_t* idx, float* w, hipStream_t s) {
   if (T == 0) return hipSuccess;
   const int S = gemm_planes_splits(T, E, H);
+  if (S > kMaxPlanes) return hipErrorInvalidValue;
   hipError_t e = launch_gemm_planes(h, H, w_router, H, T, E, H, planes, S, s);
   if (e != hipSuccess) return e;
   moe_topk_kernel<<<cdiv(T, 4), 256, 0, s>>>(planes, S, T, E, k, renorm, idx, w);
