@@ -1151,6 +1151,17 @@ hipError_t launch_gemm(const void* A, int lda, const void* B, int ldb, int M, in
   // projection) keeps the 256 x 256 tail split.
   if (epi.kind != EPI_SWIGLU && epi.kind != EPI_STORE_F32 && K <= 8192 &&
       cdiv(M, 256) * cdiv(N, 256) < cu_count()) {
+    // Plain and residual stores (no rotary pairs) take 128 x 256 tiles of
+    // eight 64 x 64 waves when those fill one round of CUs at least three
+    // quarters full: a 4096-token O projection is one round of 256 such tiles
+    // instead of two rounds of 128 x 128.
+    const int t256 = cdiv(M, 128) * cdiv(N, 256);
+    if ((epi.kind == EPI_STORE || epi.kind == EPI_RESID) && t256 <= cu_count() &&
+        4 * t256 >= 3 * cu_count()) {
+      if (epi.kind == EPI_STORE)
+        return run_gemm<128, 256, 2, 4, EPI_STORE, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
+      return run_gemm<128, 256, 2, 4, EPI_RESID, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
+    }
     switch (epi.kind) {
       case EPI_STORE: return run_gemm<128, 128, 4, 1, EPI_STORE, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
       case EPI_RESID: return run_gemm<128, 128, 4, 1, EPI_RESID, 3, kMidSH>(A, lda, B, ldb, M, N, K, epi, s);
