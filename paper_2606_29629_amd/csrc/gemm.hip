@@ -723,8 +723,17 @@ __global__ __launch_bounds__(WGM * WGN * 64, 1) void gemm_kernel(const bf16* __r
   // Blocks [0, full) run whole tiles (ids 0 .. full-1 of the grouped order);
   // the ones after it run the last tiles in `tsplit` K-splits each (fp32
   // partials to `tail`), so that a final partial round fills every CU.
+  // Half-tile mode (tsplit == 0, 128-row tiles): the grid covers the last
+  // tiles of a 256-row grid (tiles_m of 256 rows, ids from `full`) as two
+  // 128-row halves each, over the whole K; the two halves of a tile are
+  // consecutive ids, so the XCD remap keeps them in one L2.
   int tm, tn, u = -1;
-  if ((int)blockIdx.x < full) {
+  if (BM == 128 && tsplit == 0) {
+    const int id = xcd_id(blockIdx.x, (int)gridDim.x);
+    tile_of_id(full + id / 2, tiles_m, tiles_n, tm, tn);
+    tm = 2 * tm + (id & 1);
+    if (tm * BM >= M) return;  // the empty half of a last M-tile
+  } else if ((int)blockIdx.x < full) {
     tile_of_id(xcd_id(blockIdx.x, full), tiles_m, tiles_n, tm, tn);
   } else {
     u = blockIdx.x - full;
@@ -1112,6 +1121,34 @@ static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, 
   static bool attr_set = false;
   hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK, 2, SH>, smem, attr_set);
   if (e != hipSuccess) return e;
+  // A tail split in two or three (a final round a quarter to a half full) of
+  // a bf16-output 256 x 256 GEMM runs instead as 128-row halves of the tail
+  // tiles over the whole K: the same round of work with no fp32 partials and
+  // no reduction kernel.
+  constexpr bool kHalfOk = BM == 256 && BN == 256 && !(EK & kEpiF32) &&
+                           (KIND == EPI_STORE || KIND == EPI_RESID || KIND == EPI_QKV ||
+                            KIND == EPI_QKV_NORM);
+  if constexpr (kHalfOk) {
+    if (t <= 3) {
+      if (full > 0) {
+        gemm_kernel<BM, BN, WGM, WGN, EK, 2, SH><<<full, WGM * WGN * 64, smem, s>>>(
+            (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, K, epi, tiles_m, tiles_n, full, 1,
+            nullptr);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+      }
+      // q/k/v keep 128 columns per wave (rotary pairs); the others 64 x 64 waves
+      constexpr int HM = (KIND == EPI_QKV || KIND == EPI_QKV_NORM) ? 4 : 2;
+      const size_t hsmem = sizeof(GemmSmem<128, 256, 3>);
+      static bool half_attr = false;
+      e = opt_in_lds(gemm_kernel<128, 256, HM, 8 / HM, EK, 3, kMidSH>, hsmem, half_attr);
+      if (e != hipSuccess) return e;
+      gemm_kernel<128, 256, HM, 8 / HM, EK, 3, kMidSH><<<2 * n_tail, 512, hsmem, s>>>(
+          (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, K, epi, tiles_m, tiles_n, full, 0,
+          nullptr);
+      return hipGetLastError();
+    }
+  }
   gemm_kernel<BM, BN, WGM, WGN, EK, 2, SH><<<full + n_tail * t, WGM * WGN * 64, smem, s>>>(
       (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, K, epi, tiles_m, tiles_n, full, t, tail);
   e = hipGetLastError();

@@ -351,7 +351,9 @@ def test_full_size_dense_prefill_sampled():
     wl = workload("dense_prefill")
     cs = Case(wl.cfg, wl.batch, wl.n_slots, wl.max_seq)
     out, ws = cs.run()
-    rows = np.array([0, 63, 64, 2047, 2048, 5 * 2048 + 1000, 16383])
+    # (rows 12300 and up lie in the projections' last-round tiles, which run
+    # as 128-row halves)
+    rows = np.array([0, 63, 64, 2047, 2048, 5 * 2048 + 1000, 12300, 14337, 15000, 16383])
     x1, act, w = stage_parity(cs, ws, rows, label="full prefill")
     check_down(cs, out, x1, act, w, rows, "full prefill")
     s = 5

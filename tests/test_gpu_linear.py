@@ -6,7 +6,8 @@ adjacent bf16 value, with at most 1% of the elements one ulp off (fp32
 accumulation over K moves a value across a rounding boundary now and then).
 The shapes reach each GEMM path: the short-batch split-K planes (M <= 128),
 the mid-size 128-row tiles with three LDS stages (row blocks past M skipped),
-the 128 x 256 tiles that fill one round, the 256 x 256 tiles, and the tail split with uneven K splits (long K).  The
+the 128 x 256 tiles that fill one round, the 256 x 256 tiles (a final
+round a quarter to a half full as 128-row halves of its tiles), and the tail split with uneven K splits (long K).  The
 largest shapes are checked on sampled rows.
 """
 import numpy as np
@@ -30,6 +31,8 @@ SHAPES = [
     (4096, 4096, 1024),   # 256 x 256 tiles, one full round
     (4096, 2048, 4096),   # 128 x 256 tiles, one round of 256
     (3000, 2048, 1024),   # 128 x 256 tiles, 56 valid rows in the last M-tile
+    (6144, 4096, 256),    # 1.5 rounds of 256 x 256: the last 128 tiles as 128-row halves
+    (5944, 4096, 256),    # same, the last M-tile's second half empty
 ]
 
 
