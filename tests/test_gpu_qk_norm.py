@@ -136,7 +136,10 @@ def test_7b_ragged_prefill():
     (qkn(MID_D128), [2048] * 5 + [1900, 48], [0, 0, 0, 0, 0, 100, 7], 2112),
     # 65 row tiles x 4 column tiles = 260: 256 whole + 4 tail, with the bias
     (qkn(MID_D64, True), [4096] * 4 + [200], [0, 0, 0, 0, 37], 4160),
-], ids=["D128", "D64_bias"])
+    # 64 row tiles x 6 column tiles = 384: 256 whole + 128 tail tiles run as
+    # 128-row halves
+    (qkn(MID_D128), [2048] * 8, [0] * 8, 2048),
+], ids=["D128", "D64_bias", "D128_half_tail"])
 def test_whole_tiles_and_tail(cfg, q_lens, ctx, max_seq):
     n = len(q_lens)
     batch = B(np.arange(n), ctx, q_lens)
@@ -144,7 +147,8 @@ def test_whole_tiles_and_tail(cfg, q_lens, ctx, max_seq):
     out, ws = cs.run()
     qkv_all_rows(cs, ws, f"D{cfg.head_dim} tiles")
     Tn = batch.n_tokens
-    rows = np.array([0, 31, 32, 255, 256, 4000, 8191, 8192, Tn // 2 + 17, Tn - 257, Tn - 2, Tn - 1])
+    rows = np.unique([r for r in (0, 31, 32, 255, 256, 4000, 8191, 8192, Tn // 2 + 17, 12300, 14000,
+                                  Tn - 257, Tn - 2, Tn - 1) if r < Tn])
     x1, act, w = stage_parity(cs, ws, rows, label=f"D{cfg.head_dim} tiles")
     check_down(cs, out, x1, act, w, rows, f"D{cfg.head_dim} tiles")
     s = n - 1
