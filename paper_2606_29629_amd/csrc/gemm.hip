@@ -1450,8 +1450,10 @@ __global__ __launch_bounds__(kNormRowThreads) void splitk_resid_norm_kernel(
 // projections -- every one resident at once, each a short run of weight rows,
 // which keeps the HBM pages streaming -- and split-K multiplies the
 // workgroups of the narrow projections until ~200 are in flight (~400 for
-// q/k/v, whose K is short).  Without a split the epilogue is fused; with one,
-// fp32 partial planes go to the workspace and splitk_epi_kernel finishes.
+// q/k/v, whose K is short; ~200 again for q/k/v over 128-row tiles, whose fp32
+// partial planes would otherwise weigh as much as its weights).  Without a
+// split the epilogue is fused; with one, fp32 partial planes go to the
+// workspace and splitk_epi_kernel finishes.
 // q/k/v always splits (its fused epilogue needs a whole head per wave).  The
 // split runs of up to two workgroups per CU keep four k-tiles in LDS (three
 // in flight), the rest two.
@@ -1461,7 +1463,7 @@ static int skinny_bm(int M) { return M <= 64 ? 64 : 128; }
 
 int skinny_splits(int M, int N, int K, int kind) {
   const int tiles = cdiv(M, skinny_bm(M)) * cdiv(N, kSkinnyBN);
-  const int target = kind == EPI_QKV ? 400 : 200;
+  const int target = kind == EPI_QKV && M <= 64 ? 400 : 200;
   int s = 1;
   while ((tiles * s < target || (kind == EPI_QKV && s == 1)) && s < 16 &&
          K % (kBK * 2 * s) == 0)
