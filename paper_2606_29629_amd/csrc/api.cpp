@@ -102,17 +102,20 @@ size_t part_bytes(const tri_layer_config* c, const tri_batch* b) {
   size_t p = flash_part_bytes(c, b) +
              attn_decode_partial_bytes(b->n_seqs, c->n_q_heads, D, b->max_ctx_len + 1);
   if (T > 0) {
-    // Skinny-path partials; a larger batch reserves them for the largest
-    // skinny batch, so that the size never shrinks as n_tokens grows.
-    const int Ts = T <= kSkinnyMaxRows ? T : kSkinnyMaxRows;
+    // Skinny-path partials.  64-row and 128-row batches split K differently,
+    // so a batch reserves them for the largest batch of each kind up to its
+    // own size: the size never shrinks as n_tokens grows.
     auto mx = [](size_t a, size_t b2) { return a > b2 ? a : b2; };
-    size_t g = skinny_partial_bytes(Ts, Nqkv, H, EPI_QKV);
-    g = mx(g, skinny_partial_bytes(Ts, H, c->n_q_heads * D, EPI_RESID));
-    if (!is_moe(c)) {
-      g = mx(g, skinny_partial_bytes(Ts, 2 * c->ffn_dim, H, EPI_SWIGLU));
-      g = mx(g, skinny_partial_bytes(Ts, H, c->ffn_dim, EPI_RESID));
-    }
-    p = mx(p, g);
+    auto skinny = [&](int Ts) {
+      size_t g = skinny_partial_bytes(Ts, Nqkv, H, EPI_QKV);
+      g = mx(g, skinny_partial_bytes(Ts, H, c->n_q_heads * D, EPI_RESID));
+      if (!is_moe(c)) {
+        g = mx(g, skinny_partial_bytes(Ts, 2 * c->ffn_dim, H, EPI_SWIGLU));
+        g = mx(g, skinny_partial_bytes(Ts, H, c->ffn_dim, EPI_RESID));
+      }
+      return g;
+    };
+    p = mx(p, mx(skinny(T < 64 ? T : 64), skinny(T <= kSkinnyMaxRows ? T : kSkinnyMaxRows)));
     // Large-M GEMMs: fp32 partials of their tail tiles (a constant bound, so
     // the size stays non-decreasing in n_tokens).
     if (T > kSkinnyMaxRows) p = mx(p, gemm_tail_bytes());

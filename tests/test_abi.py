@@ -376,3 +376,25 @@ def test_paged_cache_validation(lib):
     assert lib.tri_kvcache_append(ctypes.byref(cfg()), ctypes.byref(
         T.KVCache(FAKE, FAKE + 256, 1, 128, tab, 48, 4)), ctypes.byref(b), kn, kn + 4096,
         None) == T.TRI_ERR_UNSUPPORTED
+
+
+def test_workspace_size_never_shrinks_as_tokens_grow(lib):
+    """tri_workspace_size is non-decreasing in n_tokens for a fixed config (the
+    header's promise): a workspace sized for the largest batch serves every
+    smaller one.  Checked token by token across the short-batch paths, whose
+    64-row and 128-row tiles split K differently, and past them."""
+    dense = cfg(hidden=3584, n_q_heads=28, n_kv_heads=4, head_dim=128, ffn_dim=18944)
+    moe = cfg(hidden=2048, n_q_heads=32, n_kv_heads=4, head_dim=128, ffn_dim=0,
+              n_experts=128, top_k=8, expert_ffn_dim=768, flags=T.TRI_F_MOE)
+    shapes = (lambda n: batch(n_seqs=n, n_tokens=n, max_q=1, max_ctx=4096),  # decode steps
+              lambda n: batch(n_seqs=1, n_tokens=n, max_q=n, max_ctx=0))     # one prompt
+    for c in (dense, moe):
+        for shape in shapes:
+            prev = 0
+            for n in list(range(1, 300)) + [512, 1024, 4096]:
+                b = shape(n)
+                s = ctypes.c_size_t()
+                assert lib.tri_workspace_size(ctypes.byref(c), ctypes.byref(b),
+                                              ctypes.byref(s)) == 0
+                assert s.value >= prev, (c.hidden, n, s.value, prev)
+                prev = s.value
