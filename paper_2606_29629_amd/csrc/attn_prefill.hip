@@ -39,6 +39,8 @@ namespace tri {
 
 constexpr int kFaBQ = 128;  // queries per workgroup
 constexpr int kFaBK = 64;   // keys per tile
+constexpr int kMaxFaSplit = 8;  // key-range splits of a query tile, at most
+constexpr int kCombQ = 32;      // queries per workgroup of the split merge
 
 // K/V tiles: four separate LDS arrays (K and V of buffers 0 and 1), [key][d]
 // with chunks swizzled by kv_chunk (common.hpp).  Separate arrays, and a loop
@@ -418,29 +420,39 @@ __global__ __launch_bounds__(256) void attn_prefill_combine_kernel(
   const int s = blockIdx.z, qh = blockIdx.y;
   const int q0 = cu_q[s], n = cu_q[s + 1] - q0, c = ctx_len[s], sl = slot[s];
   if (n <= 0 || (n == 1 && !include_single) || q0 < 0 || q0 + n > n_tokens) return;
-  const int qt = (int)gridDim.x - 1 - (int)blockIdx.x;
-  if (qt * kFaBQ >= n) return;
+  const int qc = blockIdx.x;  // kCombQ-query chunk
+  if (qc * kCombQ >= n) return;
   if (sl < 0 || sl >= kv.n_slots || c < 0 || c + n > kv.max_seq) return;
+  const int qt = qc * kCombQ / kFaBQ;  // the flash query tile of the chunk
   const int nkt = cdiv(c + min(n, (qt + 1) * kFaBQ), kFaBK);
   const int tps = cdiv(nkt, nsplit);
-  const int ns = cdiv(nkt, tps);  // non-empty splits
+  const int ns = cdiv(nkt, tps);  // non-empty splits (<= kMaxFaSplit)
   constexpr int TPQ = D / 4;      // threads per query
   const int d = 4 * ((int)threadIdx.x % TPQ);
   const int64_t plane = (int64_t)n_tokens * Hq * (D + 2);
-  for (int qi = qt * kFaBQ + (int)threadIdx.x / TPQ; qi < min(n, (qt + 1) * kFaBQ);
+  for (int qi = qc * kCombQ + (int)threadIdx.x / TPQ; qi < min(n, (qc + 1) * kCombQ);
        qi += 256 / TPQ) {
     const float* pp = part + ((int64_t)(q0 + qi) * Hq + qh) * (D + 2);
+    // every split's partial is loaded before the fold (splits past ns re-read
+    // the last one and are dropped), so the loads are in flight together
+    float m[kMaxFaSplit], l[kMaxFaSplit];
+    f32x4 a[kMaxFaSplit];
+#pragma unroll
+    for (int j = 0; j < kMaxFaSplit; ++j) {
+      const float* pj = pp + min(j, ns - 1) * plane;
+      m[j] = pj[D];
+      l[j] = pj[D + 1];
+      a[j] = *(const f32x4*)(pj + d);
+    }
     float M = -INFINITY, L = 0.f;
     f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < ns; ++j) {
-      const float* pj = pp + j * plane;
-      const float m = pj[D], l = pj[D + 1];
-      const f32x4 a = *(const f32x4*)(pj + d);
-      if (m == -INFINITY) continue;  // no key of this split is visible to this query
-      const float Mn = fmaxf(M, m);
-      const float sc = exp2f(M - Mn), w = exp2f(m - Mn);
-      L = L * sc + l * w;
-      o = o * sc + a * w;
+#pragma unroll
+    for (int j = 0; j < kMaxFaSplit; ++j) {
+      if (j >= ns || m[j] == -INFINITY) continue;  // no key of split j visible to this query
+      const float Mn = fmaxf(M, m[j]);
+      const float sc = exp2f(M - Mn), w = exp2f(m[j] - Mn);
+      L = L * sc + l[j] * w;
+      o = o * sc + a[j] * w;
       M = Mn;
     }
     const float inv = 1.0f / L;
@@ -464,7 +476,8 @@ int attn_prefill_splits(int n_seqs, int n_tokens, int max_q_len, int max_ctx_len
   const int64_t wgs = (int64_t)cdiv(n_tokens, kFaBQ) * n_q_heads;  // query tiles of the batch
   const int max_tiles = cdiv(max_ctx_len + max_q_len, kFaBK);
   int sp = 1;
-  while (sp < 8 && wgs * sp * 2 * 4 <= (int64_t)cu_count() * 5 && max_tiles >= 16 * sp &&
+  while (sp < kMaxFaSplit && wgs * sp * 2 * 4 <= (int64_t)cu_count() * 5 &&
+         max_tiles >= 16 * sp &&
          (int64_t)n_seqs * sp * 2 <= 65535)  // the grid's z extent
     sp *= 2;
   return sp;
@@ -487,7 +500,7 @@ static hipError_t run_fa(const void* q, const void* kc, const void* vc, void* ou
       b.n_tokens, nsplit, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !SPLIT) return e;
-  dim3 cgrid(cdiv(b.max_q_len, kFaBQ), Hq, b.n_seqs);
+  dim3 cgrid(cdiv(b.max_q_len, kCombQ), Hq, b.n_seqs);
   attn_prefill_combine_kernel<D><<<cgrid, 256, 0, s>>>(part, (bf16*)out, b.cu_q, b.ctx_len, b.slot,
                                                        kv, Hq, include_single, b.n_tokens, nsplit);
   return hipGetLastError();
