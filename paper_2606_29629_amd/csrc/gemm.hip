@@ -957,6 +957,8 @@ static int tail_tiles(int total) {
   return total > G ? total % G : (total == G ? 0 : total);
 }
 
+constexpr int kMaxTailSplit = 8;  // K-parts of a tail tile, at most
+
 static int tail_split(int total, int K, int kind) {
   const int G = cu_count();
   const int rem = tail_tiles(total);
@@ -965,7 +967,7 @@ static int tail_split(int total, int K, int kind) {
   // last one the remainder: every split must keep at least one k-tile.
   const int kt = K / kBK;
   int t = G / rem;
-  if (t > 8) t = 8;
+  if (t > kMaxTailSplit) t = kMaxTailSplit;
   while (t > 1 && (t - 1) * cdiv(kt, t) >= kt) --t;
   return t;
 }
@@ -983,7 +985,9 @@ size_t gemm_tail_bytes() { return (size_t)cu_count() * 256 * 256 * sizeof(float)
 constexpr int kTailChunk = 2048;
 constexpr int kTailPer = kTailChunk / 256;
 
-template <int BM, int BN, bool F32>
+// QKV: the q/k/v instantiation (its own kernel, so that the plain path's
+// registers for every plane's values do not lower its occupancy).
+template <int BM, int BN, bool F32, bool QKV>
 __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__ tail, int tsplit,
                                                        int full, int tiles_m, int tiles_n, int M,
                                                        int N, Epi epi) {
@@ -994,7 +998,7 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
   tile_of_id(full + j, tiles_m, tiles_n, tm, tn);
   const float* __restrict__ tp = tail + (int64_t)j * tsplit * BM * BN;
   const int e0 = blockIdx.x * kTailChunk + threadIdx.x;
-  if (epi.kind != EPI_QKV) {
+  if constexpr (!QKV) {
     int idx[kTailPer];
     float v[kTailPer];
 #pragma unroll
@@ -1002,9 +1006,19 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
       idx[q] = min(e0 + 256 * q, BM * BN - 1);
       v[q] = 0.f;
     }
-    for (int sp = 0; sp < tsplit; ++sp)
+    // every plane's values are loaded before the ordered sum (tsplit <=
+    // kMaxTailSplit, a uniform bound), so the loads are in flight together
+    float pv[kMaxTailSplit][kTailPer];
 #pragma unroll
-      for (int q = 0; q < kTailPer; ++q) v[q] += tp[(int64_t)sp * BM * BN + idx[q]];
+    for (int sp = 0; sp < kMaxTailSplit; ++sp)
+#pragma unroll
+      for (int q = 0; q < kTailPer; ++q)
+        pv[sp][q] = sp < tsplit ? tp[(int64_t)sp * BM * BN + idx[q]] : 0.f;
+#pragma unroll
+    for (int sp = 0; sp < kMaxTailSplit; ++sp)
+#pragma unroll
+      for (int q = 0; q < kTailPer; ++q)
+        if (sp < tsplit) v[q] += pv[sp][q];
     float res[kTailPer];
     if (epi.kind == EPI_RESID) {
 #pragma unroll
@@ -1026,83 +1040,86 @@ __global__ __launch_bounds__(256) void tail_epi_kernel(const float* __restrict__
       }
     }
     return;
-  }
-  // q/k/v + bias + RoPE + cache write: one thread per rotary pair (a head of
-  // D columns lies inside one tile since BN is a multiple of D).
-  const int Dh = epi.head_dim, half = Dh / 2;
-  const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
-  int rr[kTailPer], cc[kTailPer];
-  float x1[kTailPer], x2[kTailPer];
-#pragma unroll
-  for (int q = 0; q < kTailPer; ++q) {
-    const int e = min(e0 + 256 * q, BM * (BN / 2) - 1);
-    const int pc = e % (BN / 2);
-    rr[q] = e / (BN / 2);
-    cc[q] = (pc / half) * Dh + pc % half;  // first-half column in the tile
-    x1[q] = x2[q] = 0.f;
-  }
-  for (int sp = 0; sp < tsplit; ++sp)
+  } else {
+    // q/k/v + bias + RoPE + cache write: one thread per rotary pair (a head of
+    // D columns lies inside one tile since BN is a multiple of D).
+    const int Dh = epi.head_dim, half = Dh / 2;
+    const int Hq = epi.n_q_heads, Hkv = epi.n_kv_heads;
+    int rr[kTailPer], cc[kTailPer];
+    float x1[kTailPer], x2[kTailPer];
 #pragma unroll
     for (int q = 0; q < kTailPer; ++q) {
-      const float* pl = tp + (int64_t)sp * BM * BN + rr[q] * BN + cc[q];
-      x1[q] += pl[0];
-      x2[q] += pl[half];
+      const int e = min(e0 + 256 * q, BM * (BN / 2) - 1);
+      const int pc = e % (BN / 2);
+      rr[q] = e / (BN / 2);
+      cc[q] = (pc / half) * Dh + pc % half;  // first-half column in the tile
+      x1[q] = x2[q] = 0.f;
     }
-  float2 cs[kTailPer];
-  int sl[kTailPer], tr[kTailPer];
-  float b1[kTailPer], b2[kTailPer], g1[kTailPer], g2[kTailPer];
+    // (plane by plane: loading every plane's pairs first needs twice the
+    // registers of the plain path and was slower)
+    for (int sp = 0; sp < tsplit; ++sp)
 #pragma unroll
-  for (int q = 0; q < kTailPer; ++q) {
-    const int row = min(tm * BM + rr[q], M - 1), col = min(tn * BN + cc[q], N - 1);
-    const int head = col / Dh, d = col % Dh;
-    cs[q] = epi.rope[(int64_t)row * half + d];
-    sl[q] = epi.tok_slot[row];
-    tr[q] = epi.tok_row[row];
-    b1[q] = epi.bias ? St::ld(epi.bias, col) : 0.f;
-    b2[q] = epi.bias ? St::ld(epi.bias, col + half) : 0.f;
-    const void* gp = head < Hq ? epi.q_norm : epi.k_norm;
-    const bool n = epi.q_norm && head < Hq + Hkv;
-    g1[q] = n ? St::ld(gp, d) : 1.f;
-    g2[q] = n ? St::ld(gp, d + half) : 1.f;
-  }
-  // Per-head RMSNorm of q and k: a head's rotary pairs are `half` consecutive
-  // elements, an aligned group of lanes, so its sum of squares is a group sum.
-  float rs[kTailPer];
+      for (int q = 0; q < kTailPer; ++q) {
+        const float* pl = tp + (int64_t)sp * BM * BN + rr[q] * BN + cc[q];
+        x1[q] += pl[0];
+        x2[q] += pl[half];
+      }
+    float2 cs[kTailPer];
+    int sl[kTailPer], tr[kTailPer];
+    float b1[kTailPer], b2[kTailPer], g1[kTailPer], g2[kTailPer];
 #pragma unroll
-  for (int q = 0; q < kTailPer; ++q) {
-    x1[q] += b1[q];
-    x2[q] += b2[q];
-    rs[q] = 1.f;
-    if (epi.q_norm) {
-      const float ss = group_sum(x1[q] * x1[q] + x2[q] * x2[q], half);
-      rs[q] = 1.0f / sqrtf(ss / (float)Dh + epi.eps);
+    for (int q = 0; q < kTailPer; ++q) {
+      const int row = min(tm * BM + rr[q], M - 1), col = min(tn * BN + cc[q], N - 1);
+      const int head = col / Dh, d = col % Dh;
+      cs[q] = epi.rope[(int64_t)row * half + d];
+      sl[q] = epi.tok_slot[row];
+      tr[q] = epi.tok_row[row];
+      b1[q] = epi.bias ? St::ld(epi.bias, col) : 0.f;
+      b2[q] = epi.bias ? St::ld(epi.bias, col + half) : 0.f;
+      const void* gp = head < Hq ? epi.q_norm : epi.k_norm;
+      const bool n = epi.q_norm && head < Hq + Hkv;
+      g1[q] = n ? St::ld(gp, d) : 1.f;
+      g2[q] = n ? St::ld(gp, d + half) : 1.f;
     }
-  }
+    // Per-head RMSNorm of q and k: a head's rotary pairs are `half` consecutive
+    // elements, an aligned group of lanes, so its sum of squares is a group sum.
+    float rs[kTailPer];
 #pragma unroll
-  for (int q = 0; q < kTailPer; ++q) {
-    const int row = tm * BM + rr[q], col = tn * BN + cc[q];
-    if (e0 + 256 * q >= BM * (BN / 2) || row >= M || col >= N) continue;
-    const int head = col / Dh, d = col % Dh;
-    float y1 = x1[q], y2 = x2[q];
-    if (head < Hq + Hkv) {
-      y1 *= rs[q] * g1[q];
-      y2 *= rs[q] * g2[q];
-      const float r1 = y1 * cs[q].x - y2 * cs[q].y;
-      const float r2 = y2 * cs[q].x + y1 * cs[q].y;
-      y1 = r1;
-      y2 = r2;
+    for (int q = 0; q < kTailPer; ++q) {
+      x1[q] += b1[q];
+      x2[q] += b2[q];
+      rs[q] = 1.f;
+      if (epi.q_norm) {
+        const float ss = group_sum(x1[q] * x1[q] + x2[q] * x2[q], half);
+        rs[q] = 1.0f / sqrtf(ss / (float)Dh + epi.eps);
+      }
     }
-    T* dst;
-    if (head < Hq) {
-      dst = (T*)epi.q + ((int64_t)row * Hq + head) * Dh + d;
-    } else {
-      if (sl[q] < 0) continue;
-      const int kvh = head < Hq + Hkv ? head - Hq : head - Hq - Hkv;
-      T* cache = (T*)(head < Hq + Hkv ? epi.kc : epi.vc);
-      dst = cache + (((int64_t)sl[q] * Hkv + kvh) * epi.max_seq + tr[q]) * Dh + d;
+#pragma unroll
+    for (int q = 0; q < kTailPer; ++q) {
+      const int row = tm * BM + rr[q], col = tn * BN + cc[q];
+      if (e0 + 256 * q >= BM * (BN / 2) || row >= M || col >= N) continue;
+      const int head = col / Dh, d = col % Dh;
+      float y1 = x1[q], y2 = x2[q];
+      if (head < Hq + Hkv) {
+        y1 *= rs[q] * g1[q];
+        y2 *= rs[q] * g2[q];
+        const float r1 = y1 * cs[q].x - y2 * cs[q].y;
+        const float r2 = y2 * cs[q].x + y1 * cs[q].y;
+        y1 = r1;
+        y2 = r2;
+      }
+      T* dst;
+      if (head < Hq) {
+        dst = (T*)epi.q + ((int64_t)row * Hq + head) * Dh + d;
+      } else {
+        if (sl[q] < 0) continue;
+        const int kvh = head < Hq + Hkv ? head - Hq : head - Hq - Hkv;
+        T* cache = (T*)(head < Hq + Hkv ? epi.kc : epi.vc);
+        dst = cache + (((int64_t)sl[q] * Hkv + kvh) * epi.max_seq + tr[q]) * Dh + d;
+      }
+      dst[0] = (T)y1;
+      dst[half] = (T)y2;
     }
-    dst[0] = (T)y1;
-    dst[half] = (T)y2;
   }
 }
 
@@ -1154,8 +1171,10 @@ static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, 
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int elems = KIND == EPI_QKV || KIND == EPI_QKV_NORM ? BM * BN / 2 : BM * BN;
-  tail_epi_kernel<BM, BN, (EK & kEpiF32) != 0><<<dim3(cdiv(elems, kTailChunk), n_tail), 256, 0, s>>>(
-      tail, t, full, tiles_m, tiles_n, M, N, epi);
+  constexpr bool kQkv = KIND == EPI_QKV || KIND == EPI_QKV_NORM;
+  tail_epi_kernel<BM, BN, (EK & kEpiF32) != 0, kQkv>
+      <<<dim3(cdiv(elems, kTailChunk), n_tail), 256, 0, s>>>(tail, t, full, tiles_m, tiles_n, M,
+                                                             N, epi);
   return hipGetLastError();
 }
 
