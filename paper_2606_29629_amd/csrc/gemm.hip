@@ -204,7 +204,7 @@ struct Mainloop {
                                                   __amdgpu_buffer_rsrc_t rb,
                                                   const uint32_t (&b_off)[B_BLK], int K, int wv,
                                                   int lane, acc_t (&acc)[MI][NI],
-                                                  const ResPf& rp) {
+                                                  const ResPf& rp, int kshift) {
     static_assert(MA >= 0 && MA <= MI, "active row blocks");
     static_assert(!RPF || (BM == 256 && BN == 256 && NW == 8 && S == 2),
                   "residual prefetch: two 64-row regions of 32 pieces per buffer");
@@ -216,8 +216,15 @@ struct Mainloop {
     // kill = 0x80000000 pushes every offset past the buffer's range, so the
     // load writes zeros instead of touching memory (used past the last tile,
     // keeping the schedule free of branches).
+    // k-tile kt of the loop reads k-tile (kt + kshift) mod KT of the operands
+    // (a rotation: the loop still visits every k-tile once, in a fixed order)
+    const int KTr = K / kBK;
+    auto kbyte = [&](int kt) {
+      const int kk = kt + kshift;
+      return (kk >= KTr ? kk - KTr : kk) * kBK * 2;
+    };
     auto gload = [&](int kt, int buf, uint32_t kill) {
-      const int kb = kt * kBK * 2;
+      const int kb = kbyte(kt);
 #pragma unroll
       for (int j = 0; j < A_BLK; ++j)
         buffer_load_lds16(ra, &sm.a[buf][(wv + NW * j) * 8 * kBK], a_off[j] | kill, kb);
@@ -264,7 +271,7 @@ struct Mainloop {
     };
     // Load piece p of a tile: p < A_BLK -> A block p, else B block p - A_BLK.
     auto gpiece = [&](int kt, int buf, uint32_t kill, int p) {
-      const int kb = kt * kBK * 2;
+      const int kb = kbyte(kt);
       if (p < A_BLK)
         buffer_load_lds16(ra, &sm.a[buf][(wv + NW * p) * 8 * kBK], a_off[p] | kill, kb);
       else
@@ -347,14 +354,14 @@ struct Mainloop {
                                                    __amdgpu_buffer_rsrc_t rb,
                                                    const uint32_t (&b_off)[B_BLK], int K, int wv,
                                                    int lane, acc_t (&acc)[MI][NI],
-                                                   const ResPf& rp = ResPf{}) {
+                                                   const ResPf& rp = ResPf{}, int kshift = 0) {
     const int wm = wv / WGN;
     const int act = (rows - wm * WM + SH - 1) / SH;  // row blocks holding valid rows
     if constexpr (MA == 0) {
-      run_rows<0, RPF>(sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp);
+      run_rows<0, RPF>(sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp, kshift);
     } else {
-      if (act >= MA) run_rows<MA, RPF>(sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp);
-      else run_valid<MA - 1, RPF>(rows, sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp);
+      if (act >= MA) run_rows<MA, RPF>(sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp, kshift);
+      else run_valid<MA - 1, RPF>(rows, sm, ra, a_off, rb, b_off, K, wv, lane, acc, rp, kshift);
     }
   }
 };
@@ -896,7 +903,12 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
     b_off[j] = gr < n_rows_b ? (uint32_t)(((int64_t)gr * K + swz(tr, lane & 7) * 8) * 2) : 0x80000000u;
   }
   typename ML::acc_t acc[MI][NI];
-  ML::run_valid(p_end - p0, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc);
+  // Short-row tiles (decode) stream their weights at HBM rate with every
+  // workgroup in flight at once; started at the same k-tile, all of them
+  // would read at one offset modulo the weight row (4 KB rows for H = 2048),
+  // so each rotates its k-loop by its own amount.
+  const int kshift = BM <= 32 ? (int)(((unsigned)id * 7u) % (unsigned)(K / kBK)) : 0;
+  ML::run_valid(p_end - p0, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc, ResPf{}, kshift);
 
   const int lr = Geo::lane_row(lane), lc = Geo::lane_col(lane);
   const int row0 = p0 + wm * WM + lr;
