@@ -1430,15 +1430,23 @@ __global__ __launch_bounds__(kNormRowThreads) void splitk_resid_norm_kernel(
     }
     v[c] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  for (int sp = 0; sp < splits; ++sp) {
-    f32x4 t[kNormRowChunks];
+  // planes in groups of four: a group's loads are in flight together, then
+  // added in plane order
+  for (int sp0 = 0; sp0 < splits; sp0 += 4) {
+    f32x4 t[4][kNormRowChunks];
 #pragma unroll
-    for (int c = 0; c < kNormRowChunks; ++c) {
-      const int ch = min(tid + c * kNormRowThreads, nch - 1);
-      t[c] = *(const f32x4*)(part + sp * MN + (int64_t)row * N + ch * 4);
-    }
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int c = 0; c < kNormRowChunks; ++c) v[c] += t[c];
+      for (int c = 0; c < kNormRowChunks; ++c) {
+        const int ch = min(tid + c * kNormRowThreads, nch - 1);
+        const int sp = min(sp0 + j, splits - 1);  // past the last plane: re-read, dropped
+        t[j][c] = *(const f32x4*)(part + sp * MN + (int64_t)row * N + ch * 4);
+      }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int c = 0; c < kNormRowChunks; ++c)
+        if (sp0 + j < splits) v[c] += t[j][c];
   }
   float ss = 0.f;
   bf16 x1[kNormRowChunks][4];
