@@ -906,8 +906,11 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_grouped_kernel(
   // Short-row tiles (decode) stream their weights at HBM rate with every
   // workgroup in flight at once; started at the same k-tile, all of them
   // would read at one offset modulo the weight row (4 KB rows for H = 2048),
-  // so each rotates its k-loop by its own amount.
-  const int kshift = BM <= 32 ? (int)(((unsigned)id * 7u) % (unsigned)(K / kBK)) : 0;
+  // so each rotates its k-loop by its own amount.  The prefill down
+  // projection (fp32 output) gains from it too; the prefill gate/up, whose
+  // tiles of one expert share their k-slices in L2, does not.
+  const bool rotate = BM <= 32 || KIND == EPI_STORE_F32;
+  const int kshift = rotate ? (int)(((unsigned)id * 7u) % (unsigned)(K / kBK)) : 0;
   ML::run_valid(p_end - p0, sm, rsrc_a, a_off, rsrc_b, b_off, K, wv, lane, acc, ResPf{}, kshift);
 
   const int lr = Geo::lane_row(lane), lc = Geo::lane_col(lane);
