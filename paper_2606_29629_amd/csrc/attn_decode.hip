@@ -188,10 +188,19 @@ __global__ __launch_bounds__(64, 2) void attn_decode_kernel(
       tbl = (blk >= 0 && blk < kv.n_blocks) ? blk : -1;
     }
   }
+  // The loop's tile i is the split's tile (i + rot) mod nt: the waves of one
+  // split index start at different tiles, so the grid does not read every
+  // (sequence, head) region at the same offset at once.  Tiles past the
+  // split stay past it (empty).
+  const int rot = (int)(((unsigned)s * 7u + (unsigned)kvh * 3u) % (unsigned)nt);
+  auto phys = [&](int i) {
+    const int j = i + rot;
+    return i < nt ? (j >= nt ? j - nt : j) : i;
+  };
   // Buffer descriptor of tile i's rows of one cache operand: keys past the
   // sequence, tiles past the split and blocks outside the pool read as zero.
   auto tile_rsrc = [&](const bf16* base, int i) {
-    const int key0 = k_begin + kDecTile * i;
+    const int key0 = k_begin + kDecTile * phys(i);
     int panel = sl, prow = key0, rows = 0;
     if (i < nt) {
       rows = min(kDecTile, k_end - key0);
@@ -276,7 +285,7 @@ __global__ __launch_bounds__(64, 2) void attn_decode_kernel(
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPI) : "memory");  // tile i landed
     issue_v(i + 2);  // into the stage of tile i - 1, whose reads fed issued MFMAs
     const int st = i % kDecStages;
-    const int key0 = k_begin + kDecTile * i;
+    const int key0 = k_begin + kDecTile * phys(i);
     // S^T = K Q^T; element e: key key0 + 8 (e / 4) + 4 g + e % 4, head r.
     f32x16 sacc = f32x16{0.f};
 #pragma unroll
