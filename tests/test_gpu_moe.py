@@ -207,6 +207,21 @@ def test_moe_decode_full_size_sampled():
     assert_e2e(to_host_f64(c.out)[pick], exact["out"], "MoE decode rows", emul=forced["out"])
 
 
+def test_moe_decode_twice_bit_identical():
+    """The MoE decode launch twice on the same inputs: output, routes and
+    weights bit-identical (each expert workgroup's k-order and each decode
+    attention wave's tile order are fixed functions of the tile and wave)."""
+    import torch
+    wl = workload("moe_decode")
+    c = MoECase(wl.cfg, wl.batch, wl.n_slots, wl.max_seq, decode=True)
+    out0, idx0, w0 = c.out.clone(), c.idx.clone(), c.w.clone()
+    out1, _ = T.layer_decode(c.dl.cfg, c.dl.w, c.cache, c.db, to_device_bf16(c.xb),
+                             route_idx=c.idx, route_w=c.w)
+    torch.cuda.synchronize()
+    assert torch.equal(idx0, c.idx) and torch.equal(w0, c.w)
+    assert torch.equal(out0, out1)
+
+
 @pytest.mark.parametrize("n_tok", [600, 1000], ids=["128-row tiles", "256-row tiles"])
 def test_moe_grouped_tile_sizes(n_tok):
     """The grouped expert GEMMs pick their tile rows from the mean rows per
