@@ -1153,15 +1153,15 @@ static hipError_t run_gemm_tail(const void* A, int lda, const void* B, int ldb, 
   static bool attr_set = false;
   hipError_t e = opt_in_lds(gemm_kernel<BM, BN, WGM, WGN, EK, 2, SH>, smem, attr_set);
   if (e != hipSuccess) return e;
-  // A tail split in two or three (a final round a quarter to a half full) of
-  // a bf16-output 256 x 256 GEMM runs instead as 128-row halves of the tail
-  // tiles over the whole K: the same round of work with no fp32 partials and
-  // no reduction kernel.
+  // A tail split in two or three (a final round a quarter to a half full), or
+  // in four over a short K, of a bf16-output 256 x 256 GEMM runs instead as
+  // 128-row halves of the tail tiles over the whole K: the same round of work
+  // (or a little more) with no fp32 partials and no reduction kernel.
   constexpr bool kHalfOk = BM == 256 && BN == 256 && !(EK & kEpiF32) &&
                            (KIND == EPI_STORE || KIND == EPI_RESID || KIND == EPI_QKV ||
                             KIND == EPI_QKV_NORM);
   if constexpr (kHalfOk) {
-    if (t <= 3) {
+    if (t <= 3 || (t == 4 && K <= 4096)) {
       if (full > 0) {
         gemm_kernel<BM, BN, WGM, WGN, EK, 2, SH><<<full, WGM * WGN * 64, smem, s>>>(
             (const bf16*)A, lda, (const bf16*)B, ldb, M, N, K, K, epi, tiles_m, tiles_n, full, 1,

@@ -33,6 +33,7 @@ SHAPES = [
     (3000, 2048, 1024),   # 128 x 256 tiles, 56 valid rows in the last M-tile
     (6144, 4096, 256),    # 1.5 rounds of 256 x 256: the last 128 tiles as 128-row halves
     (5944, 4096, 256),    # same, the last M-tile's second half empty
+    (5120, 4096, 512),    # 64 tail tiles (a four-way split at short K) as 128-row halves
 ]
 
 

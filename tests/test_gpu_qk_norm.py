@@ -139,7 +139,9 @@ def test_7b_ragged_prefill():
     # 64 row tiles x 6 column tiles = 384: 256 whole + 128 tail tiles run as
     # 128-row halves
     (qkn(MID_D128), [2048] * 8, [0] * 8, 2048),
-], ids=["D128", "D64_bias", "D128_half_tail"])
+    # 53 row tiles x 6 = 318: 62 tail tiles (four-way split at K = 1024) as halves
+    (qkn(MID_D128), [2048] * 6 + [1280], [0] * 7, 2048),
+], ids=["D128", "D64_bias", "D128_half_tail", "D128_half_tail4"])
 def test_whole_tiles_and_tail(cfg, q_lens, ctx, max_seq):
     n = len(q_lens)
     batch = B(np.arange(n), ctx, q_lens)
