@@ -148,6 +148,8 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, KvDev kv, int
   }
   const int plane = lane < sec.s0 ? 0 : (lane < sec.s01 ? 1 : 2);
   const int pos = b.pos[(int64_t)(lane < half ? plane : 0) * b.n_tokens + t];
+  // The frequency needs no memory: it is formed while the loads are in flight.
+  const double inv_freq = lane < half ? pow(base, -2.0 * (double)lane / (double)(2 * half)) : 0.0;
   int sq = 0;
   for (int j0 = 0; j0 < b.n_seqs; j0 += 64 * kMapChunks) {
     int end[kMapChunks];
@@ -161,19 +163,12 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, KvDev kv, int
     for (int c = 0; c < kMapChunks; ++c)
       sq += __builtin_popcountll(__builtin_amdgcn_ballot_w64(end[c] <= t));
   }
-  if (lane == 0) {
-    bool ok = sq < b.n_seqs;
-    const int sc = ok ? sq : 0;
-    const int q0 = b.cu_q[sc], q1 = b.cu_q[sc + 1], sl = b.slot[sc], c0 = b.ctx_len[sc];
-    const int row = c0 + (t - q0);
-    ok = ok && sl >= 0 && sl < kv.n_slots && row >= 0 && row < kv.max_seq && t >= q0 && t < q1;
-    int prow = -1;
-    const int panel = ok ? kv_panel(kv, sl, row, prow) : -1;
-    tok_slot[t] = panel;
-    tok_row[t] = panel >= 0 ? prow : -1;
-  }
+  // The sequence's descriptors (the same for the whole wave) are loaded here
+  // and used last, so their latency overlaps the rotary table and the norm.
+  const bool in_batch = sq < b.n_seqs;
+  const int sc = in_batch ? sq : 0;
+  const int q0 = b.cu_q[sc], q1 = b.cu_q[sc + 1], sl = b.slot[sc], c0 = b.ctx_len[sc];
   if (lane < half) {
-    const double inv_freq = pow(base, -2.0 * (double)lane / (double)(2 * half));
     const double ang = (double)pos * inv_freq;
     double sn, cs;
     sincos(ang, &sn, &cs);
@@ -182,31 +177,40 @@ __global__ __launch_bounds__(256) void prologue_kernel(BatchDev b, KvDev kv, int
   if constexpr (F32) {
     rmsnorm_row_f32((const float*)xv + (int64_t)t * hidden, (const float*)gv_,
                     (float*)yv + (int64_t)t * hidden, hidden, eps, lane);
-    return;
-  }
-  float ss = 0.f;
+  } else {
+    float ss = 0.f;
 #pragma unroll
-  for (int c = 0; c < kNormMaxChunks; ++c) {
-    const int ch = lane + c * 64;
-    if (ch < nchunk) {
+    for (int c = 0; c < kNormMaxChunks; ++c) {
+      const int ch = lane + c * 64;
+      if (ch < nchunk) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float f = bf2f(v[c].e[e]);
-        ss += f * f;
+        for (int e = 0; e < 8; ++e) {
+          const float f = bf2f(v[c].e[e]);
+          ss += f * f;
+        }
+      }
+    }
+    ss = wave_sum(ss);
+    const float r = 1.0f / sqrtf(ss / (float)hidden + eps);
+#pragma unroll
+    for (int c = 0; c < kNormMaxChunks; ++c) {
+      const int ch = lane + c * 64;
+      if (ch < nchunk) {
+        Pack8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o.e[e] = f2bf(bf2f(v[c].e[e]) * r * bf2f(gv[c].e[e]));
+        stg16(y + (int64_t)t * hidden + ch * 8, o.u);
       }
     }
   }
-  ss = wave_sum(ss);
-  const float r = 1.0f / sqrtf(ss / (float)hidden + eps);
-#pragma unroll
-  for (int c = 0; c < kNormMaxChunks; ++c) {
-    const int ch = lane + c * 64;
-    if (ch < nchunk) {
-      Pack8 o;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o.e[e] = f2bf(bf2f(v[c].e[e]) * r * bf2f(gv[c].e[e]));
-      stg16(y + (int64_t)t * hidden + ch * 8, o.u);
-    }
+  if (lane == 0) {
+    const int row = c0 + (t - q0);
+    const bool ok = in_batch && sl >= 0 && sl < kv.n_slots && row >= 0 && row < kv.max_seq &&
+                    t >= q0 && t < q1;
+    int prow = -1;
+    const int panel = ok ? kv_panel(kv, sl, row, prow) : -1;
+    tok_slot[t] = panel;
+    tok_row[t] = panel >= 0 ? prow : -1;
   }
 }
 
