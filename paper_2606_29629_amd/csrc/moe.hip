@@ -211,28 +211,34 @@ hipError_t launch_moe_route_bf16(const void* h, const void* w_router, int T, int
 }
 
 // One workgroup per expert: rank of every pair routed to it, in pair order.
-// The pairs are scanned kCountUnroll x 256 at a time: the loads of a batch
-// are issued together and one barrier per batch publishes the waves' counts.
+// The pairs are scanned U x (64 NW) at a time: the loads of a batch are
+// issued together and one barrier per batch publishes the waves' counts.  A
+// workgroup's batches run one after another, so long pair lists (a
+// prefill's) take 16 waves per workgroup and short ones (decode) 4; the
+// 16-wave form unrolls 8 deep, which keeps its per-wave counts in registers.
 constexpr int kCountUnroll = 16;
 
-__global__ __launch_bounds__(256) void moe_count_kernel(const int32_t* __restrict__ idx,
-                                                        int n_pairs, int32_t* __restrict__ rank,
-                                                        int32_t* __restrict__ counts) {
-  __shared__ int wsum[2][kCountUnroll][4];
+template <int NW, int U = (NW > 4 ? 8 : kCountUnroll)>
+__global__ __launch_bounds__(NW * 64) void moe_count_kernel(const int32_t* __restrict__ idx,
+                                                            int n_pairs,
+                                                            int32_t* __restrict__ rank,
+                                                            int32_t* __restrict__ counts) {
+  constexpr int NT = NW * 64;
+  __shared__ int wsum[2][U][NW];
   const int e = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const unsigned long long below = (1ull << lane) - 1ull;
   int base = 0, buf = 0;
-  for (int p0 = 0; p0 < n_pairs; p0 += 256 * kCountUnroll, buf ^= 1) {
-    bool f[kCountUnroll];
+  for (int p0 = 0; p0 < n_pairs; p0 += NT * U, buf ^= 1) {
+    bool f[U];
 #pragma unroll
-    for (int u = 0; u < kCountUnroll; ++u) {
-      const int p = p0 + 256 * u + tid;
+    for (int u = 0; u < U; ++u) {
+      const int p = p0 + NT * u + tid;
       const int v = idx[min(p, n_pairs - 1)];  // clamped: no branch around the load
       f[u] = p < n_pairs && v == e;
     }
-    int within[kCountUnroll];
+    int within[U];
 #pragma unroll
-    for (int u = 0; u < kCountUnroll; ++u) {
+    for (int u = 0; u < U; ++u) {
       const unsigned long long m = __ballot(f[u]);
       within[u] = __popcll(m & below);
       if (lane == 0) wsum[buf][u][wave] = __popcll(m);
@@ -241,14 +247,14 @@ __global__ __launch_bounds__(256) void moe_count_kernel(const int32_t* __restric
     __syncthreads();
     int run = base;
 #pragma unroll
-    for (int u = 0; u < kCountUnroll; ++u) {
+    for (int u = 0; u < U; ++u) {
       int pre = 0, tot = 0;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < NW; ++w) {
         pre += w < wave ? wsum[buf][u][w] : 0;
         tot += wsum[buf][u][w];
       }
-      if (f[u]) rank[p0 + 256 * u + tid] = run + pre + within[u];
+      if (f[u]) rank[p0 + NT * u + tid] = run + pre + within[u];
       run += tot;
     }
     base = run;
@@ -295,7 +301,10 @@ hipError_t launch_moe_permute(const int32_t* idx, int n_pairs, int E, int bm, in
                               int32_t* counts, int32_t* perm, int32_t* inv, int32_t* seg,
                               int32_t* tile_off, hipStream_t s) {
   if (n_pairs == 0) return hipSuccess;
-  moe_count_kernel<<<E, 256, 0, s>>>(idx, n_pairs, rank, counts);
+  if (n_pairs > 256 * kCountUnroll)
+    moe_count_kernel<16><<<E, 1024, 0, s>>>(idx, n_pairs, rank, counts);
+  else
+    moe_count_kernel<4><<<E, 256, 0, s>>>(idx, n_pairs, rank, counts);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   moe_scatter_kernel<<<cdiv(n_pairs, 256), 256, 0, s>>>(idx, rank, counts, n_pairs, E, bm, perm,
