@@ -1491,21 +1491,21 @@ __global__ __launch_bounds__(kNormRowThreads) void splitk_resid_norm_kernel(
 // 64 x 64 tiles (two or four waves) give ~600 workgroups on the large
 // projections -- every one resident at once, each a short run of weight rows,
 // which keeps the HBM pages streaming -- and split-K multiplies the
-// workgroups of the narrow projections until ~200 are in flight (~400 for
-// q/k/v, whose K is short; ~200 again for q/k/v over 128-row tiles, whose fp32
-// partial planes would otherwise weigh as much as its weights).  Without a
+// workgroups of the narrow projections until ~200 are in flight.  Without a
 // split the epilogue is fused; with one, fp32 partial planes go to the
 // workspace and splitk_epi_kernel finishes.
 // q/k/v always splits (its fused epilogue needs a whole head per wave).  The
 // split runs of up to two workgroups per CU keep four k-tiles in LDS (three
-// in flight), the rest two.
+// in flight), the rest two.  For q/k/v at 64 rows, 4 splits with four stages
+// beat 8 with two: its partial planes are halved, and so is what they leave
+// dirty in the caches just before the attention streams the KV cache.
 constexpr int kSkinnyBN = 64;
 
 static int skinny_bm(int M) { return M <= 64 ? 64 : 128; }
 
 int skinny_splits(int M, int N, int K, int kind) {
   const int tiles = cdiv(M, skinny_bm(M)) * cdiv(N, kSkinnyBN);
-  const int target = kind == EPI_QKV && M <= 64 ? 400 : 200;
+  const int target = 200;
   int s = 1;
   while ((tiles * s < target || (kind == EPI_QKV && s == 1)) && s < 16 &&
          K % (kBK * 2 * s) == 0)
@@ -1522,7 +1522,7 @@ static hipError_t run_skinny_planes(const void* A, int lda, const void* B, int l
   pe.ldo = N;
   if (M > 64)
     return run_gemm<128, kSkinnyBN, 4, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
-  if (kind != EPI_QKV && cdiv(N, kSkinnyBN) * splits <= 2 * cu_count())
+  if (cdiv(N, kSkinnyBN) * splits <= 2 * cu_count())
     return run_gemm<64, kSkinnyBN, 2, 1, EPI_STORE_F32, 4>(A, lda, B, ldb, M, N, K, pe, s, splits);
   return run_gemm<64, kSkinnyBN, 2, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
 }
