@@ -1499,15 +1499,16 @@ __global__ __launch_bounds__(kNormRowThreads) void splitk_resid_norm_kernel(
 // in flight), the rest two.  For q/k/v at 64 rows, 4 splits with four stages
 // beat 8 with two: its partial planes are halved, and so is what they leave
 // dirty in the caches just before the attention streams the KV cache.  Over
-// 128-row tiles q/k/v likewise takes 2 splits with three stages (~100
-// workgroups' worth of tiles at two per CU).
+// 128-row tiles every split run likewise takes half the workgroups (~100)
+// with three stages (two workgroups per CU): fewer partial planes ahead of
+// the attention and of the weight streams that follow.
 constexpr int kSkinnyBN = 64;
 
 static int skinny_bm(int M) { return M <= 64 ? 64 : 128; }
 
 int skinny_splits(int M, int N, int K, int kind) {
   const int tiles = cdiv(M, skinny_bm(M)) * cdiv(N, kSkinnyBN);
-  const int target = kind == EPI_QKV && M > 64 ? 100 : 200;
+  const int target = M > 64 ? 100 : 200;
   int s = 1;
   while ((tiles * s < target || (kind == EPI_QKV && s == 1)) && s < 16 &&
          K % (kBK * 2 * s) == 0)
@@ -1523,7 +1524,7 @@ static hipError_t run_skinny_planes(const void* A, int lda, const void* B, int l
   pe.out = part;
   pe.ldo = N;
   if (M > 64) {
-    if (kind == EPI_QKV && cdiv(N, kSkinnyBN) * splits <= 2 * cu_count())
+    if (cdiv(N, kSkinnyBN) * splits <= 2 * cu_count())
       return run_gemm<128, kSkinnyBN, 4, 1, EPI_STORE_F32, 3>(A, lda, B, ldb, M, N, K, pe, s, splits);
     return run_gemm<128, kSkinnyBN, 4, 1, EPI_STORE_F32>(A, lda, B, ldb, M, N, K, pe, s, splits);
   }
